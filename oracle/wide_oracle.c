@@ -1,0 +1,206 @@
+/*
+ * WIDE masked-projection oracle: plain, slow, fp64 CPU reference.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may call, link or
+ * load this file; only the tests, the smoke check and the CPU-baseline leg of
+ * the benchmark use it.  It shares no code with the HIP library.
+ *
+ * What it computes (WIDE, "Token-level Dynamic Width Pruning"):
+ *   - the per-group stable sort of the routing mask (Section 3.3, the SortDesc
+ *     equation; Appendix B, Algorithm 1);
+ *   - N-axis masked projections: Q and the SwiGLU gate/up pair, pruned over
+ *     their out-features (Section 3.1, equations (1)-(3), Figure 1 caption);
+ *   - K-axis masked projections: W_o and W_down, pruned over their
+ *     in-features (Section 3.1 equations (2)-(3); Appendix B, the masked
+ *     K-axis sum that defines GEMM-K);
+ *   - the complete masked SwiGLU FFN of equation (3).
+ *
+ * Every floating-point input is widened exactly to fp64 (bf16 bit patterns or
+ * fp32 values) and every sum is accumulated in fp64 in natural index order,
+ * token by token, over the active groups only.  When `round_bf16` is set the
+ * oracle rounds to bf16 (round-to-nearest-even, straight from fp64) at the
+ * points where the bf16 data path stores a tensor: the FFN intermediate H,
+ * and every output.  Parallelised with OpenMP over tokens only; each token's
+ * arithmetic is sequential and identical to the serial loop.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ---- input widening --------------------------------------------------- */
+
+/* dtype 0: fp32 array; dtype 1: bf16 bit patterns (uint16). */
+static inline double load_elem(const void* p, int dtype, int64_t i) {
+  if (dtype == 1) {
+    uint32_t bits = ((uint32_t)((const uint16_t*)p)[i]) << 16;
+    float f;
+    memcpy(&f, &bits, sizeof f);
+    return (double)f;
+  }
+  return (double)((const float*)p)[i];
+}
+
+/* ---- bf16 rounding ------------------------------------------------------ */
+
+/* Round an fp64 value to the nearest bf16 value (8 significant bits,
+ * exponent range of fp32), ties to even, in one step from fp64 (no
+ * intermediate fp32 rounding).  Returns the rounded value as fp64. */
+double oracle_bf16_round(double v) {
+  if (isnan(v) || isinf(v) || v == 0.0) return v;
+  int e;
+  frexp(v, &e);               /* v = f * 2^e, 0.5 <= |f| < 1 */
+  if (e < -125) e = -125;     /* below the normal range the quantum is fixed */
+  double q = ldexp(1.0, e - 8);  /* spacing of bf16 values in this binade */
+  double r = nearbyint(v / q) * q;  /* v/q exact; nearbyint: ties to even */
+  const double bf16_max = 3.3895313892515355e38; /* 0x7F7F */
+  if (fabs(r) > bf16_max) r = copysign(INFINITY, v);
+  return r;
+}
+
+static inline double store_round(double v, int round_bf16) {
+  return round_bf16 ? oracle_bf16_round(v) : v;
+}
+
+static inline double silu(double a) { return a / (1.0 + exp(-a)); }
+
+/* ---- mask reordering (Section 3.3 SortDesc; Algorithm 1) -------------- */
+
+/* For each routing column g: idx[g*M + 0 .. cnt[g]) lists the tokens t with
+ * mask[t*n_groups+g] != 0 in ascending order, followed by the remaining
+ * tokens in ascending order; cnt[g] counts the active ones.  A descending
+ * sort of a 0/1 column whose ties keep token order. */
+void oracle_mask_reorder(const uint8_t* mask, int64_t M, int32_t n_groups,
+                         int32_t* idx, int32_t* cnt) {
+  for (int32_t g = 0; g < n_groups; ++g) {
+    int32_t* out = idx + (int64_t)g * M;
+    int64_t j = 0;
+    for (int64_t t = 0; t < M; ++t)
+      if (mask[t * n_groups + g] != 0) out[j++] = (int32_t)t;
+    cnt[g] = (int32_t)j;
+    for (int64_t t = 0; t < M; ++t)
+      if (mask[t * n_groups + g] == 0) out[j++] = (int32_t)t;
+  }
+}
+
+/* ---- dense projection --------------------------------------------------- */
+
+/* out[t, n] = sum_k x[t, k] * w[n, k]   (x: [M][K], w: [N][K], nn.Linear
+ * layout).  Used for the unpruned K and V projections (equation (1)). */
+void oracle_linear(int dtype, int round_bf16, int64_t M, int32_t K, int32_t N,
+                   const void* x, const void* w, double* out) {
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t t = 0; t < M; ++t) {
+    for (int32_t n = 0; n < N; ++n) {
+      double acc = 0.0;
+      for (int32_t k = 0; k < K; ++k)
+        acc += load_elem(x, dtype, t * K + k) * load_elem(w, dtype, (int64_t)n * K + k);
+      out[t * N + n] = store_round(acc, round_bf16);
+    }
+  }
+}
+
+/* ---- N-axis masked projection (Q; Section 3.1, Figure 1) ---------------- */
+
+/* The out-feature axis N is cut into n_groups = N / G contiguous groups.
+ * out[t, n] = sum_k x[t,k] w[n,k] when group n/G is active for token t,
+ * and exactly zero otherwise. */
+void oracle_nproj(int dtype, int round_bf16, int64_t M, int32_t K, int32_t N,
+                  int32_t G, const uint8_t* mask, const void* x, const void* w,
+                  double* out) {
+  const int32_t n_groups = N / G;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t t = 0; t < M; ++t) {
+    for (int32_t n = 0; n < N; ++n) out[t * N + n] = 0.0;
+    for (int32_t g = 0; g < n_groups; ++g) {
+      if (mask[t * n_groups + g] == 0) continue;
+      for (int32_t n = g * G; n < (g + 1) * G; ++n) {
+        double acc = 0.0;
+        for (int32_t k = 0; k < K; ++k)
+          acc += load_elem(x, dtype, t * K + k) * load_elem(w, dtype, (int64_t)n * K + k);
+        out[t * N + n] = store_round(acc, round_bf16);
+      }
+    }
+  }
+}
+
+/* ---- K-axis masked projection (W_o, W_down; Appendix B GEMM-K sum) ------ */
+
+/* The in-feature (reduction) axis K is cut into n_groups = K / G groups.
+ * out[t, n] = sum over active groups g of sum_{k in group g} a[t,k] w[n,k]:
+ * inactive groups contribute nothing, whatever a holds there. */
+void oracle_kproj(int dtype, int round_bf16, int64_t M, int32_t K, int32_t N,
+                  int32_t G, const uint8_t* mask, const void* a, const void* w,
+                  double* out) {
+  const int32_t n_groups = K / G;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t t = 0; t < M; ++t) {
+    for (int32_t n = 0; n < N; ++n) {
+      double acc = 0.0;
+      for (int32_t g = 0; g < n_groups; ++g) {
+        if (mask[t * n_groups + g] == 0) continue;
+        for (int32_t k = g * G; k < (g + 1) * G; ++k)
+          acc += load_elem(a, dtype, t * K + k) * load_elem(w, dtype, (int64_t)n * K + k);
+      }
+      out[t * N + n] = store_round(acc, round_bf16);
+    }
+  }
+}
+
+/* ---- masked SwiGLU FFN (Section 3.1, equation (3)) ---------------------- */
+
+/* x: [M][D]; w_gate, w_up: [Dff][D]; w_down: [D][Dff]; mask: [M][Dff/G].
+ * For each token, for each active group g and each channel j of that group:
+ *   h_j = silu(x . w_gate[j]) * (x . w_up[j])   (rounded to bf16 if asked)
+ *   y  += h_j * w_down[:, j]
+ * then y is rounded to bf16 if asked.  h (optional, [M][Dff]) receives the
+ * stored intermediate, zero at inactive groups. */
+void oracle_ffn(int dtype, int round_bf16, int64_t M, int32_t D, int32_t Dff,
+                int32_t G, const uint8_t* mask, const void* x,
+                const void* w_gate, const void* w_up, const void* w_down,
+                double* h, double* y) {
+  const int32_t n_groups = Dff / G;
+#pragma omp parallel
+  {
+    double* acc = (double*)malloc(sizeof(double) * (size_t)D);
+#pragma omp for schedule(dynamic, 1)
+    for (int64_t t = 0; t < M; ++t) {
+      for (int32_t n = 0; n < D; ++n) acc[n] = 0.0;
+      if (h)
+        for (int32_t j = 0; j < Dff; ++j) h[t * Dff + j] = 0.0;
+      for (int32_t g = 0; g < n_groups; ++g) {
+        if (mask[t * n_groups + g] == 0) continue;
+        for (int32_t j = g * G; j < (g + 1) * G; ++j) {
+          double a = 0.0, b = 0.0;
+          for (int32_t k = 0; k < D; ++k) {
+            double xv = load_elem(x, dtype, t * D + k);
+            a += xv * load_elem(w_gate, dtype, (int64_t)j * D + k);
+            b += xv * load_elem(w_up, dtype, (int64_t)j * D + k);
+          }
+          double hj = store_round(silu(a) * b, round_bf16);
+          if (h) h[t * Dff + j] = hj;
+          for (int32_t n = 0; n < D; ++n)
+            acc[n] += hj * load_elem(w_down, dtype, (int64_t)n * Dff + j);
+        }
+      }
+      for (int32_t n = 0; n < D; ++n) y[t * D + n] = store_round(acc[n], round_bf16);
+    }
+    free(acc);
+  }
+}
+
+/* Number of OpenMP threads the oracle runs with (for reporting). */
+int oracle_num_threads(void) {
+  int n = 1;
+#pragma omp parallel
+  {
+#pragma omp single
+    {
+#ifdef _OPENMP
+      extern int omp_get_num_threads(void);
+      n = omp_get_num_threads();
+#endif
+    }
+  }
+  return n;
+}

@@ -1,0 +1,309 @@
+"""Pins for the fp64 oracle, independent of the oracle's own code.
+
+Each test checks the oracle against something the paper or mathematics fixes:
+a hand-worked fixture, a closed form, a special case that reduces to a
+numpy/scipy/torch routine, an invariant, or a second formulation written
+differently (matrix form; the gather formulation of WIDE Appendix A).
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+from scipy.special import expit
+
+from paper_2607_28418_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------- helpers
+
+def f64(a):
+    return synth.as_f32(a).astype(np.float64)
+
+
+def rel_err(a, b):
+    return float(np.max(np.abs(a - b)) / max(np.max(np.abs(b)), 1e-300))
+
+
+def dense_swiglu_np(x, wg, wu, wd):
+    """Dense SwiGLU FFN in numpy fp64 (the all-ones-mask special case)."""
+    x, wg, wu, wd = f64(x), f64(wg), f64(wu), f64(wd)
+    a = x @ wg.T
+    h = a * expit(a) * (x @ wu.T)
+    return h, h @ wd.T
+
+
+def expand(mask, G):
+    return np.repeat(mask.astype(bool), G, axis=1)
+
+
+def torch_bf16(a64):
+    """fp64 -> bf16 -> fp64 via torch (rounds through fp32)."""
+    return torch.from_numpy(a64).to(torch.bfloat16).to(torch.float64).numpy()
+
+
+def small_ffn(seed=0, M=24, D=64, Dff=96, G=16, dtype="f32", mask="bernoulli", keep=0.5):
+    return synth.ffn_case(seed, M, D, Dff, G, dtype=dtype, mask=mask, keep=keep, w_std=0.1)
+
+
+# ---------------------------------------------------------------- bf16 rounding
+
+def test_bf16_round_matches_torch_on_fp32_values(orc):
+    g = synth.rng(1)
+    v = np.concatenate([g.standard_normal(2000).astype(np.float32) * 10.0 ** g.integers(-30, 30, 2000),
+                        np.array([1.0, -1.0, 65504.0, 1e-40, -3e-39], np.float32)])
+    ref = torch.from_numpy(v).to(torch.bfloat16).to(torch.float64).numpy()
+    got = np.array([orc.bf16_round(float(x)) for x in v])
+    assert np.array_equal(got, ref)
+
+
+def test_bf16_round_ties_and_direct_from_fp64(orc):
+    # ties go to the even significand
+    assert orc.bf16_round(1 + 2 ** -8) == 1.0
+    assert orc.bf16_round(1 + 3 * 2 ** -8) == 1 + 2 ** -6
+    assert orc.bf16_round(-(1 + 3 * 2 ** -8)) == -(1 + 2 ** -6)
+    # one rounding step from fp64: just above the tie rounds up (rounding via
+    # fp32 first would land on the tie and go down to 1.0)
+    assert orc.bf16_round(1 + 2 ** -8 + 2 ** -40) == 1 + 2 ** -7
+    # largest finite bf16 survives, the next step overflows to inf
+    bmax = (2 - 2 ** -7) * 2.0 ** 127
+    assert orc.bf16_round(bmax) == bmax
+    assert math.isinf(orc.bf16_round(2.0 ** 128 - 2.0 ** 119))
+    # subnormal range: quantum 2^-133, tie at half of it goes to zero (even)
+    assert orc.bf16_round(2.0 ** -133) == 2.0 ** -133
+    assert orc.bf16_round(2.0 ** -134) == 0.0
+    assert orc.bf16_round(1.5 * 2.0 ** -134) == 2.0 ** -133
+    assert orc.bf16_round(0.0) == 0.0
+
+
+# ---------------------------------------------------------------- reorder
+
+def _read_golden_reorder():
+    with open(os.path.join(GOLDEN, "reorder_hand.txt")) as f:
+        lines = [ln.split() for ln in f if ln.strip() and not ln.startswith("#")]
+    sec, data = None, {"mask": [], "cnt": [], "idx": []}
+    for ln in lines:
+        if ln[0] in data:
+            sec = ln[0]
+            continue
+        data[sec].append([int(v) for v in ln])
+    return (np.array(data["mask"], np.uint8), np.array(data["cnt"][0], np.int32),
+            np.array(data["idx"], np.int32))
+
+
+def test_reorder_hand_fixture(orc):
+    mask, cnt, idx = _read_golden_reorder()
+    i, c = orc.mask_reorder(mask)
+    assert np.array_equal(c, cnt)
+    assert np.array_equal(i, idx)
+
+
+@pytest.mark.parametrize("M,ng,p", [(1, 1, 0.5), (7, 3, 0.5), (300, 86, 0.3), (1000, 8, 0.9), (513, 24, 0.5)])
+def test_reorder_equals_stable_argsort(orc, M, ng, p):
+    g = synth.rng(M * 31 + ng)
+    mask = (g.random((M, ng)) < p).astype(np.uint8) * g.integers(1, 256, (M, ng)).astype(np.uint8)
+    idx, cnt = orc.mask_reorder(mask)
+    active = mask != 0
+    assert np.array_equal(cnt, active.sum(0).astype(np.int32))
+    for gi in range(ng):
+        ref = np.argsort(-active[:, gi].astype(np.int8), kind="stable")
+        assert np.array_equal(idx[gi], ref)
+        # invariants: a permutation whose prefix of length cnt is the active set
+        assert np.array_equal(np.sort(idx[gi]), np.arange(M))
+        assert np.array_equal(active[idx[gi], gi], np.arange(M) < cnt[gi])
+
+
+def test_reorder_degenerate(orc):
+    for mask in (np.zeros((5, 4), np.uint8), np.ones((5, 4), np.uint8)):
+        idx, cnt = orc.mask_reorder(mask)
+        assert np.array_equal(idx, np.tile(np.arange(5, dtype=np.int32), (4, 1)))
+        assert np.array_equal(cnt, np.full(4, int(mask[0, 0]) * 5, np.int32))
+    idx, cnt = orc.mask_reorder(np.zeros((0, 3), np.uint8))
+    assert idx.shape == (3, 0) and np.array_equal(cnt, np.zeros(3, np.int32))
+
+
+# ---------------------------------------------------------------- FFN
+
+def test_ffn_closed_form(orc):
+    # D = 2, Dff = 2, G = 1.  Gate pre-activations are ln 3 and 0, so
+    # silu = (3/4) ln 3 and 0; up = (2, 1); h = (1.5 ln 3, 0).
+    ln3 = np.float32(math.log(3.0))
+    x = np.array([[1.0, 0.0]], np.float32)
+    wg = np.array([[ln3, 0.0], [0.0, 5.0]], np.float32)
+    wu = np.array([[2.0, 0.0], [1.0, 1.0]], np.float32)
+    wd = np.array([[1.0, 7.0], [-2.0, 3.0]], np.float32)
+    h0 = 1.5 * math.log(3.0)   # ln3 is stored in fp32: agreement to ~1e-7
+    h, y = orc.ffn(x, wg, wu, wd, np.array([[1, 1]], np.uint8), 1)
+    assert np.allclose(h, [[h0, 0.0]], rtol=2e-7, atol=0)
+    assert np.allclose(y, [[h0, -2 * h0]], rtol=2e-7, atol=0)
+    h, y = orc.ffn(x, wg, wu, wd, np.array([[0, 1]], np.uint8), 1)
+    assert np.array_equal(h, [[0.0, 0.0]]) and np.array_equal(y, [[0.0, 0.0]])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_ffn_all_ones_is_dense_swiglu(orc, dtype):
+    c = small_ffn(dtype=dtype, mask="ones")
+    h, y = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, c.G)
+    hr, yr = dense_swiglu_np(c.x, c.w_gate, c.w_up, c.w_down)
+    assert rel_err(h, hr) < 1e-12
+    assert rel_err(y, yr) < 1e-12
+
+
+@pytest.mark.parametrize("rnd", [False, True])
+def test_ffn_all_zeros_is_exact_zero(orc, rnd):
+    c = small_ffn(dtype="bf16", mask="zeros")
+    h, y = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, c.G, round_bf16=rnd)
+    assert not h.any() and not y.any()
+    assert not np.signbit(y).any()
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_ffn_matches_masked_dense_formulation(orc, seed):
+    c = small_ffn(seed=seed, dtype="bf16", M=33, D=48, Dff=128, G=32)
+    h, y = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, c.G)
+    hd, _ = dense_swiglu_np(c.x, c.w_gate, c.w_up, c.w_down)
+    hm = hd * expand(c.mask, c.G)
+    assert rel_err(h, hm) < 1e-12
+    assert rel_err(y, hm @ f64(c.w_down).T) < 1e-12
+
+
+def test_ffn_matches_gather_formulation(orc):
+    """WIDE Appendix A: per-token gathered weight subsets (N-axis for gate/up,
+    K-axis for down), evaluated token by token with numpy."""
+    c = small_ffn(seed=5, M=9, D=20, Dff=48, G=16, keep=0.5)
+    x, wg, wu, wd = f64(c.x), f64(c.w_gate), f64(c.w_up), f64(c.w_down)
+    y_ref = np.zeros((c.M, wd.shape[0]))
+    for t in range(c.M):
+        groups = np.flatnonzero(c.mask[t])
+        cols = (groups[:, None] * c.G + np.arange(c.G)[None, :]).reshape(-1)
+        a = wg[cols] @ x[t]
+        hsub = a * expit(a) * (wu[cols] @ x[t])
+        y_ref[t] = wd[:, cols] @ hsub
+    _, y = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, c.G)
+    assert rel_err(y, y_ref) < 1e-12
+
+
+def test_ffn_disjoint_masks_add(orc):
+    c = small_ffn(seed=3, dtype="bf16")
+    g = synth.rng(99)
+    split = g.random(c.mask.shape) < 0.5
+    m1 = (c.mask.astype(bool) & split).astype(np.uint8)
+    m2 = (c.mask.astype(bool) & ~split).astype(np.uint8)
+    _, y = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, c.G)
+    _, y1 = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, m1, c.G)
+    _, y2 = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, m2, c.G)
+    assert rel_err(y1 + y2, y) < 1e-12
+
+
+def test_ffn_token_permutation_and_row_independence(orc):
+    c = small_ffn(seed=4, dtype="bf16")
+    perm = synth.rng(4).permutation(c.M)
+    h, y = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, c.G, round_bf16=True)
+    hp, yp = orc.ffn(c.x[perm], c.w_gate, c.w_up, c.w_down, c.mask[perm], c.G, round_bf16=True)
+    assert np.array_equal(yp, y[perm]) and np.array_equal(hp, h[perm])
+    sub = np.array([3, 0, 17])
+    _, ys = orc.ffn(c.x[sub], c.w_gate, c.w_up, c.w_down, c.mask[sub], c.G, round_bf16=True)
+    assert np.array_equal(ys, y[sub])
+    _, cnt = orc.mask_reorder(c.mask)
+    _, cntp = orc.mask_reorder(c.mask[perm])
+    assert np.array_equal(cnt, cntp)
+
+
+def test_ffn_bf16_storage_rounding(orc):
+    """bf16 path: H and y are the fp64 results rounded to bf16 once."""
+    c = small_ffn(seed=6, dtype="bf16")
+    h_raw, _ = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, c.G)
+    h, y = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, c.G, round_bf16=True)
+    assert np.array_equal(h, torch_bf16(h_raw))
+    assert np.array_equal(y, torch_bf16(h @ f64(c.w_down).T))
+
+
+def test_bf16_bits_widen_exactly(orc):
+    c = small_ffn(seed=7, dtype="bf16")
+    _, y_bits = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, c.G)
+    _, y_f32 = orc.ffn(*(synth.as_f32(a) for a in (c.x, c.w_gate, c.w_up, c.w_down)), c.mask, c.G)
+    assert np.array_equal(y_bits, y_f32)
+
+
+# ---------------------------------------------------------------- Q / K / V / O
+
+def small_attn(seed=0, mask="topk", dtype="bf16"):
+    return synth.attn_case(seed, M=21, D=64, n_q=8, n_kv=2, hd=8, G=16, dtype=dtype,
+                           mask=mask, keep=0.5, w_std=0.1)
+
+
+def test_linear_is_matmul(orc):
+    c = small_attn()
+    assert rel_err(orc.linear(c.x, c.w_k), f64(c.x) @ f64(c.w_k).T) < 1e-12
+    assert np.array_equal(orc.linear(c.x, c.w_v, round_bf16=True),
+                          torch_bf16(orc.linear(c.x, c.w_v)))
+
+
+def test_nproj_special_cases_and_formulations(orc):
+    c = small_attn()
+    dense = f64(c.x) @ f64(c.w_q).T
+    assert rel_err(orc.nproj(c.x, c.w_q, np.ones_like(c.mask), c.G), dense) < 1e-12
+    assert not orc.nproj(c.x, c.w_q, np.zeros_like(c.mask), c.G, round_bf16=True).any()
+    q = orc.nproj(c.x, c.w_q, c.mask, c.G)
+    assert rel_err(q, dense * expand(c.mask, c.G)) < 1e-12
+    # Appendix A N-axis gather formulation, token by token
+    x, w = f64(c.x), f64(c.w_q)
+    for t in range(c.x.shape[0]):
+        cols = (np.flatnonzero(c.mask[t])[:, None] * c.G + np.arange(c.G)).reshape(-1)
+        ref = np.zeros(w.shape[0])
+        ref[cols] = w[cols] @ x[t]
+        assert rel_err(q[t], ref) < 1e-12
+    # top-k mask keeps exactly half the groups of every token
+    assert np.all(c.mask.sum(1) == c.mask.shape[1] // 2)
+
+
+def test_kproj_special_cases_and_formulations(orc):
+    c = small_attn()
+    a, w = f64(c.a), f64(c.w_o)
+    assert rel_err(orc.kproj(c.a, c.w_o, np.ones_like(c.mask), c.G), a @ w.T) < 1e-12
+    z = orc.kproj(c.a, c.w_o, np.zeros_like(c.mask), c.G, round_bf16=True)
+    assert not z.any() and not np.signbit(z).any()
+    y = orc.kproj(c.a, c.w_o, c.mask, c.G)
+    assert rel_err(y, (a * expand(c.mask, c.G)) @ w.T) < 1e-12
+    for t in range(a.shape[0]):   # Appendix A K-axis gather formulation
+        cols = (np.flatnonzero(c.mask[t])[:, None] * c.G + np.arange(c.G)).reshape(-1)
+        assert rel_err(y[t], w[:, cols] @ a[t, cols]) < 1e-12
+    # inactive groups are never read: poisoning them changes nothing
+    ap = synth.as_f32(c.a).copy()
+    ap[~expand(c.mask, c.G)] = np.nan
+    yp = orc.kproj(ap, synth.as_f32(c.w_o), c.mask, c.G)
+    assert np.array_equal(yp, y)
+    assert np.array_equal(orc.kproj(c.a, c.w_o, c.mask, c.G, round_bf16=True), torch_bf16(y))
+
+
+def test_kproj_disjoint_masks_add(orc):
+    c = small_attn(mask="bernoulli")
+    m2 = (1 - c.mask).astype(np.uint8)
+    y = orc.kproj(c.a, c.w_o, np.ones_like(c.mask), c.G)
+    y1 = orc.kproj(c.a, c.w_o, c.mask, c.G)
+    y2 = orc.kproj(c.a, c.w_o, m2, c.G)
+    assert rel_err(y1 + y2, y) < 1e-12
+
+
+# ---------------------------------------------------------------- synthetic inputs
+
+def test_synth_bf16_quantisation_matches_torch():
+    a = synth.rng(0).standard_normal(5000).astype(np.float32) * 3
+    bits = synth.f32_to_bf16_bits(a)
+    ref = torch.from_numpy(a).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(bits, ref)
+
+
+def test_synth_masks():
+    g = synth.rng(0)
+    m = synth.mask_beta_groups(g, 20000, 86, 0.5)
+    assert abs(m.mean() - 0.5) < 0.02
+    assert synth.keep_count(86, 0.5) == 43 and synth.keep_count(86, 0.25) == 22
+    assert synth.keep_count(86, 0.75) == 65 and synth.keep_count(112, 0.25) == 28
+    t = synth.mask_topk(np.array([[1.0, 3.0, 3.0, 0.0]]), 2)
+    assert t.tolist() == [[0, 1, 1, 0]]
+    t = synth.mask_topk(np.array([[2.0, 2.0, 2.0, 0.0]]), 2)   # ties: lower index wins
+    assert t.tolist() == [[1, 1, 0, 0]]
