@@ -1,0 +1,324 @@
+#!/usr/bin/env python3
+"""Benchmark of the WIDE masked-projection hot path on one MI355X.
+
+Workload: the projections of one Llama-3-8B-shaped decoder layer (d_model
+4096, 32 q / 8 kv heads of 128 in 8 head groups of G=512, d_ff 14336 in 112
+groups of 128), synthetic bf16 inputs, per-token top-k masks from random
+router logits at 50% sparsity.  One step is the whole hot path twice:
+
+  prefill (T = 8192 tokens): mask reorder (attention and FFN masks), masked Q
+           + dense K/V, masked O, masked SwiGLU gate/up, masked down;
+  decode  (B = 32 tokens):   the same projections through the decode kernels.
+
+value = active FLOPs of the step (FLOPs of the executed groups only, the
+paper's accounting) / step time, in TFLOP/s.  The JSON line also carries the
+prefill and decode figures separately, the speedup over dense bf16 GEMMs
+(hipBLASLt through torch) and over the same kernels with an all-ones mask,
+the roofline of the dominant kernel (HIP-event durations recorded inside the
+timed region) and the fp64 CPU oracle timed on a bounded sample of the same
+workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense
+PEAK_HBM_GBPS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--keep", type=float, default=0.5, help="fraction of groups kept per token")
+    ap.add_argument("--prefill-tokens", type=int, default=8192)
+    ap.add_argument("--decode-batch", type=int, default=32)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--cpu-sample-tokens", type=int, default=48)
+    return ap.parse_args()
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+class Layer:
+    """Synthetic inputs of one decoder layer's projections (host bf16 bits)."""
+
+    def __init__(self, seed, T, B, keep):
+        from paper_2607_28418_amd import synth
+        p = synth.WORKLOADS["layer_llama3_8b"].params
+        self.D, self.Dff, self.G = p["D"], p["Dff"], p["G"]
+        self.nq, self.nkv, self.hd, self.Ga = p["n_q"], p["n_kv"], p["hd"], p["G_attn"]
+        self.Nq, self.Nkv = self.nq * self.hd, self.nkv * self.hd
+        self.ng, self.nga = self.Dff // self.G, self.Nq // self.Ga
+        g = synth.rng(seed)
+        D, Dff, Nq, Nkv = self.D, self.Dff, self.Nq, self.Nkv
+        n = synth.normal
+        self.w = dict(w_q=n(g, (Nq, D), 0.02, "bf16"), w_k=n(g, (Nkv, D), 0.02, "bf16"),
+                      w_v=n(g, (Nkv, D), 0.02, "bf16"), w_o=n(g, (D, Nq), 0.02, "bf16"),
+                      w_gate=n(g, (Dff, D), 0.02, "bf16"), w_up=n(g, (Dff, D), 0.02, "bf16"),
+                      w_down=n(g, (D, Dff), 0.02, "bf16"))
+        self.batches = {}
+        for name, M in (("prefill", T), ("decode", B)):
+            xa = n(g, (M, D), 1.0, "bf16")
+            a = n(g, (M, Nq), 1.0, "bf16")
+            ma = synth.mask_topk(synth.router_logits(g, xa, self.nga), synth.keep_count(self.nga, keep))
+            xf = n(g, (M, D), 1.0, "bf16")
+            mf = synth.mask_topk(synth.router_logits(g, xf, self.ng), synth.keep_count(self.ng, keep))
+            self.batches[name] = dict(x_attn=xa, a=a, mask_attn=ma, x_ffn=xf, mask_ffn=mf)
+
+    def active_flops(self, name, rows=None):
+        """FLOPs of the executed work: 2 per multiply-add of active groups only."""
+        b = self.batches[name]
+        ma, mf = b["mask_attn"], b["mask_ffn"]
+        if rows is not None:
+            ma, mf = ma[rows], mf[rows]
+        M = ma.shape[0]
+        q = 2.0 * self.D * self.Ga * ma.sum()
+        kv = 2.0 * 2 * M * self.D * self.Nkv
+        o = 2.0 * self.D * self.Ga * ma.sum()
+        gu = 2.0 * 2 * self.D * self.G * mf.sum()
+        down = 2.0 * self.D * self.G * mf.sum()
+        return dict(q=q, kv=kv, o=o, gate_up=gu, down=down, total=q + kv + o + gu + down)
+
+    def dense_flops(self, name):
+        M = self.batches[name]["mask_attn"].shape[0]
+        return 2.0 * M * self.D * (2 * self.Nq + 2 * self.Nkv + 3 * self.Dff)
+
+    def decode_bytes(self):
+        """Weight bytes the decode batch must read: dense K/V plus the union groups."""
+        b = self.batches["decode"]
+        ua = b["mask_attn"].any(0).sum()
+        uf = b["mask_ffn"].any(0).sum()
+        D = self.D
+        attn = 2 * (2 * self.Nkv * D) + 2 * (2 * ua * self.Ga * D)   # K,V dense; Q rows + O cols
+        ffn = 2 * (3 * uf * self.G * D)
+        dense = 2 * D * (2 * self.Nq + 2 * self.Nkv + 3 * self.Dff)
+        return int(attn + ffn), int(dense), int(ua), int(uf)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; the masked "
+                          "projections have no multi-GPU path in this build", "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    import paper_2607_28418_amd as W
+    from tests._helpers import to_dev
+
+    assert torch.cuda.is_available(), "needs a GPU"
+    W.lib()
+    dev = torch.device("cuda", 0)
+    t0 = time.time()
+    L = Layer(5, args.prefill_tokens, args.decode_batch, args.keep)
+    log(f"inputs generated in {time.time() - t0:.1f}s")
+    w = {k: to_dev(v) for k, v in L.w.items()}
+    bd = {n: {k: to_dev(v) for k, v in b.items()} for n, b in L.batches.items()}
+
+    # Preallocated outputs, reorders and workspaces (nothing is allocated per step).
+    bufs = {}
+    for n, b in bd.items():
+        M = b["x_attn"].shape[0]
+        e = lambda *s: torch.empty(s, dtype=torch.bfloat16, device=dev)
+        ws_bytes = max(W.wide_workspace_size(W.OP_QKV, W.BF16, M, L.D, L.Nq, L.Ga),
+                       W.wide_workspace_size(W.OP_O, W.BF16, M, L.D, L.Nq, L.Ga),
+                       W.wide_workspace_size(W.OP_FFN, W.BF16, M, L.D, L.Dff, L.G),
+                       W.wide_workspace_size(W.OP_REORDER, W.BF16, M, 0, L.ng, 1))
+        bufs[n] = dict(q=e(M, L.Nq), k=e(M, L.Nkv), v=e(M, L.Nkv), y_o=e(M, L.D), y_f=e(M, L.D),
+                       idx_a=torch.empty((L.nga, M), dtype=torch.int32, device=dev),
+                       cnt_a=torch.empty((L.nga,), dtype=torch.int32, device=dev),
+                       idx_f=torch.empty((L.ng, M), dtype=torch.int32, device=dev),
+                       cnt_f=torch.empty((L.ng,), dtype=torch.int32, device=dev),
+                       ws=torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev))
+
+    def run(name, masks=None):
+        b, o = bd[name], bufs[name]
+        ma = b["mask_attn"] if masks is None else masks[0]
+        mf = b["mask_ffn"] if masks is None else masks[1]
+        prefill = name == "prefill"
+        ia = ca = fi = fc = None
+        if prefill:   # one reorder per routing decision, reused by both operators
+            ia, ca = W.wide_mask_reorder(ma, o["idx_a"], o["cnt_a"], ws=o["ws"])
+            fi, fc = W.wide_mask_reorder(mf, o["idx_f"], o["cnt_f"], ws=o["ws"])
+        W.wide_qkvo_masked(W.PHASE_QKV, b["x_attn"], ma, L.Ga, L.nq, L.nkv, L.hd, w_q=w["w_q"],
+                           w_k=w["w_k"], w_v=w["w_v"], idx=ia, counts=ca, q=o["q"], k=o["k"],
+                           v=o["v"], ws=o["ws"])
+        W.wide_qkvo_masked(W.PHASE_O, b["a"], ma, L.Ga, L.nq, L.nkv, L.hd, w_o=w["w_o"], idx=ia,
+                           counts=ca, y=o["y_o"], ws=o["ws"])
+        W.wide_ffn_masked(b["x_ffn"], w["w_gate"], w["w_up"], w["w_down"], mf, L.G, idx=fi,
+                          counts=fc, y=o["y_f"], ws=o["ws"])
+
+    stream = torch.cuda.current_stream(dev)
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    for _ in range(args.warmup):
+        run("prefill")
+        run("decode")
+    torch.cuda.synchronize()
+
+    # ---- timed region ----------------------------------------------------------
+    W.wide_timing_enable(True)
+    W.wide_timing_reset()
+    marks = [(ev(), ev(), ev()) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    start, stop = ev(), ev()
+    start.record(stream)
+    for a, b_, c in marks:
+        a.record(stream)
+        run("prefill")
+        b_.record(stream)
+        run("decode")
+        c.record(stream)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    step_ms = start.elapsed_time(stop) / args.steps
+    pre_ms = float(np.median([a.elapsed_time(b_) for a, b_, _ in marks]))
+    dec_ms = float(np.median([b_.elapsed_time(c) for _, b_, c in marks]))
+    kernels = {}
+    for name in ("wide_reorder", "wide_gemm_mn<true>", "wide_gemm_mn<false>", "wide_gemm_k_dense_masked",
+                 "wide_gemm_k_scatter", "wide_tile_union", "wide_zero_f32", "wide_f32_to_bf16",
+                 "wide_gemv_n<true>", "wide_gemv_n<false>", "wide_gemv_k"):
+        ms, n = W.wide_timing_query(name)
+        if n:
+            kernels[name] = dict(avg_us=1e3 * ms / n, launches=n, per_step_us=1e3 * ms / args.steps)
+    W.wide_timing_enable(False)
+    log("kernels:", json.dumps(kernels))
+
+    fa_pre, fa_dec = L.active_flops("prefill"), L.active_flops("decode")
+    step_flops = fa_pre["total"] + fa_dec["total"]
+    value = step_flops / (step_ms * 1e-3) / 1e12
+
+    # ---- roofline of the dominant kernel ----------------------------------------
+    dom = max(kernels, key=lambda k: kernels[k]["per_step_us"])
+    per_launch_flops = {
+        "wide_gemm_mn<true>": fa_pre["gate_up"],
+        "wide_gemm_mn<false>": fa_pre["q"] + fa_pre["kv"],
+        "wide_gemm_k_dense_masked": None,   # shared by O and down: split below
+        "wide_gemm_k_scatter": None,
+    }
+    if dom in ("wide_gemm_k_dense_masked", "wide_gemm_k_scatter"):
+        alg = (fa_pre["o"] + fa_pre["down"]) / 2.0   # two launches per step (O, down)
+    else:
+        alg = per_launch_flops.get(dom)
+    roofline = None
+    if alg is not None:
+        ach = alg / (kernels[dom]["avg_us"] * 1e-6) / 1e12
+        roofline = dict(kernel=dom, bound="mfma", achieved=round(ach, 1), peak=PEAK_BF16_TFLOPS,
+                        unit="TFLOP/s", frac=round(ach / PEAK_BF16_TFLOPS, 4), traffic=None)
+
+    # ---- decode bandwidth ---------------------------------------------------------
+    dbytes, ddense, ua, uf = L.decode_bytes()
+    decode = dict(batch=args.decode_batch, ms=round(dec_ms, 4),
+                  GBps_on_min_bytes=round(dbytes / (dec_ms * 1e-3) / 1e9, 1),
+                  frac_hbm=round(dbytes / (dec_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+                  union_groups_attn=ua, union_groups_ffn=uf, min_weight_bytes=dbytes,
+                  dense_weight_bytes=ddense)
+    prefill = dict(tokens=args.prefill_tokens, ms=round(pre_ms, 4),
+                   active_TFLOPs=round(fa_pre["total"] / (pre_ms * 1e-3) / 1e12, 1),
+                   active_frac_peak=round(fa_pre["total"] / (pre_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                   ideal_speedup=round(L.dense_flops("prefill") / fa_pre["total"], 3))
+
+    # ---- dense baselines (outside the timed region) --------------------------------
+    dense = None
+    if not args.no_dense:
+        import torch.nn.functional as F
+
+        def dense_run(name):
+            b = bd[name]
+            F.linear(b["x_attn"], w["w_q"])
+            F.linear(b["x_attn"], w["w_k"])
+            F.linear(b["x_attn"], w["w_v"])
+            F.linear(b["a"], w["w_o"])
+            hg = F.linear(b["x_ffn"], w["w_gate"])
+            hu = F.linear(b["x_ffn"], w["w_up"])
+            F.linear(F.silu(hg) * hu, w["w_down"])
+
+        def timeit(fn, n):
+            for _ in range(3):
+                fn()
+            torch.cuda.synchronize()
+            s, e = ev(), ev()
+            s.record(stream)
+            for _ in range(n):
+                fn()
+            e.record(stream)
+            torch.cuda.synchronize()
+            return s.elapsed_time(e) / n
+
+        n_rep = max(5, args.steps // 2)
+        d_pre = timeit(lambda: dense_run("prefill"), n_rep)
+        d_dec = timeit(lambda: dense_run("decode"), n_rep)
+        ones = {n: (torch.ones_like(bd[n]["mask_attn"]), torch.ones_like(bd[n]["mask_ffn"])) for n in bd}
+        o_pre = timeit(lambda: run("prefill", ones["prefill"]), n_rep)
+        o_dec = timeit(lambda: run("decode", ones["decode"]), n_rep)
+        dense = dict(hipblaslt_prefill_ms=round(d_pre, 4), hipblaslt_decode_ms=round(d_dec, 4),
+                     ones_mask_prefill_ms=round(o_pre, 4), ones_mask_decode_ms=round(o_dec, 4))
+        best_pre, best_dec = min(d_pre, o_pre), min(d_dec, o_dec)
+        prefill["speedup_vs_dense"] = round(best_pre / pre_ms, 3)
+        prefill["frac_of_ideal"] = round(best_pre / pre_ms / prefill["ideal_speedup"], 3)
+        decode["speedup_vs_dense"] = round(best_dec / dec_ms, 3)
+        decode["ideal_speedup"] = round(ddense / dbytes, 3)
+
+    # ---- CPU oracle on a bounded sample --------------------------------------------
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        rows = np.arange(min(args.cpu_sample_tokens, args.prefill_tokens))
+        b = L.batches["prefill"]
+        t1 = time.time()
+        oracle.nproj(b["x_attn"][rows], L.w["w_q"], b["mask_attn"][rows], L.Ga, round_bf16=True)
+        oracle.linear(b["x_attn"][rows], L.w["w_k"], round_bf16=True)
+        oracle.linear(b["x_attn"][rows], L.w["w_v"], round_bf16=True)
+        oracle.kproj(b["a"][rows], L.w["w_o"], b["mask_attn"][rows], L.Ga, round_bf16=True)
+        oracle.ffn(b["x_ffn"][rows], L.w["w_gate"], L.w["w_up"], L.w["w_down"], b["mask_ffn"][rows],
+                   L.G, round_bf16=True, want_h=False)
+        dt = time.time() - t1
+        fl = L.active_flops("prefill", rows)["total"]
+        cpu = dict(value=round(fl / dt / 1e12, 6), unit="TFLOP/s", cores=oracle.num_threads(),
+                   kind="oracle", seconds=round(dt, 2),
+                   sample=f"the full layer's projections (Q, K, V, O, gate/up, down) for the first "
+                          f"{len(rows)} of the {args.prefill_tokens} prefill tokens, fp64, same inputs")
+
+    out = {
+        "metric": "speedup vs dense at 50% sparsity; prefill TFLOP/s, decode HBM GB/s",
+        "value": round(value, 2),
+        "unit": "TFLOP/s (active FLOPs, prefill + decode step)",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "layer_llama3_8b projections: prefill T=%d + decode B=%d, keep %.2f "
+                   "(top-k of random router logits), d_model 4096, 32q/8kv heads x 128 in 8 groups, "
+                   "d_ff 14336 in 112 groups of 128" % (args.prefill_tokens, args.decode_batch, args.keep),
+                   "prefill_tokens": args.prefill_tokens, "decode_batch": args.decode_batch,
+                   "sparsity": round(1 - args.keep, 3)},
+        "prefill": prefill,
+        "decode": decode,
+        "dense": dense,
+        "kernels_us": {k: round(v["avg_us"], 2) for k, v in kernels.items()},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

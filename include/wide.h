@@ -1,0 +1,201 @@
+/*
+ * libwide: token-level dynamic-width masked projections on MI355X (gfx950).
+ *
+ * Implements the inference hot path of WIDE ("Token-level Dynamic Width
+ * Pruning"): every token executes only the FFN channel groups and attention
+ * head groups that its binary routing mask selects.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All pointers except `ws_bytes`-sized host scalars are DEVICE pointers to
+ *    memory on the current HIP device.  All tensors are row-major and
+ *    contiguous; weights use the nn.Linear layout [out_features][in_features].
+ *  - Floating-point tensors are fp32 (WIDE_F32) or bf16 (WIDE_BF16, stored as
+ *    16-bit patterns).  On the bf16 path products accumulate in fp32 and every
+ *    stored tensor (the FFN intermediate H, Q/K/V, y) is rounded to bf16,
+ *    nearest-even.  On the fp32 path everything stays fp32.
+ *  - A routing mask is uint8 [M][n_groups], token-major; any nonzero byte
+ *    means "execute this group for this token" (class 0 of the router in
+ *    Section 3.1), zero means "skip".
+ *  - Pointers must be 16-byte aligned and row lengths (d_model, d_ff,
+ *    n_heads*head_dim) multiples of 8 elements, so every row starts on a
+ *    128-bit boundary; otherwise WIDE_ERR_INVALID_ARG.
+ *  - The caller owns every buffer, including the workspace `ws` (device
+ *    memory of at least wide_workspace_size() bytes, 256-byte aligned).  The
+ *    library allocates nothing per call, never synchronises the host with the
+ *    device, and only enqueues work on `stream` (0 = the null stream); calls
+ *    can be captured into a HIP graph.  Calls that share a workspace must be
+ *    ordered on one stream.
+ *  - Validation happens on the host before anything is enqueued.  On any
+ *    non-OK status no output has been touched and wide_last_error() describes
+ *    the problem.  No entry point throws or aborts.
+ *  - M == 0 is a valid no-op.
+ *  - Every output element is written: skipped (inactive) N-axis blocks are
+ *    +0, and a token whose mask row is all zero gets an all-zero output row.
+ *  - Only idx/counts are bit-reproducible run to run; some prefill K-axis
+ *    paths reduce with fp32 atomics whose order varies.
+ */
+#ifndef WIDE_H
+#define WIDE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  WIDE_OK = 0,
+  WIDE_ERR_INVALID_ARG = 1, /* bad pointer, shape, alignment or enum       */
+  WIDE_ERR_UNSUPPORTED = 2, /* valid per the paper but not implemented here */
+  WIDE_ERR_WORKSPACE = 3,   /* ws NULL or smaller than required             */
+  WIDE_ERR_HIP = 4          /* a HIP launch or runtime call failed          */
+} wide_status_t;
+
+typedef enum { WIDE_F32 = 0, WIDE_BF16 = 1 } wide_dtype_t;
+
+typedef enum { WIDE_PHASE_QKV = 0, WIDE_PHASE_O = 1 } wide_phase_t;
+
+typedef enum {
+  WIDE_OP_REORDER = 0,
+  WIDE_OP_FFN = 1,
+  WIDE_OP_QKV = 2,
+  WIDE_OP_O = 3
+} wide_op_t;
+
+/*
+ * Mask reordering (WIDE Section 3.3, the per-column SortDesc; Appendix B,
+ * Algorithm 1).  For every routing column g in [0, n_groups):
+ *   idx[g*M + 0 .. counts[g])  = tokens t with mask[t*n_groups+g] != 0,
+ *                                in ascending order,
+ *   idx[g*M + counts[g] .. M)  = the remaining tokens, ascending,
+ *   counts[g]                  = number of active tokens.
+ * This is the descending sort of a 0/1 column with ties kept in token order,
+ * so the result is unique and bit-exact.
+ *   mask    [M][n_groups] uint8, read only.
+ *   idx     [n_groups][M] int32, written.      counts [n_groups] int32, written.
+ *   ws      workspace of wide_workspace_size(WIDE_OP_REORDER, ., M, 0,
+ *           n_groups, 1) bytes (per-chunk counts).
+ * Limits: 0 <= M < 2^31, 1 <= n_groups <= 4096.
+ */
+wide_status_t wide_mask_reorder(const uint8_t* mask, int64_t M, int32_t n_groups,
+                                int32_t* idx, int32_t* counts, void* ws,
+                                size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Masked SwiGLU FFN (WIDE Section 3.1, equation (3), with phi = SiLU):
+ *   h[t, j] = silu(x_t . w_gate[j]) * (x_t . w_up[j])  if group j/G is active
+ *             for token t, else +0;
+ *   y[t]    = sum over active groups g of h[t, gG:(g+1)G] . w_down[:, gG:(g+1)G]^T.
+ * W_gate and W_up are pruned over their out-features (N-axis), W_down over its
+ * in-features (K-axis); one mask covers the whole FFN.
+ *   dt          WIDE_BF16 or WIDE_F32 (applies to x, weights, h_out, y).
+ *   M           tokens (B*T flattened).
+ *   d_model, d_ff, group_size (G): G must be a power of two >= 16 dividing
+ *               d_ff (Section 3.1: the tile-size set {2^k, k >= 4}).
+ *   mask        [M][d_ff/G] uint8.
+ *   idx, counts optional reorder of `mask` from wide_mask_reorder (reusable by
+ *               every operator under the same routing decision, Appendix B);
+ *               both NULL => computed internally into the workspace.  Passing
+ *               a reorder that does not match `mask` is undefined behaviour.
+ *   x           [M][d_model];  w_gate, w_up [d_ff][d_model];
+ *   w_down      [d_model][d_ff].
+ *   h_out       optional [M][d_ff] output of the intermediate (inactive
+ *               blocks +0); NULL => kept in the workspace.
+ *   y           [M][d_model] output.
+ *   ws          workspace, >= wide_workspace_size(WIDE_OP_FFN, dt, M, d_model,
+ *               d_ff, G) bytes.
+ */
+wide_status_t wide_ffn_masked(wide_dtype_t dt, int64_t M, int32_t d_model,
+                              int32_t d_ff, int32_t group_size,
+                              const uint8_t* mask, const int32_t* idx,
+                              const int32_t* counts, const void* x,
+                              const void* w_gate, const void* w_up,
+                              const void* w_down, void* h_out, void* y,
+                              void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Head-group masked attention projections (WIDE Section 3.1, equations
+ * (1)-(2) and Figure 1): W_q is pruned over its out-features and W_o over its
+ * in-features in groups of G = group_size features (whole heads, contiguous:
+ * group g holds q-heads [g*G/head_dim, (g+1)*G/head_dim)); W_k and W_v stay
+ * dense so the KV cache is never pruned.
+ *
+ * phase WIDE_PHASE_QKV:
+ *   q[t, gG:(g+1)G] = x_t . w_q[gG:(g+1)G]^T if group g is active, else +0;
+ *   k = x w_k^T and v = x w_v^T, dense.
+ *   in = x [M][d_model]; w_q [n_q*hd][d_model]; w_k, w_v [n_kv*hd][d_model];
+ *   q [M][n_q*hd]; k, v [M][n_kv*hd].  w_o and y are ignored (may be NULL).
+ * phase WIDE_PHASE_O:
+ *   y[t] = sum over active g of in[t, gG:(g+1)G] . w_o[:, gG:(g+1)G]^T
+ *   (the attention output gated by the mask before W_o, equation (2)).
+ *   in = attention output [M][n_q*hd]; w_o [d_model][n_q*hd]; y [M][d_model].
+ *   Inactive blocks of `in` are never read.  w_q/w_k/w_v/q/k/v are ignored.
+ * Shapes: n_q a multiple of n_kv; G a multiple of head_dim dividing n_q*hd
+ * (the paper's default is (n_q/n_kv)*head_dim, one KV head per group).
+ * mask [M][n_q*hd/G]; idx/counts as for wide_ffn_masked (same routing
+ * decision for both phases, Appendix B).
+ * ws >= wide_workspace_size(phase == QKV ? WIDE_OP_QKV : WIDE_OP_O, dt, M,
+ *       d_model, n_q*hd, G) bytes.
+ */
+wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M,
+                               int32_t d_model, int32_t n_q_heads,
+                               int32_t n_kv_heads, int32_t head_dim,
+                               int32_t group_size, const uint8_t* mask,
+                               const int32_t* idx, const int32_t* counts,
+                               const void* in, const void* w_q,
+                               const void* w_k, const void* w_v,
+                               const void* w_o, void* q, void* k, void* v,
+                               void* y, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
+
+/*
+ * Workspace bytes needed by one call (0 is a valid answer).
+ *   op = WIDE_OP_REORDER: d_inner = n_groups, group_size = 1, d_model unused.
+ *   op = WIDE_OP_FFN:     d_inner = d_ff.
+ *   op = WIDE_OP_QKV/O:   d_inner = n_q*head_dim.
+ * Returns SIZE_MAX for arguments the matching entry point would reject.
+ */
+size_t wide_workspace_size(wide_op_t op, wide_dtype_t dt, int64_t M,
+                           int32_t d_model, int32_t d_inner,
+                           int32_t group_size);
+
+/*
+ * Process-wide tuning knobs (not part of the paper's interface; every value
+ * gives the same result up to fp32 summation order).  Keys:
+ *   "decode_max_m"  bf16 calls with M <= value (and M <= 64) use the decode
+ *                   kernels, which skip the mask reorder; default 64.
+ *   "k_path"        schedule of the prefill K-axis product (down, O):
+ *                   0 automatic (default), 1 dense-masked (no atomics),
+ *                   2 scatter (the paper's GEMM-K with fp32 atomics).
+ * Not synchronised with calls running on other host threads.
+ */
+wide_status_t wide_set_option(const char* key, int64_t value);
+wide_status_t wide_get_option(const char* key, int64_t* value);
+
+/* Thread-local description of the last non-OK status ("" if none). */
+const char* wide_last_error(void);
+
+/*
+ * Kernel timing for measurement (not needed for correctness).  When enabled,
+ * every kernel launch is bracketed by two HIP events recorded on the launch
+ * stream; the events come from a pool created by wide_timing_enable(1) (the
+ * only call here that creates HIP objects) and recording stops silently when
+ * the pool is exhausted.  wide_timing_query() synchronises on the recorded
+ * events and returns, for kernels whose name contains `name_substr`, the total
+ * elapsed milliseconds and the number of launches.  Do not enable timing
+ * while capturing a graph.
+ */
+wide_status_t wide_timing_enable(int enable);
+wide_status_t wide_timing_reset(void);
+wide_status_t wide_timing_query(const char* name_substr, double* total_ms,
+                                int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WIDE_H */

@@ -1,0 +1,614 @@
+// C ABI of libwide: argument validation, workspace layout, dispatch.
+//
+// Every check runs on the host before anything is enqueued; on failure the
+// call returns a status and leaves all outputs untouched.  Nothing here
+// allocates device memory or synchronises with the device (timing queries
+// excepted, which are measurement-only).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "wide.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+wide_status_t fail(wide_status_t st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+wide_status_t ok() {
+  g_last_error.clear();
+  return WIDE_OK;
+}
+
+wide_status_t hip_fail(hipError_t e, const char* where) {
+  return fail(WIDE_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+// ---- tunables (wide_set_option) ---------------------------------------------
+int64_t g_decode_max_m = 64;  // M <= this uses the decode (GEMV) kernels
+int g_k_path = 0;             // 0 auto, 1 dense-masked, 2 scatter
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+// Bump allocator over the caller's workspace.
+struct Carve {
+  char* base;
+  size_t off = 0;
+  explicit Carve(void* b) : base(static_cast<char*>(b)) {}
+  template <class T>
+  T* take(size_t count) {
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += align_up(count * sizeof(T));
+    return p;
+  }
+};
+
+bool use_decode(wide_dtype_t dt, int64_t M) {
+  return dt == WIDE_BF16 && M <= g_decode_max_m && M <= wide::kDecodeMaxB;
+}
+
+int k_path_for(int G) {
+  if (g_k_path == 1 || g_k_path == 2) return g_k_path;
+  return G >= 256 ? 2 : 1;
+}
+
+// Workspace pieces of a prefill reorder held internally.
+struct ReorderWS {
+  int32_t* idx = nullptr;
+  int32_t* cnt = nullptr;
+  int32_t* chunk_cnt = nullptr;
+  int32_t* chunk_off = nullptr;
+};
+
+void carve_reorder(Carve& c, int64_t M, int ng, bool need_idx, ReorderWS& r) {
+  if (need_idx) {
+    r.idx = c.take<int32_t>((size_t)ng * (size_t)M);
+    r.cnt = c.take<int32_t>((size_t)ng);
+  }
+  const size_t sc = std::max<size_t>(wide::reorder_scratch_ints(M, ng), 1);
+  r.chunk_cnt = c.take<int32_t>(sc);
+  r.chunk_off = c.take<int32_t>(sc);
+}
+
+// K-axis scratch (fp32 accumulation or per-tile group union), worst case of
+// both schedules when `path` is 0.
+struct KWS {
+  float* acc32 = nullptr;
+  uint8_t* tu = nullptr;
+};
+
+void carve_kaxis(Carve& c, int64_t M, int N, int ng, int path, KWS& k) {
+  if (path == 0 || path == 2) k.acc32 = c.take<float>((size_t)M * (size_t)N);
+  if (path == 0 || path == 1) k.tu = c.take<uint8_t>(wide::tile_union_bytes(M, ng));
+}
+
+// ---- argument checks ----------------------------------------------------------
+wide_status_t check_ptr(const void* p, const char* name, bool need16 = true) {
+  if (!p) return fail(WIDE_ERR_INVALID_ARG, "%s is NULL", name);
+  if (need16 && !aligned16(p)) return fail(WIDE_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+  return WIDE_OK;
+}
+
+#define CHECK(expr)                          \
+  do {                                       \
+    wide_status_t st_ = (expr);              \
+    if (st_ != WIDE_OK) return st_;          \
+  } while (0)
+
+wide_status_t check_ws(void* ws, size_t ws_bytes, size_t need) {
+  if (need == 0) return WIDE_OK;
+  if (!ws) return fail(WIDE_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", need);
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign)
+    return fail(WIDE_ERR_INVALID_ARG, "workspace is not 256-byte aligned");
+  if (ws_bytes < need)
+    return fail(WIDE_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, need);
+  return WIDE_OK;
+}
+
+wide_status_t check_common(wide_dtype_t dt, int64_t M) {
+  if (dt != WIDE_F32 && dt != WIDE_BF16) return fail(WIDE_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
+  if (M < 0 || M >= (int64_t(1) << 31)) return fail(WIDE_ERR_INVALID_ARG, "M=%lld out of range", (long long)M);
+  return WIDE_OK;
+}
+
+// ---- FFN -------------------------------------------------------------------------
+wide_status_t ffn_shape(wide_dtype_t dt, int64_t M, int D, int Dff, int G) {
+  CHECK(check_common(dt, M));
+  if (D <= 0 || Dff <= 0) return fail(WIDE_ERR_INVALID_ARG, "d_model and d_ff must be positive");
+  if (!is_pow2(G) || G < 16)
+    return fail(WIDE_ERR_INVALID_ARG, "group_size=%d must be a power of two >= 16", G);
+  if (Dff % G) return fail(WIDE_ERR_INVALID_ARG, "group_size=%d does not divide d_ff=%d", G, Dff);
+  if (D % 8 || Dff % 8) return fail(WIDE_ERR_INVALID_ARG, "d_model and d_ff must be multiples of 8");
+  if (Dff / G > 4096) return fail(WIDE_ERR_UNSUPPORTED, "more than 4096 groups");
+  if (dt == WIDE_F32) {
+    if (D % 16 || Dff % 16) return fail(WIDE_ERR_UNSUPPORTED, "fp32 path needs d_model, d_ff multiples of 16");
+  } else {
+    if (D % 256) return fail(WIDE_ERR_UNSUPPORTED, "bf16 path needs d_model %% 256 == 0 (got %d)", D);
+    if (G < 64) return fail(WIDE_ERR_UNSUPPORTED, "bf16 path needs group_size >= 64 (got %d)", G);
+  }
+  return WIDE_OK;
+}
+
+size_t ffn_ws_bytes(wide_dtype_t dt, int64_t M, int D, int Dff, int G, bool need_idx, bool need_h,
+                    int kpath) {
+  Carve c(nullptr);
+  const int ng = Dff / G;
+  if (dt == WIDE_F32) {
+    if (need_h) c.take<float>((size_t)M * Dff);
+    return c.off;
+  }
+  if (need_h) c.take<uint16_t>((size_t)M * Dff);
+  if (!use_decode(dt, M)) {
+    ReorderWS r;
+    carve_reorder(c, M, ng, need_idx, r);
+    KWS k;
+    carve_kaxis(c, M, D, ng, kpath, k);
+  }
+  return c.off;
+}
+
+// ---- attention ----------------------------------------------------------------------
+struct AttnDims {
+  int D, nq, nkv, hd, G, Nq, Nkv, ng;
+};
+
+wide_status_t attn_shape(wide_dtype_t dt, int64_t M, int D, int nq, int nkv, int hd, int G,
+                         AttnDims& d) {
+  CHECK(check_common(dt, M));
+  if (D <= 0 || nq <= 0 || nkv <= 0 || hd <= 0 || G <= 0)
+    return fail(WIDE_ERR_INVALID_ARG, "dimensions must be positive");
+  if (nq % nkv) return fail(WIDE_ERR_INVALID_ARG, "n_q_heads=%d not a multiple of n_kv_heads=%d", nq, nkv);
+  if (G % hd) return fail(WIDE_ERR_INVALID_ARG, "group_size=%d not a multiple of head_dim=%d", G, hd);
+  const int Nq = nq * hd, Nkv = nkv * hd;
+  if (Nq % G) return fail(WIDE_ERR_INVALID_ARG, "group_size=%d does not divide n_q*head_dim=%d", G, Nq);
+  if (D % 8 || Nq % 8 || Nkv % 8) return fail(WIDE_ERR_INVALID_ARG, "row lengths must be multiples of 8");
+  if (Nq / G > 4096) return fail(WIDE_ERR_UNSUPPORTED, "more than 4096 groups");
+  if (dt == WIDE_F32) {
+    if (D % 16 || Nkv % 16 || G % 16)
+      return fail(WIDE_ERR_UNSUPPORTED, "fp32 path needs d_model, n_kv*head_dim, group_size multiples of 16");
+  } else {
+    if (D % 256) return fail(WIDE_ERR_UNSUPPORTED, "bf16 path needs d_model %% 256 == 0");
+    if (G % 128) return fail(WIDE_ERR_UNSUPPORTED, "bf16 path needs group_size %% 128 == 0");
+    if (Nkv % 128) return fail(WIDE_ERR_UNSUPPORTED, "bf16 path needs n_kv*head_dim %% 128 == 0");
+  }
+  d = AttnDims{D, nq, nkv, hd, G, Nq, Nkv, Nq / G};
+  return WIDE_OK;
+}
+
+size_t attn_ws_bytes(wide_phase_t ph, wide_dtype_t dt, int64_t M, const AttnDims& d, bool need_idx,
+                     int kpath) {
+  Carve c(nullptr);
+  if (dt == WIDE_F32 || use_decode(dt, M)) return 0;
+  if (ph == WIDE_PHASE_QKV) {
+    ReorderWS r;
+    if (need_idx) carve_reorder(c, M, d.ng, true, r);
+  } else {
+    ReorderWS r;
+    const int path = kpath;
+    if (need_idx && (path == 0 || path == 2)) carve_reorder(c, M, d.ng, true, r);
+    KWS k;
+    carve_kaxis(c, M, d.D, d.ng, path, k);
+  }
+  return c.off;
+}
+
+// K-axis product for down / O on the bf16 prefill path.
+wide_status_t run_kaxis(const uint16_t* a, const uint16_t* w, const uint8_t* mask,
+                        const int32_t* idx, const int32_t* cnt, uint16_t* y, int64_t M, int K,
+                        int N, int G, int path, const KWS& kws, hipStream_t s) {
+  wide::KArgs ka{};
+  ka.a = a;
+  ka.w = w;
+  ka.mask = mask;
+  ka.idx = idx;
+  ka.cnt = cnt;
+  ka.acc32 = kws.acc32;
+  ka.y = y;
+  ka.tile_union = kws.tu;
+  ka.M = M;
+  ka.K = K;
+  ka.N = N;
+  ka.G = G;
+  hipError_t e;
+  if (path == 2) {
+    if ((e = wide::launch_zero_f32(kws.acc32, M * (int64_t)N, s)) != hipSuccess) return hip_fail(e, "zero");
+    if ((e = wide::launch_gemm_k_scatter(ka, s)) != hipSuccess) return hip_fail(e, "gemm_k_scatter");
+    if ((e = wide::launch_f32_to_bf16(kws.acc32, y, M * (int64_t)N, s)) != hipSuccess)
+      return hip_fail(e, "f32_to_bf16");
+  } else {
+    if ((e = wide::launch_gemm_k_dense_masked(ka, s)) != hipSuccess)
+      return hip_fail(e, "gemm_k_dense_masked");
+  }
+  return WIDE_OK;
+}
+
+// ---- timing ----------------------------------------------------------------------------
+struct TimingRec {
+  int name;
+  hipEvent_t start, stop;
+};
+
+std::mutex g_tmu;
+bool g_timing = false;
+std::vector<TimingRec> g_pool;
+size_t g_used = 0;
+std::vector<std::string> g_names;
+
+int name_id(const char* n) {
+  for (size_t i = 0; i < g_names.size(); ++i)
+    if (g_names[i] == n) return (int)i;
+  g_names.emplace_back(n);
+  return (int)g_names.size() - 1;
+}
+
+}  // namespace
+
+namespace wide {
+
+int timing_begin(const char* name, hipStream_t s) {
+  if (!g_timing) return -1;
+  std::lock_guard<std::mutex> lk(g_tmu);
+  if (!g_timing || g_used >= g_pool.size()) return -1;
+  const int slot = (int)g_used++;
+  g_pool[slot].name = name_id(name);
+  (void)hipEventRecord(g_pool[slot].start, s);
+  return slot;
+}
+
+void timing_end(int slot, hipStream_t s) {
+  if (slot < 0) return;
+  (void)hipEventRecord(g_pool[slot].stop, s);
+}
+
+}  // namespace wide
+
+extern "C" {
+
+const char* wide_last_error(void) { return g_last_error.c_str(); }
+
+wide_status_t wide_set_option(const char* key, int64_t value) {
+  if (!key) return fail(WIDE_ERR_INVALID_ARG, "key is NULL");
+  if (!strcmp(key, "decode_max_m")) {
+    if (value < 0) return fail(WIDE_ERR_INVALID_ARG, "decode_max_m must be >= 0");
+    g_decode_max_m = value;
+    return ok();
+  }
+  if (!strcmp(key, "k_path")) {
+    if (value < 0 || value > 2) return fail(WIDE_ERR_INVALID_ARG, "k_path must be 0, 1 or 2");
+    g_k_path = (int)value;
+    return ok();
+  }
+  return fail(WIDE_ERR_INVALID_ARG, "unknown option '%s'", key);
+}
+
+wide_status_t wide_get_option(const char* key, int64_t* value) {
+  if (!key || !value) return fail(WIDE_ERR_INVALID_ARG, "NULL argument");
+  if (!strcmp(key, "decode_max_m")) *value = g_decode_max_m;
+  else if (!strcmp(key, "k_path")) *value = g_k_path;
+  else return fail(WIDE_ERR_INVALID_ARG, "unknown option '%s'", key);
+  return ok();
+}
+
+size_t wide_workspace_size(wide_op_t op, wide_dtype_t dt, int64_t M, int32_t d_model,
+                           int32_t d_inner, int32_t group_size) {
+  switch (op) {
+    case WIDE_OP_REORDER: {
+      if (M < 0 || M >= (int64_t(1) << 31) || d_inner < 1 || d_inner > 4096) return SIZE_MAX;
+      Carve c(nullptr);
+      ReorderWS r;
+      carve_reorder(c, M, d_inner, false, r);
+      return c.off;
+    }
+    case WIDE_OP_FFN:
+      if (ffn_shape(dt, M, d_model, d_inner, group_size) != WIDE_OK) return SIZE_MAX;
+      return ffn_ws_bytes(dt, M, d_model, d_inner, group_size, true, true, 0);
+    case WIDE_OP_QKV:
+    case WIDE_OP_O: {
+      // The size depends on M, d_model and the number of groups only.
+      if (check_common(dt, M) != WIDE_OK || d_model <= 0 || group_size <= 0 || d_inner <= 0 ||
+          d_inner % group_size || d_inner / group_size > 4096)
+        return SIZE_MAX;
+      AttnDims d{d_model, 0, 0, 0, group_size, d_inner, 0, d_inner / group_size};
+      return attn_ws_bytes(op == WIDE_OP_QKV ? WIDE_PHASE_QKV : WIDE_PHASE_O, dt, M, d, true, 0);
+    }
+  }
+  return SIZE_MAX;
+}
+
+wide_status_t wide_mask_reorder(const uint8_t* mask, int64_t M, int32_t n_groups, int32_t* idx,
+                                int32_t* counts, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (M < 0 || M >= (int64_t(1) << 31)) return fail(WIDE_ERR_INVALID_ARG, "M out of range");
+  if (n_groups < 1 || n_groups > 4096) return fail(WIDE_ERR_INVALID_ARG, "n_groups must be in [1, 4096]");
+  CHECK(check_ptr(counts, "counts", false));
+  if (M > 0) {
+    CHECK(check_ptr(mask, "mask", false));
+    CHECK(check_ptr(idx, "idx", false));
+  }
+  Carve c0(nullptr);
+  ReorderWS r0;
+  carve_reorder(c0, M, n_groups, false, r0);
+  CHECK(check_ws(ws, ws_bytes, M == 0 ? 0 : c0.off));
+  Carve c(ws);
+  ReorderWS r;
+  carve_reorder(c, M, n_groups, false, r);
+  hipError_t e = wide::launch_reorder(mask, M, n_groups, idx, counts, r.chunk_cnt, r.chunk_off, stream);
+  if (e != hipSuccess) return hip_fail(e, "reorder");
+  return ok();
+}
+
+wide_status_t wide_ffn_masked(wide_dtype_t dt, int64_t M, int32_t d_model, int32_t d_ff,
+                              int32_t group_size, const uint8_t* mask, const int32_t* idx,
+                              const int32_t* counts, const void* x, const void* w_gate,
+                              const void* w_up, const void* w_down, void* h_out, void* y,
+                              void* ws, size_t ws_bytes, hipStream_t stream) {
+  CHECK(ffn_shape(dt, M, d_model, d_ff, group_size));
+  if ((idx == nullptr) != (counts == nullptr))
+    return fail(WIDE_ERR_INVALID_ARG, "idx and counts must both be given or both be NULL");
+  CHECK(check_ptr(w_gate, "w_gate"));
+  CHECK(check_ptr(w_up, "w_up"));
+  CHECK(check_ptr(w_down, "w_down"));
+  if (h_out) CHECK(check_ptr(h_out, "h_out"));
+  if (M == 0) return ok();
+  CHECK(check_ptr(mask, "mask", false));
+  CHECK(check_ptr(x, "x"));
+  CHECK(check_ptr(y, "y"));
+  if (idx) {
+    CHECK(check_ptr(idx, "idx", false));
+    CHECK(check_ptr(counts, "counts", false));
+  }
+  const int D = d_model, Dff = d_ff, G = group_size, ng = Dff / G;
+  const bool decode = use_decode(dt, M);
+  const int kpath = k_path_for(G);
+  CHECK(check_ws(ws, ws_bytes, ffn_ws_bytes(dt, M, D, Dff, G, idx == nullptr, h_out == nullptr, kpath)));
+
+  Carve c(ws);
+  hipError_t e;
+  if (dt == WIDE_F32) {
+    float* h = h_out ? static_cast<float*>(h_out) : c.take<float>((size_t)M * Dff);
+    wide::F32NArgs na{static_cast<const float*>(x), static_cast<const float*>(w_gate),
+                      static_cast<const float*>(w_up), h, mask, M, D, Dff, Dff, G, ng};
+    if ((e = wide::launch_f32_nproj(na, true, stream)) != hipSuccess) return hip_fail(e, "f32 gate/up");
+    wide::F32KArgs ka{h, static_cast<const float*>(w_down), mask, static_cast<float*>(y), M, Dff, D, G, ng};
+    if ((e = wide::launch_f32_kproj(ka, stream)) != hipSuccess) return hip_fail(e, "f32 down");
+    return ok();
+  }
+
+  uint16_t* h = h_out ? static_cast<uint16_t*>(h_out) : c.take<uint16_t>((size_t)M * Dff);
+  if (decode) {
+    wide::GVNArgs na{};
+    na.x = static_cast<const uint16_t*>(x);
+    na.mask = mask;
+    na.B = (int)M;
+    na.K = D;
+    na.G = G;
+    na.n_groups = ng;
+    na.n_regions = 1;
+    na.reg[0] = wide::GVRegion{static_cast<const uint16_t*>(w_gate), static_cast<const uint16_t*>(w_up),
+                               h, Dff, Dff / 16, 1};
+    if ((e = wide::launch_gemv_n(na, true, stream)) != hipSuccess) return hip_fail(e, "gemv gate/up");
+    wide::GVKArgs ka{h, static_cast<const uint16_t*>(w_down), mask, static_cast<uint16_t*>(y),
+                     (int)M, Dff, D, G, ng};
+    if ((e = wide::launch_gemv_k(ka, stream)) != hipSuccess) return hip_fail(e, "gemv down");
+    return ok();
+  }
+
+  ReorderWS r;
+  carve_reorder(c, M, ng, idx == nullptr, r);
+  KWS kws;
+  carve_kaxis(c, M, D, ng, kpath, kws);
+  const int32_t* ix = idx;
+  const int32_t* ct = counts;
+  if (!idx) {
+    if ((e = wide::launch_reorder(mask, M, ng, r.idx, r.cnt, r.chunk_cnt, r.chunk_off, stream)) != hipSuccess)
+      return hip_fail(e, "reorder");
+    ix = r.idx;
+    ct = r.cnt;
+  }
+  wide::MNArgs ma{};
+  ma.x = static_cast<const uint16_t*>(x);
+  ma.M = M;
+  ma.K = D;
+  ma.idx = ix;
+  ma.cnt = ct;
+  ma.G = G;
+  ma.m_tiles = (int)((M + wide::kMNTileM - 1) / wide::kMNTileM);
+  ma.n_regions = 1;
+  ma.reg[0] = wide::MNRegion{static_cast<const uint16_t*>(w_gate), static_cast<const uint16_t*>(w_up), h,
+                             Dff, Dff / wide::kMNTileNSwiglu, 1};
+  if ((e = wide::launch_gemm_mn(ma, true, stream)) != hipSuccess) return hip_fail(e, "gemm_mn gate/up");
+  CHECK(run_kaxis(h, static_cast<const uint16_t*>(w_down), mask, ix, ct, static_cast<uint16_t*>(y), M, Dff,
+                  D, G, kpath, kws, stream));
+  return ok();
+}
+
+wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M, int32_t d_model,
+                               int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                               int32_t group_size, const uint8_t* mask, const int32_t* idx,
+                               const int32_t* counts, const void* in, const void* w_q,
+                               const void* w_k, const void* w_v, const void* w_o, void* q, void* k,
+                               void* v, void* y, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (phase != WIDE_PHASE_QKV && phase != WIDE_PHASE_O)
+    return fail(WIDE_ERR_INVALID_ARG, "unknown phase %d", (int)phase);
+  AttnDims d;
+  CHECK(attn_shape(dt, M, d_model, n_q_heads, n_kv_heads, head_dim, group_size, d));
+  if ((idx == nullptr) != (counts == nullptr))
+    return fail(WIDE_ERR_INVALID_ARG, "idx and counts must both be given or both be NULL");
+  if (phase == WIDE_PHASE_QKV) {
+    CHECK(check_ptr(w_q, "w_q"));
+    CHECK(check_ptr(w_k, "w_k"));
+    CHECK(check_ptr(w_v, "w_v"));
+  } else {
+    CHECK(check_ptr(w_o, "w_o"));
+  }
+  if (M == 0) return ok();
+  CHECK(check_ptr(mask, "mask", false));
+  CHECK(check_ptr(in, "in"));
+  if (phase == WIDE_PHASE_QKV) {
+    CHECK(check_ptr(q, "q"));
+    CHECK(check_ptr(k, "k"));
+    CHECK(check_ptr(v, "v"));
+  } else {
+    CHECK(check_ptr(y, "y"));
+  }
+  if (idx) {
+    CHECK(check_ptr(idx, "idx", false));
+    CHECK(check_ptr(counts, "counts", false));
+  }
+  const int kpath = k_path_for(d.G);
+  CHECK(check_ws(ws, ws_bytes, attn_ws_bytes(phase, dt, M, d, idx == nullptr, kpath)));
+  Carve c(ws);
+  hipError_t e;
+  const int ng = d.ng;
+
+  if (dt == WIDE_F32) {
+    const float* x = static_cast<const float*>(in);
+    if (phase == WIDE_PHASE_QKV) {
+      wide::F32NArgs qa{x, static_cast<const float*>(w_q), nullptr, static_cast<float*>(q), mask, M, d.D, d.Nq,
+                        d.Nq, d.G, ng};
+      if ((e = wide::launch_f32_nproj(qa, false, stream)) != hipSuccess) return hip_fail(e, "f32 q");
+      wide::F32NArgs ka{x, static_cast<const float*>(w_k), nullptr, static_cast<float*>(k), nullptr, M, d.D,
+                        d.Nkv, d.Nkv, d.Nkv, 1};
+      if ((e = wide::launch_f32_nproj(ka, false, stream)) != hipSuccess) return hip_fail(e, "f32 k");
+      ka.w0 = static_cast<const float*>(w_v);
+      ka.out = static_cast<float*>(v);
+      if ((e = wide::launch_f32_nproj(ka, false, stream)) != hipSuccess) return hip_fail(e, "f32 v");
+    } else {
+      wide::F32KArgs oa{x, static_cast<const float*>(w_o), mask, static_cast<float*>(y), M, d.Nq, d.D, d.G, ng};
+      if ((e = wide::launch_f32_kproj(oa, stream)) != hipSuccess) return hip_fail(e, "f32 o");
+    }
+    return ok();
+  }
+
+  const uint16_t* x = static_cast<const uint16_t*>(in);
+  if (use_decode(dt, M)) {
+    if (phase == WIDE_PHASE_QKV) {
+      wide::GVNArgs na{};
+      na.x = x;
+      na.mask = mask;
+      na.B = (int)M;
+      na.K = d.D;
+      na.G = d.G;
+      na.n_groups = ng;
+      na.n_regions = 3;
+      na.reg[0] = wide::GVRegion{static_cast<const uint16_t*>(w_q), nullptr, static_cast<uint16_t*>(q), d.Nq,
+                                 d.Nq / 16, 1};
+      na.reg[1] = wide::GVRegion{static_cast<const uint16_t*>(w_k), nullptr, static_cast<uint16_t*>(k), d.Nkv,
+                                 d.Nkv / 16, 0};
+      na.reg[2] = wide::GVRegion{static_cast<const uint16_t*>(w_v), nullptr, static_cast<uint16_t*>(v), d.Nkv,
+                                 d.Nkv / 16, 0};
+      if ((e = wide::launch_gemv_n(na, false, stream)) != hipSuccess) return hip_fail(e, "gemv qkv");
+    } else {
+      wide::GVKArgs ka{x, static_cast<const uint16_t*>(w_o), mask, static_cast<uint16_t*>(y), (int)M, d.Nq,
+                       d.D, d.G, ng};
+      if ((e = wide::launch_gemv_k(ka, stream)) != hipSuccess) return hip_fail(e, "gemv o");
+    }
+    return ok();
+  }
+
+  const bool need_reorder = idx == nullptr && (phase == WIDE_PHASE_QKV || kpath == 2);
+  ReorderWS r;
+  if (phase == WIDE_PHASE_QKV) {
+    if (idx == nullptr) carve_reorder(c, M, ng, true, r);
+  } else if (idx == nullptr && (kpath == 0 || kpath == 2)) {
+    carve_reorder(c, M, ng, true, r);
+  }
+  const int32_t* ix = idx;
+  const int32_t* ct = counts;
+  if (need_reorder) {
+    if ((e = wide::launch_reorder(mask, M, ng, r.idx, r.cnt, r.chunk_cnt, r.chunk_off, stream)) != hipSuccess)
+      return hip_fail(e, "reorder");
+    ix = r.idx;
+    ct = r.cnt;
+  }
+  if (phase == WIDE_PHASE_QKV) {
+    wide::MNArgs ma{};
+    ma.x = x;
+    ma.M = M;
+    ma.K = d.D;
+    ma.idx = ix;
+    ma.cnt = ct;
+    ma.G = d.G;
+    ma.m_tiles = (int)((M + wide::kMNTileM - 1) / wide::kMNTileM);
+    ma.n_regions = 3;
+    const int T = wide::kMNTileNPlain;
+    ma.reg[0] = wide::MNRegion{static_cast<const uint16_t*>(w_q), nullptr, static_cast<uint16_t*>(q), d.Nq,
+                               d.Nq / T, 1};
+    ma.reg[1] = wide::MNRegion{static_cast<const uint16_t*>(w_k), nullptr, static_cast<uint16_t*>(k), d.Nkv,
+                               d.Nkv / T, 0};
+    ma.reg[2] = wide::MNRegion{static_cast<const uint16_t*>(w_v), nullptr, static_cast<uint16_t*>(v), d.Nkv,
+                               d.Nkv / T, 0};
+    if ((e = wide::launch_gemm_mn(ma, false, stream)) != hipSuccess) return hip_fail(e, "gemm_mn qkv");
+    return ok();
+  }
+  KWS kws;
+  carve_kaxis(c, M, d.D, ng, kpath, kws);
+  CHECK(run_kaxis(x, static_cast<const uint16_t*>(w_o), mask, ix, ct, static_cast<uint16_t*>(y), M, d.Nq, d.D,
+                  d.G, kpath, kws, stream));
+  return ok();
+}
+
+wide_status_t wide_timing_enable(int enable) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  if (enable && g_pool.empty()) {
+    g_pool.resize(16384);
+    for (auto& r : g_pool) {
+      hipError_t e1 = hipEventCreate(&r.start);
+      hipError_t e2 = hipEventCreate(&r.stop);
+      if (e1 != hipSuccess || e2 != hipSuccess) {
+        g_pool.clear();
+        return hip_fail(e1 != hipSuccess ? e1 : e2, "hipEventCreate");
+      }
+    }
+  }
+  g_timing = enable != 0;
+  return ok();
+}
+
+wide_status_t wide_timing_reset(void) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  g_used = 0;
+  return ok();
+}
+
+wide_status_t wide_timing_query(const char* name_substr, double* total_ms, int64_t* launches) {
+  if (!name_substr || !total_ms || !launches) return fail(WIDE_ERR_INVALID_ARG, "NULL argument");
+  std::lock_guard<std::mutex> lk(g_tmu);
+  double tot = 0.0;
+  int64_t n = 0;
+  for (size_t i = 0; i < g_used; ++i) {
+    if (g_names[g_pool[i].name].find(name_substr) == std::string::npos) continue;
+    hipError_t e = hipEventSynchronize(g_pool[i].stop);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, g_pool[i].start, g_pool[i].stop);
+    if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+    tot += ms;
+    ++n;
+  }
+  *total_ms = tot;
+  *launches = n;
+  return ok();
+}
+
+}  // extern "C"

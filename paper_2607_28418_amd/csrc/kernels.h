@@ -1,0 +1,117 @@
+// Kernel argument blocks and host launchers of libwide (internal).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace wide {
+
+// ---- mask reorder ---------------------------------------------------------
+hipError_t launch_reorder(const uint8_t* mask, int64_t M, int n_groups,
+                          int32_t* idx, int32_t* counts, int32_t* chunk_cnt,
+                          int32_t* chunk_off, hipStream_t s);
+size_t reorder_scratch_ints(int64_t M, int n_groups);
+
+// ---- prefill N-axis GEMM ---------------------------------------------------
+// A region is a run of output tiles sharing one weight (or gate/up pair) and
+// one output tensor; Q, K and V of one projection call are three regions.
+struct MNRegion {
+  const uint16_t* w0;  // weight [N][K] (gate weight in SwiGLU mode)
+  const uint16_t* w1;  // up weight in SwiGLU mode, else unused
+  uint16_t* out;       // [M][ldo]
+  int ldo;             // output row stride in elements
+  int n_tiles;         // output tiles in this region
+  int masked;          // 1: rows follow idx/cnt of the tile's group; 0: dense
+};
+
+struct MNArgs {
+  const uint16_t* x;   // [M][K]
+  int64_t M;
+  int K;
+  const int32_t* idx;  // [n_groups][M]
+  const int32_t* cnt;  // [n_groups]
+  int G;               // group width in output columns
+  int m_tiles;
+  int n_regions;
+  MNRegion reg[3];
+};
+
+constexpr int kMNTileM = 128;
+constexpr int kMNTileNSwiglu = 64;
+constexpr int kMNTileNPlain = 128;
+constexpr int kMNTileK = 64;
+
+hipError_t launch_gemm_mn(const MNArgs& a, bool swiglu, hipStream_t s);
+
+// ---- prefill K-axis GEMM ---------------------------------------------------
+struct KArgs {
+  const uint16_t* a;   // [M][K] activations (H or attention output)
+  const uint16_t* w;   // [N][K]
+  const uint8_t* mask; // [M][K/G]
+  const int32_t* idx;  // [n_groups][M]   (scatter variant)
+  const int32_t* cnt;  // [n_groups]      (scatter variant)
+  float* acc32;        // [M][N] fp32 accumulation (scatter variant)
+  uint16_t* y;         // [M][N] bf16 output (dense-masked variant)
+  uint8_t* tile_union; // [ceil(M/128)][K/G] scratch (dense-masked variant)
+  int64_t M;
+  int K, N, G;
+};
+
+constexpr int kKTileM = 128;
+constexpr int kKTileN = 128;
+constexpr int kKTileK = 64;
+
+hipError_t launch_gemm_k_dense_masked(const KArgs& a, hipStream_t s);
+inline size_t tile_union_bytes(int64_t M, int n_groups) {
+  return (size_t)((M + kKTileM - 1) / kKTileM) * (size_t)n_groups;
+}
+hipError_t launch_gemm_k_scatter(const KArgs& a, hipStream_t s);
+hipError_t launch_zero_f32(float* p, int64_t n, hipStream_t s);
+hipError_t launch_f32_to_bf16(const float* src, uint16_t* dst, int64_t n, hipStream_t s);
+
+// ---- decode GEMV ------------------------------------------------------------
+struct GVRegion {
+  const uint16_t* w0;  // [N][K] (gate in SwiGLU mode)
+  const uint16_t* w1;  // up in SwiGLU mode
+  uint16_t* out;       // [B][ldo]
+  int ldo;
+  int n_blocks;        // 16-column blocks in this region
+  int masked;
+};
+
+struct GVNArgs {
+  const uint16_t* x;   // [B][K]
+  const uint8_t* mask; // [B][n_groups]
+  int B, K, G, n_groups;
+  int n_regions;
+  GVRegion reg[3];
+};
+
+struct GVKArgs {
+  const uint16_t* a;   // [B][K]
+  const uint16_t* w;   // [N][K]
+  const uint8_t* mask; // [B][K/G]
+  uint16_t* y;         // [B][N]
+  int B, K, N, G, n_groups;
+};
+
+constexpr int kDecodeMaxB = 64;
+
+hipError_t launch_gemv_n(const GVNArgs& a, bool swiglu, hipStream_t s);
+hipError_t launch_gemv_k(const GVKArgs& a, hipStream_t s);
+
+// ---- fp32 path ---------------------------------------------------------------
+struct F32NArgs {
+  const float* x; const float* w0; const float* w1; float* out;
+  const uint8_t* mask;  // nullptr => dense
+  int64_t M; int K, N, ldo, G, n_groups;
+};
+struct F32KArgs {
+  const float* a; const float* w; const uint8_t* mask; float* y;
+  int64_t M; int K, N, G, n_groups;
+};
+hipError_t launch_f32_nproj(const F32NArgs& a, bool swiglu, hipStream_t s);
+hipError_t launch_f32_kproj(const F32KArgs& a, hipStream_t s);
+
+}  // namespace wide

@@ -1,0 +1,108 @@
+"""CPU-only checks of the C ABI: every declared symbol is exported, and the
+host-side validation rejects bad arguments before touching the device (no
+compute call is made here; the fake pointers below are never dereferenced)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_28418_amd as W
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "wide.h")
+
+A = ctypes.c_void_p(0x10000)      # aligned, never dereferenced
+MIS = ctypes.c_void_p(0x10008)    # 8-byte aligned only
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(wide_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert {"wide_mask_reorder", "wide_ffn_masked", "wide_qkvo_masked",
+            "wide_workspace_size", "wide_last_error"} <= set(names)
+    lib = ctypes.CDLL(W.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def ffn(dt=W.BF16, M=128, D=4096, Dff=11008, G=128, mask=A, idx=None, cnt=None, x=A, wg=A, wu=A,
+        wd=A, h=None, y=A, ws=A, ws_bytes=1 << 40):
+    return W.lib().wide_ffn_masked(dt, M, D, Dff, G, mask, idx, cnt, x, wg, wu, wd, h, y, ws,
+                                   ws_bytes, None)
+
+
+def err():
+    return W.lib().wide_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(G=48), W.ERR_INVALID_ARG, "power of two"),
+    (dict(G=8), W.ERR_INVALID_ARG, "power of two"),
+    (dict(Dff=11000), W.ERR_INVALID_ARG, "does not divide"),
+    (dict(G=32, Dff=1024), W.ERR_UNSUPPORTED, "group_size >= 64"),
+    (dict(D=4000), W.ERR_UNSUPPORTED, "256"),
+    (dict(M=-1), W.ERR_INVALID_ARG, "out of range"),
+    (dict(dt=7), W.ERR_INVALID_ARG, "dtype"),
+    (dict(x=None), W.ERR_INVALID_ARG, "x is NULL"),
+    (dict(wd=MIS), W.ERR_INVALID_ARG, "aligned"),
+    (dict(idx=A), W.ERR_INVALID_ARG, "both"),
+    (dict(ws=None), W.ERR_WORKSPACE, "NULL"),
+    (dict(ws_bytes=1000), W.ERR_WORKSPACE, "needed"),
+    (dict(ws=ctypes.c_void_p(0x10010)), W.ERR_INVALID_ARG, "256-byte"),
+])
+def test_ffn_validation(kw, status, msg):
+    assert ffn(**kw) == status
+    assert msg in err()
+
+
+def test_m_zero_is_ok_without_touching_anything():
+    assert ffn(M=0, x=None, y=None, mask=None, ws=None) == W.OK
+
+
+def test_qkvo_validation():
+    L = W.lib()
+    def call(phase=W.PHASE_QKV, dt=W.BF16, M=16, D=4096, nq=32, nkv=8, hd=128, G=512, **p):
+        args = dict(mask=A, idx=None, cnt=None, inp=A, wq=A, wk=A, wv=A, wo=A, q=A, k=A, v=A, y=A,
+                    ws=A, wsb=1 << 40)
+        args.update(p)
+        return L.wide_qkvo_masked(phase, dt, M, D, nq, nkv, hd, G, args["mask"], args["idx"],
+                                  args["cnt"], args["inp"], args["wq"], args["wk"], args["wv"],
+                                  args["wo"], args["q"], args["k"], args["v"], args["y"],
+                                  args["ws"], args["wsb"], None)
+    assert call(nq=30, nkv=8) == W.ERR_INVALID_ARG and "multiple of n_kv" in err()
+    assert call(G=500) == W.ERR_INVALID_ARG and "head_dim" in err()
+    assert call(G=384) == W.ERR_INVALID_ARG and "divide" in err()
+    assert call(phase=5) == W.ERR_INVALID_ARG
+    assert call(wq=None) == W.ERR_INVALID_ARG and "w_q" in err()
+    assert call(phase=W.PHASE_O, wo=None) == W.ERR_INVALID_ARG and "w_o" in err()
+    assert call(hd=64, G=64, dt=W.BF16) == W.ERR_UNSUPPORTED
+    assert call(M=0, inp=None, mask=None, q=None, k=None, v=None) == W.OK
+
+
+def test_workspace_sizes():
+    s = W.wide_workspace_size
+    assert s(W.OP_FFN, W.BF16, 4096, 4096, 11008, 48) == W.SIZE_MAX
+    pre = s(W.OP_FFN, W.BF16, 4096, 4096, 11008, 128)
+    # H (bf16) + fp32 K-axis buffer + reorder index at least
+    assert pre >= 4096 * 11008 * 2 + 4096 * 4096 * 4 + 86 * 4096 * 4
+    dec = s(W.OP_FFN, W.BF16, 16, 4096, 11008, 128)
+    assert 16 * 11008 * 2 <= dec < pre
+    assert s(W.OP_REORDER, W.BF16, 8192, 0, 112, 1) >= 2 * 32 * 112 * 4
+    assert s(W.OP_QKV, W.BF16, 16, 4096, 4096, 512) == 0
+    assert s(W.OP_O, W.BF16, 8192, 4096, 4096, 512) >= 8192 * 4096 * 4
+    assert s(W.OP_FFN, W.F32, 128, 512, 1536, 64) >= 128 * 1536 * 4
+
+
+def test_options():
+    W.wide_set_option("decode_max_m", 8)
+    assert W.wide_get_option("decode_max_m") == 8
+    W.wide_set_option("decode_max_m", 64)
+    with pytest.raises(W.WideError):
+        W.wide_set_option("k_path", 9)
+    with pytest.raises(W.WideError):
+        W.wide_set_option("nope", 1)

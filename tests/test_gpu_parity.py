@@ -1,0 +1,308 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Every case prints its name before it runs so that a failing GPU run names it.
+Sizes: small cases span several tiles with ragged tails and are checked
+element by element; full-size cases run the whole problem on the GPU and
+check sampled token rows against the oracle (rows are independent).
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_28418_amd as W
+from paper_2607_28418_amd import synth
+from tests._helpers import assert_close, dev, to_dev, to_np64
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print("[case]", *a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(autouse=True)
+def _options():
+    W.lib()
+    yield
+    W.wide_set_option("decode_max_m", 64)
+    W.wide_set_option("k_path", 0)
+
+
+def ffn_dev(c):
+    return [to_dev(a) for a in (c.x, c.w_gate, c.w_up, c.w_down)] + [to_dev(c.mask)]
+
+
+# ------------------------------------------------------------------ reorder
+
+@pytest.mark.parametrize("M,ng,kind", [
+    (1, 1, "bernoulli"), (7, 3, "bernoulli"), (255, 24, "bernoulli"), (256, 86, "beta"),
+    (257, 86, "bernoulli"), (300, 4096, "bernoulli"), (2048, 8, "bernoulli"),
+    (4096, 86, "topk"), (8192, 112, "topk"), (1000, 5, "zeros"), (1000, 5, "ones")])
+def test_reorder_bit_exact(orc, M, ng, kind):
+    say("reorder", M, ng, kind)
+    g = synth.rng(M + ng)
+    if kind == "topk":
+        x = g.standard_normal((M, 64), dtype=np.float32)
+        mask = synth.mask_topk(synth.router_logits(g, x, ng), synth.keep_count(ng, 0.5))
+    else:
+        mask = synth.make_mask(g, kind, M, ng, 0.5)
+    mask = mask * g.integers(1, 256, mask.shape).astype(np.uint8)   # any nonzero byte is active
+    idx, cnt = W.wide_mask_reorder(to_dev(mask))
+    torch.cuda.synchronize()
+    ridx, rcnt = orc.mask_reorder(mask)
+    assert np.array_equal(cnt.cpu().numpy(), rcnt)
+    assert np.array_equal(idx.cpu().numpy(), ridx)
+
+
+def test_reorder_empty():
+    say("reorder M=0")
+    idx, cnt = W.wide_mask_reorder(torch.zeros((0, 9), dtype=torch.uint8, device=dev()))
+    torch.cuda.synchronize()
+    assert idx.shape == (9, 0) and not cnt.cpu().numpy().any()
+
+
+# ------------------------------------------------------------------ FFN bf16
+
+@pytest.mark.parametrize("M,D,Dff,G,kind,kpath", [
+    (300, 256, 512, 64, "bernoulli", 1), (300, 256, 512, 64, "bernoulli", 2),
+    (129, 512, 1024, 128, "beta", 1), (129, 512, 1024, 128, "beta", 2),
+    (1000, 256, 1024, 256, "topk", 0), (65, 256, 256, 128, "bernoulli", 1)])
+def test_ffn_bf16_prefill_small(orc, M, D, Dff, G, kind, kpath):
+    say("ffn prefill", M, D, Dff, G, kind, kpath)
+    W.wide_set_option("decode_max_m", 0)
+    W.wide_set_option("k_path", kpath)
+    c = synth.ffn_case(M * 7 + G, M, D, Dff, G, mask=kind)
+    x, wg, wu, wd, m = ffn_dev(c)
+    h = torch.empty((M, Dff), dtype=torch.bfloat16, device=dev())
+    y = W.wide_ffn_masked(x, wg, wu, wd, m, G, h_out=h)
+    torch.cuda.synchronize()
+    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, G, round_bf16=True)
+    assert_close(h, rh, what="h")
+    assert_close(y, ry, what="y")
+
+
+@pytest.mark.parametrize("B", [1, 4, 16, 64])
+def test_ffn_bf16_decode_small(orc, B):
+    say("ffn decode small", B)
+    c = synth.ffn_case(B, B, 512, 1024, 128, mask="beta")
+    x, wg, wu, wd, m = ffn_dev(c)
+    h = torch.empty((B, 1024), dtype=torch.bfloat16, device=dev())
+    y = W.wide_ffn_masked(x, wg, wu, wd, m, 128, h_out=h)
+    torch.cuda.synchronize()
+    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, 128, round_bf16=True)
+    assert_close(h, rh, what="h")
+    assert_close(y, ry, what="y")
+
+
+def test_ffn_decode_equals_prefill_rows(orc):
+    """Rows are independent: a decode call on rows [0,16) and a prefill call on
+    all 200 rows agree with the oracle and with each other on those rows."""
+    say("ffn decode vs prefill rows")
+    c = synth.ffn_case(11, 200, 512, 1024, 128, mask="bernoulli")
+    x, wg, wu, wd, m = ffn_dev(c)
+    y_pre = W.wide_ffn_masked(x, wg, wu, wd, m, 128)
+    y_dec = W.wide_ffn_masked(x[:16].contiguous(), wg, wu, wd, m[:16].contiguous(), 128)
+    torch.cuda.synchronize()
+    _, ry = orc.ffn(c.x[:16], c.w_gate, c.w_up, c.w_down, c.mask[:16], 128, round_bf16=True)
+    assert_close(y_pre[:16], ry, what="prefill rows")
+    assert_close(y_dec, ry, what="decode rows")
+
+
+@pytest.mark.parametrize("kind", ["zeros", "ones"])
+@pytest.mark.parametrize("M", [5, 300])
+def test_ffn_degenerate_masks(orc, kind, M):
+    say("ffn degenerate", kind, M)
+    c = synth.ffn_case(3, M, 256, 512, 64 if M > 64 else 128, mask=kind)
+    G = c.G
+    x, wg, wu, wd, m = ffn_dev(c)
+    h = torch.full((M, 512), float("nan"), dtype=torch.bfloat16, device=dev())
+    y = torch.full((M, 256), float("nan"), dtype=torch.bfloat16, device=dev())
+    W.wide_ffn_masked(x, wg, wu, wd, m, G, h_out=h, y=y)
+    torch.cuda.synchronize()
+    if kind == "zeros":
+        assert not to_np64(y).any() and not to_np64(h).any()
+        assert not torch.signbit(y.float()).any()
+    else:
+        rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, G, round_bf16=True)
+        assert_close(h, rh, what="h")
+        assert_close(y, ry, what="y")
+
+
+def test_ffn_m_zero_is_noop():
+    say("ffn M=0")
+    e = torch.empty((0, 256), dtype=torch.bfloat16, device=dev())
+    w = torch.zeros((512, 256), dtype=torch.bfloat16, device=dev())
+    wd = torch.zeros((256, 512), dtype=torch.bfloat16, device=dev())
+    y = W.wide_ffn_masked(e, w, w, wd, torch.empty((0, 4), dtype=torch.uint8, device=dev()), 128)
+    assert y.shape == (0, 256)
+
+
+@pytest.mark.parametrize("M,kpath", [(40, 0), (300, 1), (300, 2)])
+def test_ffn_poisoned_unused_groups(orc, M, kpath):
+    """Weights of groups no token uses are never read: NaN there changes nothing."""
+    say("ffn poison", M, kpath)
+    W.wide_set_option("k_path", kpath)
+    c = synth.ffn_case(21, M, 256, 1024, 128, mask="bernoulli")
+    c.mask[:, [1, 5]] = 0
+    x, wg, wu, wd, m = ffn_dev(c)
+    y0 = W.wide_ffn_masked(x, wg, wu, wd, m, 128).clone()
+    nan = float("nan")
+    for gi in (1, 5):
+        wg[gi * 128:(gi + 1) * 128] = nan
+        wu[gi * 128:(gi + 1) * 128] = nan
+        wd[:, gi * 128:(gi + 1) * 128] = nan
+    y1 = W.wide_ffn_masked(x, wg, wu, wd, m, 128)
+    torch.cuda.synchronize()
+    assert torch.isfinite(y1.float()).all()
+    _, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, 128, round_bf16=True)
+    assert_close(y0, ry, what="clean")
+    assert_close(y1, ry, what="poisoned")
+
+
+def test_ffn_reuses_given_reorder(orc):
+    say("ffn given idx")
+    c = synth.ffn_case(5, 400, 256, 512, 128, mask="bernoulli")
+    x, wg, wu, wd, m = ffn_dev(c)
+    idx, cnt = W.wide_mask_reorder(m)
+    W.wide_set_option("k_path", 1)
+    y_a = W.wide_ffn_masked(x, wg, wu, wd, m, 128, idx=idx, counts=cnt)
+    y_b = W.wide_ffn_masked(x, wg, wu, wd, m, 128)
+    torch.cuda.synchronize()
+    assert torch.equal(y_a, y_b)   # dense-masked K path: no atomics, deterministic
+
+
+@pytest.mark.parametrize("keep", [0.5, 0.25])
+def test_ffn_bf16_prefill_full_llama7b_sampled(orc, keep):
+    say("ffn prefill llama7b T=4096 keep", keep)
+    c = synth.ffn_case(3, 4096, 4096, 11008, 128, mask="topk", keep=keep)
+    x, wg, wu, wd, m = ffn_dev(c)
+    y = W.wide_ffn_masked(x, wg, wu, wd, m, 128)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, 4095], synth.rng(0).integers(0, 4096, 14)]))
+    _, ry = orc.ffn(c.x[rows], c.w_gate, c.w_up, c.w_down, c.mask[rows], 128, round_bf16=True)
+    assert_close(y[torch.from_numpy(rows).to(dev())], ry, what="sampled rows")
+
+
+@pytest.mark.parametrize("B", [1, 4, 16, 64])
+def test_ffn_bf16_decode_full_llama7b(orc, B):
+    say("ffn decode llama7b B", B)
+    c = synth.ffn_case(2, B, 4096, 11008, 128, mask="beta")
+    x, wg, wu, wd, m = ffn_dev(c)
+    y = W.wide_ffn_masked(x, wg, wu, wd, m, 128)
+    torch.cuda.synchronize()
+    rows = np.arange(B) if B <= 16 else np.unique(synth.rng(1).integers(0, B, 16))
+    _, ry = orc.ffn(c.x[rows], c.w_gate, c.w_up, c.w_down, c.mask[rows], 128, round_bf16=True)
+    assert_close(y[torch.from_numpy(rows).to(dev())], ry, what="decode rows")
+
+
+# ------------------------------------------------------------------ FFN fp32
+
+def test_ffn_fp32_small_full(orc):
+    say("ffn fp32 D=512 Dff=1536 G=64 T=128")
+    c = synth.ffn_case(1, 128, 512, 1536, 64, dtype="f32", mask="bernoulli")
+    x, wg, wu, wd, m = ffn_dev(c)
+    h = torch.empty((128, 1536), dtype=torch.float32, device=dev())
+    y = W.wide_ffn_masked(x, wg, wu, wd, m, 64, h_out=h)
+    torch.cuda.synchronize()
+    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, 64)
+    assert_close(h, rh, kind="f32", what="h")
+    assert_close(y, ry, kind="f32", what="y")
+
+
+# ------------------------------------------------------------------ attention
+
+def attn_dev(c):
+    return {k: to_dev(getattr(c, k)) for k in ("x", "w_q", "w_k", "w_v", "w_o", "a", "mask")}
+
+
+def check_qkvo(orc, c, kind="bf16", kpath=0):
+    d = attn_dev(c)
+    W.wide_set_option("k_path", kpath)
+    q, k, v = W.wide_qkvo_masked(W.PHASE_QKV, d["x"], d["mask"], c.G, c.n_q, c.n_kv, c.hd,
+                                 w_q=d["w_q"], w_k=d["w_k"], w_v=d["w_v"])
+    y = W.wide_qkvo_masked(W.PHASE_O, d["a"], d["mask"], c.G, c.n_q, c.n_kv, c.hd, w_o=d["w_o"])
+    torch.cuda.synchronize()
+    rnd = kind == "bf16"
+    assert_close(q, orc.nproj(c.x, c.w_q, c.mask, c.G, round_bf16=rnd), kind, "q")
+    assert_close(k, orc.linear(c.x, c.w_k, round_bf16=rnd), kind, "k")
+    assert_close(v, orc.linear(c.x, c.w_v, round_bf16=rnd), kind, "v")
+    assert_close(y, orc.kproj(c.a, c.w_o, c.mask, c.G, round_bf16=rnd), kind, "o")
+
+
+@pytest.mark.parametrize("M,n_q,n_kv,G,kpath", [
+    (300, 8, 2, 512, 1), (300, 8, 2, 512, 2), (130, 8, 4, 256, 0), (40, 8, 2, 512, 0),
+    (1, 8, 8, 128, 0), (64, 16, 4, 512, 0)])
+def test_qkvo_bf16_small(orc, M, n_q, n_kv, G, kpath):
+    say("qkvo bf16", M, n_q, n_kv, G, kpath)
+    c = synth.attn_case(M + G, M, 256, n_q, n_kv, 128, G, mask="topk")
+    check_qkvo(orc, c, kpath=kpath)
+
+
+def test_qkvo_fp32_small(orc):
+    say("qkvo fp32")
+    c = synth.attn_case(4, 70, 128, 8, 2, 32, 64, dtype="f32", mask="bernoulli")
+    check_qkvo(orc, c, kind="f32")
+
+
+def test_o_poisoned_inactive_blocks(orc):
+    """Inactive blocks of the attention output are never read."""
+    for M, kpath in ((300, 1), (300, 2), (20, 0)):
+        say("o poison", M, kpath)
+        W.wide_set_option("k_path", kpath)
+        c = synth.attn_case(9, M, 256, 8, 2, 128, 256, mask="bernoulli")
+        d = attn_dev(c)
+        a = d["a"].clone()
+        inactive = torch.from_numpy(np.repeat(c.mask == 0, c.G, axis=1)).to(dev())
+        a[inactive] = float("nan")
+        y = W.wide_qkvo_masked(W.PHASE_O, a, d["mask"], c.G, 8, 2, 128, w_o=d["w_o"])
+        torch.cuda.synchronize()
+        assert_close(y, orc.kproj(c.a, c.w_o, c.mask, c.G, round_bf16=True), what="o poisoned")
+
+
+@pytest.mark.parametrize("name", ["attn_proj_mha", "layer_llama3_8b"])
+def test_qkvo_bf16_full_sampled(orc, name):
+    p = synth.WORKLOADS[name].params
+    say("qkvo full", name)
+    M = 2048
+    c = synth.attn_case(4, M, p["D"], p["n_q"], p["n_kv"], p["hd"], p.get("G_attn", p.get("G")),
+                        mask="topk")
+    d = attn_dev(c)
+    q, k, v = W.wide_qkvo_masked(W.PHASE_QKV, d["x"], d["mask"], c.G, c.n_q, c.n_kv, c.hd,
+                                 w_q=d["w_q"], w_k=d["w_k"], w_v=d["w_v"])
+    y = W.wide_qkvo_masked(W.PHASE_O, d["a"], d["mask"], c.G, c.n_q, c.n_kv, c.hd, w_o=d["w_o"])
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, M - 1], synth.rng(2).integers(0, M, 10)]))
+    r = torch.from_numpy(rows).to(dev())
+    assert_close(q[r], orc.nproj(c.x[rows], c.w_q, c.mask[rows], c.G, round_bf16=True), what="q")
+    assert_close(k[r], orc.linear(c.x[rows], c.w_k, round_bf16=True), what="k")
+    assert_close(y[r], orc.kproj(c.a[rows], c.w_o, c.mask[rows], c.G, round_bf16=True), what="o")
+
+
+# ------------------------------------------------------------------ errors, timing
+
+def test_errors_leave_outputs_untouched():
+    say("errors")
+    x = torch.zeros((8, 256), dtype=torch.bfloat16, device=dev())
+    w = torch.zeros((480, 256), dtype=torch.bfloat16, device=dev())
+    wd = torch.zeros((256, 480), dtype=torch.bfloat16, device=dev())
+    y = torch.full((8, 256), 3.0, dtype=torch.bfloat16, device=dev())
+    with pytest.raises(W.WideError) as ei:
+        W.wide_ffn_masked(x, w, w, wd, torch.ones((8, 10), dtype=torch.uint8, device=dev()), 48, y=y,
+                          ws=torch.empty(1 << 20, dtype=torch.uint8, device=dev()))
+    assert ei.value.status == 1 and "power of two" in str(ei.value)
+    torch.cuda.synchronize()
+    assert (y.float() == 3.0).all()
+
+
+def test_timing_records_kernels():
+    say("timing")
+    c = synth.ffn_case(1, 256, 256, 512, 128, mask="bernoulli")
+    x, wg, wu, wd, m = ffn_dev(c)
+    W.wide_timing_enable(True)
+    W.wide_timing_reset()
+    W.wide_ffn_masked(x, wg, wu, wd, m, 128)
+    ms, n = W.wide_timing_query("wide_gemm_mn")
+    W.wide_timing_enable(False)
+    assert n == 1 and ms > 0
