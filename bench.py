@@ -45,7 +45,7 @@ def parse():
     ap.add_argument("--decode-batch", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
-    ap.add_argument("--cpu-sample-tokens", type=int, default=48)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=1024)
     return ap.parse_args()
 
 
