@@ -39,13 +39,15 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--keep", type=float, default=0.5, help="fraction of groups kept per token")
     ap.add_argument("--prefill-tokens", type=int, default=8192)
     ap.add_argument("--decode-batch", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=1024)
+    ap.add_argument("--ring-bk", type=int, default=0, help="k depth of a 256x256 stage (0: library default)")
+    ap.add_argument("--k-path", type=int, default=0, help="K-axis schedule (0: library default)")
     return ap.parse_args()
 
 
@@ -121,6 +123,10 @@ def main():
 
     assert torch.cuda.is_available(), "needs a GPU"
     W.lib()
+    if args.ring_bk:
+        W.wide_set_option("ring_bk", args.ring_bk)
+    if args.k_path:
+        W.wide_set_option("k_path", args.k_path)
     dev = torch.device("cuda", 0)
     t0 = time.time()
     L = Layer(5, args.prefill_tokens, args.decode_batch, args.keep)
@@ -188,9 +194,10 @@ def main():
     pre_ms = float(np.median([a.elapsed_time(b_) for a, b_, _ in marks]))
     dec_ms = float(np.median([b_.elapsed_time(c) for _, b_, c in marks]))
     kernels = {}
-    for name in ("wide_reorder", "wide_gemm_mn<true>", "wide_gemm_mn<false>", "wide_gemm_k_dense_masked",
-                 "wide_gemm_k_scatter", "wide_tile_union", "wide_zero_f32", "wide_f32_to_bf16",
-                 "wide_gemv_n<true>", "wide_gemv_n<false>", "wide_gemv_k"):
+    for name in ("wide_reorder_count", "wide_reorder_scan", "wide_reorder_scatter", "wide_mn256<true>",
+                 "wide_mn256<false>", "wide_kd256", "wide_ks256", "wide_gemm_mn<true>", "wide_gemm_mn<false>",
+                 "wide_gemm_k_dense_masked", "wide_gemm_k_scatter", "wide_tile_union", "wide_zero_f32",
+                 "wide_f32_to_bf16", "wide_gemv_n<true>", "wide_gemv_n<false>", "wide_gemv_k"):
         ms, n = W.wide_timing_query(name)
         if n:
             kernels[name] = dict(avg_us=1e3 * ms / n, launches=n, per_step_us=1e3 * ms / args.steps)
@@ -198,19 +205,27 @@ def main():
     log("kernels:", json.dumps(kernels))
 
     fa_pre, fa_dec = L.active_flops("prefill"), L.active_flops("decode")
+    kpath_auto = lambda G: 2 if G >= 256 else 1
+    kp = W.wide_get_option("k_path")
+    big = W.wide_get_option("big_tiles")
+    kname = lambda G: ({1: "wide_kd256", 2: "wide_ks256"} if big else
+                       {1: "wide_gemm_k_dense_masked", 2: "wide_gemm_k_scatter"})[kp or kpath_auto(G)]
+    kernel_of = {"o": kname(L.Ga), "down": kname(L.G)}
     step_flops = fa_pre["total"] + fa_dec["total"]
     value = step_flops / (step_ms * 1e-3) / 1e12
 
     # ---- roofline of the dominant kernel ----------------------------------------
     dom = max(kernels, key=lambda k: kernels[k]["per_step_us"])
     per_launch_flops = {
-        "wide_gemm_mn<true>": fa_pre["gate_up"],
-        "wide_gemm_mn<false>": fa_pre["q"] + fa_pre["kv"],
-        "wide_gemm_k_dense_masked": None,   # shared by O and down: split below
-        "wide_gemm_k_scatter": None,
+        "wide_mn256<true>": fa_pre["gate_up"], "wide_gemm_mn<true>": fa_pre["gate_up"],
+        "wide_mn256<false>": fa_pre["q"] + fa_pre["kv"], "wide_gemm_mn<false>": fa_pre["q"] + fa_pre["kv"],
     }
-    if dom in ("wide_gemm_k_dense_masked", "wide_gemm_k_scatter"):
-        alg = (fa_pre["o"] + fa_pre["down"]) / 2.0   # two launches per step (O, down)
+    if dom in ("wide_kd256", "wide_ks256", "wide_gemm_k_dense_masked", "wide_gemm_k_scatter"):
+        # O and down share these kernels; count the launches this kernel served
+        served = 0.0
+        for k_name, flops in (("o", fa_pre["o"]), ("down", fa_pre["down"])):
+            served += flops if kernel_of[k_name] == dom else 0.0
+        alg = served / (kernels[dom]["launches"] / args.steps)
     else:
         alg = per_launch_flops.get(dom)
     roofline = None

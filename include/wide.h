@@ -171,6 +171,10 @@ size_t wide_workspace_size(wide_op_t op, wide_dtype_t dt, int64_t M,
  *   "k_path"        schedule of the prefill K-axis product (down, O):
  *                   0 automatic (default), 1 dense-masked (no atomics),
  *                   2 scatter (the paper's GEMM-K with fp32 atomics).
+ *   "big_tiles"     1 (default): prefill GEMMs use 256x256 tiles where the
+ *                   shape allows; 0: always the 128x128 tiles.
+ *   "ring_bk"       k depth of a 256x256 pipeline stage: 64 (two stages,
+ *                   default) or 32 (four stages).
  * Not synchronised with calls running on other host threads.
  */
 wide_status_t wide_set_option(const char* key, int64_t value);

@@ -44,6 +44,7 @@ wide_status_t hip_fail(hipError_t e, const char* where) {
 // ---- tunables (wide_set_option) ---------------------------------------------
 int64_t g_decode_max_m = 64;  // M <= this uses the decode (GEMV) kernels
 int g_k_path = 0;             // 0 auto, 1 dense-masked, 2 scatter
+int g_big_tiles = 1;          // 1: 256x256 tile kernels where the shape allows
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
@@ -70,7 +71,9 @@ bool use_decode(wide_dtype_t dt, int64_t M) {
 
 int k_path_for(int G) {
   if (g_k_path == 1 || g_k_path == 2) return g_k_path;
-  return G >= 256 ? 2 : 1;
+  // fp32 atomics ran at ~1 TB/s on MI355X, which makes the scatter schedule
+  // slower than the dense-masked one unless G is very large.
+  return G >= 2048 ? 2 : 1;
 }
 
 // Workspace pieces of a prefill reorder held internally.
@@ -231,14 +234,17 @@ wide_status_t run_kaxis(const uint16_t* a, const uint16_t* w, const uint8_t* mas
   ka.N = N;
   ka.G = G;
   hipError_t e;
+  const bool big = g_big_tiles && N % wide::kT256 == 0;
   if (path == 2) {
     if ((e = wide::launch_zero_f32(kws.acc32, M * (int64_t)N, s)) != hipSuccess) return hip_fail(e, "zero");
-    if ((e = wide::launch_gemm_k_scatter(ka, s)) != hipSuccess) return hip_fail(e, "gemm_k_scatter");
+    e = big ? wide::launch_ks256(ka, s) : wide::launch_gemm_k_scatter(ka, s);
+    if (e != hipSuccess) return hip_fail(e, "gemm_k scatter");
     if ((e = wide::launch_f32_to_bf16(kws.acc32, y, M * (int64_t)N, s)) != hipSuccess)
       return hip_fail(e, "f32_to_bf16");
   } else {
-    if ((e = wide::launch_gemm_k_dense_masked(ka, s)) != hipSuccess)
-      return hip_fail(e, "gemm_k_dense_masked");
+    e = big && K / G <= wide::kKd256MaxGroups ? wide::launch_kd256(ka, s)
+                                              : wide::launch_gemm_k_dense_masked(ka, s);
+    if (e != hipSuccess) return hip_fail(e, "gemm_k dense-masked");
   }
   return WIDE_OK;
 }
@@ -299,6 +305,16 @@ wide_status_t wide_set_option(const char* key, int64_t value) {
     g_k_path = (int)value;
     return ok();
   }
+  if (!strcmp(key, "ring_bk")) {
+    if (value != 32 && value != 64) return fail(WIDE_ERR_INVALID_ARG, "ring_bk must be 32 or 64");
+    wide::set_ring_bk((int)value);
+    return ok();
+  }
+  if (!strcmp(key, "big_tiles")) {
+    if (value < 0 || value > 1) return fail(WIDE_ERR_INVALID_ARG, "big_tiles must be 0 or 1");
+    g_big_tiles = (int)value;
+    return ok();
+  }
   return fail(WIDE_ERR_INVALID_ARG, "unknown option '%s'", key);
 }
 
@@ -306,6 +322,8 @@ wide_status_t wide_get_option(const char* key, int64_t* value) {
   if (!key || !value) return fail(WIDE_ERR_INVALID_ARG, "NULL argument");
   if (!strcmp(key, "decode_max_m")) *value = g_decode_max_m;
   else if (!strcmp(key, "k_path")) *value = g_k_path;
+  else if (!strcmp(key, "big_tiles")) *value = g_big_tiles;
+  else if (!strcmp(key, "ring_bk")) *value = wide::get_ring_bk();
   else return fail(WIDE_ERR_INVALID_ARG, "unknown option '%s'", key);
   return ok();
 }
@@ -425,18 +443,32 @@ wide_status_t wide_ffn_masked(wide_dtype_t dt, int64_t M, int32_t d_model, int32
     ix = r.idx;
     ct = r.cnt;
   }
-  wide::MNArgs ma{};
-  ma.x = static_cast<const uint16_t*>(x);
-  ma.M = M;
-  ma.K = D;
-  ma.idx = ix;
-  ma.cnt = ct;
-  ma.G = G;
-  ma.m_tiles = (int)((M + wide::kMNTileM - 1) / wide::kMNTileM);
-  ma.n_regions = 1;
-  ma.reg[0] = wide::MNRegion{static_cast<const uint16_t*>(w_gate), static_cast<const uint16_t*>(w_up), h,
-                             Dff, Dff / wide::kMNTileNSwiglu, 1};
-  if ((e = wide::launch_gemm_mn(ma, true, stream)) != hipSuccess) return hip_fail(e, "gemm_mn gate/up");
+  if (g_big_tiles && G % 128 == 0) {
+    wide::MN256Args ma{};
+    ma.x = static_cast<const uint16_t*>(x);
+    ma.M = M;
+    ma.K = D;
+    ma.idx = ix;
+    ma.cnt = ct;
+    ma.m_tiles = (int)((M + wide::kT256 - 1) / wide::kT256);
+    ma.n_regions = 1;
+    ma.reg[0] = wide::MN256Region{static_cast<const uint16_t*>(w_gate), static_cast<const uint16_t*>(w_up), h,
+                                  Dff, G, 1, ng * ma.m_tiles * (G / 128)};
+    if ((e = wide::launch_mn256(ma, true, stream)) != hipSuccess) return hip_fail(e, "mn256 gate/up");
+  } else {
+    wide::MNArgs ma{};
+    ma.x = static_cast<const uint16_t*>(x);
+    ma.M = M;
+    ma.K = D;
+    ma.idx = ix;
+    ma.cnt = ct;
+    ma.G = G;
+    ma.m_tiles = (int)((M + wide::kMNTileM - 1) / wide::kMNTileM);
+    ma.n_regions = 1;
+    ma.reg[0] = wide::MNRegion{static_cast<const uint16_t*>(w_gate), static_cast<const uint16_t*>(w_up), h,
+                               Dff, Dff / wide::kMNTileNSwiglu, 1};
+    if ((e = wide::launch_gemm_mn(ma, true, stream)) != hipSuccess) return hip_fail(e, "gemm_mn gate/up");
+  }
   CHECK(run_kaxis(h, static_cast<const uint16_t*>(w_down), mask, ix, ct, static_cast<uint16_t*>(y), M, Dff,
                   D, G, kpath, kws, stream));
   return ok();
@@ -542,6 +574,28 @@ wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M, i
     ct = r.cnt;
   }
   if (phase == WIDE_PHASE_QKV) {
+    const uint16_t* wq = static_cast<const uint16_t*>(w_q);
+    const uint16_t* wk = static_cast<const uint16_t*>(w_k);
+    const uint16_t* wv = static_cast<const uint16_t*>(w_v);
+    if (g_big_tiles && d.G % wide::kT256 == 0 && d.Nkv % wide::kT256 == 0) {
+      wide::MN256Args ma{};
+      ma.x = x;
+      ma.M = M;
+      ma.K = d.D;
+      ma.idx = ix;
+      ma.cnt = ct;
+      ma.m_tiles = (int)((M + wide::kT256 - 1) / wide::kT256);
+      ma.n_regions = 3;
+      const int T = wide::kT256;
+      ma.reg[0] = wide::MN256Region{wq, nullptr, static_cast<uint16_t*>(q), d.Nq, d.G, 1,
+                                    ng * ma.m_tiles * (d.G / T)};
+      ma.reg[1] = wide::MN256Region{wk, nullptr, static_cast<uint16_t*>(k), d.Nkv, d.Nkv, 0,
+                                    ma.m_tiles * (d.Nkv / T)};
+      ma.reg[2] = wide::MN256Region{wv, nullptr, static_cast<uint16_t*>(v), d.Nkv, d.Nkv, 0,
+                                    ma.m_tiles * (d.Nkv / T)};
+      if ((e = wide::launch_mn256(ma, false, stream)) != hipSuccess) return hip_fail(e, "mn256 qkv");
+      return ok();
+    }
     wide::MNArgs ma{};
     ma.x = x;
     ma.M = M;
@@ -552,12 +606,9 @@ wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M, i
     ma.m_tiles = (int)((M + wide::kMNTileM - 1) / wide::kMNTileM);
     ma.n_regions = 3;
     const int T = wide::kMNTileNPlain;
-    ma.reg[0] = wide::MNRegion{static_cast<const uint16_t*>(w_q), nullptr, static_cast<uint16_t*>(q), d.Nq,
-                               d.Nq / T, 1};
-    ma.reg[1] = wide::MNRegion{static_cast<const uint16_t*>(w_k), nullptr, static_cast<uint16_t*>(k), d.Nkv,
-                               d.Nkv / T, 0};
-    ma.reg[2] = wide::MNRegion{static_cast<const uint16_t*>(w_v), nullptr, static_cast<uint16_t*>(v), d.Nkv,
-                               d.Nkv / T, 0};
+    ma.reg[0] = wide::MNRegion{wq, nullptr, static_cast<uint16_t*>(q), d.Nq, d.Nq / T, 1};
+    ma.reg[1] = wide::MNRegion{wk, nullptr, static_cast<uint16_t*>(k), d.Nkv, d.Nkv / T, 0};
+    ma.reg[2] = wide::MNRegion{wv, nullptr, static_cast<uint16_t*>(v), d.Nkv, d.Nkv / T, 0};
     if ((e = wide::launch_gemm_mn(ma, false, stream)) != hipSuccess) return hip_fail(e, "gemm_mn qkv");
     return ok();
   }

@@ -1,0 +1,363 @@
+// Large-tile prefill kernels (256 x 256 tiles, 8 waves, direct-to-LDS loads).
+//
+//   wide_mn256<SWIGLU,BK>  N-axis masked projection (GEMM-MN): gate/up + SwiGLU
+//                          (one tile = 256 sorted tokens x one 128-column slice
+//                          of a group: 128 gate rows + 128 up rows), or plain
+//                          Q/K/V (one tile = 256 tokens x 256 output columns).
+//   wide_kd256<BK>         K-axis masked projection, dense-masked schedule.
+//   wide_ks256<BK>         K-axis masked projection, scatter schedule (GEMM-K).
+//
+// Semantics, skipping levels and the two K-axis schedules are those of the
+// 128-tile kernels in gemm_mn.hip / gemm_k.hip (WIDE Section 3.1 equations
+// (1)-(3); Section 3.3; Appendix B, Algorithms 2 and 3); only the tile engine
+// differs (tile256.h).  Tiles whose 256 rows are all active take the
+// all-active path (no per-fragment tests), as the paper does for full tiles
+// of a sorted column.
+#include "common.h"
+#include "kernels.h"
+#include "launch.h"
+#include "tile256.h"
+
+namespace wide {
+
+using namespace t256;
+
+namespace {
+__device__ __attribute__((aligned(16))) uint16_t g_zero_blk[64];  // stays zero: never written
+
+template <int BK, class Src>
+__device__ __forceinline__ void run_tile(uint16_t* smem, int nsteps, Src src, int brow0, int brow1,
+                                         int live, f32x16 (&acc)[4][2]) {
+  live = __builtin_amdgcn_readfirstlane(live);
+  if (live == 0xF)
+    mainloop<BK, true>(smem, nsteps, src, brow0, brow1, live, acc);
+  else
+    mainloop<BK, false>(smem, nsteps, src, brow0, brow1, live, acc);
+}
+}  // namespace
+
+// --------------------------------------------------------------------- GEMM-MN
+template <bool SWIGLU, int BK>
+__global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+  using Rg = Ring<BK>;
+  constexpr int S = Rg::SLOTS;
+  constexpr int BNO = SWIGLU ? 128 : 256;  // output columns per tile
+  const uint16_t* zero = g_zero_blk;
+
+  int tile = xcd_remap(blockIdx.x, gridDim.x);
+  MN256Region R = a.reg[0];
+  if (a.n_regions > 1 && tile >= a.reg[0].tiles) {
+    tile -= a.reg[0].tiles;
+    R = a.reg[1];
+    if (a.n_regions > 2 && tile >= a.reg[1].tiles) {
+      tile -= a.reg[1].tiles;
+      R = a.reg[2];
+    }
+  }
+  // Tile order: group, then sorted m-tile, then column tile inside the
+  // group, so the tiles an XCD runs together share the group's weight panel
+  // in L2 (measured faster than blocking m-tiles across groups).
+  const int ntpg = R.gw / BNO;  // tiles per group
+  const int nt_in = tile % ntpg;
+  const int m_tile = (tile / ntpg) % a.m_tiles;
+  const int g = tile / (ntpg * a.m_tiles);
+  const int n0 = g * R.gw + nt_in * BNO;
+  const int64_t M = a.M;
+  const int K = a.K;
+  const int32_t* rows = R.masked ? a.idx + (int64_t)g * M : nullptr;
+  const int64_t cnt = R.masked ? (int64_t)a.cnt[g] : M;
+  const int64_t m0 = (int64_t)m_tile * BM;
+  const int tid = threadIdx.x;
+
+  if (m0 >= cnt) {  // l = 0: the whole tile is inactive for group g
+    constexpr int CH = BNO / 8;
+    const int64_t pend = min(m0 + BM, M);
+    for (int i = tid; i < BM * CH; i += NT) {
+      const int64_t p = m0 + i / CH;
+      if (p < pend) {
+        const int64_t t = rows ? rows[p] : p;
+        stg16(R.out + t * R.ldo + n0 + (i % CH) * 8, u32x4{0, 0, 0, 0});
+      }
+    }
+    return;
+  }
+
+  const uint16_t* abase[S];
+  const uint16_t* bbase[S];
+#pragma unroll
+  for (int j = 0; j < S; ++j) {
+    const int rr = Rg::slot_row(j);
+    const int c8 = Rg::slot_chunk(j) * 8;
+    const int64_t p = m0 + rr;
+    // l = 1: rows past the active prefix read the zero block
+    abase[j] = p < cnt ? a.x + (rows ? (int64_t)rows[p] : p) * K + c8 : nullptr;
+    if (SWIGLU)
+      bbase[j] = rr < 128 ? R.w0 + (int64_t)(n0 + rr) * K + c8 : R.w1 + (int64_t)(n0 + rr - 128) * K + c8;
+    else
+      bbase[j] = R.w0 + (int64_t)(n0 + rr) * K + c8;
+  }
+  const int lane = lane_id(), w = wave_id();
+  const int wm = w >> 2, wn = w & 3;
+  const int l32 = lane & 31;
+  const int brow0 = SWIGLU ? wn * 32 + l32 : wn * 64 + l32;
+  const int brow1 = SWIGLU ? 128 + wn * 32 + l32 : wn * 64 + 32 + l32;
+  int live = 0;  // l = 2: fragments wholly past the active prefix issue no MFMA
+#pragma unroll
+  for (int fm = 0; fm < 4; ++fm)
+    if (m0 + wm * 128 + fm * 32 < cnt) live |= 1 << fm;
+
+  f32x16 acc[4][2];
+  zero_acc(acc);
+  auto src = [&](int s, const uint16_t* (&ap)[S], const uint16_t* (&bp)[S]) {
+    const int k0 = s * BK;
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      ap[j] = abase[j] ? abase[j] + k0 : zero;
+      bp[j] = bbase[j] + k0;
+    }
+  };
+  run_tile<BK>(smem, K / BK, src, brow0, brow1, live, acc);
+
+  // Epilogue: rows back to token order; rows past cnt hold +0 accumulators.
+  const int col = acc_col();
+#pragma unroll
+  for (int fm = 0; fm < 4; ++fm) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int64_t p = m0 + acc_row(fm, i);
+      if (p >= M) continue;
+      const int64_t t = rows ? rows[p] : p;
+      uint16_t* o = R.out + t * R.ldo + n0;
+      if (SWIGLU) {
+        o[wn * 32 + col] = f32_to_bf16(silu(acc[fm][0][i]) * acc[fm][1][i]);
+      } else {
+        o[wn * 64 + col] = f32_to_bf16(acc[fm][0][i]);
+        o[wn * 64 + 32 + col] = f32_to_bf16(acc[fm][1][i]);
+      }
+    }
+  }
+}
+
+// ----------------------------------------------------------- K-axis, dense-masked
+template <int BK>
+__global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+  __shared__ uint32_t s_mbits[BM][kKd256MaxGroups / 32];  // mask bits of the tile's rows
+  __shared__ uint16_t s_groups[kKd256MaxGroups];          // groups with an active row, ascending
+  __shared__ int s_ng_live;
+  using Rg = Ring<BK>;
+  constexpr int S = Rg::SLOTS;
+  const uint16_t* zero = g_zero_blk;
+  const int n_tiles = a.N / BN;
+  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int m_tile = tile / n_tiles, n_tile = tile % n_tiles;  // m-major: n-tiles share the A panel
+  const int64_t m0 = (int64_t)m_tile * BM;
+  const int n0 = n_tile * BN;
+  const int ng = a.K / a.G;
+  const int nw = (ng + 31) / 32;
+  const int tid = threadIdx.x;
+
+  for (int i = tid; i < BM * nw; i += NT) {
+    const int r = i / nw, wd = i % nw;
+    const int64_t t = m0 + r;
+    uint32_t bits = 0;
+    if (t < a.M) {
+      const uint8_t* mr = a.mask + t * ng + wd * 32;
+      const int n = min(32, ng - wd * 32);
+      for (int b = 0; b < n; ++b) bits |= (uint32_t)(mr[b] != 0) << b;
+    }
+    s_mbits[r][wd] = bits;
+  }
+  if (tid == 0) {
+    int n = 0;
+    const uint8_t* tu = a.tile_union + (int64_t)m_tile * ng;
+    for (int gg = 0; gg < ng; ++gg)
+      if (tu[gg]) s_groups[n++] = (uint16_t)gg;
+    s_ng_live = n;
+  }
+  __syncthreads();
+  const int spg = a.G / BK;  // k steps per group
+  const int nsteps = s_ng_live * spg;
+
+  int srow[S];
+  const uint16_t* abase[S];
+  const uint16_t* bbase[S];
+#pragma unroll
+  for (int j = 0; j < S; ++j) {
+    const int rr = Rg::slot_row(j);
+    const int c8 = Rg::slot_chunk(j) * 8;
+    const int64_t t = m0 + rr;
+    srow[j] = rr;
+    abase[j] = t < a.M ? a.a + t * a.K + c8 : nullptr;
+    bbase[j] = a.w + (int64_t)(n0 + rr) * a.K + c8;
+  }
+  const int lane = lane_id(), w = wave_id();
+  const int wm = w >> 2, wn = w & 3;
+  const int l32 = lane & 31;
+  const int brow0 = wn * 64 + l32, brow1 = wn * 64 + 32 + l32;
+  int live = 0;
+#pragma unroll
+  for (int fm = 0; fm < 4; ++fm)
+    if (m0 + wm * 128 + fm * 32 < a.M) live |= 1 << fm;
+
+  f32x16 acc[4][2];
+  zero_acc(acc);
+  auto src = [&](int s, const uint16_t* (&ap)[S], const uint16_t* (&bp)[S]) {
+    const int gg = s_groups[s / spg];
+    const int k0 = gg * a.G + (s % spg) * BK;
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      const bool on = abase[j] && ((s_mbits[srow[j]][gg >> 5] >> (gg & 31)) & 1u);
+      ap[j] = on ? abase[j] + k0 : zero;  // inactive (t, g) blocks are never read
+      bp[j] = bbase[j] + k0;
+    }
+  };
+  run_tile<BK>(smem, nsteps, src, brow0, brow1, live, acc);
+
+  const int col = acc_col();
+#pragma unroll
+  for (int fm = 0; fm < 4; ++fm)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int64_t t = m0 + acc_row(fm, i);
+      if (t >= a.M) continue;
+      uint16_t* o = a.y + t * a.N + n0 + wn * 64;
+      o[col] = f32_to_bf16(acc[fm][0][i]);
+      o[32 + col] = f32_to_bf16(acc[fm][1][i]);
+    }
+}
+
+// -------------------------------------------------------------- K-axis, scatter
+template <int BK>
+__global__ __launch_bounds__(NT, 1) void wide_ks256(KArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+  using Rg = Ring<BK>;
+  constexpr int S = Rg::SLOTS;
+  const uint16_t* zero = g_zero_blk;
+  const int n_tiles = a.N / BN;
+  const int m_tiles = (int)((a.M + BM - 1) / BM);
+  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int n_tile = tile % n_tiles;
+  const int m_tile = (tile / n_tiles) % m_tiles;
+  const int g = tile / (n_tiles * m_tiles);
+  const int64_t cnt = a.cnt[g];
+  const int64_t m0 = (int64_t)m_tile * BM;
+  if (m0 >= cnt) return;  // l = 0
+  const int n0 = n_tile * BN;
+  const int32_t* rows = a.idx + (int64_t)g * a.M;
+
+  const uint16_t* abase[S];
+  const uint16_t* bbase[S];
+#pragma unroll
+  for (int j = 0; j < S; ++j) {
+    const int rr = Rg::slot_row(j);
+    const int c8 = Rg::slot_chunk(j) * 8;
+    const int64_t p = m0 + rr;
+    abase[j] = p < cnt ? a.a + (int64_t)rows[p] * a.K + c8 : nullptr;  // l = 1
+    bbase[j] = a.w + (int64_t)(n0 + rr) * a.K + c8;
+  }
+  const int lane = lane_id(), w = wave_id();
+  const int wm = w >> 2, wn = w & 3;
+  const int l32 = lane & 31;
+  const int brow0 = wn * 64 + l32, brow1 = wn * 64 + 32 + l32;
+  int live = 0;  // l = 2
+#pragma unroll
+  for (int fm = 0; fm < 4; ++fm)
+    if (m0 + wm * 128 + fm * 32 < cnt) live |= 1 << fm;
+
+  f32x16 acc[4][2];
+  zero_acc(acc);
+  const int kbeg = g * a.G;
+  auto src = [&](int s, const uint16_t* (&ap)[S], const uint16_t* (&bp)[S]) {
+    const int k0 = kbeg + s * BK;
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      ap[j] = abase[j] ? abase[j] + k0 : zero;
+      bp[j] = bbase[j] + k0;
+    }
+  };
+  run_tile<BK>(smem, a.G / BK, src, brow0, brow1, live, acc);
+
+  const int col = acc_col();
+#pragma unroll
+  for (int fm = 0; fm < 4; ++fm) {
+    if (!(live & (1 << fm))) continue;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int64_t p = m0 + acc_row(fm, i);
+      if (p >= cnt) continue;
+      float* o = a.acc32 + (int64_t)rows[p] * a.N + n0 + wn * 64;
+      unsafeAtomicAdd(o + col, acc[fm][0][i]);
+      unsafeAtomicAdd(o + 32 + col, acc[fm][1][i]);
+    }
+  }
+}
+
+// ------------------------------------------------------------------ launchers
+namespace {
+int g_ring_bk = 64;
+
+template <class F>
+hipError_t allow_big_lds(F* f) {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(f),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
+}
+
+// Raise the dynamic-LDS limit of one kernel instance once per process.
+template <auto Kern>
+hipError_t prepare() {
+  static const hipError_t e = allow_big_lds(Kern);
+  return e;
+}
+}  // namespace
+
+void set_ring_bk(int bk) { g_ring_bk = bk; }
+int get_ring_bk() { return g_ring_bk; }
+
+#define WIDE_RING_LAUNCH(NAME, KT, GRID, STREAM, ARGS)                                  \
+  do {                                                                                  \
+    hipError_t e_ = g_ring_bk == 32 ? prepare<KT(32)>() : prepare<KT(64)>();            \
+    if (e_ != hipSuccess) return e_;                                                    \
+    if (g_ring_bk == 32)                                                                \
+      WIDE_LAUNCH_NAMED(NAME "/bk32", (KT(32)), dim3(GRID), dim3(NT), LDS_BYTES, STREAM, ARGS); \
+    else                                                                                \
+      WIDE_LAUNCH_NAMED(NAME "/bk64", (KT(64)), dim3(GRID), dim3(NT), LDS_BYTES, STREAM, ARGS); \
+  } while (0)
+
+#define MN_SW(bk) wide_mn256<true, bk>
+#define MN_PL(bk) wide_mn256<false, bk>
+#define KD(bk) wide_kd256<bk>
+#define KS(bk) wide_ks256<bk>
+
+hipError_t launch_mn256(const MN256Args& a, bool swiglu, hipStream_t s) {
+  int64_t total = 0;
+  for (int i = 0; i < a.n_regions; ++i) total += a.reg[i].tiles;
+  if (total == 0) return hipSuccess;
+  if (swiglu)
+    WIDE_RING_LAUNCH("wide_mn256<true>", MN_SW, (unsigned)total, s, a);
+  else
+    WIDE_RING_LAUNCH("wide_mn256<false>", MN_PL, (unsigned)total, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_kd256(const KArgs& a, hipStream_t s) {
+  const int64_t m_tiles = (a.M + BM - 1) / BM;
+  const int64_t total = m_tiles * (a.N / BN);
+  if (total == 0) return hipSuccess;
+  if (a.K / a.G > kKd256MaxGroups) return hipErrorInvalidValue;
+  hipError_t e = launch_tile_union(a.mask, a.M, a.K / a.G, BM, a.tile_union, s);
+  if (e != hipSuccess) return e;
+  WIDE_RING_LAUNCH("wide_kd256", KD, (unsigned)total, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_ks256(const KArgs& a, hipStream_t s) {
+  const int64_t m_tiles = (a.M + BM - 1) / BM;
+  const int64_t total = (int64_t)(a.K / a.G) * m_tiles * (a.N / BN);
+  if (total == 0) return hipSuccess;
+  WIDE_RING_LAUNCH("wide_ks256", KS, (unsigned)total, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace wide

@@ -39,7 +39,9 @@ namespace {
 constexpr int BM = kKTileM, BN = kKTileN, BK = kKTileK, NT = 256;
 
 __device__ __forceinline__ int swz(int row, int chunk) {
-  return row * BK + ((chunk ^ (row & 7)) << 3);
+  // 16 lanes of a 128-bit LDS read hit 64 banks together: keep rows r and
+  // r + 8 on different chunks (see tile256.h)
+  return row * BK + ((chunk ^ ((row & 7) ^ ((row >> 3) & 1))) << 3);
 }
 
 __device__ __forceinline__ int xcd_remap(int id, int n) {
@@ -218,17 +220,25 @@ __global__ __launch_bounds__(NT, 2) void wide_gemm_k_scatter(KArgs a) {
   }
 }
 
-// tu[mt][g] = 1 iff some token of the 128-token tile mt is active in group g.
+// tu[mt][g] = 1 iff some token of the tile_m-token tile mt is active in group g.
 __global__ __launch_bounds__(256) void wide_tile_union(const uint8_t* __restrict__ mask,
-                                                       int64_t M, int n_groups,
+                                                       int64_t M, int n_groups, int tile_m,
                                                        uint8_t* __restrict__ tu) {
-  const int64_t t0 = (int64_t)blockIdx.x * BM;
-  const int64_t tn = min((int64_t)BM, M - t0);
+  const int64_t t0 = (int64_t)blockIdx.x * tile_m;
+  const int64_t tn = min((int64_t)tile_m, M - t0);
   for (int g = threadIdx.x; g < n_groups; g += blockDim.x) {
     uint8_t any = 0;
     for (int64_t r = 0; r < tn && !any; ++r) any = mask[(t0 + r) * n_groups + g] != 0;
     tu[blockIdx.x * (int64_t)n_groups + g] = any;
   }
+}
+
+hipError_t launch_tile_union(const uint8_t* mask, int64_t M, int n_groups, int tile_m, uint8_t* tu,
+                             hipStream_t s) {
+  const int64_t m_tiles = (M + tile_m - 1) / tile_m;
+  if (m_tiles == 0) return hipSuccess;
+  WIDE_LAUNCH(wide_tile_union, dim3((unsigned)m_tiles), dim3(256), 0, s, mask, M, n_groups, tile_m, tu);
+  return hipGetLastError();
 }
 
 __global__ void wide_zero_f32(float* __restrict__ p, int64_t n) {
@@ -270,8 +280,8 @@ hipError_t launch_gemm_k_dense_masked(const KArgs& a, hipStream_t s) {
   const int64_t m_tiles = (a.M + BM - 1) / BM;
   const int64_t total = m_tiles * (a.N / BN);
   if (total == 0) return hipSuccess;
-  WIDE_LAUNCH(wide_tile_union, dim3((unsigned)m_tiles), dim3(256), 0, s, a.mask, a.M,
-              a.K / a.G, a.tile_union);
+  hipError_t e = launch_tile_union(a.mask, a.M, a.K / a.G, BM, a.tile_union, s);
+  if (e != hipSuccess) return e;
   WIDE_LAUNCH(wide_gemm_k_dense_masked, dim3((unsigned)total), dim3(NT), 0, s, a);
   return hipGetLastError();
 }

@@ -47,7 +47,9 @@ __device__ __forceinline__ int xcd_remap(int id, int n) {
 }
 
 __device__ __forceinline__ int swz(int row, int chunk) {  // element offset in a [rows][64] tile
-  return row * BK + ((chunk ^ (row & 7)) << 3);
+  // 16 lanes of a 128-bit LDS read hit 64 banks together: keep rows r and
+  // r + 8 on different chunks (see tile256.h)
+  return row * BK + ((chunk ^ ((row & 7) ^ ((row >> 3) & 1))) << 3);
 }
 
 }  // namespace

@@ -67,6 +67,41 @@ inline size_t tile_union_bytes(int64_t M, int n_groups) {
   return (size_t)((M + kKTileM - 1) / kKTileM) * (size_t)n_groups;
 }
 hipError_t launch_gemm_k_scatter(const KArgs& a, hipStream_t s);
+hipError_t launch_tile_union(const uint8_t* mask, int64_t M, int n_groups, int tile_m, uint8_t* tu,
+                             hipStream_t s);
+
+// ---- large-tile (256 x 256) prefill kernels ----------------------------------------
+// A region of the large-tile GEMM-MN: output columns [0, N) of one tensor cut
+// into groups of `gw` columns (gw = G for a masked region, gw = N for a dense
+// one); tiles = (N / gw) * m_tiles * (gw / tile_cols).
+struct MN256Region {
+  const uint16_t* w0;
+  const uint16_t* w1;
+  uint16_t* out;
+  int ldo;
+  int gw;
+  int masked;
+  int tiles;
+};
+
+struct MN256Args {
+  const uint16_t* x;
+  int64_t M;
+  int K;
+  const int32_t* idx;
+  const int32_t* cnt;
+  int m_tiles;
+  int n_regions;
+  MN256Region reg[3];
+};
+
+constexpr int kT256 = 256;
+hipError_t launch_mn256(const MN256Args& a, bool swiglu, hipStream_t s);
+hipError_t launch_kd256(const KArgs& a, hipStream_t s);
+hipError_t launch_ks256(const KArgs& a, hipStream_t s);
+constexpr int kKd256MaxGroups = 512;
+void set_ring_bk(int bk);   // 64 (two stages) or 32 (four stages)
+int get_ring_bk();
 hipError_t launch_zero_f32(float* p, int64_t n, hipStream_t s);
 hipError_t launch_f32_to_bf16(const float* src, uint16_t* dst, int64_t n, hipStream_t s);
 

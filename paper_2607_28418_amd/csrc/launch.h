@@ -12,10 +12,14 @@ void timing_end(int slot, hipStream_t s);
 
 }  // namespace wide
 
-// KERN may be a parenthesised template instance: (kern<A, B>).
-#define WIDE_LAUNCH(KERN, GRID, BLOCK, SHMEM, STREAM, ...)                \
+// KERN may be a parenthesised template instance: (kern<A, B>).  NAME is the
+// label timing queries match against.
+#define WIDE_LAUNCH_NAMED(NAME, KERN, GRID, BLOCK, SHMEM, STREAM, ...)    \
   do {                                                                    \
-    const int wide_slot_ = ::wide::timing_begin(#KERN, (STREAM));         \
+    const int wide_slot_ = ::wide::timing_begin((NAME), (STREAM));        \
     hipLaunchKernelGGL(KERN, (GRID), (BLOCK), (SHMEM), (STREAM), __VA_ARGS__); \
     ::wide::timing_end(wide_slot_, (STREAM));                             \
   } while (0)
+
+#define WIDE_LAUNCH(KERN, GRID, BLOCK, SHMEM, STREAM, ...) \
+  WIDE_LAUNCH_NAMED(#KERN, KERN, GRID, BLOCK, SHMEM, STREAM, __VA_ARGS__)

@@ -5,122 +5,166 @@
 // Algorithm 1).  With ties kept in token order this is a stable partition:
 // idx[g][0:cnt[g]] = active tokens ascending, idx[g][cnt[g]:M] = the rest.
 //
-// Three short kernels, all wave64, no host synchronisation:
-//   count   one workgroup per chunk of 256 tokens; each wave ballots the
-//           active bits of its 64 tokens per group and the chunk's count per
-//           group lands in chunk_cnt[chunk][g];
-//   scan    one thread per group: exclusive prefix of the chunk counts over
-//           chunks (chunk_off[chunk][g]) and the group total (counts[g]);
-//   scatter one workgroup per chunk again; ballot + mbcnt give each token its
-//           rank among the active (or inactive) tokens of its wave, an LDS
-//           exchange of the four wave totals gives the rank inside the chunk,
-//           and chunk_off places it in the group's list.
+// Three short kernels, no host synchronisation.  The mask is cut into chunks
+// of 64 tokens, one wave each (one token per lane):
+//   count    the chunk's mask rows (64 x n_groups bytes, contiguous in
+//            memory) are staged in LDS with coalesced loads, in slabs of 512
+//            groups; for every group a wave ballot over the 64 tokens gives
+//            the chunk's active count, stored transposed as ccnt[g][chunk];
+//   scan     one workgroup per group: block-wide exclusive prefix of
+//            ccnt[g][:] over chunks (coff[g][chunk]) and the total counts[g];
+//   scatter  the chunk's rows are staged again; per group the ballot and
+//            mbcnt give each token its rank among the chunk's active (or
+//            inactive) tokens, and coff[g][chunk] / counts[g] place it.
 #include "common.h"
+#include "kernels.h"
 #include "launch.h"
 
 namespace wide {
 
-constexpr int kChunk = 256;          // tokens per workgroup (4 waves)
-constexpr int kChunkWaves = kChunk / kWave;
+namespace {
+constexpr int kChunk = 64;     // tokens per chunk = one wave
+constexpr int kSlab = 512;     // groups staged in LDS at a time (32 KB)
+constexpr int kScanThreads = 256;
 
-__global__ __launch_bounds__(kChunk) void wide_reorder_count(
-    const uint8_t* __restrict__ mask, int64_t M, int n_groups,
-    int32_t* __restrict__ chunk_cnt) {
-  __shared__ int32_t wcnt[kChunkWaves][64];
-  const int64_t t = (int64_t)blockIdx.x * kChunk + threadIdx.x;
-  const bool in_range = t < M;
-  const uint8_t* row = mask + t * n_groups;
-  const int w = wave_id();
-  for (int g0 = 0; g0 < n_groups; g0 += 64) {
-    const int gn = min(64, n_groups - g0);
+// Stage mask[t0 .. t0+rows)[g0 .. g0+gn) into s[r * gn + j] (bytes).  Whole
+// rows are one contiguous run: copied 16 bytes per lane when the run is
+// 16-byte aligned, so that many loads are in flight at once.
+__device__ __forceinline__ void stage_mask(const uint8_t* __restrict__ mask, int64_t t0, int rows,
+                                           int n_groups, int g0, int gn, uint8_t* s) {
+  const int n = rows * gn;
+  if (gn == n_groups) {
+    const uint8_t* src = mask + t0 * n_groups;
+    int done = 0;
+    if ((reinterpret_cast<uintptr_t>(src) & 15) == 0) {
+      const int nv = n / 16;
+#pragma unroll 4
+      for (int i = threadIdx.x; i < nv; i += kChunk)
+        *reinterpret_cast<u32x4*>(s + 16 * i) = ldg16(src + 16 * i);
+      done = nv * 16;
+    }
+    for (int i = done + threadIdx.x; i < n; i += kChunk) s[i] = src[i];
+  } else {
+#pragma unroll 4
+    for (int i = threadIdx.x; i < n; i += kChunk) {
+      const int r = i / gn, j = i % gn;
+      s[i] = mask[(t0 + r) * n_groups + g0 + j];
+    }
+  }
+}
+}  // namespace
+
+__global__ __launch_bounds__(kChunk) void wide_reorder_count(const uint8_t* __restrict__ mask,
+                                                             int64_t M, int n_groups, int n_chunks,
+                                                             int32_t* __restrict__ ccnt) {
+  __shared__ uint8_t s[kChunk * kSlab];
+  const int c = blockIdx.x;
+  const int64_t t0 = (int64_t)c * kChunk;
+  const int rows = (int)min((int64_t)kChunk, M - t0);
+  const int lane = threadIdx.x;
+  for (int g0 = 0; g0 < n_groups; g0 += kSlab) {
+    const int gn = min(kSlab, n_groups - g0);
+    stage_mask(mask, t0, rows, n_groups, g0, gn, s);
+    __syncthreads();
     for (int j = 0; j < gn; ++j) {
-      const bool a = in_range && row[g0 + j] != 0;
+      const bool a = lane < rows && s[lane * gn + j] != 0;
       const uint64_t b = __ballot(a);
-      if (lane_id() == 0) wcnt[w][j] = __popcll(b);
-    }
-    __syncthreads();
-    if (threadIdx.x < gn) {
-      int s = 0;
-      for (int i = 0; i < kChunkWaves; ++i) s += wcnt[i][threadIdx.x];
-      chunk_cnt[(int64_t)blockIdx.x * n_groups + g0 + threadIdx.x] = s;
+      if (lane == 0) ccnt[(int64_t)(g0 + j) * n_chunks + c] = __popcll(b);
     }
     __syncthreads();
   }
 }
 
-__global__ __launch_bounds__(256) void wide_reorder_scan(
-    const int32_t* __restrict__ chunk_cnt, int n_chunks, int n_groups,
-    int32_t* __restrict__ chunk_off, int32_t* __restrict__ counts) {
-  const int g = blockIdx.x * blockDim.x + threadIdx.x;
-  if (g >= n_groups) return;
+__global__ __launch_bounds__(kScanThreads) void wide_reorder_scan(const int32_t* __restrict__ ccnt,
+                                                                  int n_chunks,
+                                                                  int32_t* __restrict__ coff,
+                                                                  int32_t* __restrict__ counts) {
+  __shared__ int32_t wsum[kScanThreads / kWave];
+  const int g = blockIdx.x;
+  const int32_t* in = ccnt + (int64_t)g * n_chunks;
+  int32_t* out = coff + (int64_t)g * n_chunks;
+  const int lane = lane_id(), w = wave_id();
   int32_t run = 0;
-  for (int c = 0; c < n_chunks; ++c) {
-    const int64_t o = (int64_t)c * n_groups + g;
-    const int32_t v = chunk_cnt[o];
-    chunk_off[o] = run;
-    run += v;
+  for (int base = 0; base < n_chunks; base += kScanThreads) {
+    const int c = base + threadIdx.x;
+    const int32_t v = c < n_chunks ? in[c] : 0;
+    // inclusive scan inside the wave
+    int32_t x = v;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+      const int32_t y = __shfl_up(x, d, kWave);
+      if (lane >= d) x += y;
+    }
+    if (lane == kWave - 1) wsum[w] = x;
+    __syncthreads();
+    int32_t before = run;
+    for (int i = 0; i < w; ++i) before += wsum[i];
+    int32_t tile_total = 0;
+    for (int i = 0; i < kScanThreads / kWave; ++i) tile_total += wsum[i];
+    if (c < n_chunks) out[c] = before + x - v;
+    run += tile_total;
+    __syncthreads();
   }
-  counts[g] = run;
+  if (threadIdx.x == 0) counts[g] = run;
 }
 
-__global__ __launch_bounds__(kChunk) void wide_reorder_scatter(
-    const uint8_t* __restrict__ mask, int64_t M, int n_groups,
-    const int32_t* __restrict__ chunk_off, const int32_t* __restrict__ counts,
-    int32_t* __restrict__ idx) {
-  __shared__ int32_t wact[2][kChunkWaves];
-  const int64_t c0 = (int64_t)blockIdx.x * kChunk;
-  const int64_t t = c0 + threadIdx.x;
-  const bool in_range = t < M;
-  const uint8_t* row = mask + t * n_groups;
-  const int w = wave_id();
-  const int lane = lane_id();
+__global__ __launch_bounds__(kChunk) void wide_reorder_scatter(const uint8_t* __restrict__ mask,
+                                                               int64_t M, int n_groups,
+                                                               int n_chunks,
+                                                               const int32_t* __restrict__ coff,
+                                                               const int32_t* __restrict__ counts,
+                                                               int32_t* __restrict__ idx) {
+  __shared__ uint8_t s[kChunk * kSlab];
+  __shared__ int32_t s_off[kSlab], s_cnt[kSlab];
+  const int c = blockIdx.x;
+  const int64_t t0 = (int64_t)c * kChunk;
+  const int rows = (int)min((int64_t)kChunk, M - t0);
+  const int lane = threadIdx.x;
+  const int64_t t = t0 + lane;
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  const uint64_t valid_wave = __ballot(in_range);
-  for (int g = 0; g < n_groups; ++g) {
-    const bool a = in_range && row[g] != 0;
-    const uint64_t b = __ballot(a);
-    const int buf = g & 1;
-    if (lane == 0) wact[buf][w] = __popcll(b);
-    __syncthreads();
-    int act_before = 0, tok_before = 0;
-    for (int i = 0; i < w; ++i) {
-      act_before += wact[buf][i];
-      tok_before += kWave;
+  const uint64_t valid = __ballot(lane < rows);
+  for (int g0 = 0; g0 < n_groups; g0 += kSlab) {
+    const int gn = min(kSlab, n_groups - g0);
+    stage_mask(mask, t0, rows, n_groups, g0, gn, s);
+    for (int j = lane; j < gn; j += kChunk) {  // independent loads, all in flight
+      s_off[j] = coff[(int64_t)(g0 + j) * n_chunks + c];
+      s_cnt[j] = counts[g0 + j];
     }
-    if (in_range) {
-      const int32_t off = chunk_off[blockIdx.x * (int64_t)n_groups + g];
-      int32_t* out = idx + (int64_t)g * M;
-      const int r_act = __popcll(b & below);
-      if (a) {
-        out[off + act_before + r_act] = (int32_t)t;
-      } else {
-        const int r_inact = __popcll(valid_wave & ~b & below);
-        const int64_t inact_before_chunk = c0 - off;  // inactive tokens in earlier chunks
-        out[counts[g] + inact_before_chunk + (tok_before - act_before) + r_inact] = (int32_t)t;
+    __syncthreads();
+    for (int j = 0; j < gn; ++j) {
+      const int g = g0 + j;
+      const bool a = lane < rows && s[lane * gn + j] != 0;
+      const uint64_t b = __ballot(a);
+      if (lane < rows) {
+        const int32_t off = s_off[j];  // active tokens in earlier chunks
+        int32_t* out = idx + (int64_t)g * M;
+        if (a) {
+          out[off + __popcll(b & below)] = (int32_t)t;
+        } else {
+          const int64_t inact_before = t0 - off;  // inactive tokens in earlier chunks
+          out[s_cnt[j] + inact_before + __popcll(valid & ~b & below)] = (int32_t)t;
+        }
       }
     }
-    // wact[buf] is rewritten two groups later, after the next barrier.
+    __syncthreads();
   }
 }
 
-// Host-side launcher (called from api.cpp after validation).
-hipError_t launch_reorder(const uint8_t* mask, int64_t M, int n_groups,
-                          int32_t* idx, int32_t* counts, int32_t* chunk_cnt,
-                          int32_t* chunk_off, hipStream_t s) {
-  if (M == 0) {
-    const int blocks = (n_groups + 255) / 256;
-    // counts of an empty column are zero: one scan over zero chunks.
-    WIDE_LAUNCH(wide_reorder_scan, dim3(blocks), dim3(256), 0, s,
-                chunk_cnt, 0, n_groups, chunk_off, counts);
-    return hipGetLastError();
-  }
-  const int n_chunks = (int)((M + kChunk - 1) / kChunk);
-  WIDE_LAUNCH(wide_reorder_count, dim3(n_chunks), dim3(kChunk), 0, s,
-              mask, M, n_groups, chunk_cnt);
-  WIDE_LAUNCH(wide_reorder_scan, dim3((n_groups + 255) / 256), dim3(256), 0, s,
-              chunk_cnt, n_chunks, n_groups, chunk_off, counts);
-  WIDE_LAUNCH(wide_reorder_scatter, dim3(n_chunks), dim3(kChunk), 0, s,
-              mask, M, n_groups, chunk_off, counts, idx);
+// Host-side launcher (called from api.cpp after validation).  ccnt and coff
+// each hold n_groups * ceil(M / 64) ints.
+hipError_t launch_reorder(const uint8_t* mask, int64_t M, int n_groups, int32_t* idx,
+                          int32_t* counts, int32_t* ccnt, int32_t* coff, hipStream_t s) {
+  const int64_t n_chunks64 = (M + kChunk - 1) / kChunk;
+  if (n_chunks64 > 0x7fffffff) return hipErrorInvalidValue;
+  const int n_chunks = (int)n_chunks64;
+  if (n_chunks > 0)
+    WIDE_LAUNCH(wide_reorder_count, dim3(n_chunks), dim3(kChunk), 0, s, mask, M, n_groups,
+                n_chunks, ccnt);
+  WIDE_LAUNCH(wide_reorder_scan, dim3(n_groups), dim3(kScanThreads), 0, s, ccnt, n_chunks, coff,
+              counts);
+  if (n_chunks > 0)
+    WIDE_LAUNCH(wide_reorder_scatter, dim3(n_chunks), dim3(kChunk), 0, s, mask, M, n_groups,
+                n_chunks, coff, counts, idx);
   return hipGetLastError();
 }
 
