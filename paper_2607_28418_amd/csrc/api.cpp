@@ -135,6 +135,24 @@ wide_status_t check_common(wide_dtype_t dt, int64_t M) {
   return WIDE_OK;
 }
 
+
+// Decode-path argument blocks (pointers may be null when only sizes are needed).
+wide::GVNArgs ffn_gvn(int64_t M, int D, int Dff, int G, const uint8_t* mask, const void* x, const void* wg,
+                      const void* wu, uint16_t* h) {
+  wide::GVNArgs na{};
+  na.x = static_cast<const uint16_t*>(x);
+  na.mask = mask;
+  na.B = (int)M;
+  na.K = D;
+  na.G = G;
+  na.n_groups = Dff / G;
+  na.n_regions = 1;
+  na.reg[0] = wide::GVRegion{static_cast<const uint16_t*>(wg), static_cast<const uint16_t*>(wu), h, Dff,
+                             Dff / 16, 1, 0};
+  na.k_split = wide::gemv_n_split(na);
+  return na;
+}
+
 // ---- FFN -------------------------------------------------------------------------
 wide_status_t ffn_shape(wide_dtype_t dt, int64_t M, int D, int Dff, int G) {
   CHECK(check_common(dt, M));
@@ -162,7 +180,12 @@ size_t ffn_ws_bytes(wide_dtype_t dt, int64_t M, int D, int Dff, int G, bool need
     return c.off;
   }
   if (need_h) c.take<uint16_t>((size_t)M * Dff);
-  if (!use_decode(dt, M)) {
+  if (use_decode(dt, M)) {
+    const size_t pn = wide::gemv_n_part_floats(ffn_gvn(M, D, Dff, G, nullptr, nullptr, nullptr, nullptr, nullptr), true);
+    if (pn) c.take<float>(pn);
+    const int ks = wide::gemv_k_split(D);
+    if (ks > 1) c.take<float>((size_t)ks * M * D);
+  } else {
     ReorderWS r;
     carve_reorder(c, M, ng, need_idx, r);
     KWS k;
@@ -199,10 +222,46 @@ wide_status_t attn_shape(wide_dtype_t dt, int64_t M, int D, int nq, int nkv, int
   return WIDE_OK;
 }
 
+
+wide::GVNArgs qkv_gvn(int64_t M, const AttnDims& d, const uint8_t* mask, const void* x, const void* wq,
+                      const void* wk, const void* wv, void* q, void* k, void* v) {
+  wide::GVNArgs na{};
+  na.x = static_cast<const uint16_t*>(x);
+  na.mask = mask;
+  na.B = (int)M;
+  na.K = d.D;
+  na.G = d.G;
+  na.n_groups = d.ng;
+  na.n_regions = 3;
+  na.reg[0] = wide::GVRegion{static_cast<const uint16_t*>(wq), nullptr, static_cast<uint16_t*>(q), d.Nq,
+                             d.Nq / 16, 1, 0};
+  na.reg[1] = wide::GVRegion{static_cast<const uint16_t*>(wk), nullptr, static_cast<uint16_t*>(k), d.Nkv,
+                             d.Nkv / 16, 0, d.Nq};
+  na.reg[2] = wide::GVRegion{static_cast<const uint16_t*>(wv), nullptr, static_cast<uint16_t*>(v), d.Nkv,
+                             d.Nkv / 16, 0, d.Nq + d.Nkv};
+  na.k_split = wide::gemv_n_split(na);
+  return na;
+}
+
 size_t attn_ws_bytes(wide_phase_t ph, wide_dtype_t dt, int64_t M, const AttnDims& d, bool need_idx,
                      int kpath) {
   Carve c(nullptr);
-  if (dt == WIDE_F32 || use_decode(dt, M)) return 0;
+  if (dt == WIDE_F32) return 0;
+  if (use_decode(dt, M)) {
+    if (ph == WIDE_PHASE_QKV) {
+      // d.Nkv < 0: sizing query without n_kv; bound the split (<= 8) and the
+      // columns (n_kv <= n_q, so at most 3 * n_q * head_dim).
+      const size_t pn = d.Nkv < 0 ? (size_t)8 * M * 3 * d.Nq
+                                  : wide::gemv_n_part_floats(qkv_gvn(M, d, nullptr, nullptr, nullptr, nullptr,
+                                                                     nullptr, nullptr, nullptr, nullptr),
+                                                             false);
+      if (pn) c.take<float>(pn);
+    } else {
+      const int ks = wide::gemv_k_split(d.D);
+      if (ks > 1) c.take<float>((size_t)ks * M * d.D);
+    }
+    return c.off;
+  }
   if (ph == WIDE_PHASE_QKV) {
     ReorderWS r;
     if (need_idx) carve_reorder(c, M, d.ng, true, r);
@@ -347,7 +406,7 @@ size_t wide_workspace_size(wide_op_t op, wide_dtype_t dt, int64_t M, int32_t d_m
       if (check_common(dt, M) != WIDE_OK || d_model <= 0 || group_size <= 0 || d_inner <= 0 ||
           d_inner % group_size || d_inner / group_size > 4096)
         return SIZE_MAX;
-      AttnDims d{d_model, 0, 0, 0, group_size, d_inner, 0, d_inner / group_size};
+      AttnDims d{d_model, 0, 0, 0, group_size, d_inner, -1, d_inner / group_size};
       return attn_ws_bytes(op == WIDE_OP_QKV ? WIDE_PHASE_QKV : WIDE_PHASE_O, dt, M, d, true, 0);
     }
   }
@@ -414,19 +473,14 @@ wide_status_t wide_ffn_masked(wide_dtype_t dt, int64_t M, int32_t d_model, int32
 
   uint16_t* h = h_out ? static_cast<uint16_t*>(h_out) : c.take<uint16_t>((size_t)M * Dff);
   if (decode) {
-    wide::GVNArgs na{};
-    na.x = static_cast<const uint16_t*>(x);
-    na.mask = mask;
-    na.B = (int)M;
-    na.K = D;
-    na.G = G;
-    na.n_groups = ng;
-    na.n_regions = 1;
-    na.reg[0] = wide::GVRegion{static_cast<const uint16_t*>(w_gate), static_cast<const uint16_t*>(w_up),
-                               h, Dff, Dff / 16, 1};
+    wide::GVNArgs na = ffn_gvn(M, D, Dff, G, mask, x, w_gate, w_up, h);
+    const size_t pn = wide::gemv_n_part_floats(na, true);
+    na.part = pn ? c.take<float>(pn) : nullptr;
     if ((e = wide::launch_gemv_n(na, true, stream)) != hipSuccess) return hip_fail(e, "gemv gate/up");
+    const int ks = wide::gemv_k_split(D);
+    float* part = ks > 1 ? c.take<float>((size_t)ks * M * D) : nullptr;
     wide::GVKArgs ka{h, static_cast<const uint16_t*>(w_down), mask, static_cast<uint16_t*>(y),
-                     (int)M, Dff, D, G, ng};
+                     (int)M, Dff, D, G, ng, ks, part};
     if ((e = wide::launch_gemv_k(ka, stream)) != hipSuccess) return hip_fail(e, "gemv down");
     return ok();
   }
@@ -535,24 +589,15 @@ wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M, i
   const uint16_t* x = static_cast<const uint16_t*>(in);
   if (use_decode(dt, M)) {
     if (phase == WIDE_PHASE_QKV) {
-      wide::GVNArgs na{};
-      na.x = x;
-      na.mask = mask;
-      na.B = (int)M;
-      na.K = d.D;
-      na.G = d.G;
-      na.n_groups = ng;
-      na.n_regions = 3;
-      na.reg[0] = wide::GVRegion{static_cast<const uint16_t*>(w_q), nullptr, static_cast<uint16_t*>(q), d.Nq,
-                                 d.Nq / 16, 1};
-      na.reg[1] = wide::GVRegion{static_cast<const uint16_t*>(w_k), nullptr, static_cast<uint16_t*>(k), d.Nkv,
-                                 d.Nkv / 16, 0};
-      na.reg[2] = wide::GVRegion{static_cast<const uint16_t*>(w_v), nullptr, static_cast<uint16_t*>(v), d.Nkv,
-                                 d.Nkv / 16, 0};
+      wide::GVNArgs na = qkv_gvn(M, d, mask, x, w_q, w_k, w_v, q, k, v);
+      const size_t pn = wide::gemv_n_part_floats(na, false);
+      na.part = pn ? c.take<float>(pn) : nullptr;
       if ((e = wide::launch_gemv_n(na, false, stream)) != hipSuccess) return hip_fail(e, "gemv qkv");
     } else {
+      const int ks = wide::gemv_k_split(d.D);
+      float* part = ks > 1 ? c.take<float>((size_t)ks * M * d.D) : nullptr;
       wide::GVKArgs ka{x, static_cast<const uint16_t*>(w_o), mask, static_cast<uint16_t*>(y), (int)M, d.Nq,
-                       d.D, d.G, ng};
+                       d.D, d.G, ng, ks, part};
       if ((e = wide::launch_gemv_k(ka, stream)) != hipSuccess) return hip_fail(e, "gemv o");
     }
     return ok();

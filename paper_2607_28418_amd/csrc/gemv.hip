@@ -8,24 +8,27 @@
 // and nothing else, with full-cache-line 128-bit loads and many loads in
 // flight per lane.
 //
-// gemv_n  (N-axis: gate/up + SwiGLU, Q; dense K/V).  A workgroup owns 16
+// gemv_n  (N-axis: gate/up + SwiGLU, Q; dense K/V).  A workgroup owns 16*NCB
 //         output columns of one group; its 8 waves take turns over the
 //         64-wide steps of the reduction dimension K.  If no token of the
 //         batch is active in the group, the workgroup writes +0 and exits
 //         before touching a weight byte.  Otherwise lane l streams 32
 //         contiguous bytes of weight row l%16 per k step (four lanes cover a
-//         128-byte line), four steps at a time together with the matching
-//         activations, which ride along as the other MFMA operand (16x16x32,
+//         128-byte line), two steps of NCB blocks at a time together with the
+//         matching activations, which ride along as the other MFMA operand
+//         (16x16x32,
 //         tokens as rows); both operands use the same permutation of k inside
 //         a step, so the sum is unchanged.  Inactive (token, group) outputs
 //         are +0.
 //
-// gemv_k  (K-axis: down, O).  A workgroup owns 16 output rows n; its 8 waves
-//         take turns over the k steps of the union groups; for each union
-//         group a wave reads the 2G-byte segments w[n, gG:(g+1)G] of its 16
-//         rows and the matching activations of the tokens active in the group
-//         (inactive blocks are never read).  The batch's mask sits in LDS as
-//         one 64-bit token set per group.  No atomics.
+// gemv_k  (K-axis: down, O).  A workgroup owns 16*NCB output rows n and a
+//         share of the k steps of the union groups (k_split workgroups per row
+//         block; their fp32 partial sums are added in a fixed order by a small
+//         finishing kernel); its 8 waves take turns over those steps.  For
+//         each union group a wave reads the 2G-byte segments w[n, gG:(g+1)G]
+//         of its rows and the matching activations of the tokens active in
+//         the group (inactive blocks are never read).  The batch's mask sits
+//         in LDS as one 64-bit token set per group.  No atomics.
 //
 // Both reduce the 8 waves' partial sums through LDS in a fixed order, so the
 // results are deterministic.  NTB (1, 2 or 4 blocks of 16 tokens) sizes the
@@ -39,7 +42,6 @@ namespace wide {
 namespace {
 constexpr int NW = 8;                  // waves per workgroup
 constexpr int NT = NW * kWave;
-constexpr int U = 4;                   // k steps in flight per lane
 
 // Sum 8 waves' [NTB*16 tokens][16 cols] partials: waves 4..7 park theirs,
 // waves 0..3 add theirs on top, then out(b, c, sums) runs per output.
@@ -79,43 +81,61 @@ __device__ __forceinline__ void reduce_out(float (*red)[kDecodeMaxB][16], const 
   }
 }
 
-// Loads of one k step: weights of NV row sets and activations of NTB token
-// blocks.
-template <int NV, int NTB>
-struct StepRegs {
-  u32x4 w[NV][2];
-  u32x4 x[NTB][2];
-};
-
-template <int NV, int NTB>
-__device__ __forceinline__ void step_mfma(const StepRegs<NV, NTB>& r, f32x4 (&acc)[NV][NTB]) {
-#pragma unroll
-  for (int tb = 0; tb < NTB; ++tb)
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      acc[v][tb] = mfma16(r.x[tb][0], r.w[v][0], acc[v][tb]);
-      acc[v][tb] = mfma16(r.x[tb][1], r.w[v][1], acc[v][tb]);
-    }
+__device__ __host__ __forceinline__ int gv_total_cols(const GVNArgs& a) {
+  int n = 0;
+  for (int i = 0; i < a.n_regions; ++i) n += a.reg[i].n_blocks * 16;
+  return n;
 }
+
 }  // namespace
 
-template <bool SWIGLU, int NTB>
+// Sum the k_split partials of every (token, column) in a fixed order, apply
+// SwiGLU (gate/up pair) and the mask, store bf16.
+template <bool SWIGLU>
+__global__ __launch_bounds__(256) void wide_gemv_n_finish(GVNArgs a) {
+  constexpr int NV = SWIGLU ? 2 : 1;
+  const int ncols = gv_total_cols(a);
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)a.B * ncols) return;
+  const int b = (int)(i / ncols);
+  int col = (int)(i % ncols);
+  GVRegion R = a.reg[0];
+  if (a.n_regions > 1 && col >= a.reg[1].col0) R = a.reg[1];
+  if (a.n_regions > 2 && col >= a.reg[2].col0) R = a.reg[2];
+  const int lc = col - R.col0;
+  const bool on = !R.masked || a.mask[(int64_t)b * a.n_groups + lc / a.G] != 0;
+  float o = 0.f;
+  if (on) {
+    float s[NV];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      s[v] = 0.f;
+      for (int q = 0; q < a.k_split; ++q) s[v] += a.part[(((int64_t)q * NV + v) * a.B + b) * ncols + col];
+    }
+    o = SWIGLU ? silu(s[0]) * s[NV - 1] : s[0];
+  }
+  R.out[(int64_t)b * R.ldo + lc] = f32_to_bf16(o);
+}
+
+template <bool SWIGLU, int NTB, int NCB>
 __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
   constexpr int NV = SWIGLU ? 2 : 1;
+  constexpr int UN = 2;  // k steps in flight (NCB blocks of weights each)
   __shared__ float red[NW / 2 * NV][kDecodeMaxB][16];
   __shared__ int any_active;
 
-  int nb = blockIdx.x;
+  const int kq = blockIdx.x % a.k_split;  // this workgroup's share of the k steps
+  int nb = blockIdx.x / a.k_split;
   GVRegion R = a.reg[0];
-  if (a.n_regions > 1 && nb >= a.reg[0].n_blocks) {
-    nb -= a.reg[0].n_blocks;
+  if (a.n_regions > 1 && nb >= a.reg[0].n_blocks / NCB) {
+    nb -= a.reg[0].n_blocks / NCB;
     R = a.reg[1];
-    if (a.n_regions > 2 && nb >= a.reg[1].n_blocks) {
-      nb -= a.reg[1].n_blocks;
+    if (a.n_regions > 2 && nb >= a.reg[1].n_blocks / NCB) {
+      nb -= a.reg[1].n_blocks / NCB;
       R = a.reg[2];
     }
   }
-  const int n0 = nb * 16;
+  const int n0 = nb * 16 * NCB;  // the NCB blocks lie in one group (16*NCB divides G)
   const int g = n0 / a.G;
   const int tid = threadIdx.x;
   const int B = a.B, K = a.K;
@@ -125,9 +145,11 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
   if (R.masked && tid < B && a.mask[(int64_t)tid * a.n_groups + g] != 0) any_active = 1;
   __syncthreads();
   if (!any_active) {
-    // group unused by the whole batch: no weight reads, outputs +0
-    for (int i = tid; i < B * 2; i += NT) {
-      const int b = i / 2, h = i % 2;
+    // group unused by the whole batch: no weight reads, outputs +0 (with a
+    // k split the finishing kernel writes them)
+    if (a.k_split > 1) return;
+    for (int i = tid; i < B * 2 * NCB; i += NT) {
+      const int b = i / (2 * NCB), h = i % (2 * NCB);
       stg16(R.out + (int64_t)b * R.ldo + n0 + h * 8, u32x4{0, 0, 0, 0});
     }
     return;
@@ -135,12 +157,17 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
 
   const int w = wave_id(), lane = lane_id();
   const int ln = lane & 15, lq = lane >> 4;
-  // The K/64 steps are dealt round-robin to the 8 waves.
-  const int nsteps = K / 64;
+  // This workgroup's share of the K/64 steps, dealt round-robin to the 8 waves.
+  const int all_steps = K / 64;
+  const int s_beg = (int)((int64_t)all_steps * kq / a.k_split);
+  const int nsteps = (int)((int64_t)all_steps * (kq + 1) / a.k_split) - s_beg;
   const int my_steps = nsteps > w ? (nsteps - w + NW - 1) / NW : 0;
-  const uint16_t* wrow[NV];
-  wrow[0] = R.w0 + (int64_t)(n0 + ln) * K + lq * 16;
-  if (SWIGLU) wrow[NV - 1] = R.w1 + (int64_t)(n0 + ln) * K + lq * 16;
+  const uint16_t* wrow[NCB][NV];
+#pragma unroll
+  for (int c = 0; c < NCB; ++c) {
+    wrow[c][0] = R.w0 + (int64_t)(n0 + c * 16 + ln) * K + lq * 16;
+    if (SWIGLU) wrow[c][NV - 1] = R.w1 + (int64_t)(n0 + c * 16 + ln) * K + lq * 16;
+  }
   const uint16_t* xrow[NTB];
   bool xon[NTB];
 #pragma unroll
@@ -150,47 +177,78 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
     xrow[tb] = a.x + (int64_t)(xon[tb] ? b : 0) * K + lq * 16;
   }
 
-  f32x4 acc[NV][NTB];
+  f32x4 acc[NCB][NV][NTB];
 #pragma unroll
-  for (int v = 0; v < NV; ++v)
+  for (int c = 0; c < NCB; ++c)
 #pragma unroll
-    for (int i = 0; i < NTB; ++i) acc[v][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int i = 0; i < NTB; ++i) acc[c][v][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto load = [&](int k, StepRegs<NV, NTB>& r) {
+  struct Regs {
+    u32x4 w[NCB][NV][2];
+    u32x4 x[NTB][2];
+  };
+  auto load = [&](int k, Regs& r) {
 #pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      r.w[v][0] = ldg16(wrow[v] + k);
-      r.w[v][1] = ldg16(wrow[v] + k + 8);
-    }
+    for (int c = 0; c < NCB; ++c)
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        r.w[c][v][0] = ldg16(wrow[c][v] + k);
+        r.w[c][v][1] = ldg16(wrow[c][v] + k + 8);
+      }
 #pragma unroll
     for (int tb = 0; tb < NTB; ++tb) {
       r.x[tb][0] = xon[tb] ? ldg16(xrow[tb] + k) : u32x4{0, 0, 0, 0};
       r.x[tb][1] = xon[tb] ? ldg16(xrow[tb] + k + 8) : u32x4{0, 0, 0, 0};
     }
   };
+  auto mma = [&](const Regs& r) {
+#pragma unroll
+    for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+      for (int c = 0; c < NCB; ++c)
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          acc[c][v][tb] = mfma16(r.x[tb][0], r.w[c][v][0], acc[c][v][tb]);
+          acc[c][v][tb] = mfma16(r.x[tb][1], r.w[c][v][1], acc[c][v][tb]);
+        }
+  };
   int q = 0;
-  for (; q + U <= my_steps; q += U) {
-    StepRegs<NV, NTB> r[U];
+  for (; q + UN <= my_steps; q += UN) {
+    Regs r[UN];
 #pragma unroll
-    for (int s = 0; s < U; ++s) load((w + (q + s) * NW) * 64, r[s]);
+    for (int s2 = 0; s2 < UN; ++s2) load((s_beg + w + (q + s2) * NW) * 64, r[s2]);
 #pragma unroll
-    for (int s = 0; s < U; ++s) step_mfma(r[s], acc);
+    for (int s2 = 0; s2 < UN; ++s2) mma(r[s2]);
   }
   for (; q < my_steps; ++q) {
-    StepRegs<NV, NTB> r;
-    load((w + q * NW) * 64, r);
-    step_mfma(r, acc);
+    Regs r;
+    load((s_beg + w + q * NW) * 64, r);
+    mma(r);
   }
-  // C[row = token (lane/16)*4 + i][col = lane%16]
-  reduce_out<NV, NTB>(red, acc, B, [&](int b, int c, const float (&s)[NV]) {
-    const bool on = !R.masked || a.mask[(int64_t)b * a.n_groups + g] != 0;
-    const float o = on ? (SWIGLU ? silu(s[0]) * s[NV - 1] : s[0]) : 0.f;
-    R.out[(int64_t)b * R.ldo + n0 + c] = f32_to_bf16(o);
-  });
+  // C[row = token (lane/16)*4 + i][col = lane%16], one column block at a time
+#pragma unroll
+  for (int c = 0; c < NCB; ++c) {
+    reduce_out<NV, NTB>(red, acc[c], B, [&](int b, int cc, const float (&sm)[NV]) {
+      if (a.k_split > 1) {  // fp32 partials, finished by wide_gemv_n_finish
+        const int ncols = gv_total_cols(a);
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+          a.part[(((int64_t)kq * NV + v) * B + b) * ncols + R.col0 + n0 + c * 16 + cc] = sm[v];
+        return;
+      }
+      const bool on = !R.masked || a.mask[(int64_t)b * a.n_groups + g] != 0;
+      const float o = on ? (SWIGLU ? silu(sm[0]) * sm[NV - 1] : sm[0]) : 0.f;
+      R.out[(int64_t)b * R.ldo + n0 + c * 16 + cc] = f32_to_bf16(o);
+    });
+    __syncthreads();
+  }
 }
 
-template <int NTB>
+template <int NTB, int NCB>
 __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
+  constexpr int UK = 2;  // k steps in flight
   __shared__ float red[NW / 2][kDecodeMaxB][16];
   __shared__ unsigned long long s_act[4096];  // bit b: token b active in group g
   __shared__ uint16_t ulist[4096];
@@ -199,7 +257,8 @@ __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
 
   const int tid = threadIdx.x;
   const int B = a.B, K = a.K, G = a.G, ng = a.n_groups;
-  const int n0 = blockIdx.x * 16;
+  const int kq = blockIdx.x % a.k_split;            // this workgroup's share of the union steps
+  const int n0 = (blockIdx.x / a.k_split) * 16 * NCB;
   const int w = wave_id(), lane = lane_id();
   for (int i = tid; i < ng; i += NT) s_act[i] = 0ull;
   __syncthreads();
@@ -229,15 +288,22 @@ __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
     __syncthreads();
   }
   const int nu = n_union;
-  const int spg = G / 64;        // k steps per group
-  const int nsteps = nu * spg;   // steps of the union, dealt round-robin to the waves
+  const int spg = G / 64;  // k steps per group
+  const int all_steps = nu * spg;
+  const int s_beg = (int)((int64_t)all_steps * kq / a.k_split);
+  const int s_end = (int)((int64_t)all_steps * (kq + 1) / a.k_split);
+  const int nsteps = s_end - s_beg;  // dealt round-robin to the waves
   const int my_steps = nsteps > w ? (nsteps - w + NW - 1) / NW : 0;
 
   const int ln = lane & 15, lq = lane >> 4;
-  f32x4 acc[1][NTB];
+  f32x4 acc[NCB][NTB];
 #pragma unroll
-  for (int i = 0; i < NTB; ++i) acc[0][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const uint16_t* wrow = a.w + (int64_t)(n0 + ln) * K + lq * 16;
+  for (int c = 0; c < NCB; ++c)
+#pragma unroll
+    for (int i = 0; i < NTB; ++i) acc[c][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const uint16_t* wrow[NCB];
+#pragma unroll
+  for (int c = 0; c < NCB; ++c) wrow[c] = a.w + (int64_t)(n0 + c * 16 + ln) * K + lq * 16;
   const uint16_t* xrow[NTB];
   int tok[NTB];
 #pragma unroll
@@ -246,13 +312,20 @@ __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
     xrow[tb] = a.a + (int64_t)(tok[tb] < B ? tok[tb] : 0) * K + lq * 16;
   }
 
-  auto load = [&](int q, StepRegs<1, NTB>& r) {
-    const int s = w + q * NW;
+  struct Regs {
+    u32x4 w[NCB][2];
+    u32x4 x[NTB][2];
+  };
+  auto load = [&](int q, Regs& r) {
+    const int s = s_beg + w + q * NW;
     const int g = ulist[s / spg];
     const int k = g * G + (s % spg) * 64;
     const unsigned long long act = s_act[g];
-    r.w[0][0] = ldg16(wrow + k);
-    r.w[0][1] = ldg16(wrow + k + 8);
+#pragma unroll
+    for (int c = 0; c < NCB; ++c) {
+      r.w[c][0] = ldg16(wrow[c] + k);
+      r.w[c][1] = ldg16(wrow[c] + k + 8);
+    }
 #pragma unroll
     for (int tb = 0; tb < NTB; ++tb) {
       const bool on = tok[tb] < B && ((act >> tok[tb]) & 1ull);  // inactive blocks are never read
@@ -260,53 +333,141 @@ __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
       r.x[tb][1] = on ? ldg16(xrow[tb] + k + 8) : u32x4{0, 0, 0, 0};
     }
   };
+  auto mma = [&](const Regs& r) {
+#pragma unroll
+    for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+      for (int c = 0; c < NCB; ++c) {
+        acc[c][tb] = mfma16(r.x[tb][0], r.w[c][0], acc[c][tb]);
+        acc[c][tb] = mfma16(r.x[tb][1], r.w[c][1], acc[c][tb]);
+      }
+  };
   int q = 0;
-  for (; q + U <= my_steps; q += U) {
-    StepRegs<1, NTB> r[U];
+  for (; q + UK <= my_steps; q += UK) {
+    Regs r[UK];
 #pragma unroll
-    for (int s = 0; s < U; ++s) load(q + s, r[s]);
+    for (int s2 = 0; s2 < UK; ++s2) load(q + s2, r[s2]);
 #pragma unroll
-    for (int s = 0; s < U; ++s) step_mfma(r[s], acc);
+    for (int s2 = 0; s2 < UK; ++s2) mma(r[s2]);
   }
   for (; q < my_steps; ++q) {
-    StepRegs<1, NTB> r;
+    Regs r;
     load(q, r);
-    step_mfma(r, acc);
+    mma(r);
   }
-  reduce_out<1, NTB>(red, acc, B, [&](int b, int c, const float (&s)[1]) {
-    a.y[(int64_t)b * a.N + n0 + c] = f32_to_bf16(s[0]);
-  });
+#pragma unroll
+  for (int c = 0; c < NCB; ++c) {
+    f32x4 one[1][NTB];
+#pragma unroll
+    for (int tb = 0; tb < NTB; ++tb) one[0][tb] = acc[c][tb];
+    reduce_out<1, NTB>(red, one, B, [&](int b, int cc, const float (&sm)[1]) {
+      const int64_t o = (int64_t)b * a.N + n0 + c * 16 + cc;
+      if (a.k_split == 1)
+        a.y[o] = f32_to_bf16(sm[0]);
+      else
+        a.part[(int64_t)kq * B * a.N + o] = sm[0];  // summed in fixed order by gemv_k_finish
+    });
+    __syncthreads();
+  }
+}
+
+// y = bf16(sum over the k_split partial sums), in a fixed order.
+__global__ __launch_bounds__(256) void wide_gemv_k_finish(const float* __restrict__ part, int k_split,
+                                                          int64_t n, uint16_t* __restrict__ y) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float s = 0.f;
+  for (int q = 0; q < k_split; ++q) s += part[(int64_t)q * n + i];
+  y[i] = f32_to_bf16(s);
 }
 
 namespace {
-template <bool SW>
-hipError_t gemv_n_ntb(const GVNArgs& a, int nb, hipStream_t s) {
+template <bool SW, int NCB>
+hipError_t gemv_n_launch(const GVNArgs& a, int nb, hipStream_t s) {
   const char* name = SW ? "wide_gemv_n<true>" : "wide_gemv_n<false>";
+  const int grid = nb / NCB * a.k_split;
   if (a.B <= 16)
-    WIDE_LAUNCH_NAMED(name, (wide_gemv_n<SW, 1>), dim3(nb), dim3(NT), 0, s, a);
+    WIDE_LAUNCH_NAMED(name, (wide_gemv_n<SW, 1, NCB>), dim3(grid), dim3(NT), 0, s, a);
   else if (a.B <= 32)
-    WIDE_LAUNCH_NAMED(name, (wide_gemv_n<SW, 2>), dim3(nb), dim3(NT), 0, s, a);
+    WIDE_LAUNCH_NAMED(name, (wide_gemv_n<SW, 2, NCB>), dim3(grid), dim3(NT), 0, s, a);
   else
-    WIDE_LAUNCH_NAMED(name, (wide_gemv_n<SW, 4>), dim3(nb), dim3(NT), 0, s, a);
+    WIDE_LAUNCH_NAMED(name, (wide_gemv_n<SW, 4, NCB>), dim3(grid), dim3(NT), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.k_split == 1) return e;
+  const int64_t n = (int64_t)a.B * gv_total_cols(a);
+  const dim3 fg((unsigned)((n + 255) / 256));
+  if (SW)
+    WIDE_LAUNCH_NAMED("wide_gemv_n_finish", (wide_gemv_n_finish<true>), fg, dim3(256), 0, s, a);
+  else
+    WIDE_LAUNCH_NAMED("wide_gemv_n_finish", (wide_gemv_n_finish<false>), fg, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int NCB>
+hipError_t gemv_k_launch(const GVKArgs& a, hipStream_t s) {
+  const int grid = a.N / (16 * NCB) * a.k_split;
+  if (a.B <= 16)
+    WIDE_LAUNCH_NAMED("wide_gemv_k", (wide_gemv_k<1, NCB>), dim3(grid), dim3(NT), 0, s, a);
+  else if (a.B <= 32)
+    WIDE_LAUNCH_NAMED("wide_gemv_k", (wide_gemv_k<2, NCB>), dim3(grid), dim3(NT), 0, s, a);
+  else
+    WIDE_LAUNCH_NAMED("wide_gemv_k", (wide_gemv_k<4, NCB>), dim3(grid), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 }  // namespace
+
+// Column blocks per workgroup: four when every region divides into runs of
+// four blocks inside one group (measured: 64 columns per workgroup cut the
+// activation re-reads and ran gate/up at ~5 TB/s), else two, else one.
+int gemv_n_ncb(const GVNArgs& a) {
+  for (int ncb : {4, 2}) {
+    if ((a.G / 16) % ncb) continue;
+    bool ok = true;
+    for (int i = 0; i < a.n_regions; ++i) ok = ok && a.reg[i].n_blocks % ncb == 0;
+    if (ok) return ncb;
+  }
+  return 1;
+}
+
+// Split of the k steps over workgroups.  A split costs a finishing kernel
+// (~6 us on MI355X), which only pays when the column runs alone leave most
+// CUs idle: split (at most 8 ways, at least 4 k steps per share) until there
+// are 192 workgroups.
+int gemv_n_split(const GVNArgs& a) {
+  int nb = 0;
+  for (int i = 0; i < a.n_regions; ++i) nb += a.reg[i].n_blocks;
+  const int runs = nb / gemv_n_ncb(a);
+  int ks = 1;
+  while (runs * ks < 192 && ks < 8 && a.K / 64 / (2 * ks) >= 4) ks *= 2;
+  return ks;
+}
+
+size_t gemv_n_part_floats(const GVNArgs& a, bool swiglu) {
+  const int ks = gemv_n_split(a);
+  return ks > 1 ? (size_t)ks * (swiglu ? 2 : 1) * a.B * gv_total_cols(a) : 0;
+}
 
 hipError_t launch_gemv_n(const GVNArgs& a, bool swiglu, hipStream_t s) {
   int nb = 0;
   for (int i = 0; i < a.n_regions; ++i) nb += a.reg[i].n_blocks;
   if (nb == 0 || a.B == 0) return hipSuccess;
-  return swiglu ? gemv_n_ntb<true>(a, nb, s) : gemv_n_ntb<false>(a, nb, s);
+  const int ncb = gemv_n_ncb(a);
+  if (swiglu)
+    return ncb == 4 ? gemv_n_launch<true, 4>(a, nb, s)
+                    : ncb == 2 ? gemv_n_launch<true, 2>(a, nb, s) : gemv_n_launch<true, 1>(a, nb, s);
+  return ncb == 4 ? gemv_n_launch<false, 4>(a, nb, s)
+                  : ncb == 2 ? gemv_n_launch<false, 2>(a, nb, s) : gemv_n_launch<false, 1>(a, nb, s);
 }
 
 hipError_t launch_gemv_k(const GVKArgs& a, hipStream_t s) {
   if (a.B == 0 || a.N == 0) return hipSuccess;
-  if (a.B <= 16)
-    WIDE_LAUNCH_NAMED("wide_gemv_k", (wide_gemv_k<1>), dim3(a.N / 16), dim3(NT), 0, s, a);
-  else if (a.B <= 32)
-    WIDE_LAUNCH_NAMED("wide_gemv_k", (wide_gemv_k<2>), dim3(a.N / 16), dim3(NT), 0, s, a);
-  else
-    WIDE_LAUNCH_NAMED("wide_gemv_k", (wide_gemv_k<4>), dim3(a.N / 16), dim3(NT), 0, s, a);
+  // 64 output rows per workgroup when N allows, the union steps split over
+  // k_split workgroups (chosen by the host, partials in a.part).
+  hipError_t e = a.N % 64 == 0 ? gemv_k_launch<4>(a, s) : gemv_k_launch<1>(a, s);
+  if (e != hipSuccess || a.k_split == 1) return e;
+  const int64_t n = (int64_t)a.B * a.N;
+  WIDE_LAUNCH(wide_gemv_k_finish, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a.part, a.k_split,
+              n, a.y);
   return hipGetLastError();
 }
 

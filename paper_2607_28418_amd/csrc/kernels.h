@@ -113,6 +113,7 @@ struct GVRegion {
   int ldo;
   int n_blocks;        // 16-column blocks in this region
   int masked;
+  int col0;            // first column of the region in the concatenated output space
 };
 
 struct GVNArgs {
@@ -121,7 +122,12 @@ struct GVNArgs {
   int B, K, G, n_groups;
   int n_regions;
   GVRegion reg[3];
+  int k_split;         // workgroups sharing one column run's k steps
+  float* part;         // [k_split][NV][B][total columns] partials when k_split > 1
 };
+// Decode N-axis split: enough workgroups to fill the chip (see gemv.hip).
+int gemv_n_split(const GVNArgs& a);
+size_t gemv_n_part_floats(const GVNArgs& a, bool swiglu);
 
 struct GVKArgs {
   const uint16_t* a;   // [B][K]
@@ -129,7 +135,16 @@ struct GVKArgs {
   const uint8_t* mask; // [B][K/G]
   uint16_t* y;         // [B][N]
   int B, K, N, G, n_groups;
+  int k_split;         // workgroups sharing one row block's union steps
+  float* part;         // [k_split][B][N] partial sums when k_split > 1
 };
+// Split of the decode K-axis product: enough workgroups to fill the chip.
+inline int gemv_k_split(int N) {
+  const int row_blocks = N % 64 == 0 ? N / 64 : N / 16;
+  int ks = 1;
+  while (row_blocks * ks < 256 && ks < 8) ks *= 2;
+  return ks;
+}
 
 constexpr int kDecodeMaxB = 64;
 

@@ -335,6 +335,52 @@ def test_qkvo_bf16_full_sampled(orc, name):
     assert_close(y[r], orc.kproj(c.a[rows], c.w_o, c.mask[rows], c.G, round_bf16=True), what="o")
 
 
+# ------------------------------------------------------------------ graphs
+
+@pytest.mark.parametrize("M", [24, 600])
+def test_calls_replay_in_hip_graph(orc, M):
+    """Decode and prefill calls captured in one HIP graph: every replay (with
+    eager work and syncs in between) equals the eager result."""
+    say("graph replay", M)
+    W.wide_set_option("k_path", 1)   # deterministic K path: replays compare bitwise
+    c = synth.ffn_case(M + 1, M, 512, 1024, 128, mask="topk")
+    x, wg, wu, wd, m = ffn_dev(c)
+    ca = synth.attn_case(M + 2, M, 512, 8, 2, 128, 512, mask="topk")
+    d = attn_dev(ca)
+    y = torch.empty((M, 512), dtype=torch.bfloat16, device=dev())
+    q = torch.empty((M, 1024), dtype=torch.bfloat16, device=dev())
+    kk = torch.empty((M, 256), dtype=torch.bfloat16, device=dev())
+    vv = torch.empty((M, 256), dtype=torch.bfloat16, device=dev())
+    yo = torch.empty((M, 512), dtype=torch.bfloat16, device=dev())
+    ws = torch.empty(max(W.wide_workspace_size(W.OP_FFN, W.BF16, M, 512, 1024, 128),
+                         W.wide_workspace_size(W.OP_QKV, W.BF16, M, 512, 1024, 512),
+                         W.wide_workspace_size(W.OP_O, W.BF16, M, 512, 1024, 512)),
+                     dtype=torch.uint8, device=dev())
+
+    def step():
+        W.wide_ffn_masked(x, wg, wu, wd, m, 128, y=y, ws=ws)
+        W.wide_qkvo_masked(W.PHASE_QKV, d["x"], d["mask"], 512, 8, 2, 128, w_q=d["w_q"], w_k=d["w_k"],
+                           w_v=d["w_v"], q=q, k=kk, v=vv, ws=ws)
+        W.wide_qkvo_masked(W.PHASE_O, d["a"], d["mask"], 512, 8, 2, 128, w_o=d["w_o"], y=yo, ws=ws)
+
+    step()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in (y, q, kk, vv, yo)]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for _ in range(3):
+        for t in (y, q, kk, vv, yo):
+            t.fill_(7.0)          # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for got, want in zip((y, q, kk, vv, yo), ref):
+            assert torch.equal(got, want)
+    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, 128, round_bf16=True)
+    assert_close(y, ry, what="y", abs_allow=ffn_flip_allowance(rh, synth.as_f32(c.w_down)))
+
+
 # ------------------------------------------------------------------ errors, timing
 
 def test_errors_leave_outputs_untouched():

@@ -1,0 +1,43 @@
+"""Host logic of the counter summary (no GPU)."""
+import csv
+import json
+
+from paper_2607_28418_amd import profiling
+
+FIELDS = ["Kernel_Name", "Grid_Size", "Counter_Name", "Counter_Value"]
+
+
+def _dump(path, counter, rows):
+    with open(path, "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=FIELDS)
+        w.writeheader()
+        for name, v, *grid in rows:
+            w.writerow({"Kernel_Name": name, "Grid_Size": grid[0] if grid else 256,
+                        "Counter_Name": counter, "Counter_Value": v})
+
+
+def test_summary_scales_by_copy_and_guards_sources(tmp_path):
+    k = "void wide::wide_mn256<true, 64>(wide::MN256Args)"
+    _dump(tmp_path / "f.csv", "FETCH_SIZE", [(k, 100.0), (k, 300.0), (profiling.COPY_KERNEL, 3.0, 512),
+                                  (profiling.COPY_KERNEL, 512.0, 131072)])
+    _dump(tmp_path / "w.csv", "WRITE_SIZE", [(k, 50.0), (k, 50.0), (profiling.COPY_KERNEL, 1024.0, 131072)])
+    s = profiling.summarize(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), 1024 * 1024, "cmd")
+    e = s["kernels"]["wide_mn256<true, 64>"]
+    assert s["fetch_scale"] == 2.0 and s["write_scale"] == 1.0
+    assert e["fetch_bytes"] == 200 * 1024 * 2 and e["write_bytes"] == 50 * 1024
+    p = tmp_path / "s.json"
+    p.write_text(json.dumps(s))
+    assert profiling.traffic_for(str(p), "wide_mn256<true>/bk64") == 200 * 1024 * 2 + 50 * 1024
+    s["source_sha256"] = "0" * 64
+    p.write_text(json.dumps(s))
+    assert profiling.traffic_for(str(p), "wide_mn256<true>") is None
+
+
+def test_label_matching():
+    m = profiling.label_matches
+    assert m("wide_kd256<64>", "wide_kd256")
+    assert m("wide_mn256<true, 32>", "wide_mn256<true>/bk32")
+    assert not m("wide_mn256<false, 64>", "wide_mn256<true>")
+    assert not m("wide_gemv_n_finish<true>", "wide_gemv_n<true>")
+    assert m("wide_gemv_n<true, 4, 2>", "wide_gemv_n<true>")
+    assert m("wide_reorder_count", "wide_reorder_count")
