@@ -174,7 +174,17 @@ size_t wide_workspace_size(wide_op_t op, wide_dtype_t dt, int64_t M,
  *   "big_tiles"     1 (default): prefill GEMMs use 256x256 tiles where the
  *                   shape allows; 0: always the 128x128 tiles.
  *   "ring_bk"       k depth of a 256x256 pipeline stage: 64 (two stages,
- *                   default) or 32 (four stages).
+ *                   default) or 32 (five stages; four in the K-axis kernel).
+ *   "gemv_n_ncb", "gemv_k_ncb"
+ *                   decode: at most this many blocks of 16 output columns
+ *                   (N-axis) or rows (K-axis) per workgroup: 1, 2 or 4; 0
+ *                   (default) chooses by shape.
+ *   "gemv_n_split", "gemv_k_split"
+ *                   decode: workgroups sharing one block's reduction: 1, 2, 4
+ *                   or 8; 0 (default) chooses by shape.  A split above one
+ *                   adds a small kernel that sums the partial results.
+ *                   Workspace sizes depend on these four options: query
+ *                   wide_workspace_size after setting them.
  * Not synchronised with calls running on other host threads.
  */
 wide_status_t wide_set_option(const char* key, int64_t value);

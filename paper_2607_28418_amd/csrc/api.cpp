@@ -149,6 +149,7 @@ wide::GVNArgs ffn_gvn(int64_t M, int D, int Dff, int G, const uint8_t* mask, con
   na.n_regions = 1;
   na.reg[0] = wide::GVRegion{static_cast<const uint16_t*>(wg), static_cast<const uint16_t*>(wu), h, Dff,
                              Dff / 16, 1, 0};
+  na.swiglu = 1;
   na.k_split = wide::gemv_n_split(na);
   return na;
 }
@@ -239,6 +240,7 @@ wide::GVNArgs qkv_gvn(int64_t M, const AttnDims& d, const uint8_t* mask, const v
                              d.Nkv / 16, 0, d.Nq};
   na.reg[2] = wide::GVRegion{static_cast<const uint16_t*>(wv), nullptr, static_cast<uint16_t*>(v), d.Nkv,
                              d.Nkv / 16, 0, d.Nq + d.Nkv};
+  na.swiglu = 0;
   na.k_split = wide::gemv_n_split(na);
   return na;
 }
@@ -374,6 +376,20 @@ wide_status_t wide_set_option(const char* key, int64_t value) {
     g_big_tiles = (int)value;
     return ok();
   }
+  for (const char* k : {"gemv_n_ncb", "gemv_k_ncb"})
+    if (!strcmp(key, k)) {
+      if (value != 0 && value != 1 && value != 2 && value != 4)
+        return fail(WIDE_ERR_INVALID_ARG, "%s must be 0, 1, 2 or 4", key);
+      (key[5] == 'n' ? wide::decode_tuning().n_ncb : wide::decode_tuning().k_ncb) = (int)value;
+      return ok();
+    }
+  for (const char* k : {"gemv_n_split", "gemv_k_split"})
+    if (!strcmp(key, k)) {
+      if (value != 0 && value != 1 && value != 2 && value != 4 && value != 8)
+        return fail(WIDE_ERR_INVALID_ARG, "%s must be 0, 1, 2, 4 or 8", key);
+      (key[5] == 'n' ? wide::decode_tuning().n_split : wide::decode_tuning().k_split) = (int)value;
+      return ok();
+    }
   return fail(WIDE_ERR_INVALID_ARG, "unknown option '%s'", key);
 }
 
@@ -383,6 +399,10 @@ wide_status_t wide_get_option(const char* key, int64_t* value) {
   else if (!strcmp(key, "k_path")) *value = g_k_path;
   else if (!strcmp(key, "big_tiles")) *value = g_big_tiles;
   else if (!strcmp(key, "ring_bk")) *value = wide::get_ring_bk();
+  else if (!strcmp(key, "gemv_n_ncb")) *value = wide::decode_tuning().n_ncb;
+  else if (!strcmp(key, "gemv_n_split")) *value = wide::decode_tuning().n_split;
+  else if (!strcmp(key, "gemv_k_ncb")) *value = wide::decode_tuning().k_ncb;
+  else if (!strcmp(key, "gemv_k_split")) *value = wide::decode_tuning().k_split;
   else return fail(WIDE_ERR_INVALID_ARG, "unknown option '%s'", key);
   return ok();
 }

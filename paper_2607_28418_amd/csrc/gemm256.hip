@@ -25,14 +25,21 @@ using namespace t256;
 namespace {
 __device__ __attribute__((aligned(16))) uint16_t g_zero_blk[64];  // stays zero: never written
 
-template <int BK, class Src>
+// Rings: two stages of BK = 64 or five of BK = 32 (all of LDS); the
+// K-axis dense-masked kernel keeps 17 KB for the tile's mask bits, so four.
+template <int BK>
+using RingMN = Ring<BK, BK == 64 ? 2 : 5>;
+template <int BK>
+using RingKD = Ring<BK, BK == 64 ? 2 : 4>;
+
+template <class Rg, class Src>
 __device__ __forceinline__ void run_tile(uint16_t* smem, int nsteps, Src src, int brow0, int brow1,
                                          int live, f32x16 (&acc)[4][2]) {
   live = __builtin_amdgcn_readfirstlane(live);
   if (live == 0xF)
-    mainloop<BK, true>(smem, nsteps, src, brow0, brow1, live, acc);
+    mainloop<Rg, true>(smem, nsteps, src, brow0, brow1, live, acc);
   else
-    mainloop<BK, false>(smem, nsteps, src, brow0, brow1, live, acc);
+    mainloop<Rg, false>(smem, nsteps, src, brow0, brow1, live, acc);
 }
 }  // namespace
 
@@ -40,7 +47,7 @@ __device__ __forceinline__ void run_tile(uint16_t* smem, int nsteps, Src src, in
 template <bool SWIGLU, int BK>
 __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
-  using Rg = Ring<BK>;
+  using Rg = RingMN<BK>;
   constexpr int S = Rg::SLOTS;
   constexpr int BNO = SWIGLU ? 128 : 256;  // output columns per tile
   const uint16_t* zero = g_zero_blk;
@@ -117,7 +124,7 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
       bp[j] = bbase[j] + k0;
     }
   };
-  run_tile<BK>(smem, K / BK, src, brow0, brow1, live, acc);
+  run_tile<Rg>(smem, K / BK, src, brow0, brow1, live, acc);
 
   // Epilogue: rows back to token order; rows past cnt hold +0 accumulators.
   const int col = acc_col();
@@ -146,7 +153,7 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
   __shared__ uint32_t s_mbits[BM][kKd256MaxGroups / 32];  // mask bits of the tile's rows
   __shared__ uint16_t s_groups[kKd256MaxGroups];          // groups with an active row, ascending
   __shared__ int s_ng_live;
-  using Rg = Ring<BK>;
+  using Rg = RingKD<BK>;
   constexpr int S = Rg::SLOTS;
   const uint16_t* zero = g_zero_blk;
   const int n_tiles = a.N / BN;
@@ -213,7 +220,7 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
       bp[j] = bbase[j] + k0;
     }
   };
-  run_tile<BK>(smem, nsteps, src, brow0, brow1, live, acc);
+  run_tile<Rg>(smem, nsteps, src, brow0, brow1, live, acc);
 
   const int col = acc_col();
 #pragma unroll
@@ -232,7 +239,7 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
 template <int BK>
 __global__ __launch_bounds__(NT, 1) void wide_ks256(KArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
-  using Rg = Ring<BK>;
+  using Rg = RingMN<BK>;
   constexpr int S = Rg::SLOTS;
   const uint16_t* zero = g_zero_blk;
   const int n_tiles = a.N / BN;
@@ -277,7 +284,7 @@ __global__ __launch_bounds__(NT, 1) void wide_ks256(KArgs a) {
       bp[j] = bbase[j] + k0;
     }
   };
-  run_tile<BK>(smem, a.G / BK, src, brow0, brow1, live, acc);
+  run_tile<Rg>(smem, a.G / BK, src, brow0, brow1, live, acc);
 
   const int col = acc_col();
 #pragma unroll
@@ -299,15 +306,15 @@ namespace {
 int g_ring_bk = 64;
 
 template <class F>
-hipError_t allow_big_lds(F* f) {
+hipError_t allow_big_lds(F* f, int bytes) {
   return hipFuncSetAttribute(reinterpret_cast<const void*>(f),
-                             hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
+                             hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
 }
 
 // Raise the dynamic-LDS limit of one kernel instance once per process.
-template <auto Kern>
+template <auto Kern, int Bytes>
 hipError_t prepare() {
-  static const hipError_t e = allow_big_lds(Kern);
+  static const hipError_t e = allow_big_lds(Kern, Bytes);
   return e;
 }
 }  // namespace
@@ -315,14 +322,14 @@ hipError_t prepare() {
 void set_ring_bk(int bk) { g_ring_bk = bk; }
 int get_ring_bk() { return g_ring_bk; }
 
-#define WIDE_RING_LAUNCH(NAME, KT, GRID, STREAM, ARGS)                                  \
-  do {                                                                                  \
-    hipError_t e_ = g_ring_bk == 32 ? prepare<KT(32)>() : prepare<KT(64)>();            \
-    if (e_ != hipSuccess) return e_;                                                    \
-    if (g_ring_bk == 32)                                                                \
-      WIDE_LAUNCH_NAMED(NAME "/bk32", (KT(32)), dim3(GRID), dim3(NT), LDS_BYTES, STREAM, ARGS); \
-    else                                                                                \
-      WIDE_LAUNCH_NAMED(NAME "/bk64", (KT(64)), dim3(GRID), dim3(NT), LDS_BYTES, STREAM, ARGS); \
+#define WIDE_RING_LAUNCH(NAME, KT, RG, GRID, STREAM, ARGS)                                        \
+  do {                                                                                            \
+    hipError_t e_ = g_ring_bk == 32 ? prepare<KT(32), RG<32>::LDS>() : prepare<KT(64), RG<64>::LDS>(); \
+    if (e_ != hipSuccess) return e_;                                                              \
+    if (g_ring_bk == 32)                                                                          \
+      WIDE_LAUNCH_NAMED(NAME "/bk32", (KT(32)), dim3(GRID), dim3(NT), RG<32>::LDS, STREAM, ARGS); \
+    else                                                                                          \
+      WIDE_LAUNCH_NAMED(NAME "/bk64", (KT(64)), dim3(GRID), dim3(NT), RG<64>::LDS, STREAM, ARGS); \
   } while (0)
 
 #define MN_SW(bk) wide_mn256<true, bk>
@@ -335,9 +342,9 @@ hipError_t launch_mn256(const MN256Args& a, bool swiglu, hipStream_t s) {
   for (int i = 0; i < a.n_regions; ++i) total += a.reg[i].tiles;
   if (total == 0) return hipSuccess;
   if (swiglu)
-    WIDE_RING_LAUNCH("wide_mn256<true>", MN_SW, (unsigned)total, s, a);
+    WIDE_RING_LAUNCH("wide_mn256<true>", MN_SW, RingMN, (unsigned)total, s, a);
   else
-    WIDE_RING_LAUNCH("wide_mn256<false>", MN_PL, (unsigned)total, s, a);
+    WIDE_RING_LAUNCH("wide_mn256<false>", MN_PL, RingMN, (unsigned)total, s, a);
   return hipGetLastError();
 }
 
@@ -348,7 +355,7 @@ hipError_t launch_kd256(const KArgs& a, hipStream_t s) {
   if (a.K / a.G > kKd256MaxGroups) return hipErrorInvalidValue;
   hipError_t e = launch_tile_union(a.mask, a.M, a.K / a.G, BM, a.tile_union, s);
   if (e != hipSuccess) return e;
-  WIDE_RING_LAUNCH("wide_kd256", KD, (unsigned)total, s, a);
+  WIDE_RING_LAUNCH("wide_kd256", KD, RingKD, (unsigned)total, s, a);
   return hipGetLastError();
 }
 
@@ -356,7 +363,7 @@ hipError_t launch_ks256(const KArgs& a, hipStream_t s) {
   const int64_t m_tiles = (a.M + BM - 1) / BM;
   const int64_t total = (int64_t)(a.K / a.G) * m_tiles * (a.N / BN);
   if (total == 0) return hipSuccess;
-  WIDE_RING_LAUNCH("wide_ks256", KS, (unsigned)total, s, a);
+  WIDE_RING_LAUNCH("wide_ks256", KS, RingMN, (unsigned)total, s, a);
   return hipGetLastError();
 }
 

@@ -12,14 +12,14 @@
 //         output columns of one group; its 8 waves take turns over the
 //         64-wide steps of the reduction dimension K.  If no token of the
 //         batch is active in the group, the workgroup writes +0 and exits
-//         before touching a weight byte.  Otherwise lane l streams 32
-//         contiguous bytes of weight row l%16 per k step (four lanes cover a
-//         128-byte line), two steps of NCB blocks at a time together with the
-//         matching activations, which ride along as the other MFMA operand
-//         (16x16x32,
-//         tokens as rows); both operands use the same permutation of k inside
-//         a step, so the sum is unchanged.  Inactive (token, group) outputs
-//         are +0.
+//         before touching a weight byte.  Otherwise, per 64-wide k step,
+//         lane l reads two 16-byte pieces of weight row l%16, at bytes
+//         16*(l/16) and 64 + 16*(l/16) of the row's 128-byte line, so each
+//         load instruction covers whole 64-byte halves of 16 lines.  The
+//         matching activations ride along as the other MFMA operand
+//         (16x16x32, tokens as rows) with the same k order, so the sum is
+//         unchanged.  Two register sets keep about two steps of NCB blocks in
+//         flight per lane.  Inactive (token, group) outputs are +0.
 //
 // gemv_k  (K-axis: down, O).  A workgroup owns 16*NCB output rows n and a
 //         share of the k steps of the union groups (k_split workgroups per row
@@ -81,6 +81,30 @@ __device__ __forceinline__ void reduce_out(float (*red)[kDecodeMaxB][16], const 
   }
 }
 
+// A wave's k steps as a software pipeline over D register sets: the loads
+// of step q+D go out right after step q's MFMAs, so D steps of weights stay
+// in flight per lane for the whole loop (loading a few steps and then
+// multiplying them drains the memory pipeline at every iteration).  D is
+// as large as about 160 registers of staging allow, from 2 to 4.
+template <class Regs, class Load, class Mma>
+__device__ __forceinline__ void stream_steps(int n, Load load, Mma mma) {
+  constexpr int per = (int)(sizeof(Regs) / 4);
+  constexpr int D = 160 / per >= 4 ? 4 : 160 / per >= 3 ? 3 : 2;
+  Regs r[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j)
+    if (j < n) load(j, r[j]);
+  for (int q = 0; q < n; q += D) {
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+      if (q + j < n) {
+        mma(r[j]);
+        if (q + j + D < n) load(q + j + D, r[j]);
+      }
+    }
+  }
+}
+
 __device__ __host__ __forceinline__ int gv_total_cols(const GVNArgs& a) {
   int n = 0;
   for (int i = 0; i < a.n_regions; ++i) n += a.reg[i].n_blocks * 16;
@@ -120,7 +144,6 @@ __global__ __launch_bounds__(256) void wide_gemv_n_finish(GVNArgs a) {
 template <bool SWIGLU, int NTB, int NCB>
 __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
   constexpr int NV = SWIGLU ? 2 : 1;
-  constexpr int UN = 2;  // k steps in flight (NCB blocks of weights each)
   __shared__ float red[NW / 2 * NV][kDecodeMaxB][16];
   __shared__ int any_active;
 
@@ -165,8 +188,8 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
   const uint16_t* wrow[NCB][NV];
 #pragma unroll
   for (int c = 0; c < NCB; ++c) {
-    wrow[c][0] = R.w0 + (int64_t)(n0 + c * 16 + ln) * K + lq * 16;
-    if (SWIGLU) wrow[c][NV - 1] = R.w1 + (int64_t)(n0 + c * 16 + ln) * K + lq * 16;
+    wrow[c][0] = R.w0 + (int64_t)(n0 + c * 16 + ln) * K + lq * 8;
+    if (SWIGLU) wrow[c][NV - 1] = R.w1 + (int64_t)(n0 + c * 16 + ln) * K + lq * 8;
   }
   const uint16_t* xrow[NTB];
   bool xon[NTB];
@@ -174,7 +197,7 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
   for (int tb = 0; tb < NTB; ++tb) {
     const int b = tb * 16 + ln;
     xon[tb] = b < B;
-    xrow[tb] = a.x + (int64_t)(xon[tb] ? b : 0) * K + lq * 16;
+    xrow[tb] = a.x + (int64_t)(xon[tb] ? b : 0) * K + lq * 8;
   }
 
   f32x4 acc[NCB][NV][NTB];
@@ -195,12 +218,12 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
 #pragma unroll
       for (int v = 0; v < NV; ++v) {
         r.w[c][v][0] = ldg16(wrow[c][v] + k);
-        r.w[c][v][1] = ldg16(wrow[c][v] + k + 8);
+        r.w[c][v][1] = ldg16(wrow[c][v] + k + 32);
       }
 #pragma unroll
     for (int tb = 0; tb < NTB; ++tb) {
       r.x[tb][0] = xon[tb] ? ldg16(xrow[tb] + k) : u32x4{0, 0, 0, 0};
-      r.x[tb][1] = xon[tb] ? ldg16(xrow[tb] + k + 8) : u32x4{0, 0, 0, 0};
+      r.x[tb][1] = xon[tb] ? ldg16(xrow[tb] + k + 32) : u32x4{0, 0, 0, 0};
     }
   };
   auto mma = [&](const Regs& r) {
@@ -214,19 +237,7 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
           acc[c][v][tb] = mfma16(r.x[tb][1], r.w[c][v][1], acc[c][v][tb]);
         }
   };
-  int q = 0;
-  for (; q + UN <= my_steps; q += UN) {
-    Regs r[UN];
-#pragma unroll
-    for (int s2 = 0; s2 < UN; ++s2) load((s_beg + w + (q + s2) * NW) * 64, r[s2]);
-#pragma unroll
-    for (int s2 = 0; s2 < UN; ++s2) mma(r[s2]);
-  }
-  for (; q < my_steps; ++q) {
-    Regs r;
-    load((s_beg + w + q * NW) * 64, r);
-    mma(r);
-  }
+  stream_steps<Regs>(my_steps, [&](int q, Regs& r) { load((s_beg + w + q * NW) * 64, r); }, mma);
   // C[row = token (lane/16)*4 + i][col = lane%16], one column block at a time
 #pragma unroll
   for (int c = 0; c < NCB; ++c) {
@@ -248,7 +259,6 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
 
 template <int NTB, int NCB>
 __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
-  constexpr int UK = 2;  // k steps in flight
   __shared__ float red[NW / 2][kDecodeMaxB][16];
   __shared__ unsigned long long s_act[4096];  // bit b: token b active in group g
   __shared__ uint16_t ulist[4096];
@@ -303,13 +313,13 @@ __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
     for (int i = 0; i < NTB; ++i) acc[c][i] = f32x4{0.f, 0.f, 0.f, 0.f};
   const uint16_t* wrow[NCB];
 #pragma unroll
-  for (int c = 0; c < NCB; ++c) wrow[c] = a.w + (int64_t)(n0 + c * 16 + ln) * K + lq * 16;
+  for (int c = 0; c < NCB; ++c) wrow[c] = a.w + (int64_t)(n0 + c * 16 + ln) * K + lq * 8;
   const uint16_t* xrow[NTB];
   int tok[NTB];
 #pragma unroll
   for (int tb = 0; tb < NTB; ++tb) {
     tok[tb] = tb * 16 + ln;
-    xrow[tb] = a.a + (int64_t)(tok[tb] < B ? tok[tb] : 0) * K + lq * 16;
+    xrow[tb] = a.a + (int64_t)(tok[tb] < B ? tok[tb] : 0) * K + lq * 8;
   }
 
   struct Regs {
@@ -324,13 +334,13 @@ __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
 #pragma unroll
     for (int c = 0; c < NCB; ++c) {
       r.w[c][0] = ldg16(wrow[c] + k);
-      r.w[c][1] = ldg16(wrow[c] + k + 8);
+      r.w[c][1] = ldg16(wrow[c] + k + 32);
     }
 #pragma unroll
     for (int tb = 0; tb < NTB; ++tb) {
       const bool on = tok[tb] < B && ((act >> tok[tb]) & 1ull);  // inactive blocks are never read
       r.x[tb][0] = on ? ldg16(xrow[tb] + k) : u32x4{0, 0, 0, 0};
-      r.x[tb][1] = on ? ldg16(xrow[tb] + k + 8) : u32x4{0, 0, 0, 0};
+      r.x[tb][1] = on ? ldg16(xrow[tb] + k + 32) : u32x4{0, 0, 0, 0};
     }
   };
   auto mma = [&](const Regs& r) {
@@ -342,19 +352,7 @@ __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
         acc[c][tb] = mfma16(r.x[tb][1], r.w[c][1], acc[c][tb]);
       }
   };
-  int q = 0;
-  for (; q + UK <= my_steps; q += UK) {
-    Regs r[UK];
-#pragma unroll
-    for (int s2 = 0; s2 < UK; ++s2) load(q + s2, r[s2]);
-#pragma unroll
-    for (int s2 = 0; s2 < UK; ++s2) mma(r[s2]);
-  }
-  for (; q < my_steps; ++q) {
-    Regs r;
-    load(q, r);
-    mma(r);
-  }
+  stream_steps<Regs>(my_steps, load, mma);
 #pragma unroll
   for (int c = 0; c < NCB; ++c) {
     f32x4 one[1][NTB];
@@ -390,6 +388,8 @@ hipError_t gemv_n_launch(const GVNArgs& a, int nb, hipStream_t s) {
     WIDE_LAUNCH_NAMED(name, (wide_gemv_n<SW, 1, NCB>), dim3(grid), dim3(NT), 0, s, a);
   else if (a.B <= 32)
     WIDE_LAUNCH_NAMED(name, (wide_gemv_n<SW, 2, NCB>), dim3(grid), dim3(NT), 0, s, a);
+  else if constexpr (SW && NCB == 4)
+    return hipErrorInvalidValue;  // not instantiated: gemv_n_ncb never picks it
   else
     WIDE_LAUNCH_NAMED(name, (wide_gemv_n<SW, 4, NCB>), dim3(grid), dim3(NT), 0, s, a);
   hipError_t e = hipGetLastError();
@@ -416,15 +416,30 @@ hipError_t gemv_k_launch(const GVKArgs& a, hipStream_t s) {
 }
 }  // namespace
 
-// Column blocks per workgroup: four when every region divides into runs of
-// four blocks inside one group (measured: 64 columns per workgroup cut the
-// activation re-reads and ran gate/up at ~5 TB/s), else two, else one.
+DecodeTuning& decode_tuning() {
+  static DecodeTuning t{0, 0, 0, 0};
+  return t;
+}
+
+// Column blocks per workgroup: the most (4, 2 or 1) that divide every region
+// into runs inside one group and still leave at least 160 runs, so that the
+// chip is busy without a k split.  Measured on MI355X (B = 32, Llama-3-8B
+// projections): 64 columns per workgroup ran gate/up fastest even at 224
+// workgroups (activation re-reads fall with the run width), and Q/K/V at
+// 32 columns and no split beat 64 columns with a split plus its finishing
+// kernel.
 int gemv_n_ncb(const GVNArgs& a) {
+  const int forced = decode_tuning().n_ncb;
+  int nb = 0;
+  for (int i = 0; i < a.n_regions; ++i) nb += a.reg[i].n_blocks;
   for (int ncb : {4, 2}) {
+    if (forced && ncb > forced) continue;
+    // gate/up at more than 32 tokens: four blocks would not fit the registers
+    if (ncb == 4 && a.swiglu && a.B > 32) continue;
     if ((a.G / 16) % ncb) continue;
     bool ok = true;
     for (int i = 0; i < a.n_regions; ++i) ok = ok && a.reg[i].n_blocks % ncb == 0;
-    if (ok) return ncb;
+    if (ok && (forced || nb / ncb >= 160)) return ncb;
   }
   return 1;
 }
@@ -432,13 +447,45 @@ int gemv_n_ncb(const GVNArgs& a) {
 // Split of the k steps over workgroups.  A split costs a finishing kernel
 // (~6 us on MI355X), which only pays when the column runs alone leave most
 // CUs idle: split (at most 8 ways, at least 4 k steps per share) until there
-// are 192 workgroups.
+// are 160 workgroups.
 int gemv_n_split(const GVNArgs& a) {
   int nb = 0;
   for (int i = 0; i < a.n_regions; ++i) nb += a.reg[i].n_blocks;
   const int runs = nb / gemv_n_ncb(a);
   int ks = 1;
-  while (runs * ks < 192 && ks < 8 && a.K / 64 / (2 * ks) >= 4) ks *= 2;
+  const int forced = decode_tuning().n_split;
+  if (forced) {
+    while (ks < forced && a.K / 64 / (2 * ks) >= 1) ks *= 2;
+    return ks;
+  }
+  while (runs * ks < 160 && ks < 8 && a.K / 64 / (2 * ks) >= 4) ks *= 2;
+  return ks;
+}
+
+// Output rows per workgroup (16 * ncb): one block, unless that leaves fewer
+// than 192 workgroups.  Measured on MI355X (B = 32): 16 rows per workgroup
+// and no split read O and down fastest, ahead of wider blocks with a split
+// and its finishing kernel.
+int gemv_k_ncb(int N) {
+  const int forced = decode_tuning().k_ncb;
+  if (forced) {
+    for (int ncb : {4, 2})
+      if (ncb <= forced && N % (16 * ncb) == 0) return ncb;
+    return 1;
+  }
+  if (N / 16 >= 192) return 1;
+  for (int ncb : {4, 2})
+    if (N % (16 * ncb) == 0) return ncb;
+  return 1;
+}
+
+// Split the union steps until there are 192 workgroups (at most 8 ways).
+int gemv_k_split(int N) {
+  const int row_blocks = N / (16 * gemv_k_ncb(N));
+  const int forced = decode_tuning().k_split;
+  if (forced) return forced;
+  int ks = 1;
+  while (row_blocks * ks < 192 && ks < 8) ks *= 2;
   return ks;
 }
 
@@ -461,9 +508,10 @@ hipError_t launch_gemv_n(const GVNArgs& a, bool swiglu, hipStream_t s) {
 
 hipError_t launch_gemv_k(const GVKArgs& a, hipStream_t s) {
   if (a.B == 0 || a.N == 0) return hipSuccess;
-  // 64 output rows per workgroup when N allows, the union steps split over
+  // 16 * gemv_k_ncb output rows per workgroup, the union steps split over
   // k_split workgroups (chosen by the host, partials in a.part).
-  hipError_t e = a.N % 64 == 0 ? gemv_k_launch<4>(a, s) : gemv_k_launch<1>(a, s);
+  const int ncb = gemv_k_ncb(a.N);
+  hipError_t e = ncb == 4 ? gemv_k_launch<4>(a, s) : ncb == 2 ? gemv_k_launch<2>(a, s) : gemv_k_launch<1>(a, s);
   if (e != hipSuccess || a.k_split == 1) return e;
   const int64_t n = (int64_t)a.B * a.N;
   WIDE_LAUNCH(wide_gemv_k_finish, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a.part, a.k_split,

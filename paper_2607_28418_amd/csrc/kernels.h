@@ -124,6 +124,7 @@ struct GVNArgs {
   GVRegion reg[3];
   int k_split;         // workgroups sharing one column run's k steps
   float* part;         // [k_split][NV][B][total columns] partials when k_split > 1
+  int swiglu;          // gate/up pair + SwiGLU (NV = 2) rather than plain columns
 };
 // Decode N-axis split: enough workgroups to fill the chip (see gemv.hip).
 int gemv_n_split(const GVNArgs& a);
@@ -139,12 +140,17 @@ struct GVKArgs {
   float* part;         // [k_split][B][N] partial sums when k_split > 1
 };
 // Split of the decode K-axis product: enough workgroups to fill the chip.
-inline int gemv_k_split(int N) {
-  const int row_blocks = N % 64 == 0 ? N / 64 : N / 16;
-  int ks = 1;
-  while (row_blocks * ks < 256 && ks < 8) ks *= 2;
-  return ks;
-}
+// Decode K-axis: output rows per workgroup (16 * gemv_k_ncb) and the split of
+// the union steps over workgroups (see gemv.hip).
+int gemv_k_ncb(int N);
+int gemv_k_split(int N);
+
+// Decode tuning overrides, 0 = automatic (wide_set_option keys gemv_n_ncb,
+// gemv_n_split, gemv_k_ncb, gemv_k_split).
+struct DecodeTuning {
+  int n_ncb, n_split, k_ncb, k_split;
+};
+DecodeTuning& decode_tuning();
 
 constexpr int kDecodeMaxB = 64;
 

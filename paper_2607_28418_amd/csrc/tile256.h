@@ -7,8 +7,9 @@
 // moves 1 KB, lane i landing at byte 16*i of the destination.  A stage holds
 // A [256 rows][BK] and B [256 rows][BK] in bf16; NS stages of 128 KB in total
 // form a ring, so the loads of step k+NS-1 are in flight while step k is
-// multiplied.  Two shapes of the ring are compiled: BK = 64 x 2 stages and
-// BK = 32 x 4 stages (deeper prefetch, twice the barriers).
+// multiplied.  Two shapes of the ring are compiled: BK = 64 x 2 stages
+// (128 KB) and BK = 32 x 4 or 5 stages (128 or 160 KB: a prefetch distance
+// of 96 or 128 k instead of 64, at twice the barriers).
 //
 // LDS layout: a row of BK bf16 is BK/8 chunks of 16 bytes.  Logical chunk c
 // of row r sits at physical chunk c ^ f(r).  A 128-bit LDS read is served 16
@@ -33,20 +34,22 @@ namespace wide {
 namespace t256 {
 
 constexpr int BM = 256, BN = 256, NT = 512;
-constexpr int LDS_BYTES = 131072;
+constexpr int LDS_MAX = 163840;  // bytes of LDS one workgroup may use on gfx950
 
 typedef const void __attribute__((address_space(1)))* gptr_t;
 typedef void __attribute__((address_space(3)))* lptr_t;
 
-template <int BK>
+template <int BK_, int NS_>
 struct Ring {
+  static constexpr int BK = BK_;
+  static constexpr int NS = NS_;                  // stages in the ring
   static constexpr int CPR = BK / 8;              // 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;            // rows per wave load instruction
   static constexpr int SLOTS = BM / (8 * RPI);    // load slots per lane per operand
   static constexpr int A_ELEMS = BM * BK;
   static constexpr int STAGE = (BM + BN) * BK;    // bf16 elements per stage
-  static constexpr int NS = LDS_BYTES / (STAGE * 2);
-  static_assert(NS >= 2 && NS <= 4, "ring of two to four stages");
+  static constexpr int LDS = NS * STAGE * 2;      // bytes
+  static_assert(NS >= 2 && NS <= 5 && LDS <= LDS_MAX, "ring of two to five stages");
 
   __device__ static __forceinline__ int f(int row) {
     return CPR == 8 ? ((row & 7) ^ ((row >> 3) & 1)) : ((row >> 2) & 3);
@@ -87,52 +90,72 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// MFMAs of one stage.  B fragment rows brow0/brow1; A fragment fm covers rows
-// wm*128 + fm*32 + lane%32 and is skipped unless bit fm of `live` is set
-// (FULL: all four live, no test).  mid() runs after the first half of the
-// sub-steps (the loop uses it to issue the second half of the next step's
-// loads).
-template <int BK, bool FULL, class Mid>
-__device__ __forceinline__ void mma_stage(const uint16_t* stage, int brow0, int brow1, int live,
-                                          f32x16 (&acc)[4][2], Mid mid) {
-  using Rg = Ring<BK>;
-  constexpr int KK = BK / 16;
+// Workgroup barrier after this wave's LDS reads have returned.  Unlike
+// __syncthreads() it does not wait for the wave's outstanding global loads,
+// so the deeper stages of the ring stay in flight across it; the memory
+// clobber keeps the compiler from moving LDS accesses or loads across it.
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// One 16-wide k sub-step of this wave's operands: B fragment rows brow0 and
+// brow1, A fragment fm covering tile rows wm*128 + fm*32 + lane%32.
+struct Frags {
+  u32x4 a[4];
+  u32x4 b0, b1;
+};
+
+template <class Rg>
+__device__ __forceinline__ void read_frags(const uint16_t* stage, int kk, int brow0, int brow1,
+                                           Frags& f) {
   const int lane = lane_id();
   const int wm = wave_id() >> 2;
   const int l32 = lane & 31, lhi = lane >> 5;
+  const int ch = kk * 2 + lhi;
   const uint16_t* As = stage;
   const uint16_t* Bs = stage + Rg::A_ELEMS;
+  f.b0 = *reinterpret_cast<const u32x4*>(&Bs[Rg::swz(brow0, ch)]);
+  f.b1 = *reinterpret_cast<const u32x4*>(&Bs[Rg::swz(brow1, ch)]);
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk) {
-    const int ch = kk * 2 + lhi;
-    const u32x4 b0 = *reinterpret_cast<const u32x4*>(&Bs[Rg::swz(brow0, ch)]);
-    const u32x4 b1 = *reinterpret_cast<const u32x4*>(&Bs[Rg::swz(brow1, ch)]);
-    u32x4 a[4];
+  for (int fm = 0; fm < 4; ++fm)
+    f.a[fm] = *reinterpret_cast<const u32x4*>(&As[Rg::swz(wm * 128 + fm * 32 + l32, ch)]);
+}
+
+// A fragment is skipped unless bit fm of `live` is set (FULL: all four live,
+// no test).
+template <bool FULL, int F0 = 0, int F1 = 4>
+__device__ __forceinline__ void mma_frags(const Frags& f, int live, f32x16 (&acc)[4][2]) {
 #pragma unroll
-    for (int fm = 0; fm < 4; ++fm)
-      a[fm] = *reinterpret_cast<const u32x4*>(&As[Rg::swz(wm * 128 + fm * 32 + l32, ch)]);
-#pragma unroll
-    for (int fm = 0; fm < 4; ++fm) {
-      if (FULL || (live & (1 << fm))) {
-        acc[fm][0] = mfma32(a[fm], b0, acc[fm][0]);
-        acc[fm][1] = mfma32(a[fm], b1, acc[fm][1]);
-      }
+  for (int fm = F0; fm < F1; ++fm) {
+    if (FULL || (live & (1 << fm))) {
+      acc[fm][0] = mfma32(f.a[fm], f.b0, acc[fm][0]);
+      acc[fm][1] = mfma32(f.a[fm], f.b1, acc[fm][1]);
     }
-    if (kk == KK / 2 - 1) mid();
   }
 }
 
 // The pipelined k loop over `nsteps` steps.  src(s, a, b) fills the lane's
 // source pointers of step s.  Every wave issues LOADS_PER_STEP loads per
 // step, so "step s has landed" is a vmcnt bound on the younger steps.
-template <int BK, bool FULL, class Src>
+//
+// Schedule of step kt (KK = BK/16 sub-steps):
+//   - the loads of step kt+NS-1 go out into the stage that step kt-1 used
+//     (with two stages all at once, the stage must land within one step;
+//     with more, spread over the sub-steps);
+//   - sub-step kk issues the LDS reads of sub-step kk+1 after its first two
+//     MFMAs and before the other six, so LDS latency hides behind the matrix
+//     core;
+//   - at the last sub-step the wave waits for step kt+1, meets the others at
+//     the barrier (which also retires every read of step kt's stage) and
+//     reads step kt+1's first fragments between its first two and its last
+//     six MFMAs: the barrier wait overlaps the MFMAs already in the pipe.
+template <class Rg, bool FULL, class Src>
 __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Src src, int brow0, int brow1,
                                          int live, f32x16 (&acc)[4][2]) {
-  using Rg = Ring<BK>;
-  constexpr int NS = Rg::NS, L = Rg::LOADS_PER_STEP;
-  auto issue = [&](int s) {
-    const uint16_t* ap[Rg::SLOTS];
-    const uint16_t* bp[Rg::SLOTS];
+  constexpr int NS = Rg::NS, L = Rg::LOADS_PER_STEP, S = Rg::SLOTS, KK = Rg::BK / 16;
+  auto issue_all = [&](int s) {
+    const uint16_t* ap[S];
+    const uint16_t* bp[S];
     src(s, ap, bp);
     Rg::issue(smem + (s % NS) * Rg::STAGE, ap, bp);
   };
@@ -141,32 +164,50 @@ __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Src src, in
     const int younger = last - s;  // 0 .. NS-2 steps issued after step s
     if (NS == 2 || younger <= 0) wait_vm<0>();
     else if (younger == 1) wait_vm<L>();
-    else wait_vm<2 * L>();
+    else if (NS == 3 || younger == 2) wait_vm<2 * L>();
+    else wait_vm<3 * L>();
   };
   if (nsteps <= 0) return;
   const int pro = min(NS - 1, nsteps);
-  for (int s = 0; s < pro; ++s) issue(s);
+  for (int s = 0; s < pro; ++s) issue_all(s);
   wait_step(0, pro - 1);
-  __syncthreads();
-  // The next step's loads go out in two halves, one before the MFMAs and one
-  // half-way through them: this spreads the memory requests over the step
-  // and measured about 10% faster than issuing them in one burst.
-  constexpr int S = Rg::SLOTS;
+  stage_barrier();
+  // Sub-step kk works on fr[kk & 1] and fills fr[(kk + 1) & 1]; KK is even,
+  // so the parity carries over from one step to the next without copies.
+  static_assert(KK % 2 == 0, "even number of sub-steps");
+  Frags fr[2];
+  read_frags<Rg>(smem, 0, brow0, brow1, fr[0]);
   for (int kt = 0; kt < nsteps; ++kt) {
     const int nxt = kt + NS - 1;
     const bool more = nxt < nsteps;
     const uint16_t* ap[S];
     const uint16_t* bp[S];
     uint16_t* nstage = smem + (nxt % NS) * Rg::STAGE;
-    if (more) {
-      src(nxt, ap, bp);
-      Rg::issue(nstage, ap, bp, 0, S / 2);
+    const uint16_t* cstage = smem + (kt % NS) * Rg::STAGE;
+    if (more) src(nxt, ap, bp);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      if (more) {
+        if (NS == 2) {
+          if (kk == 0) Rg::issue(nstage, ap, bp);
+        } else {
+          Rg::issue(nstage, ap, bp, kk * S / KK, (kk + 1) * S / KK);
+        }
+      }
+      // The first two MFMAs go out before the next fragment reads (and
+      // before the barrier), so the matrix core is busy while they wait.
+      mma_frags<FULL, 0, 1>(fr[kk & 1], live, acc);
+      __builtin_amdgcn_sched_barrier(0);
+      if (kk + 1 < KK) {
+        read_frags<Rg>(cstage, kk + 1, brow0, brow1, fr[(kk + 1) & 1]);
+      } else if (kt + 1 < nsteps) {
+        wait_step(kt + 1, min(nxt, nsteps - 1));
+        stage_barrier();
+        read_frags<Rg>(smem + ((kt + 1) % NS) * Rg::STAGE, 0, brow0, brow1, fr[0]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      mma_frags<FULL, 1, 4>(fr[kk & 1], live, acc);
     }
-    mma_stage<BK, FULL>(smem + (kt % NS) * Rg::STAGE, brow0, brow1, live, acc, [&]() {
-      if (more) Rg::issue(nstage, ap, bp, S / 2, S);
-    });
-    if (kt + 1 < nsteps) wait_step(kt + 1, min(nxt, nsteps - 1));
-    __syncthreads();
   }
 }
 
