@@ -304,6 +304,43 @@ def main():
 
         n_rep = max(5, args.steps // 2)
         d_pre = timeit(lambda: dense_run("prefill"), n_rep)
+        # per operator, prefill: hipBLASLt GEMMs (and the SwiGLU elementwise a
+        # dense layer needs) against the library's calls / kernels
+        b, o = bd["prefill"], bufs["prefill"]
+        hg = F.linear(b["x_ffn"], w["w_gate"])
+        hu = F.linear(b["x_ffn"], w["w_up"])
+        hh = F.silu(hg) * hu
+        dense_ops = {
+            "qkv": timeit(lambda: (F.linear(b["x_attn"], w["w_q"]), F.linear(b["x_attn"], w["w_k"]),
+                                   F.linear(b["x_attn"], w["w_v"])), n_rep),
+            "o": timeit(lambda: F.linear(b["a"], w["w_o"]), n_rep),
+            "gate_up": timeit(lambda: (F.linear(b["x_ffn"], w["w_gate"]), F.linear(b["x_ffn"], w["w_up"])), n_rep),
+            "swiglu_elementwise": timeit(lambda: F.silu(hg) * hu, n_rep),
+            "down": timeit(lambda: F.linear(hh, w["w_down"]), n_rep),
+        }
+        del hg, hu, hh
+        ia, ca = W.wide_mask_reorder(b["mask_attn"], o["idx_a"], o["cnt_a"], ws=o["ws"])
+        fi, fc = W.wide_mask_reorder(b["mask_ffn"], o["idx_f"], o["cnt_f"], ws=o["ws"])
+        wide_ops = {
+            "reorders": timeit(lambda: (W.wide_mask_reorder(b["mask_attn"], o["idx_a"], o["cnt_a"], ws=o["ws"]),
+                                        W.wide_mask_reorder(b["mask_ffn"], o["idx_f"], o["cnt_f"], ws=o["ws"])),
+                               n_rep),
+            "qkv": timeit(lambda: W.wide_qkvo_masked(W.PHASE_QKV, b["x_attn"], b["mask_attn"], L.Ga, L.nq, L.nkv,
+                                                     L.hd, w_q=w["w_q"], w_k=w["w_k"], w_v=w["w_v"], idx=ia,
+                                                     counts=ca, q=o["q"], k=o["k"], v=o["v"], ws=o["ws"]), n_rep),
+            "o": timeit(lambda: W.wide_qkvo_masked(W.PHASE_O, b["a"], b["mask_attn"], L.Ga, L.nq, L.nkv, L.hd,
+                                                   w_o=w["w_o"], idx=ia, counts=ca, y=o["y_o"], ws=o["ws"]), n_rep),
+            "ffn": timeit(lambda: W.wide_ffn_masked(b["x_ffn"], w["w_gate"], w["w_up"], w["w_down"],
+                                                    b["mask_ffn"], L.G, idx=fi, counts=fc, y=o["y_f"],
+                                                    ws=o["ws"]), n_rep),
+        }
+        per_op = dict(dense_ms={k: round(v, 4) for k, v in dense_ops.items()},
+                      wide_ms={k: round(v, 4) for k, v in wide_ops.items()},
+                      speedup={"qkv": round(dense_ops["qkv"] / wide_ops["qkv"], 3),
+                               "o": round(dense_ops["o"] / wide_ops["o"], 3),
+                               "ffn_gemms_only": round((dense_ops["gate_up"] + dense_ops["down"]) / wide_ops["ffn"], 3),
+                               "ffn_with_elementwise": round((dense_ops["gate_up"] + dense_ops["swiglu_elementwise"]
+                                                              + dense_ops["down"]) / wide_ops["ffn"], 3)})
         dense_graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(dense_graph):
             dense_run("decode")
@@ -315,7 +352,8 @@ def main():
             run("decode", ones["decode"])
         o_dec = timeit(ones_graph.replay, n_rep)
         dense = dict(hipblaslt_prefill_ms=round(d_pre, 4), hipblaslt_decode_ms=round(d_dec, 4),
-                     ones_mask_prefill_ms=round(o_pre, 4), ones_mask_decode_ms=round(o_dec, 4))
+                     ones_mask_prefill_ms=round(o_pre, 4), ones_mask_decode_ms=round(o_dec, 4),
+                     prefill_per_op=per_op)
         best_pre, best_dec = min(d_pre, o_pre), min(d_dec, o_dec)
         prefill["speedup_vs_dense"] = round(best_pre / pre_ms, 3)
         prefill["frac_of_ideal"] = round(best_pre / pre_ms / prefill["ideal_speedup"], 3)
