@@ -208,7 +208,7 @@ def main():
     pre_ms = float(np.median([a.elapsed_time(b_) for a, b_, _ in marks]))
     dec_ms = float(np.median([b_.elapsed_time(c) for _, b_, c in marks]))
     kernels = {}
-    for name in ("wide_reorder_count", "wide_reorder_scan", "wide_reorder_scatter", "wide_mn256<true>",
+    for name in ("wide_reorder_fused", "wide_reorder_count", "wide_reorder_scan", "wide_reorder_scatter", "wide_mn256<true>",
                  "wide_mn256<false>", "wide_kd256", "wide_ks256", "wide_gemm_mn<true>", "wide_gemm_mn<false>",
                  "wide_gemm_k_dense_masked", "wide_gemm_k_scatter", "wide_tile_union", "wide_zero_f32",
                  "wide_f32_to_bf16", "wide_gemv_n<true>", "wide_gemv_n<false>", "wide_gemv_k"):

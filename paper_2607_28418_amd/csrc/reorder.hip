@@ -5,7 +5,8 @@
 // Algorithm 1).  With ties kept in token order this is a stable partition:
 // idx[g][0:cnt[g]] = active tokens ascending, idx[g][cnt[g]:M] = the rest.
 //
-// Three short kernels, no host synchronisation.  The mask is cut into chunks
+// Up to 32768 tokens a single kernel does it (wide_reorder_fused, below).
+// Beyond, three short kernels, no host synchronisation.  The mask is cut into chunks
 // of 64 tokens, one wave each (one token per lane):
 //   count    the chunk's mask rows (64 x n_groups bytes, contiguous in
 //            memory) are staged in LDS with coalesced loads, in slabs of 512
@@ -150,13 +151,82 @@ __global__ __launch_bounds__(kChunk) void wide_reorder_scatter(const uint8_t* __
   }
 }
 
+// Single-kernel variant for M <= 32768: one workgroup of 1024 threads per
+// group.  Thread tid owns tokens i*1024 + tid (i < 32); their mask bytes are
+// loaded up front into a bit set, so the only memory latency is one round of
+// independent loads.  Ballots give per-(chunk, wave) active counts; one
+// block-wide exclusive scan over those (token order = (chunk, wave, lane))
+// gives every token its rank among the active tokens, and the inactive
+// tokens follow at cnt + (t - active tokens before t).
+namespace {
+constexpr int kFusedThreads = 1024;
+constexpr int kFusedChunks = 32;
+constexpr int kFusedWaves = kFusedThreads / kWave;
+}  // namespace
+
+__global__ __launch_bounds__(kFusedThreads) void wide_reorder_fused(const uint8_t* __restrict__ mask,
+                                                                     int M, int n_groups,
+                                                                     int32_t* __restrict__ idx,
+                                                                     int32_t* __restrict__ counts) {
+  __shared__ int32_t s_cnt[kFusedChunks * kFusedWaves];
+  __shared__ int32_t s_wsum[kFusedWaves];
+  const int g = blockIdx.x, tid = threadIdx.x;
+  const int w = wave_id(), lane = lane_id();
+  const int nch = (M + kFusedThreads - 1) / kFusedThreads;
+  uint32_t bits = 0;
+  for (int i = 0; i < nch; ++i) {
+    const int t = i * kFusedThreads + tid;
+    if (t < M && mask[(int64_t)t * n_groups + g] != 0) bits |= 1u << i;
+  }
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int i = 0; i < nch; ++i) {
+    const uint64_t b = __ballot((bits >> i) & 1u);
+    if (lane == 0) s_cnt[i * kFusedWaves + w] = __popcll(b);
+  }
+  __syncthreads();
+  // exclusive scan of the nch*16 (chunk, wave) counts, in token order
+  const int n = nch * kFusedWaves;
+  const int32_t v = tid < n ? s_cnt[tid] : 0;
+  int32_t x = v;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int32_t y = __shfl_up(x, d, kWave);
+    if (lane >= d) x += y;
+  }
+  if (lane == kWave - 1) s_wsum[w] = x;
+  __syncthreads();
+  int32_t before = 0, cnt = 0;
+  for (int i = 0; i < kFusedWaves; ++i) {
+    before += i < w ? s_wsum[i] : 0;
+    cnt += s_wsum[i];
+  }
+  if (tid < n) s_cnt[tid] = before + x - v;
+  __syncthreads();
+  if (tid == 0) counts[g] = cnt;
+  int32_t* out = idx + (int64_t)g * M;
+  for (int i = 0; i < nch; ++i) {
+    const int t = i * kFusedThreads + tid;
+    const bool a = (bits >> i) & 1u;
+    const uint64_t b = __ballot(a);
+    if (t < M) {
+      const int32_t act_before = s_cnt[i * kFusedWaves + w] + __popcll(b & below);
+      out[a ? act_before : cnt + (t - act_before)] = t;
+    }
+  }
+}
+
 // Host-side launcher (called from api.cpp after validation).  ccnt and coff
-// each hold n_groups * ceil(M / 64) ints.
+// each hold n_groups * ceil(M / 64) ints (unused by the single-kernel path).
 hipError_t launch_reorder(const uint8_t* mask, int64_t M, int n_groups, int32_t* idx,
                           int32_t* counts, int32_t* ccnt, int32_t* coff, hipStream_t s) {
   const int64_t n_chunks64 = (M + kChunk - 1) / kChunk;
   if (n_chunks64 > 0x7fffffff) return hipErrorInvalidValue;
   const int n_chunks = (int)n_chunks64;
+  if (M > 0 && M <= (int64_t)kFusedThreads * kFusedChunks) {
+    WIDE_LAUNCH(wide_reorder_fused, dim3(n_groups), dim3(kFusedThreads), 0, s, mask, (int)M, n_groups,
+                idx, counts);
+    return hipGetLastError();
+  }
   if (n_chunks > 0)
     WIDE_LAUNCH(wide_reorder_count, dim3(n_chunks), dim3(kChunk), 0, s, mask, M, n_groups,
                 n_chunks, ccnt);

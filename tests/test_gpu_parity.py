@@ -41,7 +41,10 @@ def ffn_dev(c):
 @pytest.mark.parametrize("M,ng,kind", [
     (1, 1, "bernoulli"), (7, 3, "bernoulli"), (255, 24, "bernoulli"), (256, 86, "beta"),
     (257, 86, "bernoulli"), (300, 4096, "bernoulli"), (2048, 8, "bernoulli"),
-    (4096, 86, "topk"), (8192, 112, "topk"), (1000, 5, "zeros"), (1000, 5, "ones")])
+    (4096, 86, "topk"), (8192, 112, "topk"), (1000, 5, "zeros"), (1000, 5, "ones"),
+    # single-kernel path up to 32768 tokens (1024-token chunks, ragged tails), three-kernel beyond
+    (1024, 7, "bernoulli"), (1025, 3, "bernoulli"), (32768, 24, "bernoulli"), (32769, 24, "bernoulli"),
+    (65573, 112, "topk")])
 def test_reorder_bit_exact(orc, M, ng, kind):
     say("reorder", M, ng, kind)
     g = synth.rng(M + ng)
