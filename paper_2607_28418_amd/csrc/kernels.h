@@ -139,7 +139,6 @@ struct GVKArgs {
   int k_split;         // workgroups sharing one row block's union steps
   float* part;         // [k_split][B][N] partial sums when k_split > 1
 };
-// Split of the decode K-axis product: enough workgroups to fill the chip.
 // Decode K-axis: output rows per workgroup (16 * gemv_k_ncb) and the split of
 // the union steps over workgroups (see gemv.hip).
 int gemv_k_ncb(int N);
