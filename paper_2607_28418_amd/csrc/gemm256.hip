@@ -152,6 +152,7 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   __shared__ uint32_t s_mbits[BM][kKd256MaxGroups / 32];  // mask bits of the tile's rows
   __shared__ uint16_t s_groups[kKd256MaxGroups];          // groups with an active row, ascending
+  __shared__ uint32_t s_union[kKd256MaxGroups / 32];       // union of the tile's mask rows
   __shared__ int s_ng_live;
   using Rg = RingKD<BK>;
   constexpr int S = Rg::SLOTS;
@@ -165,6 +166,8 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
   const int nw = (ng + 31) / 32;
   const int tid = threadIdx.x;
 
+  if (tid < nw) s_union[tid] = 0u;
+  __syncthreads();
   for (int i = tid; i < BM * nw; i += NT) {
     const int r = i / nw, wd = i % nw;
     const int64_t t = m0 + r;
@@ -175,12 +178,13 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
       for (int b = 0; b < n; ++b) bits |= (uint32_t)(mr[b] != 0) << b;
     }
     s_mbits[r][wd] = bits;
+    if (bits) atomicOr(&s_union[wd], bits);
   }
-  if (tid == 0) {
+  __syncthreads();
+  if (tid == 0) {  // groups some row of the tile uses, ascending
     int n = 0;
-    const uint8_t* tu = a.tile_union + (int64_t)m_tile * ng;
-    for (int gg = 0; gg < ng; ++gg)
-      if (tu[gg]) s_groups[n++] = (uint16_t)gg;
+    for (int wd = 0; wd < nw; ++wd)
+      for (uint32_t u = s_union[wd]; u; u &= u - 1) s_groups[n++] = (uint16_t)(wd * 32 + __builtin_ctz(u));
     s_ng_live = n;
   }
   __syncthreads();
@@ -353,8 +357,6 @@ hipError_t launch_kd256(const KArgs& a, hipStream_t s) {
   const int64_t total = m_tiles * (a.N / BN);
   if (total == 0) return hipSuccess;
   if (a.K / a.G > kKd256MaxGroups) return hipErrorInvalidValue;
-  hipError_t e = launch_tile_union(a.mask, a.M, a.K / a.G, BM, a.tile_union, s);
-  if (e != hipSuccess) return e;
   WIDE_RING_LAUNCH("wide_kd256", KD, RingKD, (unsigned)total, s, a);
   return hipGetLastError();
 }
