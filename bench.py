@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--cpu-sample-tokens", type=int, default=1024)
     ap.add_argument("--ring-bk", type=int, default=0, help="k depth of a 256x256 stage (0: library default)")
     ap.add_argument("--k-path", type=int, default=0, help="K-axis schedule (0: library default)")
+    ap.add_argument("--no-sweeps", action="store_true",
+                    help="skip the decode batch sweep and the prefill keep sweep")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="end with two 1 GiB device copies (counter calibration under rocprofv3)")
     return ap.parse_args()
@@ -360,6 +362,88 @@ def main():
         decode["speedup_vs_dense"] = round(best_dec / dec_ms, 3)
         decode["ideal_speedup"] = round(ddense / dbytes, 3)
 
+    # ---- sweeps (outside the timed region, context for the headline line) ---------
+    sweeps = None
+    if not args.no_sweeps:
+        import torch.nn.functional as F
+        from paper_2607_28418_amd import synth
+
+        def graph_ms(fn, reps=20):
+            side = torch.cuda.Stream()
+            side.wait_stream(stream)
+            with torch.cuda.stream(side):
+                for _ in range(3):
+                    fn()
+            stream.wait_stream(side)
+            torch.cuda.synchronize()
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr):
+                fn()
+            for _ in range(3):
+                gr.replay()
+            torch.cuda.synchronize()
+            s0, s1 = ev(), ev()
+            s0.record(stream)
+            for _ in range(reps):
+                gr.replay()
+            s1.record(stream)
+            torch.cuda.synchronize()
+            return s0.elapsed_time(s1) / reps
+
+        # decode FFN at the Llama-7B shape (d_model 4096, d_ff 11008 in 86 groups
+        # of 128), per-group Beta(2,2) activation rates with mean 0.5
+        D7, F7, G7 = 4096, 11008, 128
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(7)
+
+        def rnd(*shape, std=0.02):
+            return (torch.randn(*shape, device=dev, generator=gen) * std).to(torch.bfloat16)
+
+        wg7, wu7, wd7 = rnd(F7, D7), rnd(F7, D7), rnd(D7, F7)
+        dec_rows = []
+        for bq in (1, 4, 16, 64):
+            mk = synth.mask_beta_groups(synth.rng(100 + bq), bq, F7 // G7, 0.5)
+            xq, mq = rnd(bq, D7, std=1.0), to_dev(mk)
+            yq = torch.empty(bq, D7, dtype=torch.bfloat16, device=dev)
+            wsq = torch.empty(max(W.wide_workspace_size(W.OP_FFN, W.BF16, bq, D7, F7, G7), 256),
+                              dtype=torch.uint8, device=dev)
+            t_w = graph_ms(lambda: W.wide_ffn_masked(xq, wg7, wu7, wd7, mq, G7, y=yq, ws=wsq))
+            t_d = graph_ms(lambda: F.linear(F.silu(F.linear(xq, wg7)) * F.linear(xq, wu7), wd7))
+            u = int(mk.any(0).sum())
+            ub = 3 * u * G7 * D7 * 2
+            dec_rows.append(dict(batch=bq, ms=round(t_w, 4), hipblaslt_ms=round(t_d, 4), union_groups=u,
+                                 union_bytes=ub, GBps=round(ub / (t_w * 1e-3) / 1e9, 1),
+                                 frac_hbm=round(ub / (t_w * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+                                 speedup_vs_dense=round(t_d / t_w, 3),
+                                 ideal_speedup=round((F7 // G7) / u, 3)))
+        del wg7, wu7, wd7
+        # prefill of the layer at other keep fractions (same tokens, new top-k masks)
+        pre_rows = []
+        bp = L.batches["prefill"]
+        for keep in (0.25, 0.75):
+            hg = synth.rng(200 + int(round(keep * 100)))
+            ma = synth.mask_topk(synth.router_logits(hg, bp["x_attn"], L.nga), synth.keep_count(L.nga, keep))
+            mf = synth.mask_topk(synth.router_logits(hg, bp["x_ffn"], L.ng), synth.keep_count(L.ng, keep))
+            md = (to_dev(ma), to_dev(mf))
+            for _ in range(3):
+                run("prefill", md)
+            torch.cuda.synchronize()
+            s0, s1 = ev(), ev()
+            s0.record(stream)
+            for _ in range(10):
+                run("prefill", md)
+            s1.record(stream)
+            torch.cuda.synchronize()
+            t = s0.elapsed_time(s1) / 10
+            act = (2.0 * L.D * L.Ga * ma.sum() * 2 + 4.0 * ma.shape[0] * L.D * L.Nkv
+                   + 6.0 * L.D * L.G * mf.sum())
+            row = dict(keep=keep, ms=round(t, 4), active_TFLOPs=round(act / (t * 1e-3) / 1e12, 1),
+                       ideal_speedup=round(L.dense_flops("prefill") / act, 3))
+            if dense is not None:
+                row["speedup_vs_dense"] = round(dense["hipblaslt_prefill_ms"] / t, 3)
+            pre_rows.append(row)
+        sweeps = dict(decode_ffn_llama7b=dec_rows, prefill_layer_keep=pre_rows)
+
     # ---- CPU oracle on a bounded sample --------------------------------------------
     cpu = None
     if not args.no_cpu_baseline:
@@ -404,6 +488,7 @@ def main():
         "kernels_us": {k: round(v["avg_us"], 2) for k, v in kernels.items()},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "sweeps": sweeps,
     }
     print(json.dumps(out), flush=True)
     if args.calibration_copy:
