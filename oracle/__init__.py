@@ -18,6 +18,9 @@ Sources followed (WIDE, "Token-level Dynamic Width Pruning"):
                        Appendix B: W_o / W_down pruned over in-features.
   * ``ffn``            Section 3.1, equation (3), with phi = SiLU (SwiGLU).
   * ``linear``         dense K/V projections, equation (1).
+  * ``router``         Section 3.1, Routing Components: logits X W1 W2 as
+                       n_groups (execute, skip) pairs; the mask bit is 1 when
+                       class 0 wins (argmax, first index on a tie).
   * ``bf16_round``     storage rounding of the bf16 data path (the paper states
                        no precision; the reading is recorded with the design
                        notes).
@@ -64,6 +67,7 @@ def _load():
         lib.oracle_nproj.argtypes = [ci, ci, i64, i32, i32, i32, vp, vp, vp, vp]
         lib.oracle_kproj.argtypes = [ci, ci, i64, i32, i32, i32, vp, vp, vp, vp]
         lib.oracle_ffn.argtypes = [ci, ci, i64, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
+        lib.oracle_router.argtypes = [ci, i64, i32, i32, i32, vp, vp, vp, vp, vp]
         lib.oracle_num_threads.restype = ci
         _lib = lib
     return _lib
@@ -163,3 +167,19 @@ def ffn(x, w_gate, w_up, w_down, mask, G, round_bf16=False, want_h=True):
     _load().oracle_ffn(dt, int(round_bf16), M, D, Dff, G, _p(mask), _p(x), _p(w_gate),
                        _p(w_up), _p(w_down), _p(h) if h is not None else None, _p(y))
     return h, y
+
+
+def router(x, w1, w2):
+    """Bottleneck router, inference form.  x [M][D], w1 [r][D] (W1 transposed),
+    w2 [2*n_groups][r] (W2 transposed; rows 2g and 2g+1 are group g's execute
+    and skip classes).  Returns (logits float64 [M][2*n_groups], mask uint8
+    [M][n_groups])."""
+    dt, (x, w1, w2) = _same_dtype(x, w1, w2)
+    M, D = x.shape
+    r = w1.shape[0]
+    J = w2.shape[0]
+    assert w1.shape == (r, D) and w2.shape == (J, r) and J % 2 == 0
+    logits = np.empty((M, J), np.float64)
+    mask = np.empty((M, J // 2), np.uint8)
+    _load().oracle_router(dt, M, D, r, J // 2, _p(x), _p(w1), _p(w2), _p(logits), _p(mask))
+    return logits, mask

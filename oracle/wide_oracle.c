@@ -13,7 +13,10 @@
  *   - K-axis masked projections: W_o and W_down, pruned over their
  *     in-features (Section 3.1 equations (2)-(3); Appendix B, the masked
  *     K-axis sum that defines GEMM-K);
- *   - the complete masked SwiGLU FFN of equation (3).
+ *   - the complete masked SwiGLU FFN of equation (3);
+ *   - the bottleneck router in its inference form (Section 3.1, "Routing
+ *     Components"): logits X W1 W2 read as n_groups pairs, and the mask bit
+ *     "class 0 (execute) wins the pair".
  *
  * Every floating-point input is widened exactly to fp64 (bf16 bit patterns or
  * fp32 values) and every sum is accumulated in fp64 in natural index order,
@@ -186,6 +189,44 @@ void oracle_ffn(int dtype, int round_bf16, int64_t M, int32_t D, int32_t Dff,
       for (int32_t n = 0; n < D; ++n) y[t * D + n] = store_round(acc[n], round_bf16);
     }
     free(acc);
+  }
+}
+
+/* ---- bottleneck router (Section 3.1, Routing Components) --------------- */
+
+/* Inference form of the router: R = X W1 W2 with W1 in R^{D x r} and W2 in
+ * R^{r x 2 n_groups}, reshaped to [M][n_groups][2]; the mask bit of group g
+ * is 1 when the argmax over the pair is class 0 (execution).  argmax returns
+ * the first maximal index, so a tie executes.
+ *
+ * The weights are passed transposed, as linear-layer weights: w1 is
+ * [r][D] (row i = column i of W1) and w2 is [2 n_groups][r] (row j = column
+ * j of W2).  The bottleneck activation is kept in fp64, unrounded.
+ * logits: [M][2 n_groups] fp64 out; mask: [M][n_groups] out. */
+void oracle_router(int dtype, int64_t M, int32_t D, int32_t r, int32_t n_groups,
+                   const void* x, const void* w1, const void* w2, double* logits,
+                   uint8_t* mask) {
+  const int32_t J = 2 * n_groups;
+#pragma omp parallel
+  {
+    double* h = (double*)malloc(sizeof(double) * (size_t)(r > 0 ? r : 1));
+#pragma omp for schedule(static)
+    for (int64_t t = 0; t < M; ++t) {
+      for (int32_t i = 0; i < r; ++i) {
+        double acc = 0.0;
+        for (int32_t k = 0; k < D; ++k)
+          acc += load_elem(x, dtype, t * D + k) * load_elem(w1, dtype, (int64_t)i * D + k);
+        h[i] = acc;
+      }
+      for (int32_t j = 0; j < J; ++j) {
+        double acc = 0.0;
+        for (int32_t i = 0; i < r; ++i) acc += h[i] * load_elem(w2, dtype, (int64_t)j * r + i);
+        logits[t * J + j] = acc;
+      }
+      for (int32_t g = 0; g < n_groups; ++g)
+        mask[t * n_groups + g] = logits[t * J + 2 * g] >= logits[t * J + 2 * g + 1] ? 1 : 0;
+    }
+    free(h);
   }
 }
 

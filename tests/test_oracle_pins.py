@@ -307,3 +307,54 @@ def test_synth_masks():
     assert t.tolist() == [[0, 1, 1, 0]]
     t = synth.mask_topk(np.array([[2.0, 2.0, 2.0, 0.0]]), 2)   # ties: lower index wins
     assert t.tolist() == [[1, 1, 0, 0]]
+
+
+# ---------------------------------------------------------------- router
+
+def _read_golden_router():
+    with open(os.path.join(GOLDEN, "router_hand.txt")) as f:
+        lines = [ln.split() for ln in f if ln.strip() and not ln.startswith("#")]
+    sec, data = None, {"x": [], "w1": [], "w2": [], "logits": [], "mask": []}
+    for ln in lines:
+        if ln[0] in data:
+            sec = ln[0]
+            continue
+        data[sec].append([float(v) for v in ln])
+    return {k: np.array(v) for k, v in data.items()}
+
+
+def test_router_hand_fixture(orc):
+    d = _read_golden_router()
+    logits, mask = orc.router(d["x"].astype(np.float32), d["w1"].astype(np.float32),
+                              d["w2"].astype(np.float32))
+    assert np.array_equal(logits, d["logits"])
+    assert np.array_equal(mask, d["mask"].astype(np.uint8))
+
+
+@pytest.mark.parametrize("M,D,r,ng", [(5, 64, 16, 7), (33, 128, 32, 24), (2, 256, 1, 3)])
+def test_router_matches_matrix_form_and_pair_rule(orc, M, D, r, ng):
+    g = synth.rng(M + D + r + ng)
+    x = synth.normal(g, (M, D), 1.0, "bf16")
+    w1 = synth.normal(g, (r, D), 0.05, "bf16")
+    w2 = synth.normal(g, (2 * ng, r), 0.3, "bf16")
+    logits, mask = orc.router(x, w1, w2)
+    ref = (f64(x) @ f64(w1).T) @ f64(w2).T        # (X W1) W2, the matrix form
+    assert rel_err(logits, ref) < 1e-12
+    assert np.array_equal(mask, (logits[:, 0::2] >= logits[:, 1::2]).astype(np.uint8))
+    # swapping each pair's two classes flips every decision that is not a tie
+    sw = w2.reshape(ng, 2, r)[:, ::-1].reshape(2 * ng, r).copy()
+    l2, m2 = orc.router(x, w1, sw)
+    tie = logits[:, 0::2] == logits[:, 1::2]
+    assert np.array_equal(m2[~tie], 1 - mask[~tie])
+    # a positive scale of W2 leaves every decision unchanged
+    w2s = synth.f32_to_bf16_bits(synth.as_f32(w2) * np.float32(4.0))
+    assert np.array_equal(orc.router(x, w1, w2s)[1], mask)
+
+
+def test_router_ties_execute(orc):
+    # identical class rows give exact ties: every group executes
+    x = np.ones((3, 8), np.float32)
+    w1 = np.ones((2, 8), np.float32)
+    w2 = np.tile(np.array([[1.0, -2.0]], np.float32), (6, 1))
+    logits, mask = orc.router(x, w1, w2)
+    assert (logits[:, 0::2] == logits[:, 1::2]).all() and mask.all()
