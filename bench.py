@@ -442,7 +442,25 @@ def main():
             if dense is not None:
                 row["speedup_vs_dense"] = round(dense["hipblaslt_prefill_ms"] / t, 3)
             pre_rows.append(row)
-        sweeps = dict(decode_ffn_llama7b=dec_rows, prefill_layer_keep=pre_rows)
+        # the bottleneck router (rank 32) that produces the FFN mask, with its
+        # reorder, at the prefill and decode sizes of the layer
+        rank = 32
+        w1r, w2r = rnd(rank, L.D), rnd(2 * L.ng, rank, std=0.3)
+        rt_rows = []
+        for name in ("prefill", "decode"):
+            xr = bd[name]["x_ffn"]
+            Mr = xr.shape[0]
+            mr = torch.empty((Mr, L.ng), dtype=torch.uint8, device=dev)
+            ir = torch.empty((L.ng, Mr), dtype=torch.int32, device=dev)
+            cr = torch.empty((L.ng,), dtype=torch.int32, device=dev)
+            wsr = torch.empty(max(W.wide_workspace_size(W.OP_ROUTER, W.BF16, Mr, L.D, L.ng, rank), 256),
+                              dtype=torch.uint8, device=dev)
+            t = graph_ms(lambda: W.wide_router(xr, w1r, w2r, mask=mr, reorder=True, idx=ir, counts=cr,
+                                               ws=wsr))
+            xb = Mr * L.D * 2
+            rt_rows.append(dict(tokens=Mr, n_groups=L.ng, rank=rank, ms_with_reorder=round(t, 4),
+                                x_GBps=round(xb / (t * 1e-3) / 1e9, 1)))
+        sweeps = dict(decode_ffn_llama7b=dec_rows, prefill_layer_keep=pre_rows, router_ffn=rt_rows)
 
     # ---- CPU oracle on a bounded sample --------------------------------------------
     cpu = None

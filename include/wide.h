@@ -63,7 +63,8 @@ typedef enum {
   WIDE_OP_REORDER = 0,
   WIDE_OP_FFN = 1,
   WIDE_OP_QKV = 2,
-  WIDE_OP_O = 3
+  WIDE_OP_O = 3,
+  WIDE_OP_ROUTER = 4
 } wide_op_t;
 
 /*
@@ -153,10 +154,38 @@ wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M,
                                hipStream_t stream);
 
 /*
+ * Bottleneck router, inference form (WIDE Section 3.1, "Routing Components").
+ * R = X W1 W2 is read as n_groups pairs (class 0 = execute, class 1 = skip);
+ * mask[t][g] = 1 when class 0 wins the pair, i.e. R[t][2g] >= R[t][2g+1]
+ * (argmax returns the first maximal class, so a tie executes), else 0.
+ *   x        [M][d_model] bf16.
+ *   w1       [rank][d_model] bf16: W1 transposed (linear-layer layout),
+ *            1 <= rank <= 32.
+ *   w2       [2*n_groups][rank] bf16: W2 transposed; rows 2g and 2g+1 are
+ *            group g's execute and skip logits.
+ *   mask     [M][n_groups] uint8 out (1 execute, 0 skip).
+ *   logits   optional [M][2*n_groups] fp32 out (R); NULL skips it.
+ *   idx, counts  optional, both or neither: the reorder of the new mask, as
+ *            wide_mask_reorder computes it (with M == 0 only counts is
+ *            written, all zero, and idx may be NULL).
+ *   ws       workspace of wide_workspace_size(WIDE_OP_ROUTER, WIDE_BF16, M,
+ *            d_model, n_groups, rank) bytes (used by the reorder).
+ * Arithmetic: X W1 with bf16 products summed in fp32 and kept in fp32 (not
+ * rounded to bf16); R in fp32; the decision is taken on the fp32 R.
+ * Limits: bf16 only (WIDE_ERR_UNSUPPORTED otherwise); d_model % 64 == 0;
+ * 1 <= n_groups <= 4096; 0 <= M < 2^31.
+ */
+wide_status_t wide_router(wide_dtype_t dt, int64_t M, int32_t d_model, int32_t rank,
+                          int32_t n_groups, const void* x, const void* w1, const void* w2,
+                          uint8_t* mask, float* logits, int32_t* idx, int32_t* counts,
+                          void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
  * Workspace bytes needed by one call (0 is a valid answer).
  *   op = WIDE_OP_REORDER: d_inner = n_groups, group_size = 1, d_model unused.
  *   op = WIDE_OP_FFN:     d_inner = d_ff.
  *   op = WIDE_OP_QKV/O:   d_inner = n_q*head_dim.
+ *   op = WIDE_OP_ROUTER:  d_inner = n_groups, group_size = rank.
  * Returns SIZE_MAX for arguments the matching entry point would reject.
  */
 size_t wide_workspace_size(wide_op_t op, wide_dtype_t dt, int64_t M,

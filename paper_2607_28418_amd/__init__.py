@@ -13,10 +13,10 @@ import ctypes
 import os
 
 __all__ = [
-    "WideError", "lib", "wide_mask_reorder", "wide_ffn_masked", "wide_qkvo_masked",
+    "WideError", "lib", "wide_mask_reorder", "wide_ffn_masked", "wide_qkvo_masked", "wide_router",
     "wide_workspace_size", "wide_set_option", "wide_get_option", "wide_timing_enable",
     "wide_timing_reset", "wide_timing_query", "LIB_PATH",
-    "OP_REORDER", "OP_FFN", "OP_QKV", "OP_O", "PHASE_QKV", "PHASE_O", "F32", "BF16",
+    "OP_REORDER", "OP_FFN", "OP_QKV", "OP_O", "OP_ROUTER", "PHASE_QKV", "PHASE_O", "F32", "BF16",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libwide.so")
@@ -24,7 +24,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libwide.so"
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 F32, BF16 = 0, 1
 PHASE_QKV, PHASE_O = 0, 1
-OP_REORDER, OP_FFN, OP_QKV, OP_O = 0, 1, 2, 3
+OP_REORDER, OP_FFN, OP_QKV, OP_O, OP_ROUTER = 0, 1, 2, 3, 4
 SIZE_MAX = 2 ** 64 - 1
 
 _lib = None
@@ -55,6 +55,8 @@ def lib() -> ctypes.CDLL:
         L.wide_qkvo_masked.restype = ci
         L.wide_qkvo_masked.argtypes = [ci, ci, i64, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp,
                                        vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.wide_router.restype = ci
+        L.wide_router.argtypes = [ci, i64, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.wide_workspace_size.restype = sz
         L.wide_workspace_size.argtypes = [ci, ci, i64, i32, i32, i32]
         L.wide_set_option.restype = ci
@@ -227,3 +229,37 @@ def wide_qkvo_masked(phase, inp, mask, group_size, n_q_heads, n_kv_heads, head_d
         _p(counts), _p(inp), _p(w_q), _p(w_k), _p(w_v), _p(w_o), _p(q), _p(k), _p(v), _p(y),
         _p(ws), nbytes, _stream(inp)))
     return (q, k, v) if phase == PHASE_QKV else y
+
+
+def wide_router(x, w1, w2, mask=None, logits=False, reorder=False, idx=None, counts=None, ws=None):
+    """Bottleneck router (inference).  x [M][d_model] bf16, w1 [rank][d_model],
+    w2 [2*n_groups][rank].  Returns the mask [M][n_groups] uint8, followed by
+    the fp32 logits [M][2*n_groups] if `logits`, and (idx, counts) if
+    `reorder`."""
+    torch = _torch()
+    _contig(x, w1, w2, mask, idx, counts)
+    M, D = x.shape
+    rank = w1.shape[0]
+    ng = w2.shape[0] // 2
+    if mask is None:
+        mask = torch.empty((M, ng), dtype=torch.uint8, device=x.device)
+    lg = torch.empty((M, 2 * ng), dtype=torch.float32, device=x.device) if logits else None
+    if reorder:
+        if idx is None:
+            idx = torch.empty((ng, M), dtype=torch.int32, device=x.device)
+        if counts is None:
+            counts = torch.empty((ng,), dtype=torch.int32, device=x.device)
+    else:
+        idx = counts = None
+    if ws is None and reorder:
+        ws = _workspace(wide_workspace_size(OP_ROUTER, _dtype_code(x), M, D, ng, rank), x.device)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("wide_router", lib().wide_router(
+        _dtype_code(x), M, D, rank, ng, _p(x), _p(w1), _p(w2), _p(mask), _p(lg), _p(idx),
+        _p(counts), _p(ws), nbytes, _stream(x)))
+    out = [mask]
+    if logits:
+        out.append(lg)
+    if reorder:
+        out += [idx, counts]
+    return out[0] if len(out) == 1 else tuple(out)

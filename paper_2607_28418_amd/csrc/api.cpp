@@ -420,6 +420,15 @@ size_t wide_workspace_size(wide_op_t op, wide_dtype_t dt, int64_t M, int32_t d_m
     case WIDE_OP_FFN:
       if (ffn_shape(dt, M, d_model, d_inner, group_size) != WIDE_OK) return SIZE_MAX;
       return ffn_ws_bytes(dt, M, d_model, d_inner, group_size, true, true, 0);
+    case WIDE_OP_ROUTER: {
+      if (check_common(dt, M) != WIDE_OK || dt != WIDE_BF16 || d_model <= 0 || d_model % 64 ||
+          group_size < 1 || group_size > wide::kRouterMaxRank || d_inner < 1 || d_inner > 4096)
+        return SIZE_MAX;
+      Carve c(nullptr);
+      ReorderWS r;
+      carve_reorder(c, M, d_inner, false, r);
+      return c.off;
+    }
     case WIDE_OP_QKV:
     case WIDE_OP_O: {
       // The size depends on M, d_model and the number of groups only.
@@ -451,6 +460,51 @@ wide_status_t wide_mask_reorder(const uint8_t* mask, int64_t M, int32_t n_groups
   carve_reorder(c, M, n_groups, false, r);
   hipError_t e = wide::launch_reorder(mask, M, n_groups, idx, counts, r.chunk_cnt, r.chunk_off, stream);
   if (e != hipSuccess) return hip_fail(e, "reorder");
+  return ok();
+}
+
+wide_status_t wide_router(wide_dtype_t dt, int64_t M, int32_t d_model, int32_t rank,
+                          int32_t n_groups, const void* x, const void* w1, const void* w2,
+                          uint8_t* mask, float* logits, int32_t* idx, int32_t* counts,
+                          void* ws, size_t ws_bytes, hipStream_t stream) {
+  CHECK(check_common(dt, M));
+  if (dt != WIDE_BF16) return fail(WIDE_ERR_UNSUPPORTED, "the router runs on bf16 inputs only");
+  if (d_model <= 0 || d_model % 64) return fail(WIDE_ERR_INVALID_ARG, "d_model must be a positive multiple of 64");
+  if (rank < 1 || rank > wide::kRouterMaxRank) return fail(WIDE_ERR_INVALID_ARG, "rank must be in [1, 32]");
+  if (n_groups < 1 || n_groups > 4096) return fail(WIDE_ERR_INVALID_ARG, "n_groups must be in [1, 4096]");
+  // (with M == 0 the index array is empty and may be NULL)
+  if (M > 0 && (idx == nullptr) != (counts == nullptr))
+    return fail(WIDE_ERR_INVALID_ARG, "idx and counts must both be given or both be NULL");
+  CHECK(check_ptr(w1, "w1"));
+  CHECK(check_ptr(w2, "w2"));
+  if (M == 0) {  // nothing to route; a requested reorder still reports zero counts
+    if (!counts) return ok();
+    CHECK(check_ptr(counts, "counts", false));
+    const hipError_t e = wide::launch_reorder(mask, 0, n_groups, idx, counts, nullptr, nullptr, stream);
+    return e == hipSuccess ? ok() : hip_fail(e, "router counts");
+  }
+  CHECK(check_ptr(x, "x"));
+  CHECK(check_ptr(mask, "mask", false));
+  if (logits) CHECK(check_ptr(logits, "logits", false));
+  if (idx) {
+    CHECK(check_ptr(idx, "idx", false));
+    CHECK(check_ptr(counts, "counts", false));
+    Carve c0(nullptr);
+    ReorderWS r0;
+    carve_reorder(c0, M, n_groups, false, r0);
+    CHECK(check_ws(ws, ws_bytes, c0.off));
+  }
+  wide::RouterArgs ra{static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w1),
+                      static_cast<const uint16_t*>(w2), mask, logits, M, d_model, rank, n_groups};
+  hipError_t e = wide::launch_router(ra, stream);
+  if (e != hipSuccess) return hip_fail(e, "router");
+  if (idx) {
+    Carve c(ws);
+    ReorderWS r;
+    carve_reorder(c, M, n_groups, false, r);
+    e = wide::launch_reorder(mask, M, n_groups, idx, counts, r.chunk_cnt, r.chunk_off, stream);
+    if (e != hipSuccess) return hip_fail(e, "router reorder");
+  }
   return ok();
 }
 

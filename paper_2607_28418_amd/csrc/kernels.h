@@ -153,6 +153,19 @@ DecodeTuning& decode_tuning();
 
 constexpr int kDecodeMaxB = 64;
 
+// ---- bottleneck router (router.hip)
+constexpr int kRouterMaxRank = 32;
+struct RouterArgs {
+  const uint16_t* x;   // [M][D] bf16
+  const uint16_t* w1;  // [r][D] bf16 (W1 transposed)
+  const uint16_t* w2;  // [2 ng][r] bf16 (W2 transposed)
+  uint8_t* mask;       // [M][ng] out
+  float* logits;       // optional [M][2 ng] out
+  int64_t M;
+  int D, r, ng;        // D % 64 == 0, 1 <= r <= 32
+};
+hipError_t launch_router(const RouterArgs& a, hipStream_t s);
+
 hipError_t launch_gemv_n(const GVNArgs& a, bool swiglu, hipStream_t s);
 hipError_t launch_gemv_k(const GVKArgs& a, hipStream_t s);
 

@@ -107,3 +107,38 @@ def test_options():
         W.wide_set_option("k_path", 9)
     with pytest.raises(W.WideError):
         W.wide_set_option("nope", 1)
+
+
+def router(dt=W.BF16, M=64, D=4096, r=32, ng=112, x=A, w1=A, w2=A, mask=A, logits=None, idx=None,
+           cnt=None, ws=A, ws_bytes=1 << 40):
+    return W.lib().wide_router(dt, M, D, r, ng, x, w1, w2, mask, logits, idx, cnt, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(dt=W.F32), W.ERR_UNSUPPORTED, "bf16"),
+    (dict(D=4000), W.ERR_INVALID_ARG, "multiple of 64"),
+    (dict(r=0), W.ERR_INVALID_ARG, "rank"),
+    (dict(r=33), W.ERR_INVALID_ARG, "rank"),
+    (dict(ng=0), W.ERR_INVALID_ARG, "n_groups"),
+    (dict(ng=4097), W.ERR_INVALID_ARG, "n_groups"),
+    (dict(idx=A), W.ERR_INVALID_ARG, "both"),
+    (dict(x=MIS), W.ERR_INVALID_ARG, "x is not 16-byte aligned"),
+    (dict(w1=None), W.ERR_INVALID_ARG, "w1 is NULL"),
+    (dict(mask=None), W.ERR_INVALID_ARG, "mask is NULL"),
+    (dict(idx=A, cnt=A, ws_bytes=0), W.ERR_WORKSPACE, "workspace"),
+    (dict(M=-1), W.ERR_INVALID_ARG, "M"),
+])
+def test_router_validation(kw, status, msg):
+    assert router(**kw) == status
+    assert msg in err()
+
+
+def test_router_m_zero_without_reorder_is_ok():
+    assert router(M=0, x=None, mask=None) == W.OK
+
+
+def test_router_workspace_size():
+    assert W.wide_workspace_size(W.OP_ROUTER, W.BF16, 8192, 4096, 112, 32) > 0
+    assert W.wide_workspace_size(W.OP_ROUTER, W.F32, 8192, 4096, 112, 32) == W.SIZE_MAX
+    assert W.wide_workspace_size(W.OP_ROUTER, W.BF16, 8192, 4000, 112, 32) == W.SIZE_MAX
+    assert W.wide_workspace_size(W.OP_ROUTER, W.BF16, 8192, 4096, 112, 33) == W.SIZE_MAX

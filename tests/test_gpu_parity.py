@@ -410,3 +410,72 @@ def test_timing_records_kernels():
     ms, n = W.wide_timing_query("wide_mn256<true>")
     W.wide_timing_enable(False)
     assert n == 1 and ms > 0
+
+
+# ------------------------------------------------------------------ router
+
+def _router_case(M, D, r, ng, seed):
+    g = synth.rng(seed)
+    x = synth.normal(g, (M, D), 1.0, "bf16")
+    w1 = synth.normal(g, (r, D), 0.02, "bf16")
+    w2 = synth.normal(g, (2 * ng, r), 0.3, "bf16")
+    return x, w1, w2
+
+
+def _router_bound(x, w1, w2):
+    """Bound on |fp32 logit - fp64 logit| from the kernel's arithmetic: X W1 is
+    a sum of D exact bf16 products in fp32 (any order), then r fp32 FMAs with
+    W2.  gamma_n = n u / (1 - n u), u = 2^-24."""
+    u = 2.0 ** -24
+    X, W1, W2 = (synth.as_f32(a).astype(np.float64) for a in (x, w1, w2))
+    D, r = X.shape[1], W1.shape[0]
+    gD, gr = D * u / (1 - D * u), (r + 1) * u / (1 - (r + 1) * u)
+    dh = gD * (np.abs(X) @ np.abs(W1).T)
+    h = np.abs(X @ W1.T)
+    return dh @ np.abs(W2).T + gr * ((h + dh) @ np.abs(W2).T)
+
+
+@pytest.mark.parametrize("M,D,r,ng", [
+    (1, 64, 16, 3), (33, 128, 32, 24), (300, 4096, 32, 112), (257, 4096, 7, 300),
+    (64, 4096, 16, 8), (2048, 4096, 32, 8), (8192, 4096, 32, 112)])
+def test_router_matches_oracle(orc, M, D, r, ng):
+    say("router", M, D, r, ng)
+    x, w1, w2 = _router_case(M, D, r, ng, M + D + r + ng)
+    mask, lg, idx, cnt = W.wide_router(to_dev(x), to_dev(w1), to_dev(w2), logits=True, reorder=True)
+    torch.cuda.synchronize()
+    ref_lg, ref_mask = orc.router(x, w1, w2)
+    bound = _router_bound(x, w1, w2)
+    got_lg = lg.cpu().numpy().astype(np.float64)
+    assert (np.abs(got_lg - ref_lg) <= bound).all(), float(np.max(np.abs(got_lg - ref_lg) - bound))
+    # the decision is fixed wherever the pair's gap exceeds both logits' bounds
+    gap = np.abs(ref_lg[:, 0::2] - ref_lg[:, 1::2])
+    amb = gap <= bound[:, 0::2] + bound[:, 1::2]
+    got_mask = mask.cpu().numpy()
+    assert np.array_equal(got_mask[~amb], ref_mask[~amb])
+    # inside the band either class is correct; the kernel must still follow its own logits
+    assert np.array_equal(got_mask, (got_lg[:, 0::2] >= got_lg[:, 1::2]).astype(np.uint8))
+    assert amb.mean() < 0.1   # the bound is a worst case (about 5% of pairs at d_model 4096)
+    # the reorder returned with it is that of the returned mask
+    ridx, rcnt = orc.mask_reorder(got_mask)
+    assert np.array_equal(cnt.cpu().numpy(), rcnt) and np.array_equal(idx.cpu().numpy(), ridx)
+
+
+def test_router_ties_execute():
+    say("router ties")
+    g = synth.rng(5)
+    x = synth.normal(g, (40, 128), 1.0, "bf16")
+    w1 = synth.normal(g, (16, 128), 0.02, "bf16")
+    half = synth.normal(g, (5, 16), 0.3, "bf16")
+    w2 = np.repeat(half, 2, axis=0)            # both classes of each group identical
+    mask = W.wide_router(to_dev(x), to_dev(w1), to_dev(w2))
+    torch.cuda.synchronize()
+    assert mask.cpu().numpy().all()
+
+
+def test_router_empty_batch():
+    say("router M=0")
+    mask, idx, cnt = W.wide_router(torch.zeros((0, 64), dtype=torch.bfloat16, device=dev()),
+                                   torch.zeros((16, 64), dtype=torch.bfloat16, device=dev()),
+                                   torch.zeros((6, 16), dtype=torch.bfloat16, device=dev()), reorder=True)
+    torch.cuda.synchronize()
+    assert mask.shape == (0, 3) and idx.shape == (3, 0) and not cnt.cpu().numpy().any()
