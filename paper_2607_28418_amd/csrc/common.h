@@ -59,7 +59,29 @@ __device__ __forceinline__ void stg16(void* p, u32x4 v) {
   *reinterpret_cast<u32x4*>(p) = v;
 }
 
-__device__ __forceinline__ int wave_id() { return threadIdx.x / kWave; }
+// Predicated 16-byte loads without branches: a raw buffer view of
+// [base, base + bytes) (bytes < 2^31).  A lane whose byte offset lies at or
+// past the end (kOffNone) reads zeros and touches no memory -- the buffer
+// unit's range check -- so lanes that must contribute nothing need neither a
+// branch nor a select around the load.
+typedef __amdgpu_buffer_rsrc_t bufview_t;
+constexpr uint32_t kOffNone = 0xFFFFFFF0u;
+
+__device__ __forceinline__ bufview_t buf_view(const void* base, uint32_t bytes) {
+  // third descriptor word of the gfx9 family: 32-bit data format, no swizzle
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ u32x4 buf_ld16(bufview_t v, uint32_t byte_off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(v, (int)byte_off, 0, 0));
+}
+
+__device__ __forceinline__ uint16_t buf_ld2(bufview_t v, uint32_t byte_off) {
+  return __builtin_bit_cast(uint16_t, __builtin_amdgcn_raw_buffer_load_b16(v, (int)byte_off, 0, 0));
+}
+
+// wave index inside the workgroup, as a wave-uniform (scalar) value
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x / kWave); }
 __device__ __forceinline__ int lane_id() { return threadIdx.x % kWave; }
 
 }  // namespace wide
