@@ -18,6 +18,9 @@ Sources followed (WIDE, "Token-level Dynamic Width Pruning"):
                        Appendix B: W_o / W_down pruned over in-features.
   * ``ffn``            Section 3.1, equation (3), with phi = SiLU (SwiGLU).
   * ``linear``         dense K/V projections, equation (1).
+  * ``attention``      Section 3.1 equations (1)-(2) and Appendix B,
+                       Algorithm 4: per (token, head group) either standard
+                       scaled dot-product attention or zeros.
   * ``router``         Section 3.1, Routing Components: logits X W1 W2 as
                        n_groups (execute, skip) pairs; the mask bit is 1 when
                        class 0 wins (argmax, first index on a tie).
@@ -68,6 +71,7 @@ def _load():
         lib.oracle_kproj.argtypes = [ci, ci, i64, i32, i32, i32, vp, vp, vp, vp]
         lib.oracle_ffn.argtypes = [ci, ci, i64, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
         lib.oracle_router.argtypes = [ci, i64, i32, i32, i32, vp, vp, vp, vp, vp]
+        lib.oracle_attention.argtypes = [ci, ci, i64, i32, i32, i32, i32, i32, i32, ci, vp, vp, vp, vp, vp]
         lib.oracle_num_threads.restype = ci
         _lib = lib
     return _lib
@@ -183,3 +187,23 @@ def router(x, w1, w2):
     mask = np.empty((M, J // 2), np.uint8)
     _load().oracle_router(dt, M, D, r, J // 2, _p(x), _p(w1), _p(w2), _p(logits), _p(mask))
     return logits, mask
+
+
+def attention(q, k, v, mask, n_seq, n_q, n_kv, d, causal, round_bf16=False):
+    """Head-group masked attention (prefill).  q [n_seq*T_q][n_q*d],
+    k/v [n_seq*T_k][n_kv*d], mask [n_seq*T_q][n_groups]; with causal masking
+    the queries are the last T_q of each sequence's T_k positions.  Returns
+    o float64 [n_seq*T_q][n_q*d]."""
+    dt, (q, k, v) = _same_dtype(q, k, v)
+    mask = _mask(mask)
+    Mq, Mk = q.shape[0], k.shape[0]
+    assert Mq % n_seq == 0 and Mk % n_seq == 0
+    assert q.shape[1] == n_q * d and k.shape == (Mk, n_kv * d) and v.shape == k.shape
+    T_q, T_k = Mq // n_seq, Mk // n_seq
+    assert not causal or T_k >= T_q
+    ng = mask.shape[1]
+    assert mask.shape[0] == Mq and n_q % ng == 0 and n_q % n_kv == 0
+    o = np.empty((Mq, n_q * d), np.float64)
+    _load().oracle_attention(dt, int(round_bf16), n_seq, T_q, T_k, n_q, n_kv, d, ng, int(causal),
+                             _p(mask), _p(q), _p(k), _p(v), _p(o))
+    return o

@@ -16,7 +16,10 @@
  *   - the complete masked SwiGLU FFN of equation (3);
  *   - the bottleneck router in its inference form (Section 3.1, "Routing
  *     Components"): logits X W1 W2 read as n_groups pairs, and the mask bit
- *     "class 0 (execute) wins the pair".
+ *     "class 0 (execute) wins the pair";
+ *   - head-group masked attention at prefill (Section 3.1 equations (1)-(2);
+ *     Appendix B, Algorithm 4): an active (token, head group) attends as in
+ *     standard scaled dot-product attention, an inactive one outputs zeros.
  *
  * Every floating-point input is widened exactly to fp64 (bf16 bit patterns or
  * fp32 values) and every sum is accumulated in fp64 in natural index order,
@@ -227,6 +230,66 @@ void oracle_router(int dtype, int64_t M, int32_t D, int32_t r, int32_t n_groups,
         mask[t * n_groups + g] = logits[t * J + 2 * g] >= logits[t * J + 2 * g + 1] ? 1 : 0;
     }
     free(h);
+  }
+}
+
+/* ---- head-group masked attention, prefill (Section 3.1; Algorithm 4) --- */
+
+/* n_seq sequences, T_q queries and T_k keys each (query row t = b*T_q + p,
+ * key row b*T_k + j).  Query head h belongs to head group h / (n_q / n_groups)
+ * and reads KV head h / (n_q / n_kv).  For an active (t, group):
+ * o[t][h] = sum_j softmax_j(q[t][h] . k[j][hkv] / sqrt(d)) v[j][hkv] over the
+ * keys of sequence b, and with causal masking only those with
+ * j <= p + (T_k - T_q) (queries are the last T_q positions of the sequence);
+ * for an inactive one o[t][h] = 0.  The softmax is the textbook one: subtract
+ * the row maximum, exponentiate, divide by the sum, all in fp64.  Layouts:
+ * q/o [n_seq*T_q][n_q*d], k/v [n_seq*T_k][n_kv*d], mask [n_seq*T_q][n_groups]. */
+void oracle_attention(int dtype, int round_bf16, int64_t n_seq, int32_t T_q, int32_t T_k,
+                      int32_t n_q, int32_t n_kv, int32_t d, int32_t n_groups, int causal,
+                      const uint8_t* mask, const void* q, const void* k, const void* v, double* o) {
+  const int64_t M = n_seq * T_q;
+  const int32_t hpg = n_q / n_groups, qpk = n_q / n_kv;
+  const int64_t delta = (int64_t)T_k - T_q;
+  const double scale = 1.0 / sqrt((double)d);
+#pragma omp parallel
+  {
+    double* s = (double*)malloc(sizeof(double) * (size_t)(T_k > 0 ? T_k : 1));
+    double* acc = (double*)malloc(sizeof(double) * (size_t)(d > 0 ? d : 1));
+#pragma omp for schedule(static)
+    for (int64_t t = 0; t < M; ++t) {
+      const int64_t b = t / T_q, p = t % T_q;
+      const int64_t nk = causal ? p + delta + 1 : T_k; /* keys 0 .. nk-1 are visible */
+      const int64_t kr0 = b * T_k;                     /* first key row of sequence b */
+      for (int32_t h = 0; h < n_q; ++h) {
+        double* out = o + t * (int64_t)n_q * d + (int64_t)h * d;
+        if (mask[t * n_groups + h / hpg] == 0) {
+          for (int32_t e = 0; e < d; ++e) out[e] = 0.0;
+          continue;
+        }
+        const int32_t hk = h / qpk;
+        double mx = -INFINITY;
+        for (int64_t j = 0; j < nk; ++j) {
+          double dot = 0.0;
+          for (int32_t e = 0; e < d; ++e)
+            dot += load_elem(q, dtype, t * (int64_t)n_q * d + (int64_t)h * d + e) *
+                   load_elem(k, dtype, (kr0 + j) * (int64_t)n_kv * d + (int64_t)hk * d + e);
+          s[j] = dot * scale;
+          if (s[j] > mx) mx = s[j];
+        }
+        double z = 0.0;
+        for (int64_t j = 0; j < nk; ++j) {
+          s[j] = exp(s[j] - mx);
+          z += s[j];
+        }
+        for (int32_t e = 0; e < d; ++e) acc[e] = 0.0;
+        for (int64_t j = 0; j < nk; ++j)
+          for (int32_t e = 0; e < d; ++e)
+            acc[e] += s[j] * load_elem(v, dtype, (kr0 + j) * (int64_t)n_kv * d + (int64_t)hk * d + e);
+        for (int32_t e = 0; e < d; ++e) out[e] = store_round(acc[e] / z, round_bf16);
+      }
+    }
+    free(s);
+    free(acc);
   }
 }
 

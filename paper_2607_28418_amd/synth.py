@@ -155,6 +155,41 @@ def attn_case(seed: int, M: int, D: int, n_q: int, n_kv: int, hd: int, G: int,
     return AttnCase(x, wq, wk, wv, wo, a, m, G, n_q, n_kv, hd, dtype)
 
 
+@dataclass
+class AttnPrefillCase:
+    q: np.ndarray          # [n_seq*T_q][n_q*hd]
+    k: np.ndarray          # [n_seq*T_k][n_kv*hd]
+    v: np.ndarray          # [n_seq*T_k][n_kv*hd]
+    mask: np.ndarray       # [n_seq*T_q][n_groups]
+    n_seq: int
+    n_q: int
+    n_kv: int
+    hd: int
+    dtype: str
+
+    @property
+    def T_q(self):
+        return self.q.shape[0] // self.n_seq
+
+    @property
+    def T_k(self):
+        return self.k.shape[0] // self.n_seq
+
+
+def attn_prefill_case(seed: int, n_seq: int, T_q: int, T_k: int, n_q: int, n_kv: int, hd: int,
+                      n_groups: int, dtype: str = "bf16", mask: str = "topk", keep: float = 0.5,
+                      qk_std: float = 1.0) -> AttnPrefillCase:
+    """q, k ~ N(0, qk_std^2) (scores q.k/sqrt(hd) then have std qk_std^2),
+    v ~ N(0,1); the mask is drawn from the q rows (top-k of a random
+    projection, as for the projections' masks)."""
+    g = rng(seed)
+    q = normal(g, (n_seq * T_q, n_q * hd), qk_std, dtype)
+    k = normal(g, (n_seq * T_k, n_kv * hd), qk_std, dtype)
+    v = normal(g, (n_seq * T_k, n_kv * hd), 1.0, dtype)
+    m = make_mask(g, mask, n_seq * T_q, n_groups, keep, q)
+    return AttnPrefillCase(q, k, v, m, n_seq, n_q, n_kv, hd, dtype)
+
+
 # ---- the paper's workloads (synthetic stand-ins) ---------------------------
 
 @dataclass
@@ -186,6 +221,13 @@ WORKLOADS = {
         "attention projections bf16: D=4096, 32 heads x 128 in 8 groups of 4 "
         "heads (G=512), T=2048, top-4 of 8 groups",
         dict(M=2048, D=4096, n_q=32, n_kv=32, hd=128, G=512, dtype="bf16",
+             mask="topk", keep=0.5)),
+    "attn_prefill_llama3_8b": Workload(
+        "attn_prefill_llama3_8b",
+        "head-group masked causal attention bf16, Llama-3-8B heads: 32 q / 8 kv "
+        "heads x 128 in 8 head groups (one KV head each), T=8192 (one sequence), "
+        "q,k,v~N(0,1), top-4 of 8 groups per token",
+        dict(n_seq=1, T=8192, n_q=32, n_kv=8, hd=128, n_groups=8, dtype="bf16",
              mask="topk", keep=0.5)),
     "layer_llama3_8b": Workload(
         "layer_llama3_8b",

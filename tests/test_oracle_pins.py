@@ -358,3 +358,149 @@ def test_router_ties_execute(orc):
     w2 = np.tile(np.array([[1.0, -2.0]], np.float32), (6, 1))
     logits, mask = orc.router(x, w1, w2)
     assert (logits[:, 0::2] == logits[:, 1::2]).all() and mask.all()
+
+
+# ---------------------------------------------------------------- masked attention (prefill)
+
+def _read_golden_attention():
+    with open(os.path.join(GOLDEN, "attention_hand.txt")) as f:
+        lines = [ln.split() for ln in f if ln.strip() and not ln.startswith("#")]
+    sec, data = None, {}
+    for ln in lines:
+        if not ln[0].lstrip("-").replace(".", "").isdigit():
+            sec = ln[0]
+            data[sec] = []
+            continue
+        data[sec].append([float(v) for v in ln])
+    return {k: np.array(v) for k, v in data.items()}
+
+
+def test_attention_hand_fixture(orc):
+    d = _read_golden_attention()
+    n_seq, T_q, T_k, n_q, n_kv, hd, ng = (int(v) for v in d["dims"][0])
+    q, k, v = (d[s].astype(np.float32) for s in ("q", "k", "v"))
+    mask = d["mask"].astype(np.uint8)
+    assert mask.shape == (n_seq * T_q, ng)
+    for causal, key in ((True, "o_causal"), (False, "o_full")):
+        o = orc.attention(q, k, v, mask, n_seq, n_q, n_kv, hd, causal)
+        assert np.max(np.abs(o - d[key])) < 1e-15, key
+
+
+def _sdpa_dense(c, causal):
+    """All-ones-mask special case: torch's scaled_dot_product_attention on CPU
+    in fp64, KV heads repeated for grouped queries, queries aligned to the end
+    of each sequence (a boolean mask in the T_q < T_k case)."""
+    import torch.nn.functional as F
+    qpk = c.n_q // c.n_kv
+    out = []
+    for b in range(c.n_seq):
+        q = torch.from_numpy(f64(c.q[b * c.T_q:(b + 1) * c.T_q])).view(c.T_q, c.n_q, c.hd).transpose(0, 1)
+        k = torch.from_numpy(f64(c.k[b * c.T_k:(b + 1) * c.T_k])).view(c.T_k, c.n_kv, c.hd).transpose(0, 1)
+        v = torch.from_numpy(f64(c.v[b * c.T_k:(b + 1) * c.T_k])).view(c.T_k, c.n_kv, c.hd).transpose(0, 1)
+        k, v = k.repeat_interleave(qpk, 0), v.repeat_interleave(qpk, 0)
+        if causal and c.T_q == c.T_k:
+            o = F.scaled_dot_product_attention(q, k, v, is_causal=True)
+        elif causal:
+            vis = torch.ones(c.T_q, c.T_k, dtype=torch.bool).tril(c.T_k - c.T_q)
+            o = F.scaled_dot_product_attention(q, k, v, attn_mask=vis)
+        else:
+            o = F.scaled_dot_product_attention(q, k, v)
+        out.append(o.transpose(0, 1).reshape(c.T_q, c.n_q * c.hd).numpy())
+    return np.concatenate(out)
+
+
+@pytest.mark.parametrize("n_seq,T_q,T_k,n_q,n_kv,ng,causal", [
+    (1, 9, 9, 4, 4, 4, True), (2, 7, 7, 8, 2, 4, True), (2, 5, 12, 8, 2, 2, True),
+    (3, 6, 4, 4, 1, 2, False), (1, 1, 1, 2, 2, 1, True)])
+def test_attention_all_ones_is_sdpa(orc, n_seq, T_q, T_k, n_q, n_kv, ng, causal):
+    c = synth.attn_prefill_case(n_seq + T_q + T_k, n_seq, T_q, T_k, n_q, n_kv, 8, ng, mask="ones",
+                                qk_std=1.5)
+    o = orc.attention(c.q, c.k, c.v, c.mask, n_seq, n_q, n_kv, c.hd, causal)
+    assert rel_err(o, _sdpa_dense(c, causal)) < 1e-12
+
+
+def test_attention_mask_zeroes_inactive_and_leaves_active_alone(orc):
+    c = synth.attn_prefill_case(3, 2, 11, 11, 8, 2, 8, 4, mask="topk", keep=0.5)
+    ones = np.ones_like(c.mask)
+    o1 = orc.attention(c.q, c.k, c.v, ones, 2, 8, 2, 8, True)
+    om = orc.attention(c.q, c.k, c.v, c.mask, 2, 8, 2, 8, True)
+    keep = np.repeat(c.mask.astype(bool), 2 * 8, axis=1)   # 2 heads of 8 per group, contiguous
+    assert 0 < c.mask.mean() < 1
+    assert np.array_equal(om[keep], o1[keep]) and not om[~keep].any()
+    assert not np.signbit(om[~keep]).any()
+    zeros = orc.attention(c.q, c.k, c.v, np.zeros_like(c.mask), 2, 8, 2, 8, True)
+    assert not zeros.any() and not np.signbit(zeros).any()
+
+
+def test_attention_closed_forms(orc):
+    g = synth.rng(5)
+    # one key: every query returns that key's value row
+    v = g.standard_normal((1, 8)).astype(np.float32)
+    k = g.standard_normal((1, 8)).astype(np.float32)
+    q = g.standard_normal((1, 16)).astype(np.float32)
+    o = orc.attention(q, k, v, np.ones((1, 2), np.uint8), 1, 2, 1, 8, True)
+    assert np.array_equal(o, np.tile(v.astype(np.float64), (1, 2)))
+    # zero queries: equal scores, so causal rows average the value prefix
+    T = 6
+    k = g.standard_normal((T, 8)).astype(np.float32)
+    v = g.standard_normal((T, 8)).astype(np.float32)
+    o = orc.attention(np.zeros((T, 8), np.float32), k, v, np.ones((T, 1), np.uint8), 1, 1, 1, 8, True)
+    pref = np.cumsum(v.astype(np.float64), 0) / np.arange(1, T + 1)[:, None]
+    assert np.max(np.abs(o - pref)) < 1e-14
+    # two keys: the weights are logistic in the score gap
+    q = np.array([[3.0, -1.0, 0.5, 2.0]], np.float32)
+    k = np.array([[0.5, 0.0, 1.0, -1.0], [-0.25, 2.0, 0.0, 0.5]], np.float32)
+    v = np.array([[1.0, 0.0, 0.0, 0.0], [0.0, 1.0, 0.0, 0.0]], np.float32)
+    o = orc.attention(q, k, v, np.ones((1, 1), np.uint8), 1, 1, 1, 4, False)
+    gap = float((q[0].astype(np.float64) @ (k[0] - k[1]).astype(np.float64)) / 2.0)
+    assert abs(o[0, 0] - expit(gap)) < 1e-15 and abs(o[0, 1] - expit(-gap)) < 1e-15
+
+
+def test_attention_invariances(orc):
+    c = synth.attn_prefill_case(8, 1, 10, 10, 4, 2, 8, 2, mask="bernoulli", keep=0.7)
+    q, k, v = (synth.as_f32(a) for a in (c.q, c.k, c.v))
+    args = (1, 4, 2, 8)
+    base_c = orc.attention(q, k, v, c.mask, *args, True)
+    base_f = orc.attention(q, k, v, c.mask, *args, False)
+    # adding one vector to every key shifts a row's scores by a constant (a
+    # dyadic shift of bf16 values, so k + shift is exact in fp32)
+    g = synth.rng(9)
+    shift = np.tile((g.integers(-8, 9, (1, 8)) / 4.0).astype(np.float32), (1, 2))
+    ks = k + shift
+    assert np.array_equal(ks.astype(np.float64), k.astype(np.float64) + shift.astype(np.float64))
+    for causal, base in ((True, base_c), (False, base_f)):
+        o = orc.attention(q, ks, v, c.mask, *args, causal)
+        assert np.max(np.abs(o - base)) < 1e-12
+    # non-causal: permuting keys and values together changes nothing; permuting
+    # queries (with their mask rows) permutes the outputs
+    perm = g.permutation(10)
+    assert np.max(np.abs(orc.attention(q, k[perm], v[perm], c.mask, *args, False) - base_f)) < 1e-12
+    o = orc.attention(q[perm], k, v, c.mask[perm], *args, False)
+    assert np.array_equal(o, base_f[perm])
+    # causal: a query never sees later keys
+    k2, v2 = k.copy(), v.copy()
+    k2[6:] = 9.0
+    v2[6:] = -7.0
+    o = orc.attention(q, k2, v2, c.mask, *args, True)
+    assert np.array_equal(o[:6], base_c[:6]) and not np.array_equal(o[6:], base_c[6:])
+
+
+def test_attention_queries_are_the_last_positions(orc):
+    # T_q < T_k with causal masking equals the last T_q rows of the square call
+    c = synth.attn_prefill_case(12, 2, 9, 9, 4, 1, 8, 2, mask="topk", keep=0.5)
+    full = orc.attention(c.q, c.k, c.v, c.mask, 2, 4, 1, 8, True)
+    rows = np.concatenate([np.arange(b * 9 + 5, b * 9 + 9) for b in range(2)])
+    o = orc.attention(c.q[rows], c.k, c.v, c.mask[rows], 2, 4, 1, 8, True)
+    assert np.array_equal(o, full[rows])
+    # sequences are independent: each one alone gives the same rows
+    for b in range(2):
+        ob = orc.attention(c.q[b * 9:(b + 1) * 9], c.k[b * 9:(b + 1) * 9], c.v[b * 9:(b + 1) * 9],
+                           c.mask[b * 9:(b + 1) * 9], 1, 4, 1, 8, True)
+        assert np.array_equal(ob, full[b * 9:(b + 1) * 9])
+
+
+def test_attention_bf16_storage_rounding(orc):
+    c = synth.attn_prefill_case(4, 1, 8, 8, 4, 2, 8, 2)
+    o = orc.attention(c.q, c.k, c.v, c.mask, 1, 4, 2, 8, True)
+    ob = orc.attention(c.q, c.k, c.v, c.mask, 1, 4, 2, 8, True, round_bf16=True)
+    assert np.array_equal(ob, torch_bf16(o))
