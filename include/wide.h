@@ -181,6 +181,52 @@ wide_status_t wide_router(wide_dtype_t dt, int64_t M, int32_t d_model, int32_t r
                           void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * Head-group masked attention, prefill (WIDE Section 3.1, equations (1)-(2);
+ * Appendix B, Algorithm 4).  For query token t = b*T_q + p of sequence b and
+ * query head h in head group g = h / (group_size/head_dim):
+ *   o[t, h] = sum_j softmax_j(q[t, h] . k[b*T_k + j, h_kv] / sqrt(head_dim))
+ *             v[b*T_k + j, h_kv]     if mask[t][g] != 0, else +0,
+ * with h_kv = h / (n_q_heads/n_kv_heads), over the keys j of sequence b;
+ * with causal = 1 only keys j <= p + (T_k - T_q) (the queries are the last
+ * T_q of the sequence's T_k positions, as after a cached prefix).
+ *   dt        WIDE_BF16 (WIDE_ERR_UNSUPPORTED otherwise).
+ *   n_seq, T_q, T_k   sequences and their query / key lengths; causal needs
+ *             T_k >= T_q, and T_k >= 1 whenever there are queries.
+ *   n_q_heads, n_kv_heads, head_dim (128 only, else WIDE_ERR_UNSUPPORTED),
+ *   group_size  as for wide_qkvo_masked (a multiple of head_dim dividing
+ *             n_q_heads*head_dim; group g holds contiguous heads).
+ *   mask      [n_seq*T_q][n_q_heads*head_dim/group_size] uint8.
+ *   idx, counts  optional reorder of `mask` (wide_mask_reorder over the
+ *             n_seq*T_q tokens: the same routing decision as the Q and O
+ *             projections, Appendix B); both NULL => computed internally.
+ *   q         [n_seq*T_q][n_q_heads*head_dim]; k, v [n_seq*T_k][n_kv_heads*head_dim].
+ *   o         [n_seq*T_q][n_q_heads*head_dim] out; every element is written
+ *             (inactive (token, group) rows +0).
+ *   ws        >= wide_attention_workspace_size(...) bytes (a transposed copy
+ *             of V, per-sequence offsets, and the reorder when idx is NULL).
+ * Arithmetic: scores as fp32 sums of bf16 products; softmax in fp32 (online,
+ * one running maximum and sum per query); the probabilities are rounded to
+ * bf16 for the P.V product, which accumulates in fp32; o is rounded to bf16.
+ * n_seq*T_q == 0 is a valid no-op.
+ */
+wide_status_t wide_attention_masked(wide_dtype_t dt, int64_t n_seq, int32_t T_q, int32_t T_k,
+                                    int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                    int32_t group_size, int32_t causal, const uint8_t* mask,
+                                    const int32_t* idx, const int32_t* counts, const void* q,
+                                    const void* k, const void* v, void* o, void* ws,
+                                    size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Workspace bytes for wide_attention_masked (with_reorder != 0: idx/counts
+ * will be NULL and the reorder is held in the workspace).  SIZE_MAX for
+ * shapes wide_attention_masked would reject (causal-only checks aside).
+ */
+size_t wide_attention_workspace_size(int64_t n_seq, int32_t T_q, int32_t T_k,
+                                     int32_t n_q_heads, int32_t n_kv_heads,
+                                     int32_t head_dim, int32_t group_size,
+                                     int32_t with_reorder);
+
+/*
  * Workspace bytes needed by one call (0 is a valid answer).
  *   op = WIDE_OP_REORDER: d_inner = n_groups, group_size = 1, d_model unused.
  *   op = WIDE_OP_FFN:     d_inner = d_ff.

@@ -14,7 +14,7 @@ import os
 
 __all__ = [
     "WideError", "lib", "wide_mask_reorder", "wide_ffn_masked", "wide_qkvo_masked", "wide_router",
-    "wide_workspace_size", "wide_set_option", "wide_get_option", "wide_timing_enable",
+    "wide_attention_masked", "wide_attention_workspace_size", "wide_workspace_size", "wide_set_option", "wide_get_option", "wide_timing_enable",
     "wide_timing_reset", "wide_timing_query", "LIB_PATH",
     "OP_REORDER", "OP_FFN", "OP_QKV", "OP_O", "OP_ROUTER", "PHASE_QKV", "PHASE_O", "F32", "BF16",
 ]
@@ -57,6 +57,11 @@ def lib() -> ctypes.CDLL:
                                        vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.wide_router.restype = ci
         L.wide_router.argtypes = [ci, i64, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.wide_attention_masked.restype = ci
+        L.wide_attention_masked.argtypes = [ci, i64, i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp,
+                                            vp, vp, vp, vp, sz, vp]
+        L.wide_attention_workspace_size.restype = sz
+        L.wide_attention_workspace_size.argtypes = [i64, i32, i32, i32, i32, i32, i32, i32]
         L.wide_workspace_size.restype = sz
         L.wide_workspace_size.argtypes = [ci, ci, i64, i32, i32, i32]
         L.wide_set_option.restype = ci
@@ -263,3 +268,32 @@ def wide_router(x, w1, w2, mask=None, logits=False, reorder=False, idx=None, cou
     if reorder:
         out += [idx, counts]
     return out[0] if len(out) == 1 else tuple(out)
+
+
+def wide_attention_workspace_size(n_seq, T_q, T_k, n_q, n_kv, head_dim, group_size, with_reorder=True):
+    return int(lib().wide_attention_workspace_size(n_seq, T_q, T_k, n_q, n_kv, head_dim, group_size,
+                                                   int(bool(with_reorder))))
+
+
+def wide_attention_masked(q, k, v, mask, n_seq, n_q, n_kv, head_dim, group_size, causal=True,
+                          idx=None, counts=None, o=None, ws=None):
+    """Head-group masked attention (prefill).  q [n_seq*T_q][n_q*head_dim],
+    k, v [n_seq*T_k][n_kv*head_dim], mask [n_seq*T_q][n_groups] uint8;
+    idx/counts optional (a reorder of `mask`).  Returns o, same shape as q."""
+    torch = _torch()
+    _contig(q, k, v, mask, idx, counts, o)
+    if n_seq > 0 and (q.shape[0] % n_seq or k.shape[0] % n_seq):
+        raise ValueError("q and k rows must split evenly into n_seq sequences")
+    T_q = q.shape[0] // n_seq if n_seq > 0 else 0
+    T_k = k.shape[0] // n_seq if n_seq > 0 else 0
+    if o is None:
+        o = torch.empty_like(q)
+    if ws is None:
+        need = wide_attention_workspace_size(n_seq, T_q, T_k, n_q, n_kv, head_dim, group_size, idx is None)
+        # (shapes the library rejects: no workspace, the call reports why)
+        ws = None if need == SIZE_MAX else _workspace(need, q.device)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("wide_attention_masked", lib().wide_attention_masked(
+        _dtype_code(q), n_seq, T_q, T_k, n_q, n_kv, head_dim, group_size, int(bool(causal)),
+        _p(mask), _p(idx), _p(counts), _p(q), _p(k), _p(v), _p(o), _p(ws), nbytes, _stream(q)))
+    return o

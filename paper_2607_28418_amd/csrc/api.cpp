@@ -7,6 +7,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -782,3 +783,129 @@ wide_status_t wide_timing_query(const char* name_substr, double* total_ms, int64
 }
 
 }  // extern "C"
+
+// ---- masked attention (prefill) -------------------------------------------------
+namespace {
+
+struct AttnShape {
+  int64_t M = 0, Mk = 0;
+  int T_kp = 0, ng = 0, hpg = 0, qpk = 0;
+};
+
+wide_status_t attention_shape(wide_dtype_t dt, int64_t n_seq, int T_q, int T_k, int nq, int nkv,
+                              int hd, int G, int causal, AttnShape& s) {
+  if (dt != WIDE_F32 && dt != WIDE_BF16) return fail(WIDE_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
+  if (n_seq < 0 || T_q < 0 || T_k < 0) return fail(WIDE_ERR_INVALID_ARG, "n_seq, T_q and T_k must be >= 0");
+  if (nq <= 0 || nkv <= 0 || hd <= 0 || G <= 0)
+    return fail(WIDE_ERR_INVALID_ARG, "head counts, head_dim and group_size must be positive");
+  if (nq % nkv) return fail(WIDE_ERR_INVALID_ARG, "n_q_heads=%d not a multiple of n_kv_heads=%d", nq, nkv);
+  if (G % hd) return fail(WIDE_ERR_INVALID_ARG, "group_size=%d not a multiple of head_dim=%d", G, hd);
+  if ((int64_t)nq * hd % G) return fail(WIDE_ERR_INVALID_ARG, "group_size=%d does not divide n_q*head_dim", G);
+  if (causal != 0 && causal != 1) return fail(WIDE_ERR_INVALID_ARG, "causal must be 0 or 1");
+  s.M = n_seq * (int64_t)T_q;
+  s.Mk = n_seq * (int64_t)T_k;
+  if (s.M >= (int64_t(1) << 31) || s.Mk >= (int64_t(1) << 31))
+    return fail(WIDE_ERR_INVALID_ARG, "n_seq*T_q and n_seq*T_k must be < 2^31");
+  if (s.M > 0 && T_k == 0) return fail(WIDE_ERR_INVALID_ARG, "queries with no keys (T_k = 0)");
+  if (causal && T_k < T_q)
+    return fail(WIDE_ERR_INVALID_ARG, "causal attention needs T_k >= T_q (queries are the last T_q positions)");
+  s.ng = (int)((int64_t)nq * hd / G);
+  if (s.ng > 4096) return fail(WIDE_ERR_UNSUPPORTED, "more than 4096 groups");
+  if (dt != WIDE_BF16) return fail(WIDE_ERR_UNSUPPORTED, "attention runs on bf16 only");
+  if (hd != wide::kAttnHeadDim) return fail(WIDE_ERR_UNSUPPORTED, "attention needs head_dim 128 (got %d)", hd);
+  s.T_kp = (int)((T_k + 63) / 64 * 64);
+  s.hpg = G / hd;
+  s.qpk = nq / nkv;
+  return WIDE_OK;
+}
+
+struct AttnWS {
+  ReorderWS r;
+  uint16_t* vt = nullptr;
+  int32_t* seq_off = nullptr;
+};
+
+void carve_attention(Carve& c, int64_t n_seq, int nkv, const AttnShape& s, bool need_idx, AttnWS& w) {
+  if (need_idx) carve_reorder(c, s.M, s.ng, true, w.r);
+  w.vt = c.take<uint16_t>((size_t)n_seq * nkv * wide::kAttnHeadDim * (size_t)s.T_kp);
+  w.seq_off = c.take<int32_t>((size_t)s.ng * (size_t)(n_seq + 1));
+}
+
+}  // namespace
+
+size_t wide_attention_workspace_size(int64_t n_seq, int32_t T_q, int32_t T_k, int32_t n_q_heads,
+                                     int32_t n_kv_heads, int32_t head_dim, int32_t group_size,
+                                     int32_t with_reorder) {
+  AttnShape s;
+  const std::string keep = g_last_error;
+  const bool bad = attention_shape(WIDE_BF16, n_seq, T_q, T_k, n_q_heads, n_kv_heads, head_dim, group_size,
+                                   0, s) != WIDE_OK;
+  g_last_error = keep;
+  if (bad) return SIZE_MAX;
+  if (s.M == 0) return 0;
+  Carve c(nullptr);
+  AttnWS w;
+  carve_attention(c, n_seq, n_kv_heads, s, with_reorder != 0, w);
+  return c.off;
+}
+
+wide_status_t wide_attention_masked(wide_dtype_t dt, int64_t n_seq, int32_t T_q, int32_t T_k,
+                                    int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                    int32_t group_size, int32_t causal, const uint8_t* mask,
+                                    const int32_t* idx, const int32_t* counts, const void* q,
+                                    const void* k, const void* v, void* o, void* ws, size_t ws_bytes,
+                                    hipStream_t stream) {
+  AttnShape s;
+  CHECK(attention_shape(dt, n_seq, T_q, T_k, n_q_heads, n_kv_heads, head_dim, group_size, causal, s));
+  if ((idx == nullptr) != (counts == nullptr))
+    return fail(WIDE_ERR_INVALID_ARG, "idx and counts must both be given or both be NULL");
+  if (s.M == 0) return ok();
+  CHECK(check_ptr(mask, "mask", false));
+  CHECK(check_ptr(q, "q"));
+  CHECK(check_ptr(k, "k"));
+  CHECK(check_ptr(v, "v"));
+  CHECK(check_ptr(o, "o"));
+  if (idx) {
+    CHECK(check_ptr(idx, "idx", false));
+    CHECK(check_ptr(counts, "counts", false));
+  }
+  {
+    Carve c0(nullptr);
+    AttnWS w0;
+    carve_attention(c0, n_seq, n_kv_heads, s, idx == nullptr, w0);
+    CHECK(check_ws(ws, ws_bytes, c0.off));
+  }
+  Carve c(ws);
+  AttnWS w;
+  carve_attention(c, n_seq, n_kv_heads, s, idx == nullptr, w);
+  hipError_t e;
+  if (!idx) {
+    if ((e = wide::launch_reorder(mask, s.M, s.ng, w.r.idx, w.r.cnt, w.r.chunk_cnt, w.r.chunk_off, stream)) !=
+        hipSuccess)
+      return hip_fail(e, "attention reorder");
+    idx = w.r.idx;
+    counts = w.r.cnt;
+  }
+  wide::AttnArgs a{};
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.vt = w.vt;
+  a.o = static_cast<uint16_t*>(o);
+  a.idx = idx;
+  a.cnt = counts;
+  a.M = s.M;
+  a.n_seq = (int)n_seq;
+  a.T_q = T_q;
+  a.T_k = T_k;
+  a.T_kp = s.T_kp;
+  a.n_q = n_q_heads;
+  a.n_kv = n_kv_heads;
+  a.ng = s.ng;
+  a.hpg = s.hpg;
+  a.qpk = s.qpk;
+  a.causal = causal;
+  a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)head_dim));
+  if ((e = wide::launch_attention(a, static_cast<const uint16_t*>(v), w.seq_off, stream)) != hipSuccess)
+    return hip_fail(e, "attention");
+  return ok();
+}

@@ -1,0 +1,371 @@
+// Head-group masked attention at prefill on gfx950 (WIDE Section 3.1,
+// equations (1)-(2); Appendix B, Algorithm 4).
+//
+// An active (token, head group) gets standard scaled dot-product attention
+// over the keys of its sequence (with causal masking, the keys up to its own
+// position, queries being the last T_q of T_k positions); an inactive one
+// outputs +0.  The mask reorder of the projections is reused: idx[g] lists
+// group g's active tokens in ascending order, so one sequence's active rows
+// are a contiguous run of it, and query tiles are cut from that run (rows of
+// one tile are active by construction, the paper's s^(1) gather).
+//
+// Work split: one workgroup of four waves per (query tile, head block).  A
+// head block is HB query heads of one group that read one KV head (HB = 4 for
+// Llama-3-8B, where a group is exactly the four heads of a KV head); the four
+// waves are HB heads x (4/HB) blocks of 32 rows, so K/V tiles loaded once
+// into LDS serve all of them.  Per wave and key tile (64 keys):
+//   S^T[keys][queries] = K Q^T     16 MFMA 32x32x16 (A = K from LDS, B = Q^T
+//                                  held in registers for the whole loop)
+//   online softmax per query lane  (a query's 64 scores sit in lanes l and
+//                                  l^32, so the row max is one swap)
+//   O^T[d][queries] += V^T P^T     16 MFMA (A = V^T from LDS, B = P^T from
+//                                  the S^T registers, rounded to bf16)
+// Keeping the transposed products puts every per-query quantity (running
+// max, sum, rescale factor) in one lane.  The A operand of the first product
+// loads its 32 key rows in a permuted order chosen so that each lane's S^T
+// registers hold 8 consecutive keys per 16-key step, which is exactly the k
+// layout the second product's B operand needs; V therefore only has to be
+// transposed (by the prep kernel below, into the workspace), not permuted.
+//
+// Skipping, following Algorithm 4: tiles past a sequence's active count
+// exit (l = 0) after clearing their share of the inactive rows; the causal
+// key range of a tile stops at its last row's position (rows are sorted);
+// a wave whose rows see none of a key tile issues no MFMA for it (l = 2);
+// only key tiles crossing a row's causal limit evaluate the per-element
+// mask.
+#include "common.h"
+#include "kernels.h"
+#include "tile256.h"
+
+namespace wide {
+namespace {
+
+using t256::gptr_t;
+using t256::lptr_t;
+
+constexpr int kHd = 128;               // head dimension
+constexpr int kBN = 64;                // keys per tile
+constexpr int kAT = 256;               // threads per workgroup (4 waves)
+constexpr int kKSub = 64 * 64;         // one K half-tile [64 keys][64 dims]
+constexpr int kVt = kHd * kBN;         // V^T tile [128 dims][64 keys]
+constexpr int kStage = 2 * kKSub + kVt;  // bf16 elements per stage (32 KB)
+
+// LDS rows are 64 bf16 = 8 chunks of 16 bytes; logical chunk c of row r sits
+// at physical chunk c ^ f(r), which spreads the 16 rows that one 16-lane
+// phase of a 128-bit read touches over distinct bank groups.
+__device__ __forceinline__ int swz_f(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+__device__ __forceinline__ int swz(int r, int c) { return r * 64 + ((c ^ swz_f(r)) << 3); }
+
+__device__ __forceinline__ u32x4 lds16(const uint16_t* p) {
+  return *reinterpret_cast<const u32x4*>(p);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+template <int HB>
+__global__ __launch_bounds__(kAT, 2) void wide_attn_fwd(AttnArgs a) {
+  constexpr int RB = 4 / HB;    // 32-row blocks per workgroup
+  constexpr int BMW = 32 * RB;  // query rows per workgroup
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kStage];
+
+  const int per_hb = a.n_seq * a.n_slots;
+  const int lid = t256::xcd_remap(blockIdx.x, gridDim.x);
+  const int hbk = lid / per_hb;
+  const int rem = lid - hbk * per_hb;
+  const int b = rem / a.n_slots;
+  const int slot = a.n_slots - 1 - (rem - b * a.n_slots);  // long key ranges first
+  const int h0 = hbk * HB;
+  const int g = h0 / a.hpg, hkv = h0 / a.qpk;
+  const int64_t M = a.M;
+  const int32_t* idx_g = a.idx + (int64_t)g * M;
+  const int cnt_g = a.cnt[g];
+  int s0 = 0, s1 = cnt_g;
+  if (a.seq_off) {
+    s0 = a.seq_off[g * (a.n_seq + 1) + b];
+    s1 = a.seq_off[g * (a.n_seq + 1) + b + 1];
+  }
+  const int c = s1 - s0;  // active rows of (sequence b, group g)
+  const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
+  const int64_t ldq = (int64_t)a.n_q * kHd;
+  const int64_t seq0 = (int64_t)b * a.T_q;
+
+  // Inactive rows of this sequence sit at idx_g[cnt_g + (b*T_q - s0) ...];
+  // slot i clears rows [i*BMW, (i+1)*BMW) of that run for its HB heads.
+  {
+    constexpr int CPR = HB * kHd / 8;  // 16-byte chunks per row
+    const int64_t ib = (int64_t)cnt_g + (seq0 - s0);
+    const int r0 = slot * BMW, r1 = min(a.T_q - c, r0 + BMW);
+    for (int i = tid; i < (r1 - r0) * CPR; i += kAT) {
+      const int64_t t = idx_g[ib + r0 + i / CPR];
+      stg16(a.o + t * ldq + (int64_t)h0 * kHd + (i % CPR) * 8, u32x4{0, 0, 0, 0});
+    }
+  }
+  const int m0 = slot * BMW;
+  if (m0 >= c) return;  // l = 0: no active row in this tile
+
+  const int delta = a.T_k - a.T_q;
+  auto limit_of = [&](int64_t t) {  // last visible key of token t
+    return a.causal ? (int)(t - seq0) + delta : a.T_k - 1;
+  };
+  const int rb = w / HB, h = h0 + (w - rb * HB);
+  const int wr0 = m0 + rb * 32;
+  const bool wave_live = wr0 < c;
+  const int wr1 = min(c, wr0 + 32);
+  const int l32 = lane & 31, hi = lane >> 5;
+  const int myr = wr0 + l32;
+  const bool valid = myr < c;
+  const int64_t t = valid ? (int64_t)idx_g[s0 + myr] : 0;
+  const int plim = valid ? limit_of(t) : -1;
+  // rows ascend by position, so the first and last rows bound the limits
+  const int wmin = wave_live ? limit_of(idx_g[s0 + wr0]) : -1;
+  const int wmax = wave_live ? limit_of(idx_g[s0 + wr1 - 1]) : -1;
+  const int gmax = limit_of(idx_g[s0 + min(c, m0 + BMW) - 1]);
+  const int n_tiles = (gmax + kBN) / kBN;
+
+  // Q^T fragments (B operand): d-step s holds dims 16s + 8*hi .. +8 of the row.
+  u32x4 qf[8];
+  {
+    const uint16_t* qrow = a.q + t * ldq + (int64_t)h * kHd + hi * 8;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) qf[s] = valid ? ldg16(qrow + 16 * s) : u32x4{0, 0, 0, 0};
+  }
+
+  // Stage loads: 32 wave instructions of 1 KB (8 LDS rows each); wave 0 loads
+  // K dims 0-63, wave 1 K dims 64-127, waves 2-3 the 128 rows of V^T.  A lane
+  // keeps a 32-bit byte offset per instruction from a per-tile uniform base.
+  const int64_t ldk = (int64_t)a.n_kv * kHd;
+  const bool kwave = w < 2;
+  const char* kb0 = reinterpret_cast<const char*>(a.k + (int64_t)b * a.T_k * ldk + hkv * kHd + w * 64);
+  const char* vb0 = reinterpret_cast<const char*>(a.vt + ((int64_t)b * a.n_kv + hkv) * kHd * (int64_t)a.T_kp);
+  uint32_t off[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const int r = kwave ? q * 8 + lane / 8 : (w - 2) * 64 + q * 8 + lane / 8;
+    const int lc = (lane & 7) ^ swz_f(r);
+    off[q] = kwave ? (uint32_t)((r * ldk + lc * 8) * 2) : (uint32_t)(((int64_t)r * a.T_kp + lc * 8) * 2);
+  }
+  auto issue = [&](int jt, uint16_t* st) {
+    const int j0 = jt * kBN;
+    uint16_t* dst = st + (kwave ? w * kKSub : 2 * kKSub + (w - 2) * 64 * 64);
+    if (kwave) {
+      const char* base = kb0 + (int64_t)j0 * ldk * 2;
+      if (j0 + kBN <= a.T_k) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          __builtin_amdgcn_global_load_lds((gptr_t)(base + off[q]), (lptr_t)(dst + q * 8 * 64), 16, 0, 0);
+      } else {  // last, partial tile: rows past the end re-read the last key (finite, masked)
+        const int kmax = a.T_k - 1 - j0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int r = q * 8 + lane / 8;
+          const int lc = (lane & 7) ^ swz_f(r);
+          const uint32_t o = (uint32_t)((min(r, kmax) * ldk + lc * 8) * 2);
+          __builtin_amdgcn_global_load_lds((gptr_t)(base + o), (lptr_t)(dst + q * 8 * 64), 16, 0, 0);
+        }
+      }
+    } else {
+      const char* base = vb0 + (int64_t)j0 * 2;
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        __builtin_amdgcn_global_load_lds((gptr_t)(base + off[q]), (lptr_t)(dst + q * 8 * 64), 16, 0, 0);
+    }
+  };
+
+  // K rows in the A operand: lane row x = 8j + 4h' + i loads key
+  // 16(j/2) + 8h' + 4(j%2) + i, so S^T register r of lane half hi holds key
+  // 16(r/8) + 8*hi + r%8 of its 32-key block.
+  const int pi = 16 * (l32 >> 4) + 8 * ((l32 >> 2) & 1) + 4 * ((l32 >> 3) & 1) + (l32 & 3);
+
+  f32x16 O[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) O[i] = f32x16{};
+  float m = -INFINITY, z = 0.0f;
+  const float sc = a.scale_log2;
+
+  issue(0, smem);
+  for (int jt = 0; jt < n_tiles; ++jt) {
+    t256::wait_vm<0>();
+    t256::stage_barrier();
+    if (jt + 1 < n_tiles) issue(jt + 1, smem + ((jt + 1) & 1) * kStage);
+    const int j0 = jt * kBN;
+    if (!wave_live || j0 > wmax) continue;  // l = 2: no row of this wave sees the tile
+    const uint16_t* st = smem + (jt & 1) * kStage;
+
+    f32x16 S[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const uint16_t* ks = st + (s >> 2) * kKSub;
+      const int ch = 2 * (s & 3) + hi;
+      const u32x4 k0 = lds16(ks + swz(pi, ch));
+      const u32x4 k1 = lds16(ks + swz(32 + pi, ch));
+      S[0] = mfma32(k0, qf[s], S[0]);
+      S[1] = mfma32(k1, qf[s], S[1]);
+    }
+
+    // Per-element mask only where the tile crosses some row's limit (or the
+    // end of the keys); every other tile is fully visible to the wave.
+    if (j0 + kBN - 1 > wmin) {
+      const int lim = plim - j0 - 8 * hi;  // key offset past which this lane's row sees nothing
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          S[kb][r] = 32 * kb + 16 * (r >> 3) + (r & 7) > lim ? -INFINITY : S[kb][r];
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, S[kb][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mnew = fmaxf(m, mx * sc);
+    const float muse = mnew == -INFINITY ? 0.0f : mnew;  // a row with nothing visible yet
+    const float alpha = fast_exp2(m - muse);
+    float zs = 0.0f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = fast_exp2(fmaf(S[kb][r], sc, -muse));
+        S[kb][r] = p;
+        zs += p;
+      }
+    }
+    z = z * alpha + zs;
+    m = mnew;
+    if (__any(alpha != 1.0f)) {  // lazy rescale: skipped once the maxima settle
+#pragma unroll
+      for (int db = 0; db < 4; ++db) O[db] *= alpha;
+    }
+
+    const uint16_t* vts = st + 2 * kKSub;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        u32x4 pf;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) pf[e] = pack_bf16x2_hw(S[kb][8 * p + 2 * e], S[kb][8 * p + 2 * e + 1]);
+        const int ch = 4 * kb + 2 * p + hi;
+#pragma unroll
+        for (int db = 0; db < 4; ++db) {
+          const u32x4 vf = lds16(vts + swz(32 * db + l32, ch));
+          O[db] = mfma32(vf, pf, O[db]);
+        }
+      }
+    }
+  }
+
+  // Epilogue: the two halves of a query's sum, normalise, scatter the row.
+  const float zt = z + __shfl_xor(z, 32);
+  if (!valid) return;
+  const float inv = 1.0f / zt;
+  uint16_t* orow = a.o + t * ldq + (int64_t)h * kHd + 4 * hi;
+#pragma unroll
+  for (int db = 0; db < 4; ++db) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      uint2 v;
+      v.x = pack_bf16x2_hw(O[db][4 * j] * inv, O[db][4 * j + 1] * inv);
+      v.y = pack_bf16x2_hw(O[db][4 * j + 2] * inv, O[db][4 * j + 3] * inv);
+      *reinterpret_cast<uint2*>(orow + 32 * db + 8 * j) = v;
+    }
+  }
+}
+
+// Prep: V [n_seq*T_k][n_kv*128] -> V^T [n_seq][n_kv][128][T_kp] (zero past
+// T_k), one workgroup per (sequence, KV head, 64 keys); then, when there is
+// more than one sequence, one wave per (group, sequence boundary) finds where
+// each sequence's active run starts in idx[g] (a 64-way search of the sorted
+// list).
+__global__ __launch_bounds__(kAT) void wide_attn_prep(AttnArgs a, const uint16_t* v, int32_t* seq_off,
+                                                      int n_vt_blocks) {
+  __shared__ __attribute__((aligned(16))) uint16_t tile[64][kHd + 8];
+  const int tid = threadIdx.x;
+  if ((int)blockIdx.x < n_vt_blocks) {
+    const int nkt = a.T_kp / 64;
+    const int kt = blockIdx.x % nkt;
+    const int bh = blockIdx.x / nkt;  // b * n_kv + hkv
+    const int b = bh / a.n_kv, hkv = bh - b * a.n_kv;
+    const int64_t ldk = (int64_t)a.n_kv * kHd;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int cidx = tid + kAT * u;
+      const int r = cidx >> 4, cc = cidx & 15;
+      const int key = kt * 64 + r;
+      u32x4 d = {0, 0, 0, 0};
+      if (key < a.T_k) d = ldg16(v + ((int64_t)b * a.T_k + key) * ldk + hkv * kHd + cc * 8);
+      *reinterpret_cast<u32x4*>(&tile[r][cc * 8]) = d;
+    }
+    __syncthreads();
+    uint16_t* vt = a.vt + (int64_t)bh * kHd * a.T_kp;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int cidx = tid + kAT * u;
+      const int d = cidx >> 3, kc = cidx & 7;
+      u32x4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        o[e] = (uint32_t)tile[kc * 8 + 2 * e][d] | ((uint32_t)tile[kc * 8 + 2 * e + 1][d] << 16);
+      stg16(vt + (int64_t)d * a.T_kp + kt * 64 + kc * 8, o);
+    }
+    return;
+  }
+  // sequence offsets
+  const int wv = (blockIdx.x - n_vt_blocks) * (kAT / kWave) + wave_id();
+  const int nb = a.n_seq + 1;
+  if (wv >= a.ng * nb) return;
+  const int g = wv / nb, b = wv - g * nb;
+  const int lane = lane_id();
+  const int32_t* idx_g = a.idx + (int64_t)g * a.M;
+  const int cnt = a.cnt[g];
+  const int64_t key = (int64_t)b * a.T_q;
+  int lo = 0, hi = cnt;  // first position in [lo, hi] whose token is >= key
+  if (b == a.n_seq) {
+    lo = cnt;
+  } else {
+    while (hi - lo > 64) {
+      const int step = (hi - lo + 63) / 64;
+      const int p = lo + lane * step;
+      const bool below = p < hi && idx_g[p] < key;
+      const int k = __popcll(__ballot(below));
+      if (k == 0) { hi = lo; break; }
+      const int nlo = lo + (k - 1) * step + 1;
+      hi = min(hi, lo + k * step);
+      lo = nlo;
+    }
+    const int p = lo + lane;
+    const bool below = p < hi && idx_g[p] < key;
+    lo += __popcll(__ballot(below));
+  }
+  if (lane == 0) seq_off[g * nb + b] = lo;
+}
+
+}  // namespace
+
+int attn_heads_per_block(int hpg, int qpk) {
+  if (hpg % 4 == 0 && qpk % 4 == 0) return 4;
+  if (hpg % 2 == 0 && qpk % 2 == 0) return 2;
+  return 1;
+}
+
+int attn_slots(int T_q, int hb) { return (T_q + 32 * (4 / hb) - 1) / (32 * (4 / hb)); }
+
+hipError_t launch_attention(AttnArgs a, const uint16_t* v, int32_t* seq_off, hipStream_t s) {
+  if (a.M == 0) return hipSuccess;
+  const int hb = attn_heads_per_block(a.hpg, a.qpk);
+  a.n_slots = attn_slots(a.T_q, hb);
+  const int n_vt = a.n_seq * a.n_kv * (a.T_kp / 64);
+  const int n_off = a.n_seq > 1 ? (a.ng * (a.n_seq + 1) + 3) / 4 : 0;
+  wide_attn_prep<<<n_vt + n_off, kAT, 0, s>>>(a, v, seq_off, n_vt);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  a.seq_off = a.n_seq > 1 ? seq_off : nullptr;
+  const int64_t grid = (int64_t)(a.n_q / hb) * a.n_seq * a.n_slots;
+  if (hb == 4) wide_attn_fwd<4><<<(unsigned)grid, kAT, 0, s>>>(a);
+  else if (hb == 2) wide_attn_fwd<2><<<(unsigned)grid, kAT, 0, s>>>(a);
+  else wide_attn_fwd<1><<<(unsigned)grid, kAT, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace wide

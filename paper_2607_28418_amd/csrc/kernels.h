@@ -166,6 +166,27 @@ struct RouterArgs {
 };
 hipError_t launch_router(const RouterArgs& a, hipStream_t s);
 
+// ---- masked attention, prefill (attention.hip)
+constexpr int kAttnHeadDim = 128;
+struct AttnArgs {
+  const uint16_t* q;        // [n_seq*T_q][n_q*128] bf16
+  const uint16_t* k;        // [n_seq*T_k][n_kv*128] bf16
+  uint16_t* vt;             // workspace: V^T [n_seq][n_kv][128][T_kp] bf16
+  uint16_t* o;              // [n_seq*T_q][n_q*128] bf16 out
+  const int32_t* idx;       // [ng][M] reorder of the mask (M = n_seq*T_q)
+  const int32_t* cnt;       // [ng]
+  const int32_t* seq_off;   // set by launch_attention
+  int64_t M;
+  int n_seq, T_q, T_k, T_kp;  // T_kp = T_k rounded up to 64
+  int n_q, n_kv, ng, hpg, qpk, causal;
+  int n_slots;              // set by launch_attention
+  float scale_log2;         // log2(e) / sqrt(128)
+};
+// seq_off: workspace of ng*(n_seq+1) ints (used when n_seq > 1).
+hipError_t launch_attention(AttnArgs a, const uint16_t* v, int32_t* seq_off, hipStream_t s);
+int attn_heads_per_block(int hpg, int qpk);
+int attn_slots(int T_q, int hb);
+
 hipError_t launch_gemv_n(const GVNArgs& a, bool swiglu, hipStream_t s);
 hipError_t launch_gemv_k(const GVKArgs& a, hipStream_t s);
 

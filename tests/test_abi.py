@@ -142,3 +142,48 @@ def test_router_workspace_size():
     assert W.wide_workspace_size(W.OP_ROUTER, W.F32, 8192, 4096, 112, 32) == W.SIZE_MAX
     assert W.wide_workspace_size(W.OP_ROUTER, W.BF16, 8192, 4000, 112, 32) == W.SIZE_MAX
     assert W.wide_workspace_size(W.OP_ROUTER, W.BF16, 8192, 4096, 112, 33) == W.SIZE_MAX
+
+
+def attention(dt=W.BF16, n_seq=1, T_q=256, T_k=256, nq=32, nkv=8, hd=128, G=512, causal=1, mask=A, idx=None,
+              cnt=None, q=A, k=A, v=A, o=A, ws=A, ws_bytes=1 << 40):
+    return W.lib().wide_attention_masked(dt, n_seq, T_q, T_k, nq, nkv, hd, G, causal, mask, idx, cnt, q, k, v,
+                                         o, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(dt=W.F32), W.ERR_UNSUPPORTED, "bf16"),
+    (dict(dt=7), W.ERR_INVALID_ARG, "dtype"),
+    (dict(hd=64, G=256), W.ERR_UNSUPPORTED, "head_dim 128"),
+    (dict(nq=30), W.ERR_INVALID_ARG, "multiple of n_kv_heads"),
+    (dict(G=192), W.ERR_INVALID_ARG, "multiple of head_dim"),
+    (dict(G=128 * 3), W.ERR_INVALID_ARG, "does not divide"),
+    (dict(T_k=100), W.ERR_INVALID_ARG, "T_k >= T_q"),
+    (dict(T_k=0, causal=0), W.ERR_INVALID_ARG, "no keys"),
+    (dict(causal=2), W.ERR_INVALID_ARG, "causal"),
+    (dict(n_seq=-1), W.ERR_INVALID_ARG, ">= 0"),
+    (dict(n_seq=1 << 20, T_q=1 << 12), W.ERR_INVALID_ARG, "2^31"),
+    (dict(idx=A), W.ERR_INVALID_ARG, "both"),
+    (dict(q=MIS), W.ERR_INVALID_ARG, "q is not 16-byte aligned"),
+    (dict(v=None), W.ERR_INVALID_ARG, "v is NULL"),
+    (dict(mask=None), W.ERR_INVALID_ARG, "mask is NULL"),
+    (dict(ws_bytes=0), W.ERR_WORKSPACE, "workspace"),
+    (dict(ws=None), W.ERR_WORKSPACE, "workspace"),
+])
+def test_attention_validation(kw, status, msg):
+    assert attention(**kw) == status
+    assert msg in err()
+
+
+def test_attention_empty_is_ok_and_non_causal_allows_short_keys():
+    assert attention(n_seq=0, mask=None, q=None, k=None, v=None, o=None, ws=None, ws_bytes=0) == W.OK
+    assert attention(T_q=0, T_k=0, mask=None, q=None, k=None, v=None, o=None, ws=None, ws_bytes=0) == W.OK
+
+
+def test_attention_workspace_size():
+    n = W.wide_attention_workspace_size(1, 8192, 8192, 32, 8, 128, 512, True)
+    n0 = W.wide_attention_workspace_size(1, 8192, 8192, 32, 8, 128, 512, False)
+    # the transposed V (8 KV heads x 128 x 8192 bf16) is always there; the reorder only on request
+    assert n0 >= 8 * 128 * 8192 * 2 and n > n0 + 8 * 8192 * 4
+    assert W.wide_attention_workspace_size(2, 100, 130, 8, 2, 128, 256, False) >= 2 * 2 * 128 * 192 * 2
+    assert W.wide_attention_workspace_size(1, 0, 0, 32, 8, 128, 512, True) == 0
+    assert W.wide_attention_workspace_size(1, 64, 64, 32, 8, 64, 512, True) == W.SIZE_MAX

@@ -1,0 +1,170 @@
+"""GPU parity of the head-group masked attention (prefill) against the fp64
+oracle, through the C ABI.
+
+Tolerance, derived from the kernel's arithmetic (it rounds the softmax
+probabilities P to bf16 for the P.V product and stores o in bf16): with unit
+roundoff u = 2^-8, the rounded P moves an output by at most
+u * sum_j w_j |v_j|, i.e. u times attention applied to |V| (w = the softmax
+weights), which the oracle computes; fp32 scores, exponentials and sums add
+at most (2^-12 + T_k 2^-24) of the same quantity; storing o in bf16 adds at
+most one bf16 ulp of the stored value.  Every element must satisfy the bound
+(inactive rows: exactly +0), and the mean error must stay under 1e-3.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_28418_amd as W
+from paper_2607_28418_amd import synth
+from tests._helpers import dev, to_dev, to_np64
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print("[case]", *a, file=sys.stderr, flush=True)
+
+
+def bf16_ulp_arr(x):
+    a = np.abs(x)
+    e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
+    return np.where(a > 0, 2.0 ** (e - 7), 0.0)
+
+
+def attention_bound(orc, q, k, v, mask, n_seq, n_q, n_kv, hd, causal, T_k):
+    vabs = np.abs(synth.as_f32(v)).astype(np.float32)
+    a_abs = orc.attention(synth.as_f32(q), synth.as_f32(k), vabs, mask, n_seq, n_q, n_kv, hd, causal)
+    return (2.0 ** -8 + 2.0 ** -12 + T_k * 2.0 ** -24) * a_abs
+
+
+def check_rows(got, ref, bound, mask_rows, hpg_feat, what):
+    """got/ref/bound [rows][n_q*hd] float64; inactive (row, group) blocks must be +0."""
+    assert np.isfinite(got).all(), f"{what}: non-finite output"
+    inactive = ~np.repeat(mask_rows.astype(bool), hpg_feat, axis=1)
+    assert not got[inactive].any() and not np.signbit(got[inactive]).any(), f"{what}: inactive rows not +0"
+    err = np.abs(got - ref)
+    allow = bound + bf16_ulp_arr(got)
+    worst = float(np.max(err - allow)) if err.size else 0.0
+    assert worst <= 0.0, f"{what}: {int((err > allow).sum())} elements over the bound (worst excess {worst:.3g})"
+    mae = float(err.mean()) if err.size else 0.0
+    assert mae <= 1e-3, f"{what}: mae {mae:.3g}"
+    return mae
+
+
+def run_case(orc, n_seq, T_q, T_k, n_q, n_kv, G, causal, mask="topk", keep=0.5, qk_std=1.0, seed=0,
+             given_reorder=False):
+    hd = 128
+    ng = n_q * hd // G
+    c = synth.attn_prefill_case(seed, n_seq, T_q, T_k, n_q, n_kv, hd, ng, mask=mask, keep=keep,
+                                qk_std=qk_std)
+    q, k, v, m = (to_dev(a) for a in (c.q, c.k, c.v, c.mask))
+    o = torch.full_like(q, float("nan"))   # every element must be written
+    idx = cnt = None
+    if given_reorder:
+        idx, cnt = W.wide_mask_reorder(m)
+    W.wide_attention_masked(q, k, v, m, n_seq, n_q, n_kv, hd, G, causal, idx=idx, counts=cnt, o=o)
+    torch.cuda.synchronize()
+    got = to_np64(o)
+    ref = orc.attention(c.q, c.k, c.v, c.mask, n_seq, n_q, n_kv, hd, causal)
+    bound = attention_bound(orc, c.q, c.k, c.v, c.mask, n_seq, n_q, n_kv, hd, causal, T_k)
+    check_rows(got, ref, bound, c.mask, G, f"attention {n_seq}x{T_q}/{T_k} {n_q}/{n_kv} G={G}")
+    return c, got
+
+
+@pytest.mark.parametrize("n_seq,T_q,T_k,n_q,n_kv,G,causal,mask,qk_std", [
+    (1, 200, 200, 8, 2, 256, True, "topk", 1.0),      # two heads per workgroup
+    (2, 150, 150, 4, 4, 128, True, "bernoulli", 1.0),  # one head, 128 rows per workgroup
+    (1, 300, 300, 8, 2, 512, True, "topk", 1.0),      # four heads of one KV head per workgroup
+    (3, 70, 130, 8, 2, 512, True, "topk", 1.0),       # queries after a 60-key prefix, 3 sequences
+    (2, 100, 37, 4, 1, 256, False, "bernoulli", 1.0),  # non-causal, ragged key tile, T_k < T_q
+    (1, 64, 64, 2, 2, 128, True, "bernoulli", 2.5),   # peaked softmax
+    (5, 1, 77, 8, 2, 512, True, "bernoulli", 1.0),    # one query per sequence
+    (2, 257, 257, 32, 8, 512, True, "topk", 1.5),     # Llama-3-8B heads
+    (1, 129, 129, 8, 8, 1024, False, "bernoulli", 1.0),
+])
+def test_attention_matches_oracle(orc, n_seq, T_q, T_k, n_q, n_kv, G, causal, mask, qk_std):
+    say("attention", n_seq, T_q, T_k, n_q, n_kv, G, causal, mask, qk_std)
+    run_case(orc, n_seq, T_q, T_k, n_q, n_kv, G, causal, mask=mask, qk_std=qk_std, seed=T_q + n_q)
+
+
+@pytest.mark.parametrize("kind", ["zeros", "ones"])
+def test_attention_degenerate_masks(orc, kind):
+    say("attention mask", kind)
+    run_case(orc, 2, 96, 96, 8, 2, 512, True, mask=kind)
+
+
+def test_attention_given_reorder_is_bitwise_same(orc):
+    say("attention given reorder")
+    c, got = run_case(orc, 2, 180, 180, 8, 2, 256, True, seed=3)
+    _, got2 = run_case(orc, 2, 180, 180, 8, 2, 256, True, seed=3, given_reorder=True)
+    assert np.array_equal(got, got2)
+
+
+def test_attention_never_reads_inactive_queries(orc):
+    say("attention poisoned inactive q")
+    n_seq, T, n_q, n_kv, G, hd = 1, 160, 8, 2, 256, 128
+    c = synth.attn_prefill_case(11, n_seq, T, T, n_q, n_kv, hd, n_q * hd // G)
+    q, k, v, m = (to_dev(a) for a in (c.q, c.k, c.v, c.mask))
+    o1 = W.wide_attention_masked(q, k, v, m, n_seq, n_q, n_kv, hd, G, True)
+    inactive = ~np.repeat(c.mask.astype(bool), G, axis=1)
+    qp = q.clone()
+    qp[torch.from_numpy(inactive).to(dev())] = float("nan")
+    o2 = W.wide_attention_masked(qp, k, v, m, n_seq, n_q, n_kv, hd, G, True)
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+
+
+def test_attention_empty():
+    say("attention empty")
+    z = torch.zeros((0, 256), dtype=torch.bfloat16, device=dev())
+    zk = torch.zeros((0, 128), dtype=torch.bfloat16, device=dev())
+    o = W.wide_attention_masked(z, zk, zk, torch.zeros((0, 2), dtype=torch.uint8, device=dev()),
+                                1, 2, 1, 128, 128, True)
+    torch.cuda.synchronize()
+    assert o.shape == (0, 256)
+
+
+@pytest.mark.parametrize("keep", [0.5, 0.25])
+def test_attention_llama3_8b_full_sampled(orc, keep):
+    """Full size (one sequence of 8192 tokens, 32/8 heads, 8 groups), checked
+    on sampled rows: the oracle computes a row at position p from keys 0..p."""
+    say("attention full llama3-8b T=8192 keep", keep)
+    T, n_q, n_kv, G, hd = 8192, 32, 8, 512, 128
+    c = synth.attn_prefill_case(21, 1, T, T, n_q, n_kv, hd, n_q * hd // G, keep=keep)
+    q, k, v, m = (to_dev(a) for a in (c.q, c.k, c.v, c.mask))
+    o = torch.full_like(q, float("nan"))
+    W.wide_attention_masked(q, k, v, m, 1, n_q, n_kv, hd, G, True, o=o)
+    torch.cuda.synchronize()
+    got = to_np64(o)
+    assert np.isfinite(got).all()
+    g = synth.rng(5)
+    rows = np.unique(np.concatenate([[0, 1, 63, 64, 4095, T - 2, T - 1], g.integers(0, T, 17)]))
+    for p in rows:
+        sl = slice(p, p + 1)
+        args = (c.q[sl], c.k[:p + 1], c.v[:p + 1], c.mask[sl], 1, n_q, n_kv, hd, True)
+        ref = orc.attention(*args)
+        bound = attention_bound(orc, *args, T_k=p + 1)
+        check_rows(got[sl], ref, bound, c.mask[sl], G, f"row {p}")
+
+
+@pytest.mark.parametrize("n_seq,T_q,T_k,n_q,n_kv,G,causal", [
+    (2, 300, 300, 8, 2, 512, True), (3, 70, 133, 8, 2, 256, True), (1, 200, 90, 4, 4, 128, False)])
+def test_attention_zero_queries_are_exact_means(orc, n_seq, T_q, T_k, n_q, n_kv, G, causal):
+    """q = 0 makes every score 0, so every probability is exactly 1 (no bf16
+    rounding of P): each active output is the mean of the visible value rows
+    up to fp32 summation, which pins key ranges, causal limits and sequence
+    boundaries far more tightly than the general bound."""
+    say("attention zero queries", n_seq, T_q, T_k, n_q, n_kv, G, causal)
+    hd = 128
+    c = synth.attn_prefill_case(7 + T_q, n_seq, T_q, T_k, n_q, n_kv, hd, n_q * hd // G, mask="bernoulli")
+    qz = np.zeros_like(c.q)
+    q, k, v, m = (to_dev(a) for a in (qz, c.k, c.v, c.mask))
+    o = W.wide_attention_masked(q, k, v, m, n_seq, n_q, n_kv, hd, G, causal)
+    torch.cuda.synchronize()
+    got = to_np64(o)
+    ref = orc.attention(qz, c.k, c.v, c.mask, n_seq, n_q, n_kv, hd, causal)
+    a_abs = orc.attention(synth.as_f32(qz), synth.as_f32(c.k), np.abs(synth.as_f32(c.v)), c.mask,
+                          n_seq, n_q, n_kv, hd, causal)
+    check_rows(got, ref, (2.0 ** -16 + T_k * 2.0 ** -24) * a_abs, c.mask, G, "zero queries")
