@@ -10,6 +10,10 @@ router logits at 50% sparsity.  One step is the whole hot path twice:
            + dense K/V, masked O, masked SwiGLU gate/up, masked down;
   decode  (B = 32 tokens):   the same projections through the decode kernels.
 
+Outside the timed step the line also reports the masked causal attention
+that sits between the Q/K/V and O projections (same tokens and attention
+mask; 25/75/100% keep; torch's fused SDPA as the dense reference).
+
 value = active FLOPs of the step (FLOPs of the executed groups only, the
 paper's accounting) / step time, in TFLOP/s.  The JSON line also carries the
 prefill and decode figures separately, the speedup over dense bf16 GEMMs
@@ -48,6 +52,8 @@ def parse():
     ap.add_argument("--cpu-sample-tokens", type=int, default=1024)
     ap.add_argument("--ring-bk", type=int, default=0, help="k depth of a 256x256 stage (0: library default)")
     ap.add_argument("--k-path", type=int, default=0, help="K-axis schedule (0: library default)")
+    ap.add_argument("--no-attention", action="store_true",
+                    help="skip the masked-attention figures (prefill, outside the timed step)")
     ap.add_argument("--no-sweeps", action="store_true",
                     help="skip the decode batch sweep and the prefill keep sweep")
     ap.add_argument("--calibration-copy", action="store_true",
@@ -462,6 +468,99 @@ def main():
                                 x_GBps=round(xb / (t * 1e-3) / 1e9, 1)))
         sweeps = dict(decode_ffn_llama7b=dec_rows, prefill_layer_keep=pre_rows, router_ffn=rt_rows)
 
+    # ---- masked attention at prefill (outside the timed region) ----------------------
+    # The step between the Q/K/V and O projections: one sequence of T tokens,
+    # 32 q / 8 kv heads, causal, the layer's attention mask (and 25/75/100%
+    # keep), q/k/v ~ N(0,1).  Active FLOPs count 4*hd per visible key of every
+    # active (token, head); dense = the same with every group active.
+    attention = None
+    if not args.no_attention:
+        from paper_2607_28418_amd import synth
+        T = args.prefill_tokens
+        ga = torch.Generator(device=dev)
+        ga.manual_seed(11)
+        qa = torch.randn(T, L.Nq, device=dev, generator=ga).to(torch.bfloat16)
+        ka = torch.randn(T, L.Nkv, device=dev, generator=ga).to(torch.bfloat16)
+        va = torch.randn(T, L.Nkv, device=dev, generator=ga).to(torch.bfloat16)
+        oa = torch.empty_like(qa)
+        wsa = torch.empty(max(W.wide_attention_workspace_size(1, T, T, L.nq, L.nkv, L.hd, L.Ga, False), 256),
+                          dtype=torch.uint8, device=dev)
+        vis = np.arange(1, T + 1, dtype=np.float64)[:, None]
+        att_flops = lambda m: 4.0 * L.hd * (L.Ga // L.hd) * float((m.astype(np.float64) * vis).sum())
+
+        def ev_ms(fn, n=20):
+            for _ in range(3):
+                fn()
+            torch.cuda.synchronize()
+            s0, s1 = ev(), ev()
+            s0.record(stream)
+            for _ in range(n):
+                fn()
+            s1.record(stream)
+            torch.cuda.synchronize()
+            return s0.elapsed_time(s1) / n
+
+        att_rows = []
+        xa = L.batches["prefill"]["x_attn"]
+        for keep in (0.25, 0.5, 0.75, 1.0):
+            if keep == 1.0:
+                ma = np.ones((T, L.nga), np.uint8)
+            elif abs(keep - args.keep) < 1e-9:
+                ma = L.batches["prefill"]["mask_attn"]
+            else:
+                ma = synth.mask_topk(synth.router_logits(synth.rng(300 + int(round(keep * 100))), xa, L.nga),
+                                     synth.keep_count(L.nga, keep))
+            md = to_dev(ma)
+            ia, ca = W.wide_mask_reorder(md)
+            call = lambda: W.wide_attention_masked(qa, ka, va, md, 1, L.nq, L.nkv, L.hd, L.Ga, True, idx=ia,
+                                                   counts=ca, o=oa, ws=wsa)
+            t = ev_ms(call)
+            W.wide_timing_enable(True)
+            W.wide_timing_reset()
+            for _ in range(10):
+                call()
+            torch.cuda.synchronize()
+            kf_ms, kf_n = W.wide_timing_query("wide_attn_fwd")
+            kp_ms, kp_n = W.wide_timing_query("wide_attn_prep")
+            W.wide_timing_enable(False)
+            fl = att_flops(ma)
+            att_rows.append(dict(keep=keep, ms=round(t, 4), active_TFLOPs=round(fl / (t * 1e-3) / 1e12, 1),
+                                 fwd_kernel_us=round(1e3 * kf_ms / kf_n, 2),
+                                 prep_kernel_us=round(1e3 * kp_ms / kp_n, 2), active_flops=fl))
+        dense_fl = att_flops(np.ones((T, L.nga), np.uint8))
+        ones_ms = att_rows[-1]["ms"]
+        sdpa_ms = None
+        try:
+            import torch.nn.functional as F
+            from torch.nn.attention import SDPBackend, sdpa_kernel
+            q4 = qa.view(1, T, L.nq, L.hd).transpose(1, 2).contiguous()
+            k4 = ka.view(1, T, L.nkv, L.hd).transpose(1, 2).contiguous()
+            v4 = va.view(1, T, L.nkv, L.hd).transpose(1, 2).contiguous()
+            with sdpa_kernel(SDPBackend.FLASH_ATTENTION):
+                sdpa_ms = ev_ms(lambda: F.scaled_dot_product_attention(q4, k4, v4, is_causal=True,
+                                                                       enable_gqa=True))
+            del q4, k4, v4
+        except Exception as e:  # no fused kernel in this torch build: report the own dense path only
+            log("sdpa flash unavailable:", repr(e)[:160])
+        best = min(ones_ms, sdpa_ms) if sdpa_ms else ones_ms
+        for r in att_rows:
+            r["ideal_speedup"] = round(dense_fl / r["active_flops"], 3)
+            r["speedup_vs_dense"] = round(best / r["ms"], 3)
+            r["frac_of_ideal"] = round(best / r["ms"] / r["ideal_speedup"], 3)
+        main_row = next(r for r in att_rows if abs(r["keep"] - args.keep) < 1e-9)
+        ach = main_row["active_flops"] / (main_row["fwd_kernel_us"] * 1e-6) / 1e12
+        attention = dict(
+            workload="masked causal attention, one sequence of %d tokens, 32 q / 8 kv heads x 128, "
+                     "8 head groups, q/k/v ~ N(0,1)" % T,
+            sdpa_flash_dense_ms=round(sdpa_ms, 4) if sdpa_ms else None,
+            sdpa_flash_dense_TFLOPs=round(dense_fl / (sdpa_ms * 1e-3) / 1e12, 1) if sdpa_ms else None,
+            ones_mask_ms=ones_ms, rows=att_rows,
+            roofline=dict(kernel="wide_attn_fwd", bound="mfma", achieved=round(ach, 1), peak=PEAK_BF16_TFLOPS,
+                          unit="TFLOP/s", frac=round(ach / PEAK_BF16_TFLOPS, 4), keep=args.keep,
+                          algorithmic_flops_per_launch=main_row["active_flops"],
+                          avg_launch_us=main_row["fwd_kernel_us"]))
+        del qa, ka, va, oa, wsa
+
     # ---- CPU oracle on a bounded sample --------------------------------------------
     cpu = None
     if not args.no_cpu_baseline:
@@ -507,6 +606,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "sweeps": sweeps,
+        "attention": attention,
     }
     print(json.dumps(out), flush=True)
     if args.calibration_copy:

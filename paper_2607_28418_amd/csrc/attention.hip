@@ -35,6 +35,7 @@
 // mask.
 #include "common.h"
 #include "kernels.h"
+#include "launch.h"
 #include "tile256.h"
 
 namespace wide {
@@ -357,14 +358,14 @@ hipError_t launch_attention(AttnArgs a, const uint16_t* v, int32_t* seq_off, hip
   a.n_slots = attn_slots(a.T_q, hb);
   const int n_vt = a.n_seq * a.n_kv * (a.T_kp / 64);
   const int n_off = a.n_seq > 1 ? (a.ng * (a.n_seq + 1) + 3) / 4 : 0;
-  wide_attn_prep<<<n_vt + n_off, kAT, 0, s>>>(a, v, seq_off, n_vt);
+  WIDE_LAUNCH(wide_attn_prep, dim3((unsigned)(n_vt + n_off)), dim3(kAT), 0, s, a, v, seq_off, n_vt);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   a.seq_off = a.n_seq > 1 ? seq_off : nullptr;
-  const int64_t grid = (int64_t)(a.n_q / hb) * a.n_seq * a.n_slots;
-  if (hb == 4) wide_attn_fwd<4><<<(unsigned)grid, kAT, 0, s>>>(a);
-  else if (hb == 2) wide_attn_fwd<2><<<(unsigned)grid, kAT, 0, s>>>(a);
-  else wide_attn_fwd<1><<<(unsigned)grid, kAT, 0, s>>>(a);
+  const dim3 grid((unsigned)((int64_t)(a.n_q / hb) * a.n_seq * a.n_slots));
+  if (hb == 4) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<4>), grid, dim3(kAT), 0, s, a);
+  else if (hb == 2) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<2>), grid, dim3(kAT), 0, s, a);
+  else WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<1>), grid, dim3(kAT), 0, s, a);
   return hipGetLastError();
 }
 

@@ -65,3 +65,36 @@ def assert_close(got, ref: np.ndarray, kind: str = "bf16", what: str = "", abs_a
     mae_tol, rel_tol = (BF16_MAE, BF16_REL) if kind == "bf16" else (F32_MAE, F32_REL)
     assert mae <= mae_tol and rel <= rel_tol, f"{what}: mae={mae:.3g} (<= {mae_tol}) maxrel={rel:.3g} (<= {rel_tol})"
     return mae, rel
+
+
+# ---- masked attention -------------------------------------------------------------
+
+def bf16_ulp_arr(x):
+    a = np.abs(x)
+    e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
+    return np.where(a > 0, 2.0 ** (e - 7), 0.0)
+
+
+def attention_bound(orc, q, k, v, mask, n_seq, n_q, n_kv, hd, causal, T_k):
+    """Per-element error bound of the bf16 attention path (probabilities
+    rounded to bf16 for P.V: unit roundoff 2^-8 times attention applied to
+    |V|; fp32 scores, exponentials and sums: (2^-12 + T_k 2^-24) of the
+    same); the stored output's own bf16 rounding is added by the check."""
+    from paper_2607_28418_amd import synth
+    vabs = np.abs(synth.as_f32(v)).astype(np.float32)
+    a_abs = orc.attention(synth.as_f32(q), synth.as_f32(k), vabs, mask, n_seq, n_q, n_kv, hd, causal)
+    return (2.0 ** -8 + 2.0 ** -12 + T_k * 2.0 ** -24) * a_abs
+
+
+def check_attention_rows(got, ref, bound, mask_rows, hpg_feat, what):
+    """got/ref/bound [rows][n_q*hd] float64; inactive (row, group) blocks must be +0."""
+    assert np.isfinite(got).all(), f"{what}: non-finite output"
+    inactive = ~np.repeat(mask_rows.astype(bool), hpg_feat, axis=1)
+    assert not got[inactive].any() and not np.signbit(got[inactive]).any(), f"{what}: inactive rows not +0"
+    err = np.abs(got - ref)
+    allow = bound + bf16_ulp_arr(got)
+    worst = float(np.max(err - allow)) if err.size else 0.0
+    assert worst <= 0.0, f"{what}: {int((err > allow).sum())} elements over the bound (worst excess {worst:.3g})"
+    mae = float(err.mean()) if err.size else 0.0
+    assert mae <= 1e-3, f"{what}: mae {mae:.3g}"
+    return mae

@@ -18,39 +18,13 @@ import torch
 
 import paper_2607_28418_amd as W
 from paper_2607_28418_amd import synth
-from tests._helpers import dev, to_dev, to_np64
+from tests._helpers import attention_bound, check_attention_rows as check_rows, dev, to_dev, to_np64
 
 pytestmark = pytest.mark.gpu
 
 
 def say(*a):
     print("[case]", *a, file=sys.stderr, flush=True)
-
-
-def bf16_ulp_arr(x):
-    a = np.abs(x)
-    e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
-    return np.where(a > 0, 2.0 ** (e - 7), 0.0)
-
-
-def attention_bound(orc, q, k, v, mask, n_seq, n_q, n_kv, hd, causal, T_k):
-    vabs = np.abs(synth.as_f32(v)).astype(np.float32)
-    a_abs = orc.attention(synth.as_f32(q), synth.as_f32(k), vabs, mask, n_seq, n_q, n_kv, hd, causal)
-    return (2.0 ** -8 + 2.0 ** -12 + T_k * 2.0 ** -24) * a_abs
-
-
-def check_rows(got, ref, bound, mask_rows, hpg_feat, what):
-    """got/ref/bound [rows][n_q*hd] float64; inactive (row, group) blocks must be +0."""
-    assert np.isfinite(got).all(), f"{what}: non-finite output"
-    inactive = ~np.repeat(mask_rows.astype(bool), hpg_feat, axis=1)
-    assert not got[inactive].any() and not np.signbit(got[inactive]).any(), f"{what}: inactive rows not +0"
-    err = np.abs(got - ref)
-    allow = bound + bf16_ulp_arr(got)
-    worst = float(np.max(err - allow)) if err.size else 0.0
-    assert worst <= 0.0, f"{what}: {int((err > allow).sum())} elements over the bound (worst excess {worst:.3g})"
-    mae = float(err.mean()) if err.size else 0.0
-    assert mae <= 1e-3, f"{what}: mae {mae:.3g}"
-    return mae
 
 
 def run_case(orc, n_seq, T_q, T_k, n_q, n_kv, G, causal, mask="topk", keep=0.5, qk_std=1.0, seed=0,
