@@ -49,7 +49,6 @@ constexpr int kBN = 64;                // keys per tile
 constexpr int kAT = 256;               // threads per workgroup (4 waves)
 constexpr int kKSub = 64 * 64;         // one K half-tile [64 keys][64 dims]
 constexpr int kVt = kHd * kBN;         // V^T tile [128 dims][64 keys]
-constexpr int kStage = 2 * kKSub + kVt;  // bf16 elements per stage (32 KB)
 
 // LDS rows are 64 bf16 = 8 chunks of 16 bytes; logical chunk c of row r sits
 // at physical chunk c ^ f(r), which spreads the 16 rows that one 16-lane
@@ -67,7 +66,7 @@ template <int HB>
 __global__ __launch_bounds__(kAT, 2) void wide_attn_fwd(AttnArgs a) {
   constexpr int RB = 4 / HB;    // 32-row blocks per workgroup
   constexpr int BMW = 32 * RB;  // query rows per workgroup
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kStage];
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (2 * kKSub + kVt)];  // 64 KB
 
   const int per_hb = a.n_seq * a.n_slots;
   const int lid = t256::xcd_remap(blockIdx.x, gridDim.x);
@@ -131,12 +130,13 @@ __global__ __launch_bounds__(kAT, 2) void wide_attn_fwd(AttnArgs a) {
     for (int s = 0; s < 8; ++s) qf[s] = valid ? ldg16(qrow + 16 * s) : u32x4{0, 0, 0, 0};
   }
 
-  // Stage loads: 32 wave instructions of 1 KB (8 LDS rows each); wave 0 loads
-  // K dims 0-63, wave 1 K dims 64-127, waves 2-3 the 128 rows of V^T.  A lane
-  // keeps a 32-bit byte offset per instruction from a per-tile uniform base.
+  // Loads: a K tile and a V^T tile are 16 instructions of 1 KB (8 LDS rows
+  // each).  Waves 0-1 load K (dims 0-63 / 64-127), waves 2-3 the 128 rows of
+  // V^T; each ring has two stages.  A lane keeps a 32-bit byte offset per
+  // instruction from a per-tile uniform base.
   const int64_t ldk = (int64_t)a.n_kv * kHd;
   const bool kwave = w < 2;
-  const char* kb0 = reinterpret_cast<const char*>(a.k + (int64_t)b * a.T_k * ldk + hkv * kHd + w * 64);
+  const char* kb0 = reinterpret_cast<const char*>(a.k + (int64_t)b * a.T_k * ldk + hkv * kHd + (w & 1) * 64);
   const char* vb0 = reinterpret_cast<const char*>(a.vt + ((int64_t)b * a.n_kv + hkv) * kHd * (int64_t)a.T_kp);
   uint32_t off[8];
 #pragma unroll
@@ -145,31 +145,33 @@ __global__ __launch_bounds__(kAT, 2) void wide_attn_fwd(AttnArgs a) {
     const int lc = (lane & 7) ^ swz_f(r);
     off[q] = kwave ? (uint32_t)((r * ldk + lc * 8) * 2) : (uint32_t)(((int64_t)r * a.T_kp + lc * 8) * 2);
   }
-  auto issue = [&](int jt, uint16_t* st) {
+  uint16_t* const kst = smem;                 // K ring: 2 x [2 halves][64 keys][64 dims]
+  uint16_t* const vst = smem + 2 * 2 * kKSub;  // V^T ring: 2 x [128 dims][64 keys]
+  auto issue_k = [&](int jt) {  // waves 0-1
     const int j0 = jt * kBN;
-    uint16_t* dst = st + (kwave ? w * kKSub : 2 * kKSub + (w - 2) * 64 * 64);
-    if (kwave) {
-      const char* base = kb0 + (int64_t)j0 * ldk * 2;
-      if (j0 + kBN <= a.T_k) {
-#pragma unroll
-        for (int q = 0; q < 8; ++q)
-          __builtin_amdgcn_global_load_lds((gptr_t)(base + off[q]), (lptr_t)(dst + q * 8 * 64), 16, 0, 0);
-      } else {  // last, partial tile: rows past the end re-read the last key (finite, masked)
-        const int kmax = a.T_k - 1 - j0;
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          const int r = q * 8 + lane / 8;
-          const int lc = (lane & 7) ^ swz_f(r);
-          const uint32_t o = (uint32_t)((min(r, kmax) * ldk + lc * 8) * 2);
-          __builtin_amdgcn_global_load_lds((gptr_t)(base + o), (lptr_t)(dst + q * 8 * 64), 16, 0, 0);
-        }
-      }
-    } else {
-      const char* base = vb0 + (int64_t)j0 * 2;
+    uint16_t* dst = kst + (jt & 1) * 2 * kKSub + w * kKSub;
+    const char* base = kb0 + (int64_t)j0 * ldk * 2;
+    if (j0 + kBN <= a.T_k) {
 #pragma unroll
       for (int q = 0; q < 8; ++q)
         __builtin_amdgcn_global_load_lds((gptr_t)(base + off[q]), (lptr_t)(dst + q * 8 * 64), 16, 0, 0);
+    } else {  // last, partial tile: rows past the end re-read the last key (finite, masked)
+      const int kmax = a.T_k - 1 - j0;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int r = q * 8 + lane / 8;
+        const int lc = (lane & 7) ^ swz_f(r);
+        const uint32_t o = (uint32_t)((min(r, kmax) * ldk + lc * 8) * 2);
+        __builtin_amdgcn_global_load_lds((gptr_t)(base + o), (lptr_t)(dst + q * 8 * 64), 16, 0, 0);
+      }
     }
+  };
+  auto issue_v = [&](int jt) {  // waves 2-3
+    uint16_t* dst = vst + (jt & 1) * kVt + (w - 2) * 64 * 64;
+    const char* base = vb0 + (int64_t)jt * kBN * 2;
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      __builtin_amdgcn_global_load_lds((gptr_t)(base + off[q]), (lptr_t)(dst + q * 8 * 64), 16, 0, 0);
   };
 
   // K rows in the A operand: lane row x = 8j + 4h' + i loads key
@@ -183,16 +185,11 @@ __global__ __launch_bounds__(kAT, 2) void wide_attn_fwd(AttnArgs a) {
   float m = -INFINITY, z = 0.0f;
   const float sc = a.scale_log2;
 
-  issue(0, smem);
-  for (int jt = 0; jt < n_tiles; ++jt) {
-    t256::wait_vm<0>();
-    t256::stage_barrier();
-    if (jt + 1 < n_tiles) issue(jt + 1, smem + ((jt + 1) & 1) * kStage);
-    const int j0 = jt * kBN;
-    if (!wave_live || j0 > wmax) continue;  // l = 2: no row of this wave sees the tile
-    const uint16_t* st = smem + (jt & 1) * kStage;
-
-    f32x16 S[2] = {f32x16{}, f32x16{}};
+  // S^T of key tile jt for this wave's 32 queries (two 32-key blocks).
+  auto qk = [&](int jt, f32x16 (&S)[2]) {
+    const uint16_t* st = kst + (jt & 1) * 2 * kKSub;
+    S[0] = f32x16{};
+    S[1] = f32x16{};
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       const uint16_t* ks = st + (s >> 2) * kKSub;
@@ -202,9 +199,13 @@ __global__ __launch_bounds__(kAT, 2) void wide_attn_fwd(AttnArgs a) {
       S[0] = mfma32(k0, qf[s], S[0]);
       S[1] = mfma32(k1, qf[s], S[1]);
     }
-
-    // Per-element mask only where the tile crosses some row's limit (or the
-    // end of the keys); every other tile is fully visible to the wave.
+  };
+  // Online softmax of tile jt's scores (masking and the new row maximum,
+  // then the exponentials and the rescale) and O^T += V^T P^T.
+  auto row_max = [&](int jt, f32x16 (&S)[2], float& alpha, float& muse) {
+    const int j0 = jt * kBN;
+    // Per-element mask only where the tile crosses some row's limit; every
+    // other tile is fully visible to the wave.
     if (j0 + kBN - 1 > wmin) {
       const int lim = plim - j0 - 8 * hi;  // key offset past which this lane's row sees nothing
 #pragma unroll
@@ -220,8 +221,11 @@ __global__ __launch_bounds__(kAT, 2) void wide_attn_fwd(AttnArgs a) {
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, S[kb][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float mnew = fmaxf(m, mx * sc);
-    const float muse = mnew == -INFINITY ? 0.0f : mnew;  // a row with nothing visible yet
-    const float alpha = fast_exp2(m - muse);
+    muse = mnew == -INFINITY ? 0.0f : mnew;  // a row with nothing visible yet
+    alpha = fast_exp2(m - muse);
+    m = mnew;
+  };
+  auto exp_pv = [&](int jt, f32x16 (&S)[2], float alpha, float muse) {
     float zs = 0.0f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
@@ -233,13 +237,11 @@ __global__ __launch_bounds__(kAT, 2) void wide_attn_fwd(AttnArgs a) {
       }
     }
     z = z * alpha + zs;
-    m = mnew;
     if (__any(alpha != 1.0f)) {  // lazy rescale: skipped once the maxima settle
 #pragma unroll
       for (int db = 0; db < 4; ++db) O[db] *= alpha;
     }
-
-    const uint16_t* vts = st + 2 * kKSub;
+    const uint16_t* vts = vst + (jt & 1) * kVt;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
@@ -255,6 +257,42 @@ __global__ __launch_bounds__(kAT, 2) void wide_attn_fwd(AttnArgs a) {
         }
       }
     }
+  };
+
+  // Key tiles this wave sees at all (a prefix of the workgroup's range).
+  const int wtiles = wave_live ? (wmax + kBN) / kBN : 0;
+  // Pipeline: iteration jt loads K of tile jt+2 and V of tile jt+1, computes
+  // the scores of tile jt+1 and then the softmax and P.V of tile jt, so the
+  // matrix core has independent work while the softmax runs.  Everything
+  // issued in one iteration lands before the next one starts.
+  if (kwave) {
+    issue_k(0);
+    if (n_tiles > 1) issue_k(1);
+  } else {
+    issue_v(0);
+  }
+  t256::wait_vm<0>();
+  t256::stage_barrier();
+  f32x16 Sa[2], Sb[2];
+  if (wtiles > 0) qk(0, Sa);
+  auto step = [&](int jt, f32x16 (&Sc)[2], f32x16 (&Sn)[2]) {
+    t256::wait_vm<0>();
+    t256::stage_barrier();
+    if (kwave) {
+      if (jt + 2 < n_tiles) issue_k(jt + 2);
+    } else {
+      if (jt + 1 < n_tiles) issue_v(jt + 1);
+    }
+    if (jt + 1 < wtiles) qk(jt + 1, Sn);
+    if (jt < wtiles) {  // l = 2: tiles past the wave's rows issue no MFMA
+      float alpha, muse;
+      row_max(jt, Sc, alpha, muse);
+      exp_pv(jt, Sc, alpha, muse);
+    }
+  };
+  for (int jt = 0; jt < n_tiles; jt += 2) {
+    step(jt, Sa, Sb);
+    if (jt + 1 < n_tiles) step(jt + 1, Sb, Sa);
   }
 
   // Epilogue: the two halves of a query's sum, normalise, scatter the row.

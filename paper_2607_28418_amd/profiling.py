@@ -46,6 +46,7 @@ def source_digest() -> str:
 def kernel_key(name: str) -> str:
     """'void wide::wide_mn256<true, 64>(wide::MN256Args)' -> 'wide_mn256<true, 64>'."""
     name = re.sub(r"^void ", "", name.strip())
+    name = name.replace("(anonymous namespace)::", "")
     name = name.split("(")[0]
     return name.replace("wide::", "")
 

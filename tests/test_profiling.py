@@ -41,3 +41,13 @@ def test_label_matching():
     assert not m("wide_gemv_n_finish<true>", "wide_gemv_n<true>")
     assert m("wide_gemv_n<true, 4, 2>", "wide_gemv_n<true>")
     assert m("wide_reorder_count", "wide_reorder_count")
+
+
+def test_kernel_key_strips_namespaces_and_arguments():
+    from paper_2607_28418_amd.profiling import kernel_key, label_matches
+    assert kernel_key("void wide::wide_mn256<true, 64>(wide::MN256Args)") == "wide_mn256<true, 64>"
+    assert kernel_key("void wide::(anonymous namespace)::wide_attn_fwd<4>(wide::AttnArgs)") == "wide_attn_fwd<4>"
+    assert kernel_key("wide::(anonymous namespace)::wide_attn_prep(wide::AttnArgs, unsigned short const*, int*, int)") \
+        == "wide_attn_prep"
+    assert label_matches("wide_attn_fwd<4>", "wide_attn_fwd")
+    assert not label_matches("wide_attn_fwd<4>", "wide_attn_prep")
