@@ -217,6 +217,41 @@ wide_status_t wide_attention_masked(wide_dtype_t dt, int64_t n_seq, int32_t T_q,
                                     size_t ws_bytes, hipStream_t stream);
 
 /*
+ * Head-group masked attention, decode (WIDE Section 3.1, equations (1)-(2);
+ * Appendix B: at decode the reorder is bypassed and the routing is checked
+ * per block).  One query token per sequence b attends to its cached keys:
+ *   o[b, h] = sum_{j < len_b} softmax_j(q[b, h] . k[b, j, h_kv] / sqrt(head_dim))
+ *             v[b, j, h_kv]      if mask[b][g(h)] != 0, else +0,
+ * with g(h) = h / (group_size/head_dim), h_kv = h / (n_q_heads/n_kv_heads)
+ * and len_b = min(kv_len[b], L) (L when kv_len is NULL; len_b <= 0 gives +0).
+ * A (sequence, KV head) none of whose query heads is active reads nothing of
+ * the cache.
+ *   dt        WIDE_BF16 (WIDE_ERR_UNSUPPORTED otherwise).
+ *   batch, L  sequences and the cache capacity (rows per sequence).
+ *   n_q_heads, n_kv_heads (at most 32 query heads per KV head), head_dim (128
+ *             only), group_size as for wide_qkvo_masked.
+ *   mask      [batch][n_q_heads*head_dim/group_size] uint8.
+ *   kv_len    optional int32 [batch] (device).
+ *   q         [batch][n_q_heads*head_dim]; k_cache, v_cache
+ *             [batch][L][n_kv_heads*head_dim]; o [batch][n_q_heads*head_dim] out.
+ *   ws        >= wide_attention_decode_workspace_size(...) bytes (per-chunk
+ *             partial maxima, sums and outputs).
+ * Arithmetic: scores from bf16 pairs with fp32 sums; softmax and P.V in fp32
+ * (probabilities are not rounded); partial results over key chunks are merged
+ * in fp32; o is rounded to bf16.
+ */
+wide_status_t wide_attention_decode(wide_dtype_t dt, int64_t batch, int32_t L, int32_t n_q_heads,
+                                    int32_t n_kv_heads, int32_t head_dim, int32_t group_size,
+                                    const uint8_t* mask, const int32_t* kv_len, const void* q,
+                                    const void* k_cache, const void* v_cache, void* o, void* ws,
+                                    size_t ws_bytes, hipStream_t stream);
+
+/* Workspace bytes for wide_attention_decode (SIZE_MAX for rejected shapes). */
+size_t wide_attention_decode_workspace_size(int64_t batch, int32_t L, int32_t n_q_heads,
+                                            int32_t n_kv_heads, int32_t head_dim,
+                                            int32_t group_size);
+
+/*
  * Workspace bytes for wide_attention_masked (with_reorder != 0: idx/counts
  * will be NULL and the reorder is held in the workspace).  SIZE_MAX for
  * shapes wide_attention_masked would reject (causal-only checks aside).

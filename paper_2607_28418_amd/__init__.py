@@ -14,7 +14,8 @@ import os
 
 __all__ = [
     "WideError", "lib", "wide_mask_reorder", "wide_ffn_masked", "wide_qkvo_masked", "wide_router",
-    "wide_attention_masked", "wide_attention_workspace_size", "wide_workspace_size", "wide_set_option", "wide_get_option", "wide_timing_enable",
+    "wide_attention_masked", "wide_attention_workspace_size", "wide_attention_decode",
+    "wide_attention_decode_workspace_size", "wide_workspace_size", "wide_set_option", "wide_get_option", "wide_timing_enable",
     "wide_timing_reset", "wide_timing_query", "LIB_PATH",
     "OP_REORDER", "OP_FFN", "OP_QKV", "OP_O", "OP_ROUTER", "PHASE_QKV", "PHASE_O", "F32", "BF16",
 ]
@@ -62,6 +63,10 @@ def lib() -> ctypes.CDLL:
                                             vp, vp, vp, vp, sz, vp]
         L.wide_attention_workspace_size.restype = sz
         L.wide_attention_workspace_size.argtypes = [i64, i32, i32, i32, i32, i32, i32, i32]
+        L.wide_attention_decode.restype = ci
+        L.wide_attention_decode.argtypes = [ci, i64, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.wide_attention_decode_workspace_size.restype = sz
+        L.wide_attention_decode_workspace_size.argtypes = [i64, i32, i32, i32, i32, i32]
         L.wide_workspace_size.restype = sz
         L.wide_workspace_size.argtypes = [ci, ci, i64, i32, i32, i32]
         L.wide_set_option.restype = ci
@@ -296,4 +301,28 @@ def wide_attention_masked(q, k, v, mask, n_seq, n_q, n_kv, head_dim, group_size,
     _check("wide_attention_masked", lib().wide_attention_masked(
         _dtype_code(q), n_seq, T_q, T_k, n_q, n_kv, head_dim, group_size, int(bool(causal)),
         _p(mask), _p(idx), _p(counts), _p(q), _p(k), _p(v), _p(o), _p(ws), nbytes, _stream(q)))
+    return o
+
+
+def wide_attention_decode_workspace_size(batch, L, n_q, n_kv, head_dim, group_size):
+    return int(lib().wide_attention_decode_workspace_size(batch, L, n_q, n_kv, head_dim, group_size))
+
+
+def wide_attention_decode(q, k_cache, v_cache, mask, n_q, n_kv, head_dim, group_size, kv_len=None,
+                          o=None, ws=None):
+    """Head-group masked attention at decode.  q [B][n_q*head_dim], k_cache and
+    v_cache [B][L][n_kv*head_dim], mask [B][n_groups] uint8, kv_len optional
+    int32 [B].  Returns o, same shape as q."""
+    _contig(q, k_cache, v_cache, mask, kv_len, o)
+    B = q.shape[0]
+    L = k_cache.shape[1] if k_cache.dim() == 3 else 0
+    if o is None:
+        o = _torch().empty_like(q)
+    if ws is None:
+        need = wide_attention_decode_workspace_size(B, L, n_q, n_kv, head_dim, group_size)
+        ws = None if need == SIZE_MAX else _workspace(need, q.device)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("wide_attention_decode", lib().wide_attention_decode(
+        _dtype_code(q), B, L, n_q, n_kv, head_dim, group_size, _p(mask), _p(kv_len), _p(q), _p(k_cache),
+        _p(v_cache), _p(o), _p(ws), nbytes, _stream(q)))
     return o

@@ -10,7 +10,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libwide.so")
 SOURCES = ["api.cpp", "reorder.hip", "gemm_mn.hip", "gemm_k.hip", "gemv.hip", "fp32.hip", "gemm256.hip", "router.hip",
-           "attention.hip"]
+           "attention.hip", "attention_decode.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -909,3 +909,86 @@ wide_status_t wide_attention_masked(wide_dtype_t dt, int64_t n_seq, int32_t T_q,
     return hip_fail(e, "attention");
   return ok();
 }
+
+// ---- masked attention (decode) ----------------------------------------------------
+namespace {
+
+wide_status_t attention_decode_shape(wide_dtype_t dt, int64_t B, int32_t L, int nq, int nkv, int hd, int G,
+                                     AttnShape& s) {
+  if (dt != WIDE_F32 && dt != WIDE_BF16) return fail(WIDE_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
+  if (B < 0 || B >= (int64_t(1) << 31) || L < 0) return fail(WIDE_ERR_INVALID_ARG, "batch and L must be >= 0");
+  if (nq <= 0 || nkv <= 0 || hd <= 0 || G <= 0)
+    return fail(WIDE_ERR_INVALID_ARG, "head counts, head_dim and group_size must be positive");
+  if (nq % nkv) return fail(WIDE_ERR_INVALID_ARG, "n_q_heads=%d not a multiple of n_kv_heads=%d", nq, nkv);
+  if (G % hd) return fail(WIDE_ERR_INVALID_ARG, "group_size=%d not a multiple of head_dim=%d", G, hd);
+  if ((int64_t)nq * hd % G) return fail(WIDE_ERR_INVALID_ARG, "group_size=%d does not divide n_q*head_dim", G);
+  if (B > 0 && L == 0) return fail(WIDE_ERR_INVALID_ARG, "a key cache of length 0");
+  if (B * (int64_t)L >= (int64_t(1) << 31)) return fail(WIDE_ERR_INVALID_ARG, "batch*L must be < 2^31");
+  s.ng = (int)((int64_t)nq * hd / G);
+  if (s.ng > 4096) return fail(WIDE_ERR_UNSUPPORTED, "more than 4096 groups");
+  if (dt != WIDE_BF16) return fail(WIDE_ERR_UNSUPPORTED, "attention runs on bf16 only");
+  if (hd != wide::kAttnHeadDim) return fail(WIDE_ERR_UNSUPPORTED, "attention needs head_dim 128 (got %d)", hd);
+  if (nq / nkv > 32) return fail(WIDE_ERR_UNSUPPORTED, "more than 32 query heads per KV head");
+  s.M = B;
+  s.Mk = B * (int64_t)L;
+  s.hpg = G / hd;
+  s.qpk = nq / nkv;
+  return WIDE_OK;
+}
+
+size_t attention_decode_ws(int64_t B, int L, int nq, int nkv) {
+  if (B == 0) return 0;
+  const int ch = wide::attn_decode_chunk((int)B, nkv, L);
+  const int nc = (L + ch - 1) / ch;
+  return align_up((size_t)B * nq * nc * (wide::kAttnHeadDim + 2) * sizeof(float));
+}
+
+}  // namespace
+
+size_t wide_attention_decode_workspace_size(int64_t batch, int32_t L, int32_t n_q_heads, int32_t n_kv_heads,
+                                            int32_t head_dim, int32_t group_size) {
+  AttnShape s;
+  const std::string keep = g_last_error;
+  const bool bad =
+      attention_decode_shape(WIDE_BF16, batch, L, n_q_heads, n_kv_heads, head_dim, group_size, s) != WIDE_OK;
+  g_last_error = keep;
+  return bad ? SIZE_MAX : attention_decode_ws(batch, L, n_q_heads, n_kv_heads);
+}
+
+wide_status_t wide_attention_decode(wide_dtype_t dt, int64_t batch, int32_t L, int32_t n_q_heads,
+                                    int32_t n_kv_heads, int32_t head_dim, int32_t group_size,
+                                    const uint8_t* mask, const int32_t* kv_len, const void* q,
+                                    const void* k_cache, const void* v_cache, void* o, void* ws,
+                                    size_t ws_bytes, hipStream_t stream) {
+  AttnShape s;
+  CHECK(attention_decode_shape(dt, batch, L, n_q_heads, n_kv_heads, head_dim, group_size, s));
+  if (batch == 0) return ok();
+  CHECK(check_ptr(mask, "mask", false));
+  if (kv_len) CHECK(check_ptr(kv_len, "kv_len", false));
+  CHECK(check_ptr(q, "q"));
+  CHECK(check_ptr(k_cache, "k_cache"));
+  CHECK(check_ptr(v_cache, "v_cache"));
+  CHECK(check_ptr(o, "o"));
+  CHECK(check_ws(ws, ws_bytes, attention_decode_ws(batch, L, n_q_heads, n_kv_heads)));
+  wide::AttnDecArgs a{};
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k_cache);
+  a.v = static_cast<const uint16_t*>(v_cache);
+  a.o = static_cast<uint16_t*>(o);
+  a.mask = mask;
+  a.kv_len = kv_len;
+  a.part = static_cast<float*>(ws);
+  a.B = (int)batch;
+  a.L = L;
+  a.n_q = n_q_heads;
+  a.n_kv = n_kv_heads;
+  a.ng = s.ng;
+  a.hpg = s.hpg;
+  a.qpk = s.qpk;
+  a.chunk = wide::attn_decode_chunk(a.B, n_kv_heads, L);
+  a.n_chunks = (L + a.chunk - 1) / a.chunk;
+  a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)head_dim));
+  const hipError_t e = wide::launch_attention_decode(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "attention decode");
+  return ok();
+}

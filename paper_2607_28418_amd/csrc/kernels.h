@@ -187,6 +187,22 @@ hipError_t launch_attention(AttnArgs a, const uint16_t* v, int32_t* seq_off, hip
 int attn_heads_per_block(int hpg, int qpk);
 int attn_slots(int T_q, int hb);
 
+// ---- masked attention, decode (attention_decode.hip)
+struct AttnDecArgs {
+  const uint16_t* q;        // [B][n_q*128] bf16, one query token per sequence
+  const uint16_t* k;        // [B][L][n_kv*128] bf16 key cache
+  const uint16_t* v;        // [B][L][n_kv*128] bf16 value cache
+  uint16_t* o;              // [B][n_q*128] bf16 out
+  const uint8_t* mask;      // [B][ng]
+  const int32_t* kv_len;    // optional [B]: keys [0, kv_len[b]) are attended (NULL: L)
+  float* part;              // workspace [B][n_q][n_chunks][2 + 128]
+  int B, L, n_q, n_kv, ng, hpg, qpk;
+  int chunk, n_chunks;      // keys per workgroup (multiple of 64), ceil(L / chunk)
+  float scale_log2;
+};
+int attn_decode_chunk(int B, int n_kv, int L);
+hipError_t launch_attention_decode(AttnDecArgs a, hipStream_t s);
+
 hipError_t launch_gemv_n(const GVNArgs& a, bool swiglu, hipStream_t s);
 hipError_t launch_gemv_k(const GVKArgs& a, hipStream_t s);
 

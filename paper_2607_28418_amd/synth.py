@@ -190,6 +190,33 @@ def attn_prefill_case(seed: int, n_seq: int, T_q: int, T_k: int, n_q: int, n_kv:
     return AttnPrefillCase(q, k, v, m, n_seq, n_q, n_kv, hd, dtype)
 
 
+@dataclass
+class AttnDecodeCase:
+    q: np.ndarray          # [B][n_q*hd]
+    k: np.ndarray          # [B][L][n_kv*hd] key cache
+    v: np.ndarray          # [B][L][n_kv*hd] value cache
+    mask: np.ndarray       # [B][n_groups]
+    kv_len: np.ndarray     # int32 [B]
+    n_q: int
+    n_kv: int
+    hd: int
+    dtype: str
+
+
+def attn_decode_case(seed: int, B: int, L: int, n_q: int, n_kv: int, hd: int, n_groups: int,
+                     dtype: str = "bf16", mask: str = "bernoulli", keep: float = 0.5,
+                     qk_std: float = 1.0, ragged: bool = False) -> AttnDecodeCase:
+    """One query token per sequence against a KV cache of capacity L; with
+    `ragged`, each sequence's length is uniform in [1, L] (else L)."""
+    g = rng(seed)
+    q = normal(g, (B, n_q * hd), qk_std, dtype)
+    k = normal(g, (B, L, n_kv * hd), qk_std, dtype)
+    v = normal(g, (B, L, n_kv * hd), 1.0, dtype)
+    m = make_mask(g, mask, B, n_groups, keep, q)
+    kv_len = (g.integers(1, L + 1, B) if ragged else np.full(B, L)).astype(np.int32)
+    return AttnDecodeCase(q, k, v, m, kv_len, n_q, n_kv, hd, dtype)
+
+
 # ---- the paper's workloads (synthetic stand-ins) ---------------------------
 
 @dataclass
@@ -229,6 +256,13 @@ WORKLOADS = {
         "q,k,v~N(0,1), top-4 of 8 groups per token",
         dict(n_seq=1, T=8192, n_q=32, n_kv=8, hd=128, n_groups=8, dtype="bf16",
              mask="topk", keep=0.5)),
+    "attn_decode_llama3_8b": Workload(
+        "attn_decode_llama3_8b",
+        "head-group masked decode attention bf16, Llama-3-8B heads: 32 q / 8 kv "
+        "heads x 128 in 8 head groups, B=32 sequences with 8192 cached keys each, "
+        "q,k,v~N(0,1), Bernoulli(0.5) per (token, group)",
+        dict(B=32, L=8192, n_q=32, n_kv=8, hd=128, n_groups=8, dtype="bf16", mask="bernoulli",
+             keep=0.5)),
     "layer_llama3_8b": Workload(
         "layer_llama3_8b",
         "full decoder-layer projections bf16, Llama-3-8B shape: D=4096, 32 q / "

@@ -187,3 +187,35 @@ def test_attention_workspace_size():
     assert W.wide_attention_workspace_size(2, 100, 130, 8, 2, 128, 256, False) >= 2 * 2 * 128 * 192 * 2
     assert W.wide_attention_workspace_size(1, 0, 0, 32, 8, 128, 512, True) == 0
     assert W.wide_attention_workspace_size(1, 64, 64, 32, 8, 64, 512, True) == W.SIZE_MAX
+
+
+def attention_decode(dt=W.BF16, B=32, L=8192, nq=32, nkv=8, hd=128, G=512, mask=A, kv_len=None, q=A, k=A,
+                     v=A, o=A, ws=A, ws_bytes=1 << 40):
+    return W.lib().wide_attention_decode(dt, B, L, nq, nkv, hd, G, mask, kv_len, q, k, v, o, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(dt=W.F32), W.ERR_UNSUPPORTED, "bf16"),
+    (dict(hd=64, G=256), W.ERR_UNSUPPORTED, "head_dim 128"),
+    (dict(nq=66, nkv=2, G=128), W.ERR_UNSUPPORTED, "32 query heads"),
+    (dict(nq=30), W.ERR_INVALID_ARG, "multiple of n_kv_heads"),
+    (dict(G=192), W.ERR_INVALID_ARG, "multiple of head_dim"),
+    (dict(L=0), W.ERR_INVALID_ARG, "length 0"),
+    (dict(B=-1), W.ERR_INVALID_ARG, ">= 0"),
+    (dict(B=1 << 20, L=1 << 12), W.ERR_INVALID_ARG, "2^31"),
+    (dict(k=MIS), W.ERR_INVALID_ARG, "k_cache is not 16-byte aligned"),
+    (dict(o=None), W.ERR_INVALID_ARG, "o is NULL"),
+    (dict(mask=None), W.ERR_INVALID_ARG, "mask is NULL"),
+    (dict(ws_bytes=0), W.ERR_WORKSPACE, "workspace"),
+])
+def test_attention_decode_validation(kw, status, msg):
+    assert attention_decode(**kw) == status
+    assert msg in err()
+
+
+def test_attention_decode_empty_and_workspace():
+    assert attention_decode(B=0, mask=None, q=None, k=None, v=None, o=None, ws=None, ws_bytes=0) == W.OK
+    n = W.wide_attention_decode_workspace_size(32, 8192, 32, 8, 128, 512)
+    assert n >= 32 * 32 * 130 * 4   # at least one chunk of (max, sum, o[128]) per (token, head)
+    assert W.wide_attention_decode_workspace_size(0, 8192, 32, 8, 128, 512) == 0
+    assert W.wide_attention_decode_workspace_size(32, 8192, 32, 8, 64, 512) == W.SIZE_MAX

@@ -142,3 +142,82 @@ def test_attention_zero_queries_are_exact_means(orc, n_seq, T_q, T_k, n_q, n_kv,
     a_abs = orc.attention(synth.as_f32(qz), synth.as_f32(c.k), np.abs(synth.as_f32(c.v)), c.mask,
                           n_seq, n_q, n_kv, hd, causal)
     check_rows(got, ref, (2.0 ** -16 + T_k * 2.0 ** -24) * a_abs, c.mask, G, "zero queries")
+
+
+# ------------------------------------------------------------------ decode
+
+def decode_bound(orc, q, k, v, mask, n_q, n_kv, hd):
+    """Decode keeps the probabilities in fp32 (no bf16 rounding of P): fp32
+    scores (128 bf16 products, error well under 2^-10 relative in p for
+    |q|,|k| ~ N(0, 1.5^2)), exponentials, sums and the merge of chunks; plus
+    the stored output's bf16 rounding (added by the check)."""
+    from paper_2607_28418_amd import synth as s
+    vabs = np.abs(s.as_f32(v)).astype(np.float32)
+    a_abs = orc.attention(s.as_f32(q), s.as_f32(k), vabs, mask, 1, n_q, n_kv, hd, False)
+    return (2.0 ** -10 + k.shape[0] * 2.0 ** -24) * a_abs
+
+
+def run_decode(orc, B, L, n_q, n_kv, G, mask="bernoulli", keep=0.5, qk_std=1.0, ragged=False, seed=0,
+               poison_unused=False):
+    hd = 128
+    c = synth.attn_decode_case(seed, B, L, n_q, n_kv, hd, n_q * hd // G, mask=mask, keep=keep,
+                               qk_std=qk_std, ragged=ragged)
+    k_host, v_host = c.k.copy(), c.v.copy()
+    if poison_unused:
+        # rows past each kv_len, and the whole cache of KV heads no active head reads
+        nan = np.uint16(0x7FC0)
+        hpg, qpk = G // hd, n_q // n_kv
+        for b in range(B):
+            k_host[b, c.kv_len[b]:] = nan
+            v_host[b, c.kv_len[b]:] = nan
+            for hk in range(n_kv):
+                if not any(c.mask[b, (hk * qpk + i) // hpg] for i in range(qpk)):
+                    k_host[b, :, hk * hd:(hk + 1) * hd] = nan
+                    v_host[b, :, hk * hd:(hk + 1) * hd] = nan
+    q, k, v, m = (to_dev(a) for a in (c.q, k_host, v_host, c.mask))
+    kl = to_dev(c.kv_len) if ragged else None
+    o = torch.full_like(q, float("nan"))
+    W.wide_attention_decode(q, k, v, m, n_q, n_kv, hd, G, kv_len=kl, o=o)
+    torch.cuda.synchronize()
+    got = to_np64(o)
+    for b in range(B):
+        n = int(c.kv_len[b])
+        args = (c.q[b:b + 1], c.k[b, :n], c.v[b, :n], c.mask[b:b + 1])
+        ref = orc.attention(*args, 1, n_q, n_kv, hd, False)
+        bound = decode_bound(orc, *args, n_q, n_kv, hd)
+        check_rows(got[b:b + 1], ref, bound, c.mask[b:b + 1], G, f"decode b={b} len={n}")
+    return c, got
+
+
+@pytest.mark.parametrize("B,L,n_q,n_kv,G,ragged", [
+    (5, 300, 8, 2, 256, False),      # ragged last 64-key step, two heads per group
+    (3, 3000, 8, 2, 512, True),      # many chunks, per-sequence lengths
+    (4, 200, 4, 4, 128, False),      # one head per KV head
+    (2, 777, 16, 2, 512, True),      # eight query heads per KV head (two per wave)
+    (2, 130, 32, 1, 1024, False),    # 32 query heads on one KV head
+    (32, 2048, 32, 8, 512, False),   # Llama-3-8B heads, 32 sequences
+])
+def test_attention_decode_matches_oracle(orc, B, L, n_q, n_kv, G, ragged):
+    say("attention decode", B, L, n_q, n_kv, G, ragged)
+    run_decode(orc, B, L, n_q, n_kv, G, ragged=ragged, qk_std=1.5, seed=B + L)
+
+
+@pytest.mark.parametrize("kind", ["zeros", "ones"])
+def test_attention_decode_degenerate_masks(orc, kind):
+    say("attention decode mask", kind)
+    run_decode(orc, 6, 500, 8, 2, 512, mask=kind)
+
+
+def test_attention_decode_never_reads_unused_cache(orc):
+    say("attention decode poisoned cache")
+    run_decode(orc, 8, 700, 8, 2, 512, ragged=True, poison_unused=True, seed=4)
+
+
+def test_attention_decode_empty():
+    say("attention decode empty")
+    o = W.wide_attention_decode(torch.zeros((0, 256), dtype=torch.bfloat16, device=dev()),
+                                torch.zeros((0, 64, 128), dtype=torch.bfloat16, device=dev()),
+                                torch.zeros((0, 64, 128), dtype=torch.bfloat16, device=dev()),
+                                torch.zeros((0, 2), dtype=torch.uint8, device=dev()), 2, 1, 128, 128)
+    torch.cuda.synchronize()
+    assert o.shape == (0, 256)
