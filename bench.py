@@ -561,6 +561,57 @@ def main():
                           avg_launch_us=main_row["fwd_kernel_us"]))
         del qa, ka, va, oa, wsa
 
+        # Decode: the layer's 32 decode tokens, each with a KV cache of T keys;
+        # the layer's decode attention mask (and all-ones).  HBM-bound: the
+        # figure of merit is GB/s on the cache bytes of active KV heads.
+        Bd, Ld = args.decode_batch, T
+        qd = torch.randn(Bd, L.Nq, device=dev, generator=ga).to(torch.bfloat16)
+        kd = torch.randn(Bd, Ld, L.Nkv, device=dev, generator=ga).to(torch.bfloat16)
+        vd = torch.randn(Bd, Ld, L.Nkv, device=dev, generator=ga).to(torch.bfloat16)
+        od = torch.empty_like(qd)
+        wsd = torch.empty(max(W.wide_attention_decode_workspace_size(Bd, Ld, L.nq, L.nkv, L.hd, L.Ga), 256),
+                          dtype=torch.uint8, device=dev)
+        dec_rows = []
+        qpk, hpg = L.nq // L.nkv, L.Ga // L.hd
+        kd_hm = kd.view(Bd, Ld, L.nkv, L.hd).transpose(1, 2).contiguous()
+        vd_hm = vd.view(Bd, Ld, L.nkv, L.hd).transpose(1, 2).contiguous()
+        for layout, (kc, vc) in (("token-major", (kd, vd)), ("head-major", (kd_hm, vd_hm))):
+            for name, md_np in (("layer mask", L.batches["decode"]["mask_attn"]),
+                                ("all-ones", np.ones((Bd, L.nga), np.uint8))):
+                mdd = to_dev(md_np)
+                call = lambda: W.wide_attention_decode(qd, kc, vc, mdd, L.nq, L.nkv, L.hd, L.Ga, o=od, ws=wsd,
+                                                       head_major=layout == "head-major")
+                t = ev_ms(call)
+                act_kv = sum(1 for b_ in range(Bd) for hk in range(L.nkv)
+                             if any(md_np[b_, (hk * qpk + i) // hpg] for i in range(qpk)))
+                by = act_kv * Ld * L.hd * 2 * 2
+                dec_rows.append(dict(layout=layout, mask=name, keep=round(float(md_np.mean()), 3),
+                                     ms=round(t, 4), active_kv_heads=act_kv, cache_bytes_read=by,
+                                     GBps=round(by / (t * 1e-3) / 1e9, 1),
+                                     frac_hbm=round(by / (t * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)))
+        del kd_hm, vd_hm
+        sdpa_dec = None
+        try:
+            import torch.nn.functional as F
+            from torch.nn.attention import SDPBackend, sdpa_kernel
+            q4 = qd.view(Bd, 1, L.nq, L.hd).transpose(1, 2).contiguous()
+            k4 = kd.view(Bd, Ld, L.nkv, L.hd).transpose(1, 2).contiguous()
+            v4 = vd.view(Bd, Ld, L.nkv, L.hd).transpose(1, 2).contiguous()
+            with sdpa_kernel(SDPBackend.FLASH_ATTENTION):
+                sdpa_dec = ev_ms(lambda: F.scaled_dot_product_attention(q4, k4, v4, enable_gqa=True))
+            del q4, k4, v4
+        except Exception as e:
+            log("sdpa flash decode unavailable:", repr(e)[:160])
+        for r in dec_rows:   # against the all-ones run of the same layout (or SDPA if faster)
+            dense_r = next(x for x in dec_rows if x["layout"] == r["layout"] and x["mask"] == "all-ones")
+            best_d = min(dense_r["ms"], sdpa_dec) if sdpa_dec else dense_r["ms"]
+            r["speedup_vs_dense"] = round(best_d / r["ms"], 3)
+            r["ideal_speedup"] = round(dense_r["cache_bytes_read"] / r["cache_bytes_read"], 3)
+        attention["decode"] = dict(
+            workload="masked decode attention, %d sequences x %d cached keys, 32 q / 8 kv heads x 128" % (Bd, Ld),
+            sdpa_flash_dense_ms=round(sdpa_dec, 4) if sdpa_dec else None, rows=dec_rows)
+        del qd, kd, vd, od, wsd
+
     # ---- CPU oracle on a bounded sample --------------------------------------------
     cpu = None
     if not args.no_cpu_baseline:

@@ -48,6 +48,11 @@ extern "C" {
 #endif
 
 typedef enum {
+  WIDE_KV_TOKEN_MAJOR = 0, /* cache [batch][L][n_kv_heads*head_dim]  */
+  WIDE_KV_HEAD_MAJOR = 1   /* cache [batch][n_kv_heads][L][head_dim] */
+} wide_kv_layout_t;
+
+typedef enum {
   WIDE_OK = 0,
   WIDE_ERR_INVALID_ARG = 1, /* bad pointer, shape, alignment or enum       */
   WIDE_ERR_UNSUPPORTED = 2, /* valid per the paper but not implemented here */
@@ -232,8 +237,11 @@ wide_status_t wide_attention_masked(wide_dtype_t dt, int64_t n_seq, int32_t T_q,
  *             only), group_size as for wide_qkvo_masked.
  *   mask      [batch][n_q_heads*head_dim/group_size] uint8.
  *   kv_len    optional int32 [batch] (device).
- *   q         [batch][n_q_heads*head_dim]; k_cache, v_cache
- *             [batch][L][n_kv_heads*head_dim]; o [batch][n_q_heads*head_dim] out.
+ *   kv_layout WIDE_KV_TOKEN_MAJOR: k_cache, v_cache [batch][L][n_kv_heads*head_dim]
+ *             (rows as the K/V projections write them); WIDE_KV_HEAD_MAJOR:
+ *             [batch][n_kv_heads][L][head_dim] (one KV head's cache contiguous,
+ *             so skipping a KV head skips a contiguous block).
+ *   q         [batch][n_q_heads*head_dim]; o [batch][n_q_heads*head_dim] out.
  *   ws        >= wide_attention_decode_workspace_size(...) bytes (per-chunk
  *             partial maxima, sums and outputs).
  * Arithmetic: scores from bf16 pairs with fp32 sums; softmax and P.V in fp32
@@ -242,9 +250,9 @@ wide_status_t wide_attention_masked(wide_dtype_t dt, int64_t n_seq, int32_t T_q,
  */
 wide_status_t wide_attention_decode(wide_dtype_t dt, int64_t batch, int32_t L, int32_t n_q_heads,
                                     int32_t n_kv_heads, int32_t head_dim, int32_t group_size,
-                                    const uint8_t* mask, const int32_t* kv_len, const void* q,
-                                    const void* k_cache, const void* v_cache, void* o, void* ws,
-                                    size_t ws_bytes, hipStream_t stream);
+                                    const uint8_t* mask, const int32_t* kv_len, int32_t kv_layout,
+                                    const void* q, const void* k_cache, const void* v_cache, void* o,
+                                    void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Workspace bytes for wide_attention_decode (SIZE_MAX for rejected shapes). */
 size_t wide_attention_decode_workspace_size(int64_t batch, int32_t L, int32_t n_q_heads,

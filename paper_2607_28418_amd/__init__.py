@@ -64,7 +64,8 @@ def lib() -> ctypes.CDLL:
         L.wide_attention_workspace_size.restype = sz
         L.wide_attention_workspace_size.argtypes = [i64, i32, i32, i32, i32, i32, i32, i32]
         L.wide_attention_decode.restype = ci
-        L.wide_attention_decode.argtypes = [ci, i64, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.wide_attention_decode.argtypes = [ci, i64, i32, i32, i32, i32, i32, vp, vp, ci, vp, vp, vp, vp, vp,
+                                            sz, vp]
         L.wide_attention_decode_workspace_size.restype = sz
         L.wide_attention_decode_workspace_size.argtypes = [i64, i32, i32, i32, i32, i32]
         L.wide_workspace_size.restype = sz
@@ -308,14 +309,21 @@ def wide_attention_decode_workspace_size(batch, L, n_q, n_kv, head_dim, group_si
     return int(lib().wide_attention_decode_workspace_size(batch, L, n_q, n_kv, head_dim, group_size))
 
 
+KV_TOKEN_MAJOR, KV_HEAD_MAJOR = 0, 1
+
+
 def wide_attention_decode(q, k_cache, v_cache, mask, n_q, n_kv, head_dim, group_size, kv_len=None,
-                          o=None, ws=None):
-    """Head-group masked attention at decode.  q [B][n_q*head_dim], k_cache and
-    v_cache [B][L][n_kv*head_dim], mask [B][n_groups] uint8, kv_len optional
-    int32 [B].  Returns o, same shape as q."""
+                          o=None, ws=None, head_major=False):
+    """Head-group masked attention at decode.  q [B][n_q*head_dim]; k_cache and
+    v_cache [B][L][n_kv*head_dim] (or [B][n_kv][L][head_dim] with head_major);
+    mask [B][n_groups] uint8; kv_len optional int32 [B].  Returns o, same
+    shape as q."""
     _contig(q, k_cache, v_cache, mask, kv_len, o)
     B = q.shape[0]
-    L = k_cache.shape[1] if k_cache.dim() == 3 else 0
+    if head_major:
+        L = k_cache.shape[2] if k_cache.dim() == 4 else 0
+    else:
+        L = k_cache.shape[1] if k_cache.dim() == 3 else 0
     if o is None:
         o = _torch().empty_like(q)
     if ws is None:
@@ -323,6 +331,7 @@ def wide_attention_decode(q, k_cache, v_cache, mask, n_q, n_kv, head_dim, group_
         ws = None if need == SIZE_MAX else _workspace(need, q.device)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check("wide_attention_decode", lib().wide_attention_decode(
-        _dtype_code(q), B, L, n_q, n_kv, head_dim, group_size, _p(mask), _p(kv_len), _p(q), _p(k_cache),
+        _dtype_code(q), B, L, n_q, n_kv, head_dim, group_size, _p(mask), _p(kv_len),
+        KV_HEAD_MAJOR if head_major else KV_TOKEN_MAJOR, _p(q), _p(k_cache),
         _p(v_cache), _p(o), _p(ws), nbytes, _stream(q)))
     return o

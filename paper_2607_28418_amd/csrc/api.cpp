@@ -957,11 +957,13 @@ size_t wide_attention_decode_workspace_size(int64_t batch, int32_t L, int32_t n_
 
 wide_status_t wide_attention_decode(wide_dtype_t dt, int64_t batch, int32_t L, int32_t n_q_heads,
                                     int32_t n_kv_heads, int32_t head_dim, int32_t group_size,
-                                    const uint8_t* mask, const int32_t* kv_len, const void* q,
-                                    const void* k_cache, const void* v_cache, void* o, void* ws,
-                                    size_t ws_bytes, hipStream_t stream) {
+                                    const uint8_t* mask, const int32_t* kv_len, int32_t kv_layout,
+                                    const void* q, const void* k_cache, const void* v_cache, void* o,
+                                    void* ws, size_t ws_bytes, hipStream_t stream) {
   AttnShape s;
   CHECK(attention_decode_shape(dt, batch, L, n_q_heads, n_kv_heads, head_dim, group_size, s));
+  if (kv_layout != WIDE_KV_TOKEN_MAJOR && kv_layout != WIDE_KV_HEAD_MAJOR)
+    return fail(WIDE_ERR_INVALID_ARG, "kv_layout must be WIDE_KV_TOKEN_MAJOR or WIDE_KV_HEAD_MAJOR");
   if (batch == 0) return ok();
   CHECK(check_ptr(mask, "mask", false));
   if (kv_len) CHECK(check_ptr(kv_len, "kv_len", false));
@@ -985,6 +987,7 @@ wide_status_t wide_attention_decode(wide_dtype_t dt, int64_t batch, int32_t L, i
   a.ng = s.ng;
   a.hpg = s.hpg;
   a.qpk = s.qpk;
+  a.head_major = kv_layout == WIDE_KV_HEAD_MAJOR;
   a.chunk = wide::attn_decode_chunk(a.B, n_kv_heads, L);
   a.n_chunks = (L + a.chunk - 1) / a.chunk;
   a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)head_dim));

@@ -18,8 +18,10 @@
 //   scores: lane = key; the lane's K row against the head's q (bf16 pairs
 //           through v_dot2 with fp32 sums), q read from LDS by broadcast;
 //   softmax: online per head over the chunk (max and sums across the wave);
-//   P.V:    lane = two of the 128 dims; each key's probability is read out
-//           of its lane (readlane) and its V row is read from LDS.
+//   P.V:    lane = (one of 4 key slots, 8 of the 128 dims); a key's
+//           probability moves from its lane by a cross-lane permute and
+//           16 bytes of its V row come from LDS; the 4 slots are added at
+//           the end of the chunk.
 // Per (token, head, chunk) the kernel leaves (max, sum, unnormalised o) in
 // the workspace; a second kernel merges the chunks (and writes +0 for
 // inactive heads).
@@ -93,8 +95,11 @@ __global__ __launch_bounds__(kDT) void wide_attn_decode(AttnDecArgs a) {
 
   // Loads of one 64-key step: K and V tiles of 16 KB = 16 wave instructions
   // each; wave w issues K instructions 4w..4w+3 and V instructions 4w..4w+3.
-  const int64_t ldk = (int64_t)a.n_kv * kHd;
-  const int64_t cache0 = (int64_t)b * a.L;
+  // token-major cache: row (b, key) holds all KV heads; head-major: the
+  // (b, KV head) cache is one contiguous [L][128] block
+  const int64_t ldk = a.head_major ? kHd : (int64_t)a.n_kv * kHd;
+  const int64_t cache0 = a.head_major ? ((int64_t)b * a.n_kv + hkv) * a.L * kHd
+                                      : (int64_t)b * a.L * ldk + hkv * kHd;
   auto issue = [&](int j0, int st) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -102,19 +107,22 @@ __global__ __launch_bounds__(kDT) void wide_attn_decode(AttnDecArgs a) {
       const int r = u * 4 + lane / 16;     // key row in the step
       const int lc = (lane & 15) ^ (r & 15);
       const int key = min(j0 + r, len - 1);  // rows past the end: any valid row (never used)
-      const int64_t g = (cache0 + key) * ldk + hkv * kHd + lc * 8;
+      const int64_t g = cache0 + key * ldk + lc * 8;
       __builtin_amdgcn_global_load_lds((gptr_t)(a.k + g), (lptr_t)(&sk[st][u * 4 * kHd]), 16, 0, 0);
       __builtin_amdgcn_global_load_lds((gptr_t)(a.v + g), (lptr_t)(&sv[st][u * 4 * kHd]), 16, 0, 0);
     }
   };
 
-  float m[HPW], zl[HPW], o0[HPW], o1[HPW];
+  // P.V layout: lane = (key slot ks = lane / 16, dim chunk dc = lane % 16);
+  // the lane accumulates dims 8*dc .. 8*dc+7 over the keys = ks (mod 4).
+  const int ks4 = lane >> 4, dc = lane & 15;
+  float m[HPW], zl[HPW], acc[HPW][8];
 #pragma unroll
   for (int i = 0; i < HPW; ++i) {
     m[i] = -INFINITY;
     zl[i] = 0.0f;
-    o0[i] = 0.0f;
-    o1[i] = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[i][e] = 0.0f;
   }
   const float sc = a.scale_log2;
   const int nsteps = (j_end - j_begin + kKeys - 1) / kKeys;
@@ -148,16 +156,21 @@ __global__ __launch_bounds__(kDT) void wide_attn_decode(AttnDecArgs a) {
       const float p = __builtin_amdgcn_exp2f(sv2 - mnew);
       m[i] = mnew;
       zl[i] = zl[i] * alpha + p;
-      float a0 = o0[i] * alpha, a1 = o1[i] * alpha;
-      // P.V: lane holds dims 2*lane, 2*lane+1 (logical chunk lane/4 of a row)
-      for (int j = 0; j < nvalid; ++j) {
-        const float pj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p), j));
-        const uint32_t vv = *reinterpret_cast<const uint32_t*>(&vs[dswz(j, lane >> 2) + 2 * (lane & 3)]);
-        a0 = fmaf(pj, bf16_to_f32((uint16_t)(vv & 0xffffu)), a0);
-        a1 = fmaf(pj, bf16_to_f32((uint16_t)(vv >> 16)), a1);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[i][e] *= alpha;
+      // P.V over the 64 keys of the step, 16 per lane (rows past kv_len hold a
+      // copy of a valid row and carry p = 0)
+#pragma unroll
+      for (int it = 0; it < kKeys / 4; ++it) {
+        const int key = 4 * it + ks4;
+        const float pj = __int_as_float(__builtin_amdgcn_ds_bpermute(key * 4, __float_as_int(p)));
+        const u32x4 vv = *reinterpret_cast<const u32x4*>(&vs[dswz(key, dc)]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[i][2 * e] = fmaf(pj, __uint_as_float(vv[e] << 16), acc[i][2 * e]);
+          acc[i][2 * e + 1] = fmaf(pj, __uint_as_float(vv[e] & 0xffff0000u), acc[i][2 * e + 1]);
+        }
       }
-      o0[i] = a0;
-      o1[i] = a1;
     }
   }
   // partials: (max, sum, o[128]) per (token, head, chunk)
@@ -166,13 +179,23 @@ __global__ __launch_bounds__(kDT) void wide_attn_decode(AttnDecArgs a) {
     const int hh = w + 4 * i;
     if (hh >= a.qpk || !(act & (1u << hh))) continue;
     const float z = wave_sum(zl[i]);
+    float o8[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {  // add the four key slots
+      float v = acc[i][e];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      o8[e] = v;
+    }
     float* part = a.part + (((int64_t)b * a.n_q + hkv * a.qpk + hh) * a.n_chunks + c) * (kHd + 2);
     if (lane == 0) {
       part[0] = m[i];
       part[1] = z;
     }
-    part[2 + 2 * lane] = o0[i];
-    part[3 + 2 * lane] = o1[i];
+    if (lane < 16) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) part[2 + 8 * lane + e] = o8[e];
+    }
   }
 }
 

@@ -190,13 +190,14 @@ int attn_slots(int T_q, int hb);
 // ---- masked attention, decode (attention_decode.hip)
 struct AttnDecArgs {
   const uint16_t* q;        // [B][n_q*128] bf16, one query token per sequence
-  const uint16_t* k;        // [B][L][n_kv*128] bf16 key cache
-  const uint16_t* v;        // [B][L][n_kv*128] bf16 value cache
+  const uint16_t* k;        // bf16 key cache: [B][L][n_kv*128], or [B][n_kv][L][128] if head_major
+  const uint16_t* v;        // bf16 value cache, same layout
   uint16_t* o;              // [B][n_q*128] bf16 out
   const uint8_t* mask;      // [B][ng]
   const int32_t* kv_len;    // optional [B]: keys [0, kv_len[b]) are attended (NULL: L)
   float* part;              // workspace [B][n_q][n_chunks][2 + 128]
   int B, L, n_q, n_kv, ng, hpg, qpk;
+  int head_major;           // cache layout (see k)
   int chunk, n_chunks;      // keys per workgroup (multiple of 64), ceil(L / chunk)
   float scale_log2;
 };

@@ -189,9 +189,10 @@ def test_attention_workspace_size():
     assert W.wide_attention_workspace_size(1, 64, 64, 32, 8, 64, 512, True) == W.SIZE_MAX
 
 
-def attention_decode(dt=W.BF16, B=32, L=8192, nq=32, nkv=8, hd=128, G=512, mask=A, kv_len=None, q=A, k=A,
-                     v=A, o=A, ws=A, ws_bytes=1 << 40):
-    return W.lib().wide_attention_decode(dt, B, L, nq, nkv, hd, G, mask, kv_len, q, k, v, o, ws, ws_bytes, None)
+def attention_decode(dt=W.BF16, B=32, L=8192, nq=32, nkv=8, hd=128, G=512, mask=A, kv_len=None, layout=0, q=A,
+                     k=A, v=A, o=A, ws=A, ws_bytes=1 << 40):
+    return W.lib().wide_attention_decode(dt, B, L, nq, nkv, hd, G, mask, kv_len, layout, q, k, v, o, ws, ws_bytes,
+                                         None)
 
 
 @pytest.mark.parametrize("kw,status,msg", [
@@ -207,6 +208,7 @@ def attention_decode(dt=W.BF16, B=32, L=8192, nq=32, nkv=8, hd=128, G=512, mask=
     (dict(o=None), W.ERR_INVALID_ARG, "o is NULL"),
     (dict(mask=None), W.ERR_INVALID_ARG, "mask is NULL"),
     (dict(ws_bytes=0), W.ERR_WORKSPACE, "workspace"),
+    (dict(layout=2), W.ERR_INVALID_ARG, "kv_layout"),
 ])
 def test_attention_decode_validation(kw, status, msg):
     assert attention_decode(**kw) == status

@@ -157,8 +157,14 @@ def decode_bound(orc, q, k, v, mask, n_q, n_kv, hd):
     return (2.0 ** -10 + k.shape[0] * 2.0 ** -24) * a_abs
 
 
+def head_major(a, n_kv, hd):
+    """[B][L][n_kv*hd] -> [B][n_kv][L][hd] (contiguous)."""
+    B, L = a.shape[:2]
+    return np.ascontiguousarray(a.reshape(B, L, n_kv, hd).transpose(0, 2, 1, 3))
+
+
 def run_decode(orc, B, L, n_q, n_kv, G, mask="bernoulli", keep=0.5, qk_std=1.0, ragged=False, seed=0,
-               poison_unused=False):
+               poison_unused=False, hm=False):
     hd = 128
     c = synth.attn_decode_case(seed, B, L, n_q, n_kv, hd, n_q * hd // G, mask=mask, keep=keep,
                                qk_std=qk_std, ragged=ragged)
@@ -174,10 +180,12 @@ def run_decode(orc, B, L, n_q, n_kv, G, mask="bernoulli", keep=0.5, qk_std=1.0, 
                 if not any(c.mask[b, (hk * qpk + i) // hpg] for i in range(qpk)):
                     k_host[b, :, hk * hd:(hk + 1) * hd] = nan
                     v_host[b, :, hk * hd:(hk + 1) * hd] = nan
+    if hm:
+        k_host, v_host = head_major(k_host, n_kv, hd), head_major(v_host, n_kv, hd)
     q, k, v, m = (to_dev(a) for a in (c.q, k_host, v_host, c.mask))
     kl = to_dev(c.kv_len) if ragged else None
     o = torch.full_like(q, float("nan"))
-    W.wide_attention_decode(q, k, v, m, n_q, n_kv, hd, G, kv_len=kl, o=o)
+    W.wide_attention_decode(q, k, v, m, n_q, n_kv, hd, G, kv_len=kl, o=o, head_major=hm)
     torch.cuda.synchronize()
     got = to_np64(o)
     for b in range(B):
@@ -197,9 +205,10 @@ def run_decode(orc, B, L, n_q, n_kv, G, mask="bernoulli", keep=0.5, qk_std=1.0, 
     (2, 130, 32, 1, 1024, False),    # 32 query heads on one KV head
     (32, 2048, 32, 8, 512, False),   # Llama-3-8B heads, 32 sequences
 ])
-def test_attention_decode_matches_oracle(orc, B, L, n_q, n_kv, G, ragged):
-    say("attention decode", B, L, n_q, n_kv, G, ragged)
-    run_decode(orc, B, L, n_q, n_kv, G, ragged=ragged, qk_std=1.5, seed=B + L)
+@pytest.mark.parametrize("hm", [False, True])
+def test_attention_decode_matches_oracle(orc, B, L, n_q, n_kv, G, ragged, hm):
+    say("attention decode", B, L, n_q, n_kv, G, ragged, "head-major" if hm else "token-major")
+    run_decode(orc, B, L, n_q, n_kv, G, ragged=ragged, qk_std=1.5, seed=B + L, hm=hm)
 
 
 @pytest.mark.parametrize("kind", ["zeros", "ones"])
@@ -208,9 +217,10 @@ def test_attention_decode_degenerate_masks(orc, kind):
     run_decode(orc, 6, 500, 8, 2, 512, mask=kind)
 
 
-def test_attention_decode_never_reads_unused_cache(orc):
-    say("attention decode poisoned cache")
-    run_decode(orc, 8, 700, 8, 2, 512, ragged=True, poison_unused=True, seed=4)
+@pytest.mark.parametrize("hm", [False, True])
+def test_attention_decode_never_reads_unused_cache(orc, hm):
+    say("attention decode poisoned cache", hm)
+    run_decode(orc, 8, 700, 8, 2, 512, ragged=True, poison_unused=True, seed=4, hm=hm)
 
 
 def test_attention_decode_empty():
