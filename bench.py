@@ -582,11 +582,22 @@ def main():
                 call = lambda: W.wide_attention_decode(qd, kc, vc, mdd, L.nq, L.nkv, L.hd, L.Ga, o=od, ws=wsd,
                                                        head_major=layout == "head-major")
                 t = ev_ms(call)
+                W.wide_timing_enable(True)
+                W.wide_timing_reset()
+                for _ in range(10):
+                    call()
+                torch.cuda.synchronize()
+                kd_ms, kd_n = W.wide_timing_query("wide_attn_decode")
+                km_ms, km_n = W.wide_timing_query("wide_attn_decode_merge")
+                W.wide_timing_enable(False)
                 act_kv = sum(1 for b_ in range(Bd) for hk in range(L.nkv)
                              if any(md_np[b_, (hk * qpk + i) // hpg] for i in range(qpk)))
                 by = act_kv * Ld * L.hd * 2 * 2
                 dec_rows.append(dict(layout=layout, mask=name, keep=round(float(md_np.mean()), 3),
-                                     ms=round(t, 4), active_kv_heads=act_kv, cache_bytes_read=by,
+                                     ms=round(t, 4), kernel_us=round(1e3 * kd_ms / kd_n, 2),
+                                     merge_us=round(1e3 * km_ms / km_n, 2),
+                                     kernel_GBps=round(by / (kd_ms / kd_n * 1e-3) / 1e9, 1),
+                                     active_kv_heads=act_kv, cache_bytes_read=by,
                                      GBps=round(by / (t * 1e-3) / 1e9, 1),
                                      frac_hbm=round(by / (t * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)))
         del kd_hm, vd_hm

@@ -233,7 +233,7 @@ wide_status_t wide_attention_masked(wide_dtype_t dt, int64_t n_seq, int32_t T_q,
  * the cache.
  *   dt        WIDE_BF16 (WIDE_ERR_UNSUPPORTED otherwise).
  *   batch, L  sequences and the cache capacity (rows per sequence).
- *   n_q_heads, n_kv_heads (at most 32 query heads per KV head), head_dim (128
+ *   n_q_heads, n_kv_heads (at most 16 query heads per KV head), head_dim (128
  *             only), group_size as for wide_qkvo_masked.
  *   mask      [batch][n_q_heads*head_dim/group_size] uint8.
  *   kv_len    optional int32 [batch] (device).

@@ -928,7 +928,7 @@ wide_status_t attention_decode_shape(wide_dtype_t dt, int64_t B, int32_t L, int 
   if (s.ng > 4096) return fail(WIDE_ERR_UNSUPPORTED, "more than 4096 groups");
   if (dt != WIDE_BF16) return fail(WIDE_ERR_UNSUPPORTED, "attention runs on bf16 only");
   if (hd != wide::kAttnHeadDim) return fail(WIDE_ERR_UNSUPPORTED, "attention needs head_dim 128 (got %d)", hd);
-  if (nq / nkv > 32) return fail(WIDE_ERR_UNSUPPORTED, "more than 32 query heads per KV head");
+  if (nq / nkv > 16) return fail(WIDE_ERR_UNSUPPORTED, "more than 16 query heads per KV head");
   s.M = B;
   s.Mk = B * (int64_t)L;
   s.hpg = G / hd;

@@ -198,7 +198,7 @@ def attention_decode(dt=W.BF16, B=32, L=8192, nq=32, nkv=8, hd=128, G=512, mask=
 @pytest.mark.parametrize("kw,status,msg", [
     (dict(dt=W.F32), W.ERR_UNSUPPORTED, "bf16"),
     (dict(hd=64, G=256), W.ERR_UNSUPPORTED, "head_dim 128"),
-    (dict(nq=66, nkv=2, G=128), W.ERR_UNSUPPORTED, "32 query heads"),
+    (dict(nq=34, nkv=2, G=128), W.ERR_UNSUPPORTED, "16 query heads"),
     (dict(nq=30), W.ERR_INVALID_ARG, "multiple of n_kv_heads"),
     (dict(G=192), W.ERR_INVALID_ARG, "multiple of head_dim"),
     (dict(L=0), W.ERR_INVALID_ARG, "length 0"),
