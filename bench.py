@@ -563,29 +563,68 @@ def main():
 
         # Decode: the layer's 32 decode tokens, each with a KV cache of T keys;
         # the layer's decode attention mask (and all-ones).  HBM-bound: the
-        # figure of merit is GB/s on the cache bytes of active KV heads.
+        # figure of merit is GB/s on the cache bytes of active KV heads.  Each
+        # call is replayed from a HIP graph (a decode step is launched that
+        # way), alternating two copies of the cache so that consecutive calls
+        # do not find each other's bytes in the caches.
         Bd, Ld = args.decode_batch, T
         qd = torch.randn(Bd, L.Nq, device=dev, generator=ga).to(torch.bfloat16)
-        kd = torch.randn(Bd, Ld, L.Nkv, device=dev, generator=ga).to(torch.bfloat16)
-        vd = torch.randn(Bd, Ld, L.Nkv, device=dev, generator=ga).to(torch.bfloat16)
+        caches = {}
+        for layout in ("token-major", "head-major"):
+            caches[layout] = []
+            for _ in range(2):
+                kd = torch.randn(Bd, Ld, L.Nkv, device=dev, generator=ga).to(torch.bfloat16)
+                vd = torch.randn(Bd, Ld, L.Nkv, device=dev, generator=ga).to(torch.bfloat16)
+                if layout == "head-major":
+                    kd = kd.view(Bd, Ld, L.nkv, L.hd).transpose(1, 2).contiguous()
+                    vd = vd.view(Bd, Ld, L.nkv, L.hd).transpose(1, 2).contiguous()
+                caches[layout].append((kd, vd))
         od = torch.empty_like(qd)
         wsd = torch.empty(max(W.wide_attention_decode_workspace_size(Bd, Ld, L.nq, L.nkv, L.hd, L.Ga), 256),
                           dtype=torch.uint8, device=dev)
+
+        def graph_pair_ms(fns, reps=20):
+            graphs = []
+            for fn in fns:
+                side = torch.cuda.Stream()
+                side.wait_stream(stream)
+                with torch.cuda.stream(side):
+                    fn()
+                stream.wait_stream(side)
+                torch.cuda.synchronize()
+                gr = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(gr):
+                    fn()
+                graphs.append(gr)
+            for gr in graphs:
+                gr.replay()
+            torch.cuda.synchronize()
+            s0, s1 = ev(), ev()
+            s0.record(stream)
+            for i in range(reps):
+                graphs[i % len(graphs)].replay()
+            s1.record(stream)
+            torch.cuda.synchronize()
+            return s0.elapsed_time(s1) / reps
+
         dec_rows = []
         qpk, hpg = L.nq // L.nkv, L.Ga // L.hd
-        kd_hm = kd.view(Bd, Ld, L.nkv, L.hd).transpose(1, 2).contiguous()
-        vd_hm = vd.view(Bd, Ld, L.nkv, L.hd).transpose(1, 2).contiguous()
-        for layout, (kc, vc) in (("token-major", (kd, vd)), ("head-major", (kd_hm, vd_hm))):
+        for layout in ("token-major", "head-major"):
+            alt = np.ones((Bd, L.nga), np.uint8)
+            alt[:, ::2] = 0
             for name, md_np in (("layer mask", L.batches["decode"]["mask_attn"]),
+                                ("every other head group off", alt),
                                 ("all-ones", np.ones((Bd, L.nga), np.uint8))):
                 mdd = to_dev(md_np)
-                call = lambda: W.wide_attention_decode(qd, kc, vc, mdd, L.nq, L.nkv, L.hd, L.Ga, o=od, ws=wsd,
-                                                       head_major=layout == "head-major")
-                t = ev_ms(call)
+                fns = [(lambda kc=kc, vc=vc: W.wide_attention_decode(
+                    qd, kc, vc, mdd, L.nq, L.nkv, L.hd, L.Ga, o=od, ws=wsd, head_major=layout == "head-major"))
+                    for kc, vc in caches[layout]]
+                W.wide_timing_enable(False)
+                t = graph_pair_ms(fns)
                 W.wide_timing_enable(True)
                 W.wide_timing_reset()
-                for _ in range(10):
-                    call()
+                for i in range(10):
+                    fns[i % 2]()
                 torch.cuda.synchronize()
                 kd_ms, kd_n = W.wide_timing_query("wide_attn_decode")
                 km_ms, km_n = W.wide_timing_query("wide_attn_decode_merge")
@@ -596,11 +635,10 @@ def main():
                 dec_rows.append(dict(layout=layout, mask=name, keep=round(float(md_np.mean()), 3),
                                      ms=round(t, 4), kernel_us=round(1e3 * kd_ms / kd_n, 2),
                                      merge_us=round(1e3 * km_ms / km_n, 2),
-                                     kernel_GBps=round(by / (kd_ms / kd_n * 1e-3) / 1e9, 1),
                                      active_kv_heads=act_kv, cache_bytes_read=by,
                                      GBps=round(by / (t * 1e-3) / 1e9, 1),
                                      frac_hbm=round(by / (t * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)))
-        del kd_hm, vd_hm
+        kd, vd = caches["token-major"][0]
         sdpa_dec = None
         try:
             import torch.nn.functional as F
@@ -621,7 +659,7 @@ def main():
         attention["decode"] = dict(
             workload="masked decode attention, %d sequences x %d cached keys, 32 q / 8 kv heads x 128" % (Bd, Ld),
             sdpa_flash_dense_ms=round(sdpa_dec, 4) if sdpa_dec else None, rows=dec_rows)
-        del qd, kd, vd, od, wsd
+        del qd, kd, vd, od, wsd, caches
 
     # ---- CPU oracle on a bounded sample --------------------------------------------
     cpu = None

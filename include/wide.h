@@ -317,13 +317,15 @@ const char* wide_last_error(void);
  * stream; the events come from a pool created by wide_timing_enable(1) (the
  * only call here that creates HIP objects) and recording stops silently when
  * the pool is exhausted.  wide_timing_query() synchronises on the recorded
- * events and returns, for kernels whose name contains `name_substr`, the total
- * elapsed milliseconds and the number of launches.  Do not enable timing
- * while capturing a graph.
+ * events and returns, for kernels whose label is `name` -- exactly, or
+ * followed by a template argument list or a "/variant" suffix ("wide_mn256"
+ * covers "wide_mn256<true>/bk64", not "wide_mn256_x") -- the total elapsed
+ * milliseconds and the number of launches.  Do not enable timing while
+ * capturing a graph.
  */
 wide_status_t wide_timing_enable(int enable);
 wide_status_t wide_timing_reset(void);
-wide_status_t wide_timing_query(const char* name_substr, double* total_ms,
+wide_status_t wide_timing_query(const char* name, double* total_ms,
                                 int64_t* launches);
 
 #ifdef __cplusplus

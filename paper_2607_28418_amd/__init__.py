@@ -162,11 +162,11 @@ def wide_timing_reset() -> None:
     _check("wide_timing_reset", lib().wide_timing_reset())
 
 
-def wide_timing_query(name_substr: str):
-    """(total milliseconds, launches) of recorded kernels whose name contains it."""
+def wide_timing_query(name: str):
+    """(total milliseconds, launches) of recorded kernels labelled `name`
+    (exactly, or followed by a template argument list or a "/variant" suffix)."""
     ms, n = ctypes.c_double(), ctypes.c_int64()
-    _check("wide_timing_query", lib().wide_timing_query(name_substr.encode(), ctypes.byref(ms),
-                                                        ctypes.byref(n)))
+    _check("wide_timing_query", lib().wide_timing_query(name.encode(), ctypes.byref(ms), ctypes.byref(n)))
     return float(ms.value), int(n.value)
 
 

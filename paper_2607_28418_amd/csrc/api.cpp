@@ -762,13 +762,17 @@ wide_status_t wide_timing_reset(void) {
   return ok();
 }
 
-wide_status_t wide_timing_query(const char* name_substr, double* total_ms, int64_t* launches) {
-  if (!name_substr || !total_ms || !launches) return fail(WIDE_ERR_INVALID_ARG, "NULL argument");
+wide_status_t wide_timing_query(const char* name, double* total_ms, int64_t* launches) {
+  if (!name || !total_ms || !launches) return fail(WIDE_ERR_INVALID_ARG, "NULL argument");
   std::lock_guard<std::mutex> lk(g_tmu);
+  const std::string want(name);
   double tot = 0.0;
   int64_t n = 0;
   for (size_t i = 0; i < g_used; ++i) {
-    if (g_names[g_pool[i].name].find(name_substr) == std::string::npos) continue;
+    const std::string& label = g_names[g_pool[i].name];
+    const bool hit = label.compare(0, want.size(), want) == 0 &&
+                     (label.size() == want.size() || label[want.size()] == '<' || label[want.size()] == '/');
+    if (!hit) continue;
     hipError_t e = hipEventSynchronize(g_pool[i].stop);
     if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
     float ms = 0.f;

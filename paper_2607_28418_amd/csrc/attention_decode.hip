@@ -27,6 +27,7 @@
 #include "common.h"
 #include "kernels.h"
 #include "launch.h"
+#include "tile256.h"
 
 namespace wide {
 namespace {
@@ -56,7 +57,11 @@ __global__ __launch_bounds__(kDT) void wide_attn_decode(AttnDecArgs a) {
   __shared__ __attribute__((aligned(16))) float s_p[4][kU][16];  // per wave: p[key][head]
   __shared__ __attribute__((aligned(16))) float s_al[4][16];     // per wave: rescale per head
   const int w = wave_id(), lane = lane_id();
-  const int64_t item = (int64_t)blockIdx.x * 4 + w;
+  // Work items in (sequence, KV head, chunk) order, four per workgroup; each
+  // XCD (workgroups are dealt round-robin to the 8 XCDs) takes a contiguous
+  // range of them, i.e. whole sequences, so masks that switch whole KV heads
+  // off still leave every XCD the same share of the work.
+  const int64_t item = (int64_t)t256::xcd_remap(blockIdx.x, gridDim.x) * 4 + w;
   if (item >= (int64_t)a.B * a.n_kv * a.n_chunks) return;
   const int c = (int)(item % a.n_chunks);
   const int bh = (int)(item / a.n_chunks);
@@ -207,7 +212,9 @@ __global__ __launch_bounds__(kDT) void wide_attn_decode(AttnDecArgs a) {
   }
 }
 
-// Merge of the chunks: one wave per (token, query head); lane = two dims.
+// Merge of the chunks: one wave per (token, query head).  Lanes take the
+// chunks for the maximum and the sum (64 at a time); for the output, lane =
+// two dims, and each chunk's weight comes out of its lane by readlane.
 __global__ __launch_bounds__(kDT) void wide_attn_decode_merge(AttnDecArgs a) {
   const int gw = blockIdx.x * (kDT / kWave) + wave_id();
   if (gw >= a.B * a.n_q) return;
@@ -222,15 +229,28 @@ __global__ __launch_bounds__(kDT) void wide_attn_decode_merge(AttnDecArgs a) {
   const int nc = (len + a.chunk - 1) / a.chunk;
   const float* part = a.part + ((int64_t)b * a.n_q + h) * a.n_chunks * (kHd + 2);
   float mx = -INFINITY;
-  for (int c = 0; c < nc; ++c) mx = fmaxf(mx, part[c * (kHd + 2)]);
+  for (int c0 = 0; c0 < nc; c0 += kWave)
+    if (c0 + lane < nc) mx = fmaxf(mx, part[(c0 + lane) * (kHd + 2)]);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
   float z = 0.0f, o0 = 0.0f, o1 = 0.0f;
-  for (int c = 0; c < nc; ++c) {
-    const float* pc = part + c * (kHd + 2);
-    const float f = __builtin_amdgcn_exp2f(pc[0] - mx);
-    z = fmaf(f, pc[1], z);
-    o0 = fmaf(f, pc[2 + 2 * lane], o0);
-    o1 = fmaf(f, pc[3 + 2 * lane], o1);
+  for (int c0 = 0; c0 < nc; c0 += kWave) {
+    const int c = c0 + lane;
+    float f = 0.0f;
+    if (c < nc) {
+      f = __builtin_amdgcn_exp2f(part[c * (kHd + 2)] - mx);
+      z = fmaf(f, part[c * (kHd + 2) + 1], z);
+    }
+    const int cnt = min(kWave, nc - c0);
+    for (int j = 0; j < cnt; ++j) {
+      const float fj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), j));
+      const float* pc = part + (c0 + j) * (kHd + 2) + 2 + 2 * lane;
+      o0 = fmaf(fj, pc[0], o0);
+      o1 = fmaf(fj, pc[1], o1);
+    }
   }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) z += __shfl_xor(z, o);
   const float inv = 1.0f / z;
   *reinterpret_cast<uint32_t*>(orow) = pack_bf16x2_hw(o0 * inv, o1 * inv);
 }

@@ -231,3 +231,15 @@ def test_attention_decode_empty():
                                 torch.zeros((0, 2), dtype=torch.uint8, device=dev()), 2, 1, 128, 128)
     torch.cuda.synchronize()
     assert o.shape == (0, 256)
+
+
+def test_attention_decode_timing_labels_are_distinct():
+    say("attention decode timing labels")
+    c = synth.attn_decode_case(2, 4, 256, 8, 2, 128, 2)
+    q, k, v, m = (to_dev(a) for a in (c.q, c.k, c.v, c.mask))
+    W.wide_timing_enable(True)
+    W.wide_timing_reset()
+    W.wide_attention_decode(q, k, v, m, 8, 2, 128, 512)
+    n_dec, n_merge = W.wide_timing_query("wide_attn_decode")[1], W.wide_timing_query("wide_attn_decode_merge")[1]
+    W.wide_timing_enable(False)
+    assert n_dec == 1 and n_merge == 1
