@@ -77,6 +77,12 @@ int k_path_for(int G) {
   return G >= 2048 ? 2 : 1;
 }
 
+// With one group (G = K, the M-axis case) the K axis runs as a row-gathered
+// N-axis GEMM over the whole output width; it needs the reorder.
+bool kaxis_row_gathered(int K, int N, int G) {
+  return G == K && g_big_tiles && N % wide::kT256 == 0 && K % 64 == 0;
+}
+
 // Workspace pieces of a prefill reorder held internally.
 struct ReorderWS {
   int32_t* idx = nullptr;
@@ -103,6 +109,7 @@ struct KWS {
 };
 
 void carve_kaxis(Carve& c, int64_t M, int N, int ng, int path, KWS& k) {
+  if (ng == 1 && g_big_tiles && N % wide::kT256 == 0) return;  // row-gathered single group: no scratch
   if (path == 0 || path == 2) k.acc32 = c.take<float>((size_t)M * (size_t)N);
   if (path == 0 || path == 1) k.tu = c.take<uint8_t>(wide::tile_union_bytes(M, ng));
 }
@@ -159,8 +166,10 @@ wide::GVNArgs ffn_gvn(int64_t M, int D, int Dff, int G, const uint8_t* mask, con
 wide_status_t ffn_shape(wide_dtype_t dt, int64_t M, int D, int Dff, int G) {
   CHECK(check_common(dt, M));
   if (D <= 0 || Dff <= 0) return fail(WIDE_ERR_INVALID_ARG, "d_model and d_ff must be positive");
-  if (!is_pow2(G) || G < 16)
-    return fail(WIDE_ERR_INVALID_ARG, "group_size=%d must be a power of two >= 16", G);
+  // G = d_ff is one group for the whole FFN (the M-axis case, App. A: a
+  // token runs the FFN or skips it); otherwise G is in {2^k, k >= 4}.
+  if ((!is_pow2(G) || G < 16) && G != Dff)
+    return fail(WIDE_ERR_INVALID_ARG, "group_size=%d must be a power of two >= 16 (or d_ff)", G);
   if (Dff % G) return fail(WIDE_ERR_INVALID_ARG, "group_size=%d does not divide d_ff=%d", G, Dff);
   if (D % 8 || Dff % 8) return fail(WIDE_ERR_INVALID_ARG, "d_model and d_ff must be multiples of 8");
   if (Dff / G > 4096) return fail(WIDE_ERR_UNSUPPORTED, "more than 4096 groups");
@@ -169,6 +178,8 @@ wide_status_t ffn_shape(wide_dtype_t dt, int64_t M, int D, int Dff, int G) {
   } else {
     if (D % 256) return fail(WIDE_ERR_UNSUPPORTED, "bf16 path needs d_model %% 256 == 0 (got %d)", D);
     if (G < 64) return fail(WIDE_ERR_UNSUPPORTED, "bf16 path needs group_size >= 64 (got %d)", G);
+    if (G == Dff && !is_pow2(G) && G % 128)
+      return fail(WIDE_ERR_UNSUPPORTED, "bf16 single-group path needs d_ff %% 128 == 0 (got %d)", G);
   }
   return WIDE_OK;
 }
@@ -271,7 +282,8 @@ size_t attn_ws_bytes(wide_phase_t ph, wide_dtype_t dt, int64_t M, const AttnDims
   } else {
     ReorderWS r;
     const int path = kpath;
-    if (need_idx && (path == 0 || path == 2)) carve_reorder(c, M, d.ng, true, r);
+    if (need_idx && (path == 0 || path == 2 || kaxis_row_gathered(d.Nq, d.D, d.G)))
+      carve_reorder(c, M, d.ng, true, r);
     KWS k;
     carve_kaxis(c, M, d.D, d.ng, path, k);
   }
@@ -297,6 +309,24 @@ wide_status_t run_kaxis(const uint16_t* a, const uint16_t* w, const uint8_t* mas
   ka.G = G;
   hipError_t e;
   const bool big = g_big_tiles && N % wide::kT256 == 0;
+  if (kaxis_row_gathered(K, N, G)) {
+    if (!idx || !cnt) return fail(WIDE_ERR_INVALID_ARG, "single-group K axis without a reorder");
+    // One group (the M-axis case): every output row takes one contribution,
+    // so the active rows run as a row-gathered N-axis GEMM over the whole
+    // output width, and the rows of inactive tokens are written +0; neither
+    // atomics nor dense-masked FLOPs are needed.
+    wide::MN256Args ma{};
+    ma.x = a;
+    ma.M = M;
+    ma.K = K;
+    ma.idx = idx;
+    ma.cnt = cnt;
+    ma.m_tiles = (int)((M + wide::kT256 - 1) / wide::kT256);
+    ma.n_regions = 1;
+    ma.reg[0] = wide::MN256Region{w, nullptr, y, N, N, 1, ma.m_tiles * (N / wide::kT256)};
+    if ((e = wide::launch_mn256(ma, false, s)) != hipSuccess) return hip_fail(e, "mn256 single-group K axis");
+    return WIDE_OK;
+  }
   if (path == 2) {
     if ((e = wide::launch_zero_f32(kws.acc32, M * (int64_t)N, s)) != hipSuccess) return hip_fail(e, "zero");
     e = big ? wide::launch_ks256(ka, s) : wide::launch_gemm_k_scatter(ka, s);
@@ -678,11 +708,12 @@ wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M, i
     return ok();
   }
 
-  const bool need_reorder = idx == nullptr && (phase == WIDE_PHASE_QKV || kpath == 2);
+  const bool rows_k = phase == WIDE_PHASE_O && kaxis_row_gathered(d.Nq, d.D, d.G);
+  const bool need_reorder = idx == nullptr && (phase == WIDE_PHASE_QKV || kpath == 2 || rows_k);
   ReorderWS r;
   if (phase == WIDE_PHASE_QKV) {
     if (idx == nullptr) carve_reorder(c, M, ng, true, r);
-  } else if (idx == nullptr && (kpath == 0 || kpath == 2)) {
+  } else if (idx == nullptr && (kpath == 0 || kpath == 2 || rows_k)) {
     carve_reorder(c, M, ng, true, r);
   }
   const int32_t* ix = idx;

@@ -221,3 +221,12 @@ def test_attention_decode_empty_and_workspace():
     assert n >= 32 * 32 * 130 * 4   # at least one chunk of (max, sum, o[128]) per (token, head)
     assert W.wide_attention_decode_workspace_size(0, 8192, 32, 8, 128, 512) == 0
     assert W.wide_attention_decode_workspace_size(32, 8192, 32, 8, 64, 512) == W.SIZE_MAX
+
+
+def test_single_group_is_accepted():
+    # group_size = d_ff (one group, the M-axis case) need not be a power of two
+    # (a valid call would launch; stop it at the workspace check instead)
+    assert ffn(Dff=14336, G=14336, ws_bytes=0) == W.ERR_WORKSPACE
+    assert ffn(Dff=14336, G=7168) == W.ERR_INVALID_ARG and "power of two" in err()
+    assert ffn(Dff=1000, G=1000, D=256) == W.ERR_UNSUPPORTED and "128" in err()
+    assert W.wide_workspace_size(W.OP_FFN, W.BF16, 8192, 4096, 14336, 14336) != W.SIZE_MAX

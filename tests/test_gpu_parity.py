@@ -479,3 +479,44 @@ def test_router_empty_batch():
                                    torch.zeros((6, 16), dtype=torch.bfloat16, device=dev()), reorder=True)
     torch.cuda.synchronize()
     assert mask.shape == (0, 3) and idx.shape == (3, 0) and not cnt.cpu().numpy().any()
+
+
+# ------------------------------------------------------------------ M axis (one group)
+
+@pytest.mark.parametrize("M,big,decode", [(300, 1, 0), (300, 0, 0), (8, 1, 1), (513, 1, 0)])
+def test_ffn_single_group_m_axis(orc, M, big, decode):
+    """group_size = d_ff: each token runs the whole FFN or skips it (App. A's
+    M-axis case); d_ff = 1152 is no power of two."""
+    say("ffn single group", M, "big", big, "decode", decode)
+    W.wide_set_option("decode_max_m", 64 if decode else 0)
+    W.wide_set_option("big_tiles", big)
+    D, Dff = 256, 1152
+    c = synth.ffn_case(M + 3, M, D, Dff, Dff, mask="bernoulli")
+    x, wg, wu, wd, m = ffn_dev(c)
+    h = torch.empty((M, Dff), dtype=torch.bfloat16, device=dev())
+    y = W.wide_ffn_masked(x, wg, wu, wd, m, Dff, h_out=h)
+    torch.cuda.synchronize()
+    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, Dff, round_bf16=True)
+    assert 0 < c.mask.mean() < 1
+    assert_close(h, rh, what="h")
+    assert_close(y, ry, what="y", abs_allow=ffn_flip_allowance(rh, synth.as_f32(c.w_down)))
+    yn = to_np64(y)
+    assert not yn[c.mask[:, 0] == 0].any()
+
+
+def test_ffn_single_group_fp32(orc):
+    say("ffn single group fp32")
+    c = synth.ffn_case(9, 100, 128, 240, 240, dtype="f32", mask="bernoulli")
+    x, wg, wu, wd, m = ffn_dev(c)
+    y = W.wide_ffn_masked(x, wg, wu, wd, m, 240)
+    torch.cuda.synchronize()
+    _, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, 240)
+    assert_close(y, ry, kind="f32", what="y")
+
+
+@pytest.mark.parametrize("M", [300, 24])
+def test_qkvo_single_group_m_axis(orc, M):
+    """group_size = n_q*head_dim: all heads form one group."""
+    say("qkvo single group", M)
+    c = synth.attn_case(M + 1, M, 512, 8, 2, 128, 1024, mask="bernoulli")
+    check_qkvo(orc, c)
