@@ -466,7 +466,60 @@ def main():
             xb = Mr * L.D * 2
             rt_rows.append(dict(tokens=Mr, n_groups=L.ng, rank=rank, ms_with_reorder=round(t, 4),
                                 x_GBps=round(xb / (t * 1e-3) / 1e9, 1)))
-        sweeps = dict(decode_ffn_llama7b=dec_rows, prefill_layer_keep=pre_rows, router_ffn=rt_rows)
+        # M axis (dynamic depth): one group per module (G = n_q*128 for the
+        # attention projections, G = d_ff for the FFN), so a token runs each
+        # module's projections or skips them; Bernoulli(0.5) per token and
+        # module.  K/V stay dense.
+        m_rows = []
+        bp_dev = bd["prefill"]
+        o_p = bufs["prefill"]
+        Mp = bp_dev["x_attn"].shape[0]
+        wsm = torch.empty(max(W.wide_workspace_size(W.OP_QKV, W.BF16, Mp, L.D, L.Nq, L.Nq),
+                              W.wide_workspace_size(W.OP_O, W.BF16, Mp, L.D, L.Nq, L.Nq),
+                              W.wide_workspace_size(W.OP_FFN, W.BF16, Mp, L.D, L.Dff, L.Dff), 256),
+                          dtype=torch.uint8, device=dev)
+        for keep in (0.5, 0.25):
+            hg = synth.rng(400 + int(round(keep * 100)))
+            ma1 = (hg.random((Mp, 1)) < keep).astype(np.uint8)
+            mf1 = (hg.random((Mp, 1)) < keep).astype(np.uint8)
+            ma_d, mf_d = to_dev(ma1), to_dev(mf1)
+            ia1 = torch.empty((1, Mp), dtype=torch.int32, device=dev)
+            ca1 = torch.empty((1,), dtype=torch.int32, device=dev)
+            if1 = torch.empty((1, Mp), dtype=torch.int32, device=dev)
+            cf1 = torch.empty((1,), dtype=torch.int32, device=dev)
+
+            def run_m():
+                W.wide_mask_reorder(ma_d, ia1, ca1, ws=wsm)
+                W.wide_mask_reorder(mf_d, if1, cf1, ws=wsm)
+                W.wide_qkvo_masked(W.PHASE_QKV, bp_dev["x_attn"], ma_d, L.Nq, L.nq, L.nkv, L.hd, w_q=w["w_q"],
+                                   w_k=w["w_k"], w_v=w["w_v"], idx=ia1, counts=ca1, q=o_p["q"], k=o_p["k"],
+                                   v=o_p["v"], ws=wsm)
+                W.wide_qkvo_masked(W.PHASE_O, bp_dev["a"], ma_d, L.Nq, L.nq, L.nkv, L.hd, w_o=w["w_o"],
+                                   idx=ia1, counts=ca1, y=o_p["y_o"], ws=wsm)
+                W.wide_ffn_masked(bp_dev["x_ffn"], w["w_gate"], w["w_up"], w["w_down"], mf_d, L.Dff, idx=if1,
+                                  counts=cf1, y=o_p["y_f"], ws=wsm)
+
+            for _ in range(3):
+                run_m()
+            torch.cuda.synchronize()
+            s0, s1 = ev(), ev()
+            s0.record(stream)
+            for _ in range(10):
+                run_m()
+            s1.record(stream)
+            torch.cuda.synchronize()
+            t = s0.elapsed_time(s1) / 10
+            na, nf = float(ma1.sum()), float(mf1.sum())
+            act = 2.0 * L.D * L.Nq * na * 2 + 4.0 * Mp * L.D * L.Nkv + 6.0 * L.D * L.Dff * nf
+            row = dict(keep=keep, tokens_attn=int(na), tokens_ffn=int(nf), ms=round(t, 4),
+                       active_TFLOPs=round(act / (t * 1e-3) / 1e12, 1),
+                       ideal_speedup=round(L.dense_flops("prefill") / act, 3))
+            if dense is not None:
+                row["speedup_vs_dense"] = round(dense["hipblaslt_prefill_ms"] / t, 3)
+            m_rows.append(row)
+        del wsm
+        sweeps = dict(decode_ffn_llama7b=dec_rows, prefill_layer_keep=pre_rows, router_ffn=rt_rows,
+                      prefill_layer_m_axis=m_rows)
 
     # ---- masked attention at prefill (outside the timed region) ----------------------
     # The step between the Q/K/V and O projections: one sequence of T tokens,

@@ -101,7 +101,10 @@ wide_status_t wide_mask_reorder(const uint8_t* mask, int64_t M, int32_t n_groups
  *   dt          WIDE_BF16 or WIDE_F32 (applies to x, weights, h_out, y).
  *   M           tokens (B*T flattened).
  *   d_model, d_ff, group_size (G): G must be a power of two >= 16 dividing
- *               d_ff (Section 3.1: the tile-size set {2^k, k >= 4}).
+ *               d_ff (Section 3.1: the tile-size set {2^k, k >= 4}), or d_ff
+ *               itself: one group, so each token runs the whole FFN or none
+ *               of it (the M-axis case of Appendix A; bf16 needs d_ff % 128
+ *               == 0 there).
  *   mask        [M][d_ff/G] uint8.
  *   idx, counts optional reorder of `mask` from wide_mask_reorder (reusable by
  *               every operator under the same routing decision, Appendix B);

@@ -64,10 +64,20 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
   }
   // Tile order: group, then sorted m-tile, then column tile inside the
   // group, so the tiles an XCD runs together share the group's weight panel
-  // in L2 (measured faster than blocking m-tiles across groups).
+  // in L2 (measured faster than blocking m-tiles across groups).  A group
+  // wider than four column tiles (one group over a whole projection, the
+  // M-axis case) goes column tile first: each XCD then covers a slice of the
+  // weight once and re-reads the gathered rows, which fit the last-level
+  // cache, instead of streaming the whole weight once per m-tile.
   const int ntpg = R.gw / BNO;  // tiles per group
-  const int nt_in = tile % ntpg;
-  const int m_tile = (tile / ntpg) % a.m_tiles;
+  int nt_in, m_tile;
+  if (ntpg > 4) {
+    nt_in = (tile / a.m_tiles) % ntpg;
+    m_tile = tile % a.m_tiles;
+  } else {
+    nt_in = tile % ntpg;
+    m_tile = (tile / ntpg) % a.m_tiles;
+  }
   const int g = tile / (ntpg * a.m_tiles);
   const int n0 = g * R.gw + nt_in * BNO;
   const int64_t M = a.M;
