@@ -421,6 +421,11 @@ wide_status_t wide_set_option(const char* key, int64_t value) {
       (key[5] == 'n' ? wide::decode_tuning().n_split : wide::decode_tuning().k_split) = (int)value;
       return ok();
     }
+  if (!strcmp(key, "attn_qb")) {
+    if (value != 1 && value != 2) return fail(WIDE_ERR_INVALID_ARG, "attn_qb must be 1 or 2");
+    wide::g_attn_qb = (int)value;
+    return ok();
+  }
   return fail(WIDE_ERR_INVALID_ARG, "unknown option '%s'", key);
 }
 
@@ -434,6 +439,7 @@ wide_status_t wide_get_option(const char* key, int64_t* value) {
   else if (!strcmp(key, "gemv_n_split")) *value = wide::decode_tuning().n_split;
   else if (!strcmp(key, "gemv_k_ncb")) *value = wide::decode_tuning().k_ncb;
   else if (!strcmp(key, "gemv_k_split")) *value = wide::decode_tuning().k_split;
+  else if (!strcmp(key, "attn_qb")) *value = wide::g_attn_qb;
   else return fail(WIDE_ERR_INVALID_ARG, "unknown option '%s'", key);
   return ok();
 }

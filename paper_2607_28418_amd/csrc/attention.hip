@@ -39,6 +39,9 @@
 #include "tile256.h"
 
 namespace wide {
+
+int g_attn_qb = 1;  // query blocks of 32 per wave in the prefill kernel (1 or 2)
+
 namespace {
 
 using t256::gptr_t;
@@ -62,10 +65,14 @@ __device__ __forceinline__ u32x4 lds16(const uint16_t* p) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-template <int HB>
-__global__ __launch_bounds__(kAT, 2) void wide_attn_fwd(AttnArgs a) {
-  constexpr int RB = 4 / HB;    // 32-row blocks per workgroup
-  constexpr int BMW = 32 * RB;  // query rows per workgroup
+// HB: query heads per workgroup (sharing one KV head); QB: 32-query blocks
+// per wave.  With QB = 2 every K / V^T fragment read from LDS feeds two
+// MFMAs (one per query block), halving the LDS reads per MFMA.
+template <int HB, int QB>
+__global__ __launch_bounds__(kAT, QB == 1 ? 2 : 1) void wide_attn_fwd(AttnArgs a) {
+  constexpr int RB = 4 / HB;         // row blocks (of 32*QB rows) per workgroup
+  constexpr int WR = 32 * QB;        // query rows per wave
+  constexpr int BMW = WR * RB;       // query rows per workgroup
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (2 * kKSub + kVt)];  // 64 KB
 
   const int per_hb = a.n_seq * a.n_slots;
@@ -108,14 +115,20 @@ __global__ __launch_bounds__(kAT, 2) void wide_attn_fwd(AttnArgs a) {
     return a.causal ? (int)(t - seq0) + delta : a.T_k - 1;
   };
   const int rb = w / HB, h = h0 + (w - rb * HB);
-  const int wr0 = m0 + rb * 32;
+  const int wr0 = m0 + rb * WR;
   const bool wave_live = wr0 < c;
-  const int wr1 = min(c, wr0 + 32);
+  const int wr1 = min(c, wr0 + WR);
   const int l32 = lane & 31, hi = lane >> 5;
-  const int myr = wr0 + l32;
-  const bool valid = myr < c;
-  const int64_t t = valid ? (int64_t)idx_g[s0 + myr] : 0;
-  const int plim = valid ? limit_of(t) : -1;
+  bool valid[QB];
+  int64_t t[QB];
+  int plim[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int myr = wr0 + 32 * qb + l32;
+    valid[qb] = myr < c;
+    t[qb] = valid[qb] ? (int64_t)idx_g[s0 + myr] : 0;
+    plim[qb] = valid[qb] ? limit_of(t[qb]) : -1;
+  }
   // rows ascend by position, so the first and last rows bound the limits
   const int wmin = wave_live ? limit_of(idx_g[s0 + wr0]) : -1;
   const int wmax = wave_live ? limit_of(idx_g[s0 + wr1 - 1]) : -1;
@@ -123,11 +136,12 @@ __global__ __launch_bounds__(kAT, 2) void wide_attn_fwd(AttnArgs a) {
   const int n_tiles = (gmax + kBN) / kBN;
 
   // Q^T fragments (B operand): d-step s holds dims 16s + 8*hi .. +8 of the row.
-  u32x4 qf[8];
-  {
-    const uint16_t* qrow = a.q + t * ldq + (int64_t)h * kHd + hi * 8;
+  u32x4 qf[QB][8];
 #pragma unroll
-    for (int s = 0; s < 8; ++s) qf[s] = valid ? ldg16(qrow + 16 * s) : u32x4{0, 0, 0, 0};
+  for (int qb = 0; qb < QB; ++qb) {
+    const uint16_t* qrow = a.q + t[qb] * ldq + (int64_t)h * kHd + hi * 8;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) qf[qb][s] = valid[qb] ? ldg16(qrow + 16 * s) : u32x4{0, 0, 0, 0};
   }
 
   // Loads: a K tile and a V^T tile are 16 instructions of 1 KB (8 LDS rows
@@ -179,81 +193,107 @@ __global__ __launch_bounds__(kAT, 2) void wide_attn_fwd(AttnArgs a) {
   // 16(r/8) + 8*hi + r%8 of its 32-key block.
   const int pi = 16 * (l32 >> 4) + 8 * ((l32 >> 2) & 1) + 4 * ((l32 >> 3) & 1) + (l32 & 3);
 
-  f32x16 O[4];
+  f32x16 O[QB][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) O[i] = f32x16{};
-  float m = -INFINITY, z = 0.0f;
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) O[qb][i] = f32x16{};
+  float m[QB], z[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    m[qb] = -INFINITY;
+    z[qb] = 0.0f;
+  }
   const float sc = a.scale_log2;
 
-  // S^T of key tile jt for this wave's 32 queries (two 32-key blocks).
-  auto qk = [&](int jt, f32x16 (&S)[2]) {
+  // S^T of key tile jt for this wave's queries (two 32-key blocks each).
+  auto qk = [&](int jt, f32x16 (&S)[QB][2]) {
     const uint16_t* st = kst + (jt & 1) * 2 * kKSub;
-    S[0] = f32x16{};
-    S[1] = f32x16{};
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      S[qb][0] = f32x16{};
+      S[qb][1] = f32x16{};
+    }
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       const uint16_t* ks = st + (s >> 2) * kKSub;
       const int ch = 2 * (s & 3) + hi;
       const u32x4 k0 = lds16(ks + swz(pi, ch));
       const u32x4 k1 = lds16(ks + swz(32 + pi, ch));
-      S[0] = mfma32(k0, qf[s], S[0]);
-      S[1] = mfma32(k1, qf[s], S[1]);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        S[qb][0] = mfma32(k0, qf[qb][s], S[qb][0]);
+        S[qb][1] = mfma32(k1, qf[qb][s], S[qb][1]);
+      }
     }
   };
-  // Online softmax of tile jt's scores (masking and the new row maximum,
-  // then the exponentials and the rescale) and O^T += V^T P^T.
-  auto row_max = [&](int jt, f32x16 (&S)[2], float& alpha, float& muse) {
+  // Online softmax of tile jt's scores per query block (masking and the new
+  // row maximum, then the exponentials and the rescale) and O^T += V^T P^T.
+  auto softmax_pv = [&](int jt, f32x16 (&S)[QB][2]) {
     const int j0 = jt * kBN;
     // Per-element mask only where the tile crosses some row's limit; every
     // other tile is fully visible to the wave.
     if (j0 + kBN - 1 > wmin) {
-      const int lim = plim - j0 - 8 * hi;  // key offset past which this lane's row sees nothing
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        const int lim = plim[qb] - j0 - 8 * hi;  // key offset past which this row sees nothing
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            S[qb][kb][r] = 32 * kb + 16 * (r >> 3) + (r & 7) > lim ? -INFINITY : S[qb][kb][r];
+      }
+    }
+    float alpha[QB];
+    bool moved = false;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float mx = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          S[kb][r] = 32 * kb + 16 * (r >> 3) + (r & 7) > lim ? -INFINITY : S[kb][r];
-    }
-    float mx = -INFINITY;
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, S[qb][kb][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mnew = fmaxf(m[qb], mx * sc);
+      const float muse = mnew == -INFINITY ? 0.0f : mnew;  // a row with nothing visible yet
+      alpha[qb] = fast_exp2(m[qb] - muse);
+      m[qb] = mnew;
+      moved = moved || alpha[qb] != 1.0f;
+      float zs = 0.0f;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, S[kb][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mnew = fmaxf(m, mx * sc);
-    muse = mnew == -INFINITY ? 0.0f : mnew;  // a row with nothing visible yet
-    alpha = fast_exp2(m - muse);
-    m = mnew;
-  };
-  auto exp_pv = [&](int jt, f32x16 (&S)[2], float alpha, float muse) {
-    float zs = 0.0f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = fast_exp2(fmaf(S[kb][r], sc, -muse));
-        S[kb][r] = p;
-        zs += p;
+        for (int r = 0; r < 16; ++r) {
+          const float p = fast_exp2(fmaf(S[qb][kb][r], sc, -muse));
+          S[qb][kb][r] = p;
+          zs += p;
+        }
       }
+      z[qb] = z[qb] * alpha[qb] + zs;
     }
-    z = z * alpha + zs;
-    if (__any(alpha != 1.0f)) {  // lazy rescale: skipped once the maxima settle
+    if (__any(moved)) {  // lazy rescale: skipped once the maxima settle
 #pragma unroll
-      for (int db = 0; db < 4; ++db) O[db] *= alpha;
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int db = 0; db < 4; ++db) O[qb][db] *= alpha[qb];
     }
     const uint16_t* vts = vst + (jt & 1) * kVt;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
       for (int p = 0; p < 2; ++p) {
-        u32x4 pf;
+        u32x4 pf[QB];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) pf[e] = pack_bf16x2_hw(S[kb][8 * p + 2 * e], S[kb][8 * p + 2 * e + 1]);
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            pf[qb][e] = pack_bf16x2_hw(S[qb][kb][8 * p + 2 * e], S[qb][kb][8 * p + 2 * e + 1]);
         const int ch = 4 * kb + 2 * p + hi;
 #pragma unroll
         for (int db = 0; db < 4; ++db) {
           const u32x4 vf = lds16(vts + swz(32 * db + l32, ch));
-          O[db] = mfma32(vf, pf, O[db]);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) O[qb][db] = mfma32(vf, pf[qb], O[qb][db]);
         }
       }
     }
@@ -265,49 +305,71 @@ __global__ __launch_bounds__(kAT, 2) void wide_attn_fwd(AttnArgs a) {
   // the scores of tile jt+1 and then the softmax and P.V of tile jt, so the
   // matrix core has independent work while the softmax runs.  Everything
   // issued in one iteration lands before the next one starts.
-  if (kwave) {
-    issue_k(0);
-    if (n_tiles > 1) issue_k(1);
-  } else {
-    issue_v(0);
-  }
-  t256::wait_vm<0>();
-  t256::stage_barrier();
-  f32x16 Sa[2], Sb[2];
-  if (wtiles > 0) qk(0, Sa);
-  auto step = [&](int jt, f32x16 (&Sc)[2], f32x16 (&Sn)[2]) {
+  if constexpr (QB == 1) {
+    if (kwave) {
+      issue_k(0);
+      if (n_tiles > 1) issue_k(1);
+    } else {
+      issue_v(0);
+    }
     t256::wait_vm<0>();
     t256::stage_barrier();
-    if (kwave) {
-      if (jt + 2 < n_tiles) issue_k(jt + 2);
-    } else {
-      if (jt + 1 < n_tiles) issue_v(jt + 1);
+    f32x16 Sa[QB][2], Sb[QB][2];
+    if (wtiles > 0) qk(0, Sa);
+    auto step = [&](int jt, f32x16 (&Sc)[QB][2], f32x16 (&Sn)[QB][2]) {
+      t256::wait_vm<0>();
+      t256::stage_barrier();
+      if (kwave) {
+        if (jt + 2 < n_tiles) issue_k(jt + 2);
+      } else {
+        if (jt + 1 < n_tiles) issue_v(jt + 1);
+      }
+      if (jt + 1 < wtiles) qk(jt + 1, Sn);
+      if (jt < wtiles) softmax_pv(jt, Sc);  // l = 2: tiles past the wave's rows issue no MFMA
+    };
+    for (int jt = 0; jt < n_tiles; jt += 2) {
+      step(jt, Sa, Sb);
+      if (jt + 1 < n_tiles) step(jt + 1, Sb, Sa);
     }
-    if (jt + 1 < wtiles) qk(jt + 1, Sn);
-    if (jt < wtiles) {  // l = 2: tiles past the wave's rows issue no MFMA
-      float alpha, muse;
-      row_max(jt, Sc, alpha, muse);
-      exp_pv(jt, Sc, alpha, muse);
+  } else {
+    // Two query blocks already give the matrix core independent work, and
+    // the registers for a second score tile are not there: scores of tile jt
+    // are computed in its own step.
+    // Both rings run one tile ahead: iteration jt loads K and V of tile jt+1
+    // into the stages tile jt-1 used.
+    f32x16 S[QB][2];
+    if (kwave) issue_k(0);
+    else issue_v(0);
+    for (int jt = 0; jt < n_tiles; ++jt) {
+      t256::wait_vm<0>();
+      t256::stage_barrier();
+      if (jt + 1 < n_tiles) {
+        if (kwave) issue_k(jt + 1);
+        else issue_v(jt + 1);
+      }
+      if (jt < wtiles) {  // l = 2: tiles past the wave's rows issue no MFMA
+        qk(jt, S);
+        softmax_pv(jt, S);
+      }
     }
-  };
-  for (int jt = 0; jt < n_tiles; jt += 2) {
-    step(jt, Sa, Sb);
-    if (jt + 1 < n_tiles) step(jt + 1, Sb, Sa);
   }
 
   // Epilogue: the two halves of a query's sum, normalise, scatter the row.
-  const float zt = z + __shfl_xor(z, 32);
-  if (!valid) return;
-  const float inv = 1.0f / zt;
-  uint16_t* orow = a.o + t * ldq + (int64_t)h * kHd + 4 * hi;
 #pragma unroll
-  for (int db = 0; db < 4; ++db) {
+  for (int qb = 0; qb < QB; ++qb) {
+    const float zt = z[qb] + __shfl_xor(z[qb], 32);
+    if (!valid[qb]) continue;
+    const float inv = 1.0f / zt;
+    uint16_t* orow = a.o + t[qb] * ldq + (int64_t)h * kHd + 4 * hi;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      uint2 v;
-      v.x = pack_bf16x2_hw(O[db][4 * j] * inv, O[db][4 * j + 1] * inv);
-      v.y = pack_bf16x2_hw(O[db][4 * j + 2] * inv, O[db][4 * j + 3] * inv);
-      *reinterpret_cast<uint2*>(orow + 32 * db + 8 * j) = v;
+    for (int db = 0; db < 4; ++db) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        uint2 v;
+        v.x = pack_bf16x2_hw(O[qb][db][4 * j] * inv, O[qb][db][4 * j + 1] * inv);
+        v.y = pack_bf16x2_hw(O[qb][db][4 * j + 2] * inv, O[qb][db][4 * j + 3] * inv);
+        *reinterpret_cast<uint2*>(orow + 32 * db + 8 * j) = v;
+      }
     }
   }
 }
@@ -388,7 +450,9 @@ int attn_heads_per_block(int hpg, int qpk) {
   return 1;
 }
 
-int attn_slots(int T_q, int hb) { return (T_q + 32 * (4 / hb) - 1) / (32 * (4 / hb)); }
+int attn_query_blocks() { return g_attn_qb; }
+
+int attn_slots(int T_q, int hb) { return (T_q + 32 * attn_query_blocks() * (4 / hb) - 1) / (32 * attn_query_blocks() * (4 / hb)); }
 
 hipError_t launch_attention(AttnArgs a, const uint16_t* v, int32_t* seq_off, hipStream_t s) {
   if (a.M == 0) return hipSuccess;
@@ -401,9 +465,15 @@ hipError_t launch_attention(AttnArgs a, const uint16_t* v, int32_t* seq_off, hip
   if (e != hipSuccess) return e;
   a.seq_off = a.n_seq > 1 ? seq_off : nullptr;
   const dim3 grid((unsigned)((int64_t)(a.n_q / hb) * a.n_seq * a.n_slots));
-  if (hb == 4) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<4>), grid, dim3(kAT), 0, s, a);
-  else if (hb == 2) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<2>), grid, dim3(kAT), 0, s, a);
-  else WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<1>), grid, dim3(kAT), 0, s, a);
+  if (g_attn_qb == 2) {
+    if (hb == 4) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<4, 2>), grid, dim3(kAT), 0, s, a);
+    else if (hb == 2) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<2, 2>), grid, dim3(kAT), 0, s, a);
+    else WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<1, 2>), grid, dim3(kAT), 0, s, a);
+  } else {
+    if (hb == 4) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<4, 1>), grid, dim3(kAT), 0, s, a);
+    else if (hb == 2) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<2, 1>), grid, dim3(kAT), 0, s, a);
+    else WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<1, 1>), grid, dim3(kAT), 0, s, a);
+  }
   return hipGetLastError();
 }
 

@@ -186,6 +186,7 @@ struct AttnArgs {
 hipError_t launch_attention(AttnArgs a, const uint16_t* v, int32_t* seq_off, hipStream_t s);
 int attn_heads_per_block(int hpg, int qpk);
 int attn_slots(int T_q, int hb);
+extern int g_attn_qb;  // 32-query blocks per wave in the prefill attention kernel (1 or 2)
 
 // ---- masked attention, decode (attention_decode.hip)
 struct AttnDecArgs {
