@@ -306,10 +306,10 @@ size_t wide_workspace_size(wide_op_t op, wide_dtype_t dt, int64_t M,
  *                   adds a small kernel that sums the partial results.
  *                   Workspace sizes depend on these four options: query
  *                   wide_workspace_size after setting them.
- * Not synchronised with calls running on other host threads.
-  *   "attn_qb"       32-query blocks per wave in the prefill attention kernel:
+ *   "attn_qb"       32-query blocks per wave in the prefill attention kernel:
  *                   1 (default) or 2 (each K/V fragment feeds two MFMAs, one
  *                   wave per SIMD; measured slower).
+ * Not synchronised with calls running on other host threads.
  */
 wide_status_t wide_set_option(const char* key, int64_t value);
 wide_status_t wide_get_option(const char* key, int64_t* value);
