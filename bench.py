@@ -709,9 +709,34 @@ def main():
             best_d = min(dense_r["ms"], sdpa_dec) if sdpa_dec else dense_r["ms"]
             r["speedup_vs_dense"] = round(best_d / r["ms"], 3)
             r["ideal_speedup"] = round(dense_r["cache_bytes_read"] / r["cache_bytes_read"], 3)
+        # Speedup against the attention group size (random 50% mask per
+        # (token, group)): below (n_q/n_kv)*head_dim a KV head is read when any
+        # of its query heads' groups is active.
+        g_rows = []
+        kc0, vc0 = caches["token-major"][0], caches["token-major"][1]
+        dense_g = next(r for r in dec_rows if r["layout"] == "token-major" and r["mask"] == "all-ones")["ms"]
+        for Gs in (128, 256, 512, 1024, 2048, 4096):
+            ngs = L.nq * L.hd // Gs
+            mg = synth.mask_bernoulli(synth.rng(500 + Gs), Bd, ngs, 0.5)
+            mgd = to_dev(mg)
+            wsg = torch.empty(max(W.wide_attention_decode_workspace_size(Bd, Ld, L.nq, L.nkv, L.hd, Gs), 256),
+                              dtype=torch.uint8, device=dev)
+            fns = [(lambda kc=kc, vc=vc: W.wide_attention_decode(qd, kc, vc, mgd, L.nq, L.nkv, L.hd, Gs, o=od,
+                                                                 ws=wsg))
+                   for kc, vc in (kc0, vc0)]
+            t = graph_pair_ms(fns)
+            hpg_s = Gs // L.hd
+            act_kv = sum(1 for b_ in range(Bd) for hk in range(L.nkv)
+                         if any(mg[b_, (hk * qpk + i) // hpg_s] for i in range(qpk)))
+            g_rows.append(dict(group_size=Gs, heads_per_group=hpg_s, ms=round(t, 4),
+                               kv_heads_read_frac=round(act_kv / (Bd * L.nkv), 3),
+                               speedup_vs_dense=round(dense_g / t, 3),
+                               ideal_speedup=round(Bd * L.nkv / max(act_kv, 1), 3)))
+            del wsg
         attention["decode"] = dict(
             workload="masked decode attention, %d sequences x %d cached keys, 32 q / 8 kv heads x 128" % (Bd, Ld),
-            sdpa_flash_dense_ms=round(sdpa_dec, 4) if sdpa_dec else None, rows=dec_rows)
+            sdpa_flash_dense_ms=round(sdpa_dec, 4) if sdpa_dec else None, rows=dec_rows,
+            vs_group_size=g_rows)
         del qd, kd, vd, od, wsd, caches
 
     # ---- CPU oracle on a bounded sample --------------------------------------------
