@@ -617,8 +617,10 @@ wide_status_t wide_ffn_masked(wide_dtype_t dt, int64_t M, int32_t d_model, int32
     ma.cnt = ct;
     ma.m_tiles = (int)((M + wide::kT256 - 1) / wide::kT256);
     ma.n_regions = 1;
+    // An H kept in the workspace is read only through its active blocks by
+    // every K-axis schedule, so its inactive blocks need no zeros.
     ma.reg[0] = wide::MN256Region{static_cast<const uint16_t*>(w_gate), static_cast<const uint16_t*>(w_up), h,
-                                  Dff, G, 1, ng * ma.m_tiles * (G / 128)};
+                                  Dff, G, 1, ng * ma.m_tiles * (G / 128), h_out == nullptr ? 1 : 0};
     if ((e = wide::launch_mn256(ma, true, stream)) != hipSuccess) return hip_fail(e, "mn256 gate/up");
   } else {
     wide::MNArgs ma{};

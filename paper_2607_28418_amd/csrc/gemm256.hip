@@ -88,6 +88,7 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
   const int tid = threadIdx.x;
 
   if (m0 >= cnt) {  // l = 0: the whole tile is inactive for group g
+    if (R.skip_zero) return;
     constexpr int CH = BNO / 8;
     const int64_t pend = min(m0 + BM, M);
     for (int i = tid; i < BM * CH; i += NT) {

@@ -82,6 +82,7 @@ struct MN256Region {
   int gw;
   int masked;
   int tiles;
+  int skip_zero;  // 1: leave the output blocks of inactive rows unwritten (no reader needs them)
 };
 
 struct MN256Args {
