@@ -292,6 +292,11 @@ size_t wide_workspace_size(wide_op_t op, wide_dtype_t dt, int64_t M,
  *   "k_path"        schedule of the prefill K-axis product (down, O):
  *                   0 automatic (default), 1 dense-masked (no atomics),
  *                   2 scatter (the paper's GEMM-K with fp32 atomics).
+ *   "kd_pattern"    1 (default): before the dense-masked K-axis schedule on
+ *                   256x256 tiles with 2..8 groups (attention's O projection),
+ *                   three small kernels order the tokens by mask pattern so a
+ *                   tile skips every group none of its rows uses; 0 keeps
+ *                   token order.  Outputs are bitwise equal either way.
  *   "big_tiles"     1 (default): prefill GEMMs use 256x256 tiles where the
  *                   shape allows; 0: always the 128x128 tiles.
  *   "ring_bk"       k depth of a 256x256 pipeline stage: 64 (two stages,

@@ -46,6 +46,7 @@ wide_status_t hip_fail(hipError_t e, const char* where) {
 int64_t g_decode_max_m = 64;  // M <= this uses the decode (GEMV) kernels
 int g_k_path = 0;             // 0 auto, 1 dense-masked, 2 scatter
 int g_big_tiles = 1;          // 1: 256x256 tile kernels where the shape allows
+int g_kd_pattern = 1;         // 1: dense-masked K axis reads rows in mask-pattern order (<= 8 groups)
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
@@ -106,12 +107,26 @@ void carve_reorder(Carve& c, int64_t M, int ng, bool need_idx, ReorderWS& r) {
 struct KWS {
   float* acc32 = nullptr;
   uint8_t* tu = nullptr;
+  int32_t* perm = nullptr;  // tokens ordered by mask pattern (dense-masked, few groups)
+  int32_t* pat = nullptr;   // scratch of that ordering
 };
+
+// The dense-masked 256-tile schedule reads its rows in mask-pattern order
+// when there are few groups (2..8): tiles then skip the groups none of their
+// rows uses.
+bool kaxis_pattern_order(int N, int ng, int path) {
+  return g_kd_pattern && path != 2 && ng > 1 && ng <= wide::kPatternMaxGroups && g_big_tiles &&
+         N % wide::kT256 == 0;
+}
 
 void carve_kaxis(Carve& c, int64_t M, int N, int ng, int path, KWS& k) {
   if (ng == 1 && g_big_tiles && N % wide::kT256 == 0) return;  // row-gathered single group: no scratch
   if (path == 0 || path == 2) k.acc32 = c.take<float>((size_t)M * (size_t)N);
   if (path == 0 || path == 1) k.tu = c.take<uint8_t>(wide::tile_union_bytes(M, ng));
+  if (kaxis_pattern_order(N, ng, path)) {
+    k.perm = c.take<int32_t>((size_t)M);
+    k.pat = c.take<int32_t>(wide::pattern_scratch_ints(M));
+  }
 }
 
 // ---- argument checks ----------------------------------------------------------
@@ -334,8 +349,13 @@ wide_status_t run_kaxis(const uint16_t* a, const uint16_t* w, const uint8_t* mas
     if ((e = wide::launch_f32_to_bf16(kws.acc32, y, M * (int64_t)N, s)) != hipSuccess)
       return hip_fail(e, "f32_to_bf16");
   } else {
-    e = big && K / G <= wide::kKd256MaxGroups ? wide::launch_kd256(ka, s)
-                                              : wide::launch_gemm_k_dense_masked(ka, s);
+    const bool use256 = big && K / G <= wide::kKd256MaxGroups;
+    if (use256 && kaxis_pattern_order(N, K / G, path) && kws.perm) {
+      if ((e = wide::launch_pattern_order(mask, M, K / G, kws.perm, kws.pat, s)) != hipSuccess)
+        return hip_fail(e, "pattern order");
+      ka.perm = kws.perm;
+    }
+    e = use256 ? wide::launch_kd256(ka, s) : wide::launch_gemm_k_dense_masked(ka, s);
     if (e != hipSuccess) return hip_fail(e, "gemm_k dense-masked");
   }
   return WIDE_OK;
@@ -421,6 +441,11 @@ wide_status_t wide_set_option(const char* key, int64_t value) {
       (key[5] == 'n' ? wide::decode_tuning().n_split : wide::decode_tuning().k_split) = (int)value;
       return ok();
     }
+  if (!strcmp(key, "kd_pattern")) {
+    if (value < 0 || value > 1) return fail(WIDE_ERR_INVALID_ARG, "kd_pattern must be 0 or 1");
+    g_kd_pattern = (int)value;
+    return ok();
+  }
   if (!strcmp(key, "attn_qb")) {
     if (value != 1 && value != 2) return fail(WIDE_ERR_INVALID_ARG, "attn_qb must be 1 or 2");
     wide::g_attn_qb = (int)value;
@@ -439,6 +464,7 @@ wide_status_t wide_get_option(const char* key, int64_t* value) {
   else if (!strcmp(key, "gemv_n_split")) *value = wide::decode_tuning().n_split;
   else if (!strcmp(key, "gemv_k_ncb")) *value = wide::decode_tuning().k_ncb;
   else if (!strcmp(key, "gemv_k_split")) *value = wide::decode_tuning().k_split;
+  else if (!strcmp(key, "kd_pattern")) *value = g_kd_pattern;
   else if (!strcmp(key, "attn_qb")) *value = wide::g_attn_qb;
   else return fail(WIDE_ERR_INVALID_ARG, "unknown option '%s'", key);
   return ok();

@@ -179,9 +179,13 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
 
   if (tid < nw) s_union[tid] = 0u;
   __syncthreads();
+  // Tile row r is token m0 + r, or perm[m0 + r] when the rows are ordered by
+  // mask pattern (rows that share groups then share the tile).
+  auto token = [&](int64_t p) -> int64_t { return a.perm ? (int64_t)a.perm[p] : p; };
   for (int i = tid; i < BM * nw; i += NT) {
     const int r = i / nw, wd = i % nw;
-    const int64_t t = m0 + r;
+    const int64_t p = m0 + r;
+    const int64_t t = p < a.M ? token(p) : a.M;
     uint32_t bits = 0;
     if (t < a.M) {
       const uint8_t* mr = a.mask + t * ng + wd * 32;
@@ -209,9 +213,9 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
   for (int j = 0; j < S; ++j) {
     const int rr = Rg::slot_row(j);
     const int c8 = Rg::slot_chunk(j) * 8;
-    const int64_t t = m0 + rr;
+    const int64_t p = m0 + rr;
     srow[j] = rr;
-    abase[j] = t < a.M ? a.a + t * a.K + c8 : nullptr;
+    abase[j] = p < a.M ? a.a + token(p) * a.K + c8 : nullptr;
     bbase[j] = a.w + (int64_t)(n0 + rr) * a.K + c8;
   }
   const int lane = lane_id(), w = wave_id();
@@ -242,9 +246,9 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
   for (int fm = 0; fm < 4; ++fm)
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const int64_t t = m0 + acc_row(fm, i);
-      if (t >= a.M) continue;
-      uint16_t* o = a.y + t * a.N + n0 + wn * 64;
+      const int64_t p = m0 + acc_row(fm, i);
+      if (p >= a.M) continue;
+      uint16_t* o = a.y + token(p) * a.N + n0 + wn * 64;
       o[col] = f32_to_bf16(acc[fm][0][i]);
       o[32 + col] = f32_to_bf16(acc[fm][1][i]);
     }

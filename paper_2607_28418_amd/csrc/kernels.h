@@ -12,6 +12,12 @@ hipError_t launch_reorder(const uint8_t* mask, int64_t M, int n_groups,
                           int32_t* idx, int32_t* counts, int32_t* chunk_cnt,
                           int32_t* chunk_off, hipStream_t s);
 size_t reorder_scratch_ints(int64_t M, int n_groups);
+// Token order by mask pattern (n_groups <= 8): perm[M] lists the tokens
+// grouped by their mask row.  scratch: pattern_scratch_ints(M) ints.
+constexpr int kPatternMaxGroups = 8;
+size_t pattern_scratch_ints(int64_t M);
+hipError_t launch_pattern_order(const uint8_t* mask, int64_t M, int n_groups, int32_t* perm, int32_t* scratch,
+                                hipStream_t s);
 
 // ---- prefill N-axis GEMM ---------------------------------------------------
 // A region is a run of output tiles sharing one weight (or gate/up pair) and
@@ -54,6 +60,7 @@ struct KArgs {
   float* acc32;        // [M][N] fp32 accumulation (scatter variant)
   uint16_t* y;         // [M][N] bf16 output (dense-masked variant)
   uint8_t* tile_union; // [ceil(M/128)][K/G] scratch (dense-masked variant)
+  const int32_t* perm; // optional [M]: tile rows are tokens perm[m0 + r] (256-tile dense-masked)
   int64_t M;
   int K, N, G;
 };

@@ -238,6 +238,98 @@ hipError_t launch_reorder(const uint8_t* mask, int64_t M, int n_groups, int32_t*
   return hipGetLastError();
 }
 
+// ---- token order by mask pattern ---------------------------------------------
+//
+// For a K-axis projection with few groups (attention's head groups), tokens
+// that share a mask row share their set of active groups.  Ordering the
+// tokens by that row makes the rows of one 256-row tile share most of their
+// groups, so the dense-masked K-axis kernel can skip the k steps of every
+// group none of the tile's rows uses.  The sort key is the row's rank in the
+// reflected binary Gray code (the row's bits, read as a Gray codeword, decoded
+// to binary): neighbouring patterns then differ in one group, and a tile that
+// straddles several of them spans fewer groups than in plain binary order
+// (for 4 of 8 groups per token, 5.75 instead of 6.2 of 8 on average).
+// Any order within a pattern is fine (each output row's sum is the same: a
+// skipped group only ever adds exact zeros), so the scatter takes positions
+// inside a chunk with LDS atomics.  Three short kernels: per-chunk pattern
+// histograms, one exclusive scan over (pattern, chunk), the scatter.
+namespace {
+constexpr int kPatChunk = 1024;  // tokens per workgroup
+constexpr int kPatMaxGroups = 8;
+constexpr int kPatKeys = 1 << kPatMaxGroups;
+
+__device__ __forceinline__ int pattern_of(const uint8_t* mask, int64_t t, int ng) {
+  int key = 0;
+  for (int g = 0; g < ng; ++g) key |= (mask[t * ng + g] != 0) << g;
+  key ^= key >> 1;  // Gray decode of an 8-bit word: prefix XOR from the top bit down
+  key ^= key >> 2;
+  key ^= key >> 4;
+  return key;
+}
+
+__global__ __launch_bounds__(kPatChunk) void wide_pattern_count(const uint8_t* mask, int64_t M, int ng,
+                                                                int n_chunks, int32_t* hist) {
+  __shared__ int h[kPatKeys];
+  const int tid = threadIdx.x;
+  for (int i = tid; i < kPatKeys; i += kPatChunk) h[i] = 0;
+  __syncthreads();
+  const int64_t t = (int64_t)blockIdx.x * kPatChunk + tid;
+  if (t < M) atomicAdd(&h[pattern_of(mask, t, ng)], 1);
+  __syncthreads();
+  for (int i = tid; i < kPatKeys; i += kPatChunk) hist[(int64_t)i * n_chunks + blockIdx.x] = h[i];
+}
+
+// hist [key][chunk] -> exclusive prefix in (key, chunk) order, in place.
+__global__ __launch_bounds__(1024) void wide_pattern_scan(int32_t* hist, int n) {
+  __shared__ int64_t part[1024];
+  const int tid = threadIdx.x;
+  const int per = (n + 1023) / 1024;
+  const int b = tid * per, e = min(n, b + per);
+  int64_t s = 0;
+  for (int i = b; i < e; ++i) s += hist[i];
+  part[tid] = s;
+  __syncthreads();
+  for (int o = 1; o < 1024; o <<= 1) {  // inclusive scan of the thread sums
+    const int64_t v = tid >= o ? part[tid - o] : 0;
+    __syncthreads();
+    part[tid] += v;
+    __syncthreads();
+  }
+  int64_t run = tid ? part[tid - 1] : 0;
+  for (int i = b; i < e; ++i) {
+    const int c = hist[i];
+    hist[i] = (int32_t)run;
+    run += c;
+  }
+}
+
+__global__ __launch_bounds__(kPatChunk) void wide_pattern_scatter(const uint8_t* mask, int64_t M, int ng,
+                                                                  int n_chunks, const int32_t* off,
+                                                                  int32_t* perm) {
+  __shared__ int cur[kPatKeys];
+  const int tid = threadIdx.x;
+  for (int i = tid; i < kPatKeys; i += kPatChunk) cur[i] = off[(int64_t)i * n_chunks + blockIdx.x];
+  __syncthreads();
+  const int64_t t = (int64_t)blockIdx.x * kPatChunk + tid;
+  if (t < M) perm[atomicAdd(&cur[pattern_of(mask, t, ng)], 1)] = (int32_t)t;
+}
+}  // namespace
+
+size_t pattern_scratch_ints(int64_t M) { return (size_t)kPatKeys * (size_t)((M + kPatChunk - 1) / kPatChunk); }
+
+hipError_t launch_pattern_order(const uint8_t* mask, int64_t M, int n_groups, int32_t* perm, int32_t* scratch,
+                                hipStream_t s) {
+  if (M == 0) return hipSuccess;
+  if (n_groups > kPatMaxGroups) return hipErrorInvalidValue;
+  const int64_t nc64 = (M + kPatChunk - 1) / kPatChunk;
+  if (nc64 * kPatKeys > 0x7fffffff) return hipErrorInvalidValue;
+  const int nc = (int)nc64;
+  WIDE_LAUNCH(wide_pattern_count, dim3(nc), dim3(kPatChunk), 0, s, mask, M, n_groups, nc, scratch);
+  WIDE_LAUNCH(wide_pattern_scan, dim3(1), dim3(1024), 0, s, scratch, nc * kPatKeys);
+  WIDE_LAUNCH(wide_pattern_scatter, dim3(nc), dim3(kPatChunk), 0, s, mask, M, n_groups, nc, scratch, perm);
+  return hipGetLastError();
+}
+
 size_t reorder_scratch_ints(int64_t M, int n_groups) {
   const int64_t n_chunks = (M + kChunk - 1) / kChunk;
   return (size_t)(n_chunks * n_groups);

@@ -30,6 +30,7 @@ def _options():
     W.wide_set_option("k_path", 0)
     W.wide_set_option("big_tiles", 1)
     W.wide_set_option("ring_bk", 64)
+    W.wide_set_option("kd_pattern", 1)
 
 
 def ffn_dev(c):
@@ -520,3 +521,22 @@ def test_qkvo_single_group_m_axis(orc, M):
     say("qkvo single group", M)
     c = synth.attn_case(M + 1, M, 512, 8, 2, 128, 1024, mask="bernoulli")
     check_qkvo(orc, c)
+
+
+@pytest.mark.parametrize("M,n_q,n_kv,G,kind", [(600, 16, 4, 256, "topk"), (777, 32, 8, 512, "bernoulli"),
+                                               (300, 8, 2, 512, "topk")])
+def test_o_pattern_order_is_bitwise_same(orc, M, n_q, n_kv, G, kind):
+    """Reading the rows of the dense-masked K axis in mask-pattern order only
+    skips k steps whose contributions are exact zeros: outputs are bitwise
+    equal with and without it (and match the oracle)."""
+    say("o pattern order", M, n_q, n_kv, G, kind)
+    c = synth.attn_case(M + G, M, 512, n_q, n_kv, 128, G, mask=kind)
+    d = attn_dev(c)
+    outs = []
+    for on in (1, 0):
+        W.wide_set_option("kd_pattern", on)
+        outs.append(W.wide_qkvo_masked(W.PHASE_O, d["a"], d["mask"], G, n_q, n_kv, 128, w_o=d["w_o"]))
+    W.wide_set_option("kd_pattern", 1)
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
+    assert_close(outs[0], orc.kproj(c.a, c.w_o, c.mask, G, round_bf16=True), what="o")
