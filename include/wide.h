@@ -292,6 +292,12 @@ size_t wide_workspace_size(wide_op_t op, wide_dtype_t dt, int64_t M,
  *   "k_path"        schedule of the prefill K-axis product (down, O):
  *                   0 automatic (default), 1 dense-masked (no atomics),
  *                   2 scatter (the paper's GEMM-K with fp32 atomics).
+ *   "mn_order"      tile order of the 256x256 N-axis kernels, two bits.
+ *                   Bit 1 (default on): each XCD runs the full tiles of its
+ *                   groups first, then their partial last m-tiles, then the
+ *                   empty ones.  Bit 0 (default off): the Q/K/V call puts the
+ *                   dense K and V tiles before the masked Q tiles (measured
+ *                   about 2% slower).  Outputs are identical for all values.
  *   "kd_pattern"    1 (default): before the dense-masked K-axis schedule on
  *                   256x256 tiles with 2..8 groups (attention's O projection),
  *                   three small kernels order the tokens by mask pattern so a

@@ -46,6 +46,7 @@ wide_status_t hip_fail(hipError_t e, const char* where) {
 int64_t g_decode_max_m = 64;  // M <= this uses the decode (GEMV) kernels
 int g_k_path = 0;             // 0 auto, 1 dense-masked, 2 scatter
 int g_big_tiles = 1;          // 1: 256x256 tile kernels where the shape allows
+int g_mn_order = 2;           // bit 0: Q/K/V launch K and V before Q; bit 1: full tiles before partial ones
 int g_kd_pattern = 1;         // 1: dense-masked K axis reads rows in mask-pattern order (<= 8 groups)
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -331,6 +332,7 @@ wide_status_t run_kaxis(const uint16_t* a, const uint16_t* w, const uint8_t* mas
     // output width, and the rows of inactive tokens are written +0; neither
     // atomics nor dense-masked FLOPs are needed.
     wide::MN256Args ma{};
+    ma.order = (g_mn_order >> 1) & 1;
     ma.x = a;
     ma.M = M;
     ma.K = K;
@@ -441,6 +443,11 @@ wide_status_t wide_set_option(const char* key, int64_t value) {
       (key[5] == 'n' ? wide::decode_tuning().n_split : wide::decode_tuning().k_split) = (int)value;
       return ok();
     }
+  if (!strcmp(key, "mn_order")) {
+    if (value < 0 || value > 3) return fail(WIDE_ERR_INVALID_ARG, "mn_order must be 0..3");
+    g_mn_order = (int)value;
+    return ok();
+  }
   if (!strcmp(key, "kd_pattern")) {
     if (value < 0 || value > 1) return fail(WIDE_ERR_INVALID_ARG, "kd_pattern must be 0 or 1");
     g_kd_pattern = (int)value;
@@ -465,6 +472,7 @@ wide_status_t wide_get_option(const char* key, int64_t* value) {
   else if (!strcmp(key, "gemv_k_ncb")) *value = wide::decode_tuning().k_ncb;
   else if (!strcmp(key, "gemv_k_split")) *value = wide::decode_tuning().k_split;
   else if (!strcmp(key, "kd_pattern")) *value = g_kd_pattern;
+  else if (!strcmp(key, "mn_order")) *value = g_mn_order;
   else if (!strcmp(key, "attn_qb")) *value = wide::g_attn_qb;
   else return fail(WIDE_ERR_INVALID_ARG, "unknown option '%s'", key);
   return ok();
@@ -636,6 +644,7 @@ wide_status_t wide_ffn_masked(wide_dtype_t dt, int64_t M, int32_t d_model, int32
   }
   if (g_big_tiles && G % 128 == 0) {
     wide::MN256Args ma{};
+    ma.order = (g_mn_order >> 1) & 1;
     ma.x = static_cast<const uint16_t*>(x);
     ma.M = M;
     ma.K = D;
@@ -764,6 +773,7 @@ wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M, i
     const uint16_t* wv = static_cast<const uint16_t*>(w_v);
     if (g_big_tiles && d.G % wide::kT256 == 0 && d.Nkv % wide::kT256 == 0) {
       wide::MN256Args ma{};
+    ma.order = (g_mn_order >> 1) & 1;
       ma.x = x;
       ma.M = M;
       ma.K = d.D;
@@ -772,12 +782,15 @@ wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M, i
       ma.m_tiles = (int)((M + wide::kT256 - 1) / wide::kT256);
       ma.n_regions = 3;
       const int T = wide::kT256;
-      ma.reg[0] = wide::MN256Region{wq, nullptr, static_cast<uint16_t*>(q), d.Nq, d.G, 1,
-                                    ng * ma.m_tiles * (d.G / T)};
-      ma.reg[1] = wide::MN256Region{wk, nullptr, static_cast<uint16_t*>(k), d.Nkv, d.Nkv, 0,
-                                    ma.m_tiles * (d.Nkv / T)};
-      ma.reg[2] = wide::MN256Region{wv, nullptr, static_cast<uint16_t*>(v), d.Nkv, d.Nkv, 0,
-                                    ma.m_tiles * (d.Nkv / T)};
+      // K and V first: the masked Q tiles, whose last m-tiles are partial
+      // or empty, then end each XCD's run of tiles.
+      const int iq = (g_mn_order & 1) ? 2 : 0, ik = iq ? 0 : 1;
+      ma.reg[ik] = wide::MN256Region{wk, nullptr, static_cast<uint16_t*>(k), d.Nkv, d.Nkv, 0,
+                                     ma.m_tiles * (d.Nkv / T)};
+      ma.reg[ik + 1] = wide::MN256Region{wv, nullptr, static_cast<uint16_t*>(v), d.Nkv, d.Nkv, 0,
+                                         ma.m_tiles * (d.Nkv / T)};
+      ma.reg[iq] = wide::MN256Region{wq, nullptr, static_cast<uint16_t*>(q), d.Nq, d.G, 1,
+                                     ng * ma.m_tiles * (d.G / T)};
       if ((e = wide::launch_mn256(ma, false, stream)) != hipSuccess) return hip_fail(e, "mn256 qkv");
       return ok();
     }

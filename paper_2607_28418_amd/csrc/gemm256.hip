@@ -32,6 +32,9 @@ using RingMN = Ring<BK, BK == 64 ? 2 : 5>;
 template <int BK>
 using RingKD = Ring<BK, BK == 64 ? 2 : 4>;
 
+// Tiles of one region that each XCD runs (the region padded to a multiple of 8).
+__host__ __device__ __forceinline__ int mn256_share(int tiles) { return (tiles + 7) / 8; }
+
 template <class Rg, class Src>
 __device__ __forceinline__ void run_tile(uint16_t* smem, int nsteps, Src src, int brow0, int brow1,
                                          int live, f32x16 (&acc)[4][2]) {
@@ -52,16 +55,26 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
   constexpr int BNO = SWIGLU ? 128 : 256;  // output columns per tile
   const uint16_t* zero = g_zero_blk;
 
-  int tile = xcd_remap(blockIdx.x, gridDim.x);
+  // Workgroups are dealt round-robin to the 8 XCDs.  Each region's tiles
+  // (padded to a multiple of 8) are cut into 8 contiguous shares and XCD x
+  // runs share x of every region in turn: a masked region whose tail tiles
+  // are mostly empty then loads the XCDs as evenly as the dense regions
+  // beside it (one contiguous range per XCD over all regions left the XCDs
+  // holding K and V with half again the work of the others).
+  const int xcd = blockIdx.x % 8;
+  int local = blockIdx.x / 8;
   MN256Region R = a.reg[0];
-  if (a.n_regions > 1 && tile >= a.reg[0].tiles) {
-    tile -= a.reg[0].tiles;
+  if (a.n_regions > 1 && local >= mn256_share(a.reg[0].tiles)) {
+    local -= mn256_share(a.reg[0].tiles);
     R = a.reg[1];
-    if (a.n_regions > 2 && tile >= a.reg[1].tiles) {
-      tile -= a.reg[1].tiles;
+    if (a.n_regions > 2 && local >= mn256_share(a.reg[1].tiles)) {
+      local -= mn256_share(a.reg[1].tiles);
       R = a.reg[2];
     }
   }
+  const int share = mn256_share(R.tiles);
+  const int tile = xcd * share + local;
+  if (tile >= R.tiles) return;  // padding
   // Tile order: group, then sorted m-tile, then column tile inside the
   // group, so the tiles an XCD runs together share the group's weight panel
   // in L2 (measured faster than blocking m-tiles across groups).  A group
@@ -69,16 +82,60 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
   // M-axis case) goes column tile first: each XCD then covers a slice of the
   // weight once and re-reads the gathered rows, which fit the last-level
   // cache, instead of streaming the whole weight once per m-tile.
+  //
+  // When an XCD's share is a whole number of groups, it runs the full tiles
+  // of its groups first (in the order above), then their partial last
+  // m-tiles, then the empty ones: the tiles left for the final partial round
+  // of the XCD are the cheap ones (the partial tiles issue MFMAs only for
+  // their live fragments; the empty ones only write zeros, or nothing).
   const int ntpg = R.gw / BNO;  // tiles per group
-  int nt_in, m_tile;
-  if (ntpg > 4) {
-    nt_in = (tile / a.m_tiles) % ntpg;
-    m_tile = tile % a.m_tiles;
+  const int per_group = ntpg * a.m_tiles;
+  int g, nt_in, m_tile;
+  if (a.order && R.masked && ntpg <= 4 && 8 * share == R.tiles && share % per_group == 0) {
+    const int gps = share / per_group, gb = xcd * gps, gl = gb + gps - 1;
+    int n_full = 0, n_part = 0;
+    for (int i = gb; i <= gl; ++i) {
+      const int c = a.cnt[i];
+      n_full += c / BM;
+      n_part += (c % BM) != 0;
+    }
+    int l = local;
+    if (l < n_full * ntpg) {
+      for (g = gb; g < gl; ++g) {
+        const int f = a.cnt[g] / BM * ntpg;
+        if (l < f) break;
+        l -= f;
+      }
+      m_tile = l / ntpg;
+      nt_in = l % ntpg;
+    } else if ((l -= n_full * ntpg) < n_part * ntpg) {
+      for (g = gb; g < gl; ++g) {
+        const int f = (a.cnt[g] % BM) != 0 ? ntpg : 0;
+        if (l < f) break;
+        l -= f;
+      }
+      m_tile = a.cnt[g] / BM;
+      nt_in = l;
+    } else {
+      l -= n_part * ntpg;
+      for (g = gb; g < gl; ++g) {
+        const int e = (a.m_tiles - (a.cnt[g] + BM - 1) / BM) * ntpg;
+        if (l < e) break;
+        l -= e;
+      }
+      m_tile = (a.cnt[g] + BM - 1) / BM + l / ntpg;
+      nt_in = l % ntpg;
+    }
   } else {
-    nt_in = tile % ntpg;
-    m_tile = (tile / ntpg) % a.m_tiles;
+    if (ntpg > 4) {
+      nt_in = (tile / a.m_tiles) % ntpg;
+      m_tile = tile % a.m_tiles;
+    } else {
+      nt_in = tile % ntpg;
+      m_tile = (tile / ntpg) % a.m_tiles;
+    }
+    g = tile / per_group;
   }
-  const int g = tile / (ntpg * a.m_tiles);
   const int n0 = g * R.gw + nt_in * BNO;
   const int64_t M = a.M;
   const int K = a.K;
@@ -358,7 +415,7 @@ int get_ring_bk() { return g_ring_bk; }
 
 hipError_t launch_mn256(const MN256Args& a, bool swiglu, hipStream_t s) {
   int64_t total = 0;
-  for (int i = 0; i < a.n_regions; ++i) total += a.reg[i].tiles;
+  for (int i = 0; i < a.n_regions; ++i) total += 8 * (int64_t)mn256_share(a.reg[i].tiles);
   if (total == 0) return hipSuccess;
   if (swiglu)
     WIDE_RING_LAUNCH("wide_mn256<true>", MN_SW, RingMN, (unsigned)total, s, a);

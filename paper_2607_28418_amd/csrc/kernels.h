@@ -100,6 +100,7 @@ struct MN256Args {
   const int32_t* cnt;
   int m_tiles;
   int n_regions;
+  int order;  // 1: each XCD runs its groups' full tiles, then the partial, then the empty ones
   MN256Region reg[3];
 };
 

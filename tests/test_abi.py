@@ -107,6 +107,13 @@ def test_options():
         W.wide_set_option("k_path", 9)
     with pytest.raises(W.WideError):
         W.wide_set_option("nope", 1)
+    for key, default, bad in (("mn_order", 2, 4), ("kd_pattern", 1, 2), ("attn_qb", 1, 3)):
+        assert W.wide_get_option(key) == default
+        W.wide_set_option(key, 0 if key != "attn_qb" else 2)
+        with pytest.raises(W.WideError):
+            W.wide_set_option(key, bad)
+        W.wide_set_option(key, default)
+        assert W.wide_get_option(key) == default
 
 
 def router(dt=W.BF16, M=64, D=4096, r=32, ng=112, x=A, w1=A, w2=A, mask=A, logits=None, idx=None,

@@ -31,6 +31,7 @@ def _options():
     W.wide_set_option("big_tiles", 1)
     W.wide_set_option("ring_bk", 64)
     W.wide_set_option("kd_pattern", 1)
+    W.wide_set_option("mn_order", 2)
 
 
 def ffn_dev(c):
@@ -540,3 +541,49 @@ def test_o_pattern_order_is_bitwise_same(orc, M, n_q, n_kv, G, kind):
     torch.cuda.synchronize()
     assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
     assert_close(outs[0], orc.kproj(c.a, c.w_o, c.mask, G, round_bf16=True), what="o")
+
+
+def _edge_count_mask(g, M, ng):
+    """Per-group active counts that hit every tile-order case: none, all,
+    whole 256-row tiles, one row more or less than a tile, random."""
+    mask = synth.mask_bernoulli(g, M, ng, 0.5)
+    forced = [0, M, 512, 256, 257, 255, 1, min(M, 768)]
+    for j, c in enumerate(forced[:ng]):
+        col = np.zeros(M, np.uint8)
+        col[g.permutation(M)[:c]] = 1
+        mask[:, j] = col
+    return mask
+
+
+@pytest.mark.parametrize("order", [2, 0])
+@pytest.mark.parametrize("M,ng", [(1000, 16), (1300, 8), (256, 8)])
+def test_ffn_tile_order_edge_counts(orc, M, ng, order):
+    """Each XCD's share of gate/up tiles runs its full tiles, then partial,
+    then empty ones; every (group, m-tile) must still be written once."""
+    say("ffn tile order", M, ng, order)
+    W.wide_set_option("decode_max_m", 0)
+    W.wide_set_option("mn_order", order)
+    G = 128
+    c = synth.ffn_case(M + ng, M, 256, ng * G, G)
+    c.mask[:] = _edge_count_mask(synth.rng(M * 3 + ng), M, ng)
+    x, wg, wu, wd, m = ffn_dev(c)
+    h = torch.full((M, ng * G), 7.0, dtype=torch.bfloat16, device=dev())
+    y = W.wide_ffn_masked(x, wg, wu, wd, m, G, h_out=h)
+    y2 = W.wide_ffn_masked(x, wg, wu, wd, m, G)  # H kept in the workspace
+    torch.cuda.synchronize()
+    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, G, round_bf16=True)
+    assert_close(h, rh, what="h")
+    assert_close(y, ry, what="y", abs_allow=ffn_flip_allowance(rh, synth.as_f32(c.w_down)))
+    assert torch.equal(y.view(torch.int16), y2.view(torch.int16))
+
+
+@pytest.mark.parametrize("order", [0, 1, 2, 3])
+@pytest.mark.parametrize("M", [1000, 300])
+def test_qkv_tile_order_edge_counts(orc, M, order):
+    """Q (8 masked groups) before or after the dense K and V regions, with or
+    without the per-XCD full/partial/empty order inside Q."""
+    say("qkv tile order", M, order)
+    W.wide_set_option("mn_order", order)
+    c = synth.attn_case(M + 11, M, 256, 16, 4, 128, 256, mask="bernoulli")
+    c.mask[:] = _edge_count_mask(synth.rng(M * 5), M, 8)
+    check_qkvo(orc, c, kpath=0)
