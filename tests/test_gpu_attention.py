@@ -255,3 +255,41 @@ def test_attention_two_query_blocks_per_wave(orc, n_seq, T_q, T_k, n_q, n_kv, G,
         run_case(orc, n_seq, T_q, T_k, n_q, n_kv, G, causal, seed=T_q + 5)
     finally:
         W.wide_set_option("attn_qb", 1)
+
+
+def test_attention_calls_replay_in_hip_graph():
+    """Prefill and decode attention captured in one HIP graph: every replay
+    (with eager work and syncs in between) equals the eager result bitwise."""
+    say("attention graph replay")
+    hd, n_q, n_kv, G = 128, 8, 2, 512
+    cp = synth.attn_prefill_case(3, 2, 150, 150, n_q, n_kv, hd, n_q * hd // G, mask="topk")
+    q, k, v, m = (to_dev(a) for a in (cp.q, cp.k, cp.v, cp.mask))
+    cd = synth.attn_decode_case(4, 6, 300, n_q, n_kv, hd, n_q * hd // G, ragged=True)
+    dq, dk, dv, dm, dl = (to_dev(a) for a in (cd.q, cd.k, cd.v, cd.mask, cd.kv_len))
+    o = torch.empty_like(q)
+    do = torch.empty_like(dq)
+    ws = torch.empty(W.wide_attention_workspace_size(2, 150, 150, n_q, n_kv, hd, G, True),
+                     dtype=torch.uint8, device=dev())
+    dws = torch.empty(W.wide_attention_decode_workspace_size(6, 300, n_q, n_kv, hd, G),
+                      dtype=torch.uint8, device=dev())
+
+    def step():
+        W.wide_attention_masked(q, k, v, m, 2, n_q, n_kv, hd, G, True, o=o, ws=ws)
+        W.wide_attention_decode(dq, dk, dv, dm, n_q, n_kv, hd, G, kv_len=dl, o=do, ws=dws)
+
+    step()
+    torch.cuda.synchronize()
+    ref = [o.clone(), do.clone()]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for _ in range(3):
+        o.fill_(7.0)
+        do.fill_(7.0)
+        ws.fill_(0x5A)   # stale workspace contents must not matter
+        dws.fill_(0x5A)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(o.view(torch.int16), ref[0].view(torch.int16))
+        assert torch.equal(do.view(torch.int16), ref[1].view(torch.int16))
