@@ -79,6 +79,18 @@ struct Ring {
       __builtin_amdgcn_global_load_lds((gptr_t)b[j], (lptr_t)(stage + A_ELEMS + r0 * BK), 16, 0, 0);
     }
   }
+  __device__ static __forceinline__ void issue_a(uint16_t* stage, const uint16_t* const (&a)[SLOTS]) {
+    const int w = wave_id();
+#pragma unroll
+    for (int j = 0; j < SLOTS; ++j)
+      __builtin_amdgcn_global_load_lds((gptr_t)a[j], (lptr_t)(stage + (w * SLOTS + j) * RPI * BK), 16, 0, 0);
+  }
+  __device__ static __forceinline__ void issue_b(uint16_t* stage, const uint16_t* const (&b)[SLOTS]) {
+    const int w = wave_id();
+#pragma unroll
+    for (int j = 0; j < SLOTS; ++j)
+      __builtin_amdgcn_global_load_lds((gptr_t)b[j], (lptr_t)(stage + A_ELEMS + (w * SLOTS + j) * RPI * BK), 16, 0, 0);
+  }
   static constexpr int LOADS_PER_STEP = 2 * SLOTS;  // per wave
 };
 
@@ -140,8 +152,10 @@ __device__ __forceinline__ void mma_frags(const Frags& f, int live, f32x16 (&acc
 //
 // Schedule of step kt (KK = BK/16 sub-steps):
 //   - the loads of step kt+NS-1 go out into the stage that step kt-1 used
-//     (with two stages all at once, the stage must land within one step;
-//     with more, spread over the sub-steps);
+//     (with two stages, A's in sub-step 0 and B's in sub-step 1: measured 1-4%
+//     faster than all at once, or than halves of both, or B first; the stage
+//     must land within the step; with more stages, spread over the
+//     sub-steps);
 //   - sub-step kk issues the LDS reads of sub-step kk+1 after its first two
 //     MFMAs and before the other six, so LDS latency hides behind the matrix
 //     core;
@@ -189,7 +203,8 @@ __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Src src, in
     for (int kk = 0; kk < KK; ++kk) {
       if (more) {
         if (NS == 2) {
-          if (kk == 0) Rg::issue(nstage, ap, bp);
+          if (kk == 0) Rg::issue_a(nstage, ap);
+          if (kk == 1) Rg::issue_b(nstage, bp);
         } else {
           Rg::issue(nstage, ap, bp, kk * S / KK, (kk + 1) * S / KK);
         }
