@@ -152,12 +152,14 @@ __device__ __forceinline__ void mma_frags(const Frags& f, int live, f32x16 (&acc
 //
 // Schedule of step kt (KK = BK/16 sub-steps):
 //   - the loads of step kt+NS-1 go out into the stage that step kt-1 used
-//     (with two stages, A's in sub-step 0 and B's in sub-step 1: measured 1-4%
-//     faster than all at once, or than halves of both, or B first; the stage
-//     must land within the step; with more stages, spread over the
-//     sub-steps);
+//     (with two stages, in sub-step 0, two after each of its first four
+//     MFMAs, and they must land within the step; with more stages, spread
+//     over the sub-steps);
 //   - sub-step kk interleaves the LDS reads of sub-step kk+1 with its own
-//     MFMAs, so LDS latency hides behind the matrix core;
+//     MFMAs (one read per MFMA), so LDS latency hides behind the matrix core;
+//   (measured in same-process A/B runs on gate/up, down and Q/K/V: issuing
+//   the stage's loads in a burst at the start of the step, or reads in a
+//   burst after two MFMAs, was 2-6% slower in total)
 //   - at the last sub-step the wave waits for step kt+1, meets the others at
 //     the barrier (which also retires every read of step kt's stage) and
 //     reads step kt+1's first fragments between its first two and its last
@@ -197,16 +199,41 @@ __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Src src, in
     const uint16_t* bp[S];
     uint16_t* nstage = smem + (nxt % NS) * Rg::STAGE;
     const uint16_t* cstage = smem + (kt % NS) * Rg::STAGE;
-    if (more) src(nxt, ap, bp);
+    constexpr bool TWO = NS == 2;
+    if (TWO) {
+      // Branch-free, so the loads can sit among the MFMAs: in the last step
+      // they fetch that step again into the stage nobody reads any more
+      // (waited for after the loop).
+      src(min(nxt, nsteps - 1), ap, bp);
+    } else if (more) {
+      src(nxt, ap, bp);
+    }
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      if (more) {
-        if (NS == 2) {
-          if (kk == 0) Rg::issue_a(nstage, ap);
-          if (kk == 1) Rg::issue_b(nstage, bp);
-        } else {
-          Rg::issue(nstage, ap, bp, kk * S / KK, (kk + 1) * S / KK);
+      if (!TWO && more) Rg::issue(nstage, ap, bp, kk * S / KK, (kk + 1) * S / KK);
+      if (TWO && kk == 0) {
+        // Sub-step 0 of a two-stage ring: the next step's loads (two per
+        // MFMA) and the six fragment reads of sub-step 1 interleave with the
+        // MFMAs.
+        __builtin_amdgcn_sched_barrier(0);
+        mma_frags<FULL, 0, 4>(fr[0], live, acc);
+        Rg::issue_a(nstage, ap);
+        Rg::issue_b(nstage, bp);
+        read_frags<Rg>(cstage, 1, brow0, brow1, fr[1]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
         }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        continue;
       }
       if (kk + 1 < KK) {
         // Inside a step: the six fragment reads of sub-step kk+1 interleave
@@ -239,6 +266,7 @@ __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Src src, in
       mma_frags<FULL, 1, 4>(fr[kk & 1], live, acc);
     }
   }
+  if (NS == 2) wait_vm<0>();  // the last step's repeated loads
 }
 
 __device__ __forceinline__ void zero_acc(f32x16 (&acc)[4][2]) {
