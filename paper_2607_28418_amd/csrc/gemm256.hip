@@ -215,7 +215,10 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
 }
 
 // ----------------------------------------------------------- K-axis, dense-masked
-template <int BK>
+// NWR: mask words (32 groups each) of the lane's slot rows held in registers
+// for the whole k loop (1: up to 32 groups, 4: up to 128); 0 reads them from
+// LDS at every step.
+template <int BK, int NWR>
 __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   __shared__ uint32_t s_mbits[BM][kKd256MaxGroups / 32];  // mask bits of the tile's rows
@@ -286,12 +289,42 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
 
   f32x16 acc[4][2];
   zero_acc(acc);
+  // Every step needs, per slot row, one bit of its mask row.  Reading them
+  // from LDS at each step put several dependent LDS round trips in front of
+  // the step's loads; with NWR > 0 the rows' mask words sit in registers
+  // (rows past M hold zero words, so their blocks read as zeros).
+  // (words past the row's last group are never selected: any value will do)
+  uint64_t mlo[S], mhi[S];
+#pragma unroll
+  for (int j = 0; j < S; ++j) {
+    mlo[j] = mhi[j] = 0;
+    if (NWR >= 1) mlo[j] = s_mbits[srow[j]][0];
+    if (NWR >= 4) {
+      mlo[j] |= (uint64_t)s_mbits[srow[j]][1] << 32;
+      mhi[j] = s_mbits[srow[j]][2] | (uint64_t)s_mbits[srow[j]][3] << 32;
+    }
+  }
+  const uint32_t u0 = s_union[0];
   auto src = [&](int s, const uint16_t* (&ap)[S], const uint16_t* (&bp)[S]) {
-    const int gg = s_groups[s / spg];
-    const int k0 = gg * a.G + (s % spg) * BK;
+    const int gi = s / spg;
+    int gg;
+    if (NWR == 1) {  // gi-th group of the tile's union (one word, kept in scalars)
+      uint32_t u = u0;
+      for (int i = 0; i < gi; ++i) u &= u - 1;
+      gg = __builtin_ctz(u);
+    } else {
+      gg = s_groups[gi];
+    }
+    const int k0 = gg * a.G + (s - gi * spg) * BK;
 #pragma unroll
     for (int j = 0; j < S; ++j) {
-      const bool on = abase[j] && ((s_mbits[srow[j]][gg >> 5] >> (gg & 31)) & 1u);
+      bool on;
+      if (NWR == 0)
+        on = (s_mbits[srow[j]][gg >> 5] >> (gg & 31)) & 1u;
+      else if (NWR == 1)
+        on = (mlo[j] >> gg) & 1u;
+      else
+        on = ((gg < 64 ? mlo[j] : mhi[j]) >> (gg & 63)) & 1u;
       ap[j] = on ? abase[j] + k0 : zero;  // inactive (t, g) blocks are never read
       bp[j] = bbase[j] + k0;
     }
@@ -410,7 +443,9 @@ int get_ring_bk() { return g_ring_bk; }
 
 #define MN_SW(bk) wide_mn256<true, bk>
 #define MN_PL(bk) wide_mn256<false, bk>
-#define KD(bk) wide_kd256<bk>
+#define KD(bk) wide_kd256<bk, 0>
+#define KD1(bk) wide_kd256<bk, 1>
+#define KD4(bk) wide_kd256<bk, 4>
 #define KS(bk) wide_ks256<bk>
 
 hipError_t launch_mn256(const MN256Args& a, bool swiglu, hipStream_t s) {
@@ -429,7 +464,13 @@ hipError_t launch_kd256(const KArgs& a, hipStream_t s) {
   const int64_t total = m_tiles * (a.N / BN);
   if (total == 0) return hipSuccess;
   if (a.K / a.G > kKd256MaxGroups) return hipErrorInvalidValue;
-  WIDE_RING_LAUNCH("wide_kd256", KD, RingKD, (unsigned)total, s, a);
+  const int ng = a.K / a.G;
+  if (ng <= 32)
+    WIDE_RING_LAUNCH("wide_kd256", KD1, RingKD, (unsigned)total, s, a);
+  else if (ng <= 128)
+    WIDE_RING_LAUNCH("wide_kd256", KD4, RingKD, (unsigned)total, s, a);
+  else
+    WIDE_RING_LAUNCH("wide_kd256", KD, RingKD, (unsigned)total, s, a);
   return hipGetLastError();
 }
 

@@ -587,3 +587,20 @@ def test_qkv_tile_order_edge_counts(orc, M, order):
     c = synth.attn_case(M + 11, M, 256, 16, 4, 128, 256, mask="bernoulli")
     c.mask[:] = _edge_count_mask(synth.rng(M * 5), M, 8)
     check_qkvo(orc, c, kpath=0)
+
+
+@pytest.mark.parametrize("Dff", [2048, 2112, 6144, 8192, 8704])
+def test_ffn_kd256_group_counts(orc, Dff):
+    """The dense-masked K-axis kernel keeps the tile rows' mask words in
+    registers for up to 32 and up to 128 groups and reads them from LDS
+    beyond; 32, 33, 96, 128 and 136 groups of 64 cover each form and edge."""
+    M, D, G = 300, 256, 64
+    say("ffn kd256 groups", Dff // G)
+    W.wide_set_option("decode_max_m", 0)
+    W.wide_set_option("k_path", 1)
+    c = synth.ffn_case(Dff + 5, M, D, Dff, G, mask="bernoulli")
+    x, wg, wu, wd, m = ffn_dev(c)
+    y = W.wide_ffn_masked(x, wg, wu, wd, m, G)
+    torch.cuda.synchronize()
+    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, G, round_bf16=True)
+    assert_close(y, ry, what="y", abs_allow=ffn_flip_allowance(rh, synth.as_f32(c.w_down)))
