@@ -37,8 +37,13 @@ __device__ __forceinline__ uint32_t pack_bf16x2_hw(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
 }
 
-// SiLU in fp32.
-__device__ __forceinline__ float silu(float a) { return a / (1.0f + __expf(-a)); }
+// One value through the same instruction (finite values round exactly as
+// f32_to_bf16 does).
+__device__ __forceinline__ uint16_t f32_to_bf16_hw(float f) { return (uint16_t)pack_bf16x2_hw(f, 0.0f); }
+
+// SiLU in fp32: a * 1/(1 + e^-a) with the hardware reciprocal (about 1 ulp),
+// rather than an IEEE division (a dozen instructions per output).
+__device__ __forceinline__ float silu(float a) { return a * __builtin_amdgcn_rcpf(1.0f + __expf(-a)); }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {
   return __builtin_bit_cast(bf16x8, v);

@@ -32,6 +32,19 @@ using RingMN = Ring<BK, BK == 64 ? 2 : 5>;
 template <int BK>
 using RingKD = Ring<BK, BK == 64 ? 2 : 4>;
 
+// Epilogue row map.  Output rows go back to token order through a per-row
+// index (the reorder, or the pattern order); fetching it per output element
+// put one dependent global load in front of every store.  Instead, thread
+// r < 256 fetches tile row r's token (-1 past the end) before the k loop,
+// and after it the map goes through the then idle ring LDS.
+__device__ __forceinline__ const int* stage_row_map(uint16_t* smem, int my_row) {
+  int* map = reinterpret_cast<int*>(smem);
+  __syncthreads();  // every wave is done with the ring
+  if (threadIdx.x < BM) map[threadIdx.x] = my_row;
+  __syncthreads();
+  return map;
+}
+
 // Tiles of one region that each XCD runs (the region padded to a multiple of 8).
 __host__ __device__ __forceinline__ int mn256_share(int tiles) { return (tiles + 7) / 8; }
 
@@ -192,23 +205,25 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
       bp[j] = bbase[j] + k0;
     }
   };
+  int my_row = -1;
+  if (tid < BM && m0 + tid < M) my_row = rows ? rows[m0 + tid] : (int)(m0 + tid);
   run_tile<Rg>(smem, K / BK, src, brow0, brow1, live, acc);
 
   // Epilogue: rows back to token order; rows past cnt hold +0 accumulators.
+  const int* map = stage_row_map(smem, my_row);
   const int col = acc_col();
 #pragma unroll
   for (int fm = 0; fm < 4; ++fm) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const int64_t p = m0 + acc_row(fm, i);
-      if (p >= M) continue;
-      const int64_t t = rows ? rows[p] : p;
-      uint16_t* o = R.out + t * R.ldo + n0;
+      const int t = map[acc_row(fm, i)];
+      if (t < 0) continue;
+      uint16_t* o = R.out + (int64_t)t * R.ldo + n0;
       if (SWIGLU) {
-        o[wn * 32 + col] = f32_to_bf16(silu(acc[fm][0][i]) * acc[fm][1][i]);
+        o[wn * 32 + col] = f32_to_bf16_hw(silu(acc[fm][0][i]) * acc[fm][1][i]);
       } else {
-        o[wn * 64 + col] = f32_to_bf16(acc[fm][0][i]);
-        o[wn * 64 + 32 + col] = f32_to_bf16(acc[fm][1][i]);
+        o[wn * 64 + col] = f32_to_bf16_hw(acc[fm][0][i]);
+        o[wn * 64 + 32 + col] = f32_to_bf16_hw(acc[fm][1][i]);
       }
     }
   }
@@ -329,18 +344,21 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
       bp[j] = bbase[j] + k0;
     }
   };
+  int my_row = -1;
+  if (tid < BM && m0 + tid < a.M) my_row = (int)token(m0 + tid);
   run_tile<Rg>(smem, nsteps, src, brow0, brow1, live, acc);
 
+  const int* map = stage_row_map(smem, my_row);
   const int col = acc_col();
 #pragma unroll
   for (int fm = 0; fm < 4; ++fm)
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const int64_t p = m0 + acc_row(fm, i);
-      if (p >= a.M) continue;
-      uint16_t* o = a.y + token(p) * a.N + n0 + wn * 64;
-      o[col] = f32_to_bf16(acc[fm][0][i]);
-      o[32 + col] = f32_to_bf16(acc[fm][1][i]);
+      const int t = map[acc_row(fm, i)];
+      if (t < 0) continue;
+      uint16_t* o = a.y + (int64_t)t * a.N + n0 + wn * 64;
+      o[col] = f32_to_bf16_hw(acc[fm][0][i]);
+      o[32 + col] = f32_to_bf16_hw(acc[fm][1][i]);
     }
 }
 
@@ -393,17 +411,20 @@ __global__ __launch_bounds__(NT, 1) void wide_ks256(KArgs a) {
       bp[j] = bbase[j] + k0;
     }
   };
+  int my_row = -1;
+  if ((int)threadIdx.x < BM && m0 + (int)threadIdx.x < cnt) my_row = rows[m0 + threadIdx.x];
   run_tile<Rg>(smem, a.G / BK, src, brow0, brow1, live, acc);
 
+  const int* map = stage_row_map(smem, my_row);
   const int col = acc_col();
 #pragma unroll
   for (int fm = 0; fm < 4; ++fm) {
     if (!(live & (1 << fm))) continue;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const int64_t p = m0 + acc_row(fm, i);
-      if (p >= cnt) continue;
-      float* o = a.acc32 + (int64_t)rows[p] * a.N + n0 + wn * 64;
+      const int t = map[acc_row(fm, i)];
+      if (t < 0) continue;
+      float* o = a.acc32 + (int64_t)t * a.N + n0 + wn * 64;
       unsafeAtomicAdd(o + col, acc[fm][0][i]);
       unsafeAtomicAdd(o + 32 + col, acc[fm][1][i]);
     }
