@@ -45,6 +45,29 @@ __device__ __forceinline__ const int* stage_row_map(uint16_t* smem, int my_row) 
   return map;
 }
 
+// Bit b of the result: byte b of the n (<= 32) mask bytes at mr is nonzero.
+// Rows of ng bytes start 16-byte aligned when 16 divides ng (the mask itself
+// is 16-byte aligned), 4-byte aligned when 4 does; the loads are as wide as
+// that allows.
+__device__ __forceinline__ uint32_t nz4(uint32_t w) {  // bit i: byte i of w != 0
+  const uint32_t m = (((w & 0x7f7f7f7fu) + 0x7f7f7f7fu) | w) & 0x80808080u;
+  return ((m >> 7) & 1u) | ((m >> 14) & 2u) | ((m >> 21) & 4u) | ((m >> 28) & 8u);
+}
+__device__ __forceinline__ uint32_t mask_bits32(const uint8_t* mr, int n, int ng) {
+  uint32_t bits = 0;
+  if (n == 32 && ng % 16 == 0) {
+    const u32x4 a = *reinterpret_cast<const u32x4*>(mr);
+    const u32x4 b = *reinterpret_cast<const u32x4*>(mr + 16);
+    bits = nz4(a[0]) | nz4(a[1]) << 4 | nz4(a[2]) << 8 | nz4(a[3]) << 12 | nz4(b[0]) << 16 |
+           nz4(b[1]) << 20 | nz4(b[2]) << 24 | nz4(b[3]) << 28;
+  } else if (ng % 4 == 0) {  // n is a multiple of 4 too
+    for (int b = 0; b < n; b += 4) bits |= nz4(*reinterpret_cast<const uint32_t*>(mr + b)) << b;
+  } else {
+    for (int b = 0; b < n; ++b) bits |= (uint32_t)(mr[b] != 0) << b;
+  }
+  return bits;
+}
+
 // Tiles of one region that each XCD runs (the region padded to a multiple of 8).
 __host__ __device__ __forceinline__ int mn256_share(int tiles) { return (tiles + 7) / 8; }
 
@@ -160,13 +183,13 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
   if (m0 >= cnt) {  // l = 0: the whole tile is inactive for group g
     if (R.skip_zero) return;
     constexpr int CH = BNO / 8;
-    const int64_t pend = min(m0 + BM, M);
+    int my_row = -1;
+    if (tid < BM && m0 + tid < M) my_row = rows ? rows[m0 + tid] : (int)(m0 + tid);
+    const int* map = stage_row_map(smem, my_row);
+#pragma unroll 4
     for (int i = tid; i < BM * CH; i += NT) {
-      const int64_t p = m0 + i / CH;
-      if (p < pend) {
-        const int64_t t = rows ? rows[p] : p;
-        stg16(R.out + t * R.ldo + n0 + (i % CH) * 8, u32x4{0, 0, 0, 0});
-      }
+      const int t = map[i / CH];
+      if (t >= 0) stg16(R.out + (int64_t)t * R.ldo + n0 + (i % CH) * 8, u32x4{0, 0, 0, 0});
     }
     return;
   }
@@ -262,11 +285,7 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
     const int64_t p = m0 + r;
     const int64_t t = p < a.M ? token(p) : a.M;
     uint32_t bits = 0;
-    if (t < a.M) {
-      const uint8_t* mr = a.mask + t * ng + wd * 32;
-      const int n = min(32, ng - wd * 32);
-      for (int b = 0; b < n; ++b) bits |= (uint32_t)(mr[b] != 0) << b;
-    }
+    if (t < a.M) bits = mask_bits32(a.mask + t * ng + wd * 32, min(32, ng - wd * 32), ng);
     s_mbits[r][wd] = bits;
     if (bits) atomicOr(&s_union[wd], bits);
   }
