@@ -290,11 +290,18 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
     if (bits) atomicOr(&s_union[wd], bits);
   }
   __syncthreads();
-  if (tid == 0) {  // groups some row of the tile uses, ascending
-    int n = 0;
-    for (int wd = 0; wd < nw; ++wd)
-      for (uint32_t u = s_union[wd]; u; u &= u - 1) s_groups[n++] = (uint16_t)(wd * 32 + __builtin_ctz(u));
-    s_ng_live = n;
+  // groups some row of the tile uses, ascending: thread g places group g at
+  // the count of union bits below it (no serial pass over the union)
+  if (tid < nw * 32) {
+    const int wd = tid >> 5, b = tid & 31;
+    int pos = __builtin_popcount(s_union[wd] & ((1u << b) - 1u));
+    for (int i = 0; i < wd; ++i) pos += __builtin_popcount(s_union[i]);
+    if ((s_union[wd] >> b) & 1u) s_groups[pos] = (uint16_t)tid;
+    if (tid == 0) {
+      int n = 0;
+      for (int i = 0; i < nw; ++i) n += __builtin_popcount(s_union[i]);
+      s_ng_live = n;
+    }
   }
   __syncthreads();
   const int spg = a.G / BK;  // k steps per group

@@ -184,7 +184,15 @@ __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Src src, in
   };
   if (nsteps <= 0) return;
   const int pro = min(NS - 1, nsteps);
-  for (int s = 0; s < pro; ++s) issue_all(s);
+  if (NS == 2) {  // B's addresses need no gathered row index: send them first
+    const uint16_t* ap[S];
+    const uint16_t* bp[S];
+    src(0, ap, bp);
+    Rg::issue_b(smem, bp);
+    Rg::issue_a(smem, ap);
+  } else {
+    for (int s = 0; s < pro; ++s) issue_all(s);
+  }
   wait_step(0, pro - 1);
   stage_barrier();
   // Sub-step kk works on fr[kk & 1] and fills fr[(kk + 1) & 1]; KK is even,
