@@ -313,6 +313,68 @@ __global__ __launch_bounds__(kPatChunk) void wide_pattern_scatter(const uint8_t*
   const int64_t t = (int64_t)blockIdx.x * kPatChunk + tid;
   if (t < M) perm[atomicAdd(&cur[pattern_of(mask, t, ng)], 1)] = (int32_t)t;
 }
+// Up to kPatFusedMax tokens: one workgroup does all three passes (histogram,
+// scan and scatter through LDS), saving two launches.  Each token's key is
+// computed once (from one 8-byte load when the mask has 8 groups) and kept
+// in LDS for the scatter; the loads of a thread's tokens go out together.
+constexpr int kPatFusedMax = 32768;
+static_assert(kPatKeys == 256, "the fused scan gives each of 64 lanes four keys");
+__device__ __forceinline__ int pattern_key8(const uint8_t* mask, int64_t t) {
+  const uint2 w = *reinterpret_cast<const uint2*>(mask + t * 8);
+  int key = 0;
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    key |= (((w.x >> (8 * b)) & 0xffu) != 0) << b;
+    key |= (((w.y >> (8 * b)) & 0xffu) != 0) << (4 + b);
+  }
+  key ^= key >> 1;  // Gray decode, as in pattern_of
+  key ^= key >> 2;
+  key ^= key >> 4;
+  return key;
+}
+__global__ __launch_bounds__(1024) void wide_pattern_fused(const uint8_t* mask, int M, int ng, int32_t* perm) {
+  __shared__ int cnt[kPatKeys];
+  __shared__ uint8_t keys[kPatFusedMax];
+  const int tid = threadIdx.x;
+  for (int i = tid; i < kPatKeys; i += 1024) cnt[i] = 0;
+  __syncthreads();
+#pragma unroll 8
+  for (int k = 0; k < kPatFusedMax / 1024; ++k) {
+    const int t = tid + k * 1024;
+    if (t < M) {
+      const int key = ng == 8 ? pattern_key8(mask, t) : pattern_of(mask, t, ng);
+      keys[t] = (uint8_t)key;
+      atomicAdd(&cnt[key], 1);
+    }
+  }
+  __syncthreads();
+  if (tid < 64) {  // exclusive scan of the 256 counts by one wave, four per lane
+    int v[4], sum = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[i] = cnt[tid * 4 + i];
+      sum += v[i];
+    }
+    int incl = sum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o, 64);
+      if (tid >= o) incl += y;
+    }
+    int run = incl - sum;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      cnt[tid * 4 + i] = run;
+      run += v[i];
+    }
+  }
+  __syncthreads();
+#pragma unroll 8
+  for (int k = 0; k < kPatFusedMax / 1024; ++k) {
+    const int t = tid + k * 1024;
+    if (t < M) perm[atomicAdd(&cnt[keys[t]], 1)] = t;
+  }
+}
 }  // namespace
 
 size_t pattern_scratch_ints(int64_t M) { return (size_t)kPatKeys * (size_t)((M + kPatChunk - 1) / kPatChunk); }
@@ -324,6 +386,10 @@ hipError_t launch_pattern_order(const uint8_t* mask, int64_t M, int n_groups, in
   const int64_t nc64 = (M + kPatChunk - 1) / kPatChunk;
   if (nc64 * kPatKeys > 0x7fffffff) return hipErrorInvalidValue;
   const int nc = (int)nc64;
+  if (M <= kPatFusedMax) {
+    WIDE_LAUNCH(wide_pattern_fused, dim3(1), dim3(1024), 0, s, mask, (int)M, n_groups, perm);
+    return hipGetLastError();
+  }
   WIDE_LAUNCH(wide_pattern_count, dim3(nc), dim3(kPatChunk), 0, s, mask, M, n_groups, nc, scratch);
   WIDE_LAUNCH(wide_pattern_scan, dim3(1), dim3(1024), 0, s, scratch, nc * kPatKeys);
   WIDE_LAUNCH(wide_pattern_scatter, dim3(nc), dim3(kPatChunk), 0, s, mask, M, n_groups, nc, scratch, perm);
