@@ -217,7 +217,8 @@ def main():
     dec_ms = float(np.median([b_.elapsed_time(c) for _, b_, c in marks]))
     kernels = {}
     for name in ("wide_reorder_fused", "wide_reorder_count", "wide_reorder_scan", "wide_reorder_scatter", "wide_mn256<true>",
-                 "wide_mn256<false>", "wide_kd256", "wide_ks256", "wide_gemm_mn<true>", "wide_gemm_mn<false>",
+                 "wide_mn256<false>", "wide_kd256<1>", "wide_kd256<4>", "wide_kd256<0>", "wide_ks256",
+                 "wide_pattern_fused", "wide_pattern_count", "wide_gemm_mn<true>", "wide_gemm_mn<false>",
                  "wide_gemm_k_dense_masked", "wide_gemm_k_scatter", "wide_tile_union", "wide_zero_f32",
                  "wide_f32_to_bf16", "wide_gemv_n<true>", "wide_gemv_n<false>", "wide_gemv_k"):
         ms, n = W.wide_timing_query(name)
@@ -239,10 +240,13 @@ def main():
     W.wide_timing_enable(False)
 
     fa_pre, fa_dec = L.active_flops("prefill"), L.active_flops("decode")
-    kpath_auto = lambda G: 2 if G >= 256 else 1
+    kpath_auto = lambda G: 2 if G >= 2048 else 1   # the library's automatic K-axis schedule
     kp = W.wide_get_option("k_path")
     big = W.wide_get_option("big_tiles")
-    kname = lambda G: ({1: "wide_kd256", 2: "wide_ks256"} if big else
+    # the dense-masked 256-tile kernel comes in variants by group count (mask
+    # words held in registers: <1> up to 32 groups, <4> up to 128, <0> beyond)
+    kd = lambda ng: "wide_kd256<1>" if ng <= 32 else "wide_kd256<4>" if ng <= 128 else "wide_kd256<0>"
+    kname = lambda G: ({1: kd((L.Nq if G == L.Ga else L.Dff) // G), 2: "wide_ks256"} if big else
                        {1: "wide_gemm_k_dense_masked", 2: "wide_gemm_k_scatter"})[kp or kpath_auto(G)]
     kernel_of = {"o": kname(L.Ga), "down": kname(L.G)}
     step_flops = fa_pre["total"] + fa_dec["total"]
@@ -254,22 +258,30 @@ def main():
         "wide_mn256<true>": fa_pre["gate_up"], "wide_gemm_mn<true>": fa_pre["gate_up"],
         "wide_mn256<false>": fa_pre["q"] + fa_pre["kv"], "wide_gemm_mn<false>": fa_pre["q"] + fa_pre["kv"],
     }
-    if dom in ("wide_kd256", "wide_ks256", "wide_gemm_k_dense_masked", "wide_gemm_k_scatter"):
-        # O and down share these kernels; count the launches this kernel served
-        served = 0.0
-        for k_name, flops in (("o", fa_pre["o"]), ("down", fa_pre["down"])):
-            served += flops if kernel_of[k_name] == dom else 0.0
-        alg = served / (kernels[dom]["launches"] / args.steps)
-    else:
-        alg = per_launch_flops.get(dom)
-    roofline = None
-    if alg is not None:
-        from paper_2607_28418_amd import profiling
-        ach = alg / (kernels[dom]["avg_us"] * 1e-6) / 1e12
-        traffic = profiling.traffic_for(os.path.join(ROOT, "profiles", "layer_llama3_8b_pmc_traffic.json"), dom)
-        roofline = dict(kernel=dom, bound="mfma", achieved=round(ach, 1), peak=PEAK_BF16_TFLOPS,
-                        unit="TFLOP/s", frac=round(ach / PEAK_BF16_TFLOPS, 4), traffic=traffic,
-                        algorithmic_flops_per_launch=alg, avg_launch_us=round(kernels[dom]["avg_us"], 2))
+    from paper_2607_28418_amd import profiling
+    traffic_json = os.path.join(ROOT, "profiles", "layer_llama3_8b_pmc_traffic.json")
+
+    def kernel_roofline(name):
+        """Active-FLOP roofline of one prefill kernel (None for others)."""
+        if name in ("wide_ks256", "wide_gemm_k_dense_masked", "wide_gemm_k_scatter") or name.startswith("wide_kd256"):
+            # O and down may share a kernel; count the launches it served
+            served = 0.0
+            for k_name, flops in (("o", fa_pre["o"]), ("down", fa_pre["down"])):
+                served += flops if kernel_of[k_name] == name else 0.0
+            alg = served / (kernels[name]["launches"] / args.steps) if served else None
+        else:
+            alg = per_launch_flops.get(name)
+        if alg is None:
+            return None
+        ach = alg / (kernels[name]["avg_us"] * 1e-6) / 1e12
+        return dict(kernel=name, bound="mfma", achieved=round(ach, 1), peak=PEAK_BF16_TFLOPS,
+                    unit="TFLOP/s", frac=round(ach / PEAK_BF16_TFLOPS, 4),
+                    traffic=profiling.traffic_for(traffic_json, name),
+                    algorithmic_flops_per_launch=alg, avg_launch_us=round(kernels[name]["avg_us"], 2))
+
+    roofline = kernel_roofline(dom)
+    # every prefill kernel, for the record (the dominant one above is the headline)
+    rooflines_all = {k: r for k in kernels if (r := kernel_roofline(k)) is not None}
 
     # ---- decode bandwidth ---------------------------------------------------------
     dbytes, ddense, ua, uf = L.decode_bytes()
@@ -782,6 +794,7 @@ def main():
         "dense": dense,
         "kernels_us": {k: round(v["avg_us"], 2) for k, v in kernels.items()},
         "roofline": roofline,
+        "rooflines_all": rooflines_all,
         "cpu_baseline": cpu,
         "sweeps": sweeps,
         "attention": attention,

@@ -4,7 +4,7 @@
 //                          (one tile = 256 sorted tokens x one 128-column slice
 //                          of a group: 128 gate rows + 128 up rows), or plain
 //                          Q/K/V (one tile = 256 tokens x 256 output columns).
-//   wide_kd256<BK>         K-axis masked projection, dense-masked schedule.
+//   wide_kd256<NWR, BK>    K-axis masked projection, dense-masked schedule.
 //   wide_ks256<BK>         K-axis masked projection, scatter schedule (GEMM-K).
 //
 // Semantics, skipping levels and the two K-axis schedules are those of the
@@ -256,7 +256,7 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
 // NWR: mask words (32 groups each) of the lane's slot rows held in registers
 // for the whole k loop (1: up to 32 groups, 4: up to 128); 0 reads them from
 // LDS at every step.
-template <int BK, int NWR>
+template <int NWR, int BK>
 __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   __shared__ uint32_t s_mbits[BM][kKd256MaxGroups / 32];  // mask bits of the tile's rows
@@ -490,9 +490,9 @@ int get_ring_bk() { return g_ring_bk; }
 
 #define MN_SW(bk) wide_mn256<true, bk>
 #define MN_PL(bk) wide_mn256<false, bk>
-#define KD(bk) wide_kd256<bk, 0>
-#define KD1(bk) wide_kd256<bk, 1>
-#define KD4(bk) wide_kd256<bk, 4>
+#define KD(bk) wide_kd256<0, bk>
+#define KD1(bk) wide_kd256<1, bk>
+#define KD4(bk) wide_kd256<4, bk>
 #define KS(bk) wide_ks256<bk>
 
 hipError_t launch_mn256(const MN256Args& a, bool swiglu, hipStream_t s) {
@@ -513,11 +513,11 @@ hipError_t launch_kd256(const KArgs& a, hipStream_t s) {
   if (a.K / a.G > kKd256MaxGroups) return hipErrorInvalidValue;
   const int ng = a.K / a.G;
   if (ng <= 32)
-    WIDE_RING_LAUNCH("wide_kd256", KD1, RingKD, (unsigned)total, s, a);
+    WIDE_RING_LAUNCH("wide_kd256<1>", KD1, RingKD, (unsigned)total, s, a);
   else if (ng <= 128)
-    WIDE_RING_LAUNCH("wide_kd256", KD4, RingKD, (unsigned)total, s, a);
+    WIDE_RING_LAUNCH("wide_kd256<4>", KD4, RingKD, (unsigned)total, s, a);
   else
-    WIDE_RING_LAUNCH("wide_kd256", KD, RingKD, (unsigned)total, s, a);
+    WIDE_RING_LAUNCH("wide_kd256<0>", KD, RingKD, (unsigned)total, s, a);
   return hipGetLastError();
 }
 

@@ -41,6 +41,11 @@ def test_label_matching():
     assert not m("wide_gemv_n_finish<true>", "wide_gemv_n<true>")
     assert m("wide_gemv_n<true, 4, 2>", "wide_gemv_n<true>")
     assert m("wide_reorder_count", "wide_reorder_count")
+    # dense-masked K-axis variants: the label carries the leading template argument
+    assert m("wide_kd256<1, 64>", "wide_kd256<1>/bk64")
+    assert m("wide_kd256<4, 32>", "wide_kd256<4>")
+    assert not m("wide_kd256<4, 64>", "wide_kd256<1>/bk64")
+    assert m("wide_kd256<0, 64>", "wide_kd256")
 
 
 def test_kernel_key_strips_namespaces_and_arguments():
