@@ -146,6 +146,7 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
   constexpr int NV = SWIGLU ? 2 : 1;
   __shared__ float red[NW / 2 * NV][kDecodeMaxB][16];
   __shared__ int any_active;
+  __shared__ uint8_t s_on[kDecodeMaxB];  // token b runs group g (read once, used by the epilogue)
 
   const int kq = blockIdx.x % a.k_split;  // this workgroup's share of the k steps
   int nb = blockIdx.x / a.k_split;
@@ -165,7 +166,11 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
 
   if (tid == 0) any_active = R.masked ? 0 : 1;
   __syncthreads();
-  if (R.masked && tid < B && a.mask[(int64_t)tid * a.n_groups + g] != 0) any_active = 1;
+  if (tid < B) {
+    const bool on = !R.masked || a.mask[(int64_t)tid * a.n_groups + g] != 0;
+    s_on[tid] = on;
+    if (on && R.masked) any_active = 1;
+  }
   __syncthreads();
   if (!any_active) {
     // group unused by the whole batch: no weight reads, outputs +0 (with a
@@ -249,7 +254,7 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
           a.part[(((int64_t)kq * NV + v) * B + b) * ncols + R.col0 + n0 + c * 16 + cc] = sm[v];
         return;
       }
-      const bool on = !R.masked || a.mask[(int64_t)b * a.n_groups + g] != 0;
+      const bool on = s_on[b] != 0;
       const float o = on ? (SWIGLU ? silu(sm[0]) * sm[NV - 1] : sm[0]) : 0.f;
       R.out[(int64_t)b * R.ldo + n0 + c * 16 + cc] = f32_to_bf16(o);
     });
