@@ -295,20 +295,57 @@ def main():
                    active_frac_peak=round(fa_pre["total"] / (pre_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
                    ideal_speedup=round(L.dense_flops("prefill") / fa_pre["total"], 3))
 
+    # ---- decode in a multi-layer graph (outside the timed region) ------------------
+    # A served model replays all its layers from one graph, so the per-graph
+    # launch cost that a one-layer replay pays is spread over the layers.
+    # Four layers with their own weight copies (no layer finds another's
+    # weights in the caches), one graph, time per layer.
+    n_layers = 4
+    wl = [w] + [{k: t.clone() for k, t in w.items()} for _ in range(n_layers - 1)]
+    bdec, odec = bd["decode"], bufs["decode"]
+
+    def decode_layer(wx):
+        W.wide_qkvo_masked(W.PHASE_QKV, bdec["x_attn"], bdec["mask_attn"], L.Ga, L.nq, L.nkv, L.hd,
+                           w_q=wx["w_q"], w_k=wx["w_k"], w_v=wx["w_v"], q=odec["q"], k=odec["k"],
+                           v=odec["v"], ws=odec["ws"])
+        W.wide_qkvo_masked(W.PHASE_O, bdec["a"], bdec["mask_attn"], L.Ga, L.nq, L.nkv, L.hd,
+                           w_o=wx["w_o"], y=odec["y_o"], ws=odec["ws"])
+        W.wide_ffn_masked(bdec["x_ffn"], wx["w_gate"], wx["w_up"], wx["w_down"], bdec["mask_ffn"], L.G,
+                          y=odec["y_f"], ws=odec["ws"])
+
+    ml_graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(ml_graph):
+        for wx in wl:
+            decode_layer(wx)
+    for _ in range(3):
+        ml_graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = ev(), ev()
+    e0.record(stream)
+    for _ in range(args.steps):
+        ml_graph.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ml_ms = e0.elapsed_time(e1) / args.steps / n_layers
+    decode["graph_of_4_layers"] = dict(
+        ms_per_layer=round(ml_ms, 4), GBps_on_min_bytes=round(dbytes / (ml_ms * 1e-3) / 1e9, 1),
+        frac_hbm=round(dbytes / (ml_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4))
+    del ml_graph
+
     # ---- dense baselines (outside the timed region) --------------------------------
     dense = None
     if not args.no_dense:
         import torch.nn.functional as F
 
-        def dense_run(name):
-            b = bd[name]
-            F.linear(b["x_attn"], w["w_q"])
-            F.linear(b["x_attn"], w["w_k"])
-            F.linear(b["x_attn"], w["w_v"])
-            F.linear(b["a"], w["w_o"])
-            hg = F.linear(b["x_ffn"], w["w_gate"])
-            hu = F.linear(b["x_ffn"], w["w_up"])
-            F.linear(F.silu(hg) * hu, w["w_down"])
+        def dense_run(name, wx=None):
+            b, wx = bd[name], wx or w
+            F.linear(b["x_attn"], wx["w_q"])
+            F.linear(b["x_attn"], wx["w_k"])
+            F.linear(b["x_attn"], wx["w_v"])
+            F.linear(b["a"], wx["w_o"])
+            hg = F.linear(b["x_ffn"], wx["w_gate"])
+            hu = F.linear(b["x_ffn"], wx["w_up"])
+            F.linear(F.silu(hg) * hu, wx["w_down"])
 
         def timeit(fn, n):
             for _ in range(3):
@@ -374,11 +411,22 @@ def main():
         dense = dict(hipblaslt_prefill_ms=round(d_pre, 4), hipblaslt_decode_ms=round(d_dec, 4),
                      ones_mask_prefill_ms=round(o_pre, 4), ones_mask_decode_ms=round(o_dec, 4),
                      prefill_per_op=per_op)
+        dml_graph = torch.cuda.CUDAGraph()   # hipBLASLt, the same four-layer graph
+        with torch.cuda.graph(dml_graph):
+            for wx in wl:
+                dense_run("decode", wx)
+        d_ml = timeit(dml_graph.replay, n_rep) / n_layers
+        del dml_graph
+        g4 = decode["graph_of_4_layers"]
+        g4["hipblaslt_ms_per_layer"] = round(d_ml, 4)
+        g4["speedup_vs_hipblaslt"] = round(d_ml / g4["ms_per_layer"], 3)
         best_pre, best_dec = min(d_pre, o_pre), min(d_dec, o_dec)
         prefill["speedup_vs_dense"] = round(best_pre / pre_ms, 3)
         prefill["frac_of_ideal"] = round(best_pre / pre_ms / prefill["ideal_speedup"], 3)
         decode["speedup_vs_dense"] = round(best_dec / dec_ms, 3)
         decode["ideal_speedup"] = round(ddense / dbytes, 3)
+
+    del wl
 
     # ---- sweeps (outside the timed region, context for the headline line) ---------
     sweeps = None
