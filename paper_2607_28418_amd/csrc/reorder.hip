@@ -174,9 +174,18 @@ __global__ __launch_bounds__(kFusedThreads) void wide_reorder_fused(const uint8_
   const int w = wave_id(), lane = lane_id();
   const int nch = (M + kFusedThreads - 1) / kFusedThreads;
   uint32_t bits = 0;
-  for (int i = 0; i < nch; ++i) {
-    const int t = i * kFusedThreads + tid;
-    if (t < M && mask[(int64_t)t * n_groups + g] != 0) bits |= 1u << i;
+  for (int i0 = 0; i0 < nch; i0 += 8) {  // eight independent loads per round, no branches
+    uint8_t v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int t = (i0 + j) * kFusedThreads + tid;
+      v[j] = mask[(t < M ? (int64_t)t * n_groups : 0) + g];
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int t = (i0 + j) * kFusedThreads + tid;
+      bits |= (uint32_t)(t < M && v[j] != 0) << (i0 + j);
+    }
   }
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   for (int i = 0; i < nch; ++i) {
