@@ -137,7 +137,7 @@ def test_qkvo_bf16_ring32(orc, M, n_q, n_kv, G):
     check_qkvo(orc, c)
 
 
-@pytest.mark.parametrize("B", [1, 4, 16, 64])
+@pytest.mark.parametrize("B", [1, 4, 16, 33, 48, 64])
 def test_ffn_bf16_decode_small(orc, B):
     say("ffn decode small", B)
     c = synth.ffn_case(B, B, 512, 1024, 128, mask="beta")
