@@ -58,7 +58,43 @@ def parse():
                     help="skip the decode batch sweep and the prefill keep sweep")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="end with two 1 GiB device copies (counter calibration under rocprofv3)")
+    ap.add_argument("--decode-bytes-case", type=int, default=0, metavar="B",
+                    help="only run the decode FFN at the Llama-7B shape for batch B (Beta(2,2) "
+                         "group rates, the sweep's masks) five times, print its union bytes and "
+                         "exit: the case whose HBM bytes rocprofv3 --pmc compares with the minimum")
     return ap.parse_args()
+
+
+def decode_bytes_case(args):
+    """The decode FFN of the sweep (Llama-7B shape) for one batch size, five
+    calls, then the calibration copies: under rocprofv3 --pmc FETCH_SIZE the
+    gemv kernels' bytes compare with the union's weight bytes printed here."""
+    import torch
+    import paper_2607_28418_amd as W
+    from paper_2607_28418_amd import synth
+    from tests._helpers import to_dev
+    dev = torch.device("cuda", 0)
+    W.lib()
+    D7, F7, G7, bq = 4096, 11008, 128, args.decode_bytes_case
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(7)
+    rnd = lambda *shape, std=0.02: (torch.randn(*shape, device=dev, generator=gen) * std).to(torch.bfloat16)
+    wg7, wu7, wd7 = rnd(F7, D7), rnd(F7, D7), rnd(D7, F7)
+    mk = synth.mask_beta_groups(synth.rng(100 + bq), bq, F7 // G7, 0.5)
+    xq, mq = rnd(bq, D7, std=1.0), to_dev(mk)
+    yq = torch.empty(bq, D7, dtype=torch.bfloat16, device=dev)
+    for _ in range(5):
+        W.wide_ffn_masked(xq, wg7, wu7, wd7, mq, G7, y=yq)
+    torch.cuda.synchronize()
+    u = int(mk.any(0).sum())
+    print(json.dumps({"case": "decode FFN, Llama-7B shape", "batch": bq, "union_groups": u,
+                      "n_groups": F7 // G7, "union_weight_bytes_per_matrix": u * G7 * D7 * 2,
+                      "dense_weight_bytes_per_matrix": F7 * D7 * 2}), flush=True)
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    torch.cuda.synchronize()
 
 
 def log(*a):
@@ -127,6 +163,9 @@ def main():
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; the masked "
                           "projections have no multi-GPU path in this build", "n_gpus": args.gpus}))
         sys.exit(2)
+    if args.decode_bytes_case:
+        decode_bytes_case(args)
+        return
     import torch
     import paper_2607_28418_amd as W
     from tests._helpers import to_dev
