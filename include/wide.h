@@ -292,12 +292,18 @@ size_t wide_workspace_size(wide_op_t op, wide_dtype_t dt, int64_t M,
  *   "k_path"        schedule of the prefill K-axis product (down, O):
  *                   0 automatic (default), 1 dense-masked (no atomics),
  *                   2 scatter (the paper's GEMM-K with fp32 atomics).
- *   "mn_order"      tile order of the 256x256 N-axis kernels, two bits.
- *                   Bit 1 (default on): each XCD runs the full tiles of its
+ *   "mn_order"      tile order of the 256x256 N-axis kernels, two bits
+ *                   (default 3).  Bit 1: each XCD runs the full tiles of its
  *                   groups first, then their partial last m-tiles, then the
- *                   empty ones.  Bit 0 (default off): the Q/K/V call puts the
- *                   dense K and V tiles before the masked Q tiles (measured
- *                   about 2% slower).  Outputs are identical for all values.
+ *                   empty ones.  Bit 0: the Q/K/V call puts the dense K and
+ *                   V tiles before the masked Q tiles, so the partial Q tiles
+ *                   come last.  Outputs are identical for all values.
+ *   "mn_tail"       1 (default): in the Q/K/V call, each XCD's last partial
+ *                   round of 256x256 tiles is cut along k into chunks run by
+ *                   extra workgroups (fp32 partial tiles in the workspace,
+ *                   added in a fixed order by a short second kernel); 0 runs
+ *                   those tiles whole.  Results differ only in fp32
+ *                   summation order.
  *   "kd_pattern"    1 (default): before the dense-masked K-axis schedule on
  *                   256x256 tiles with 2..8 groups (attention's O projection),
  *                   three small kernels order the tokens by mask pattern so a

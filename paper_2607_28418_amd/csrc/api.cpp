@@ -46,7 +46,8 @@ wide_status_t hip_fail(hipError_t e, const char* where) {
 int64_t g_decode_max_m = 64;  // M <= this uses the decode (GEMV) kernels
 int g_k_path = 0;             // 0 auto, 1 dense-masked, 2 scatter
 int g_big_tiles = 1;          // 1: 256x256 tile kernels where the shape allows
-int g_mn_order = 2;           // bit 0: Q/K/V launch K and V before Q; bit 1: full tiles before partial ones
+int g_mn_tail = 1;            // 1: 256-tile N-axis launches split each XCD's last partial round along k
+int g_mn_order = 3;           // bit 0: Q/K/V launch K and V before Q; bit 1: full tiles before partial ones
 int g_kd_pattern = 1;         // 1: dense-masked K axis reads rows in mask-pattern order (<= 8 groups)
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -273,6 +274,9 @@ wide::GVNArgs qkv_gvn(int64_t M, const AttnDims& d, const uint8_t* mask, const v
   return na;
 }
 
+// Q/K/V on 256x256 tiles (else the 128-tile kernel)
+bool qkv_big(const AttnDims& d) { return g_big_tiles && d.G % wide::kT256 == 0 && d.Nkv % wide::kT256 == 0; }
+
 size_t attn_ws_bytes(wide_phase_t ph, wide_dtype_t dt, int64_t M, const AttnDims& d, bool need_idx,
                      int kpath) {
   Carve c(nullptr);
@@ -295,6 +299,8 @@ size_t attn_ws_bytes(wide_phase_t ph, wide_dtype_t dt, int64_t M, const AttnDims
   if (ph == WIDE_PHASE_QKV) {
     ReorderWS r;
     if (need_idx) carve_reorder(c, M, d.ng, true, r);
+    // Q/K/V tail tiles (a sizing query without n_kv assumes the 256 tiles)
+    if (d.Nkv < 0 ? g_big_tiles && d.G % wide::kT256 == 0 : qkv_big(d)) c.take<float>(wide::kMN256TailFloats);
   } else {
     ReorderWS r;
     const int path = kpath;
@@ -443,6 +449,11 @@ wide_status_t wide_set_option(const char* key, int64_t value) {
       (key[5] == 'n' ? wide::decode_tuning().n_split : wide::decode_tuning().k_split) = (int)value;
       return ok();
     }
+  if (!strcmp(key, "mn_tail")) {
+    if (value < 0 || value > 1) return fail(WIDE_ERR_INVALID_ARG, "mn_tail must be 0 or 1");
+    g_mn_tail = (int)value;
+    return ok();
+  }
   if (!strcmp(key, "mn_order")) {
     if (value < 0 || value > 3) return fail(WIDE_ERR_INVALID_ARG, "mn_order must be 0..3");
     g_mn_order = (int)value;
@@ -473,6 +484,7 @@ wide_status_t wide_get_option(const char* key, int64_t* value) {
   else if (!strcmp(key, "gemv_k_split")) *value = wide::decode_tuning().k_split;
   else if (!strcmp(key, "kd_pattern")) *value = g_kd_pattern;
   else if (!strcmp(key, "mn_order")) *value = g_mn_order;
+  else if (!strcmp(key, "mn_tail")) *value = g_mn_tail;
   else if (!strcmp(key, "attn_qb")) *value = wide::g_attn_qb;
   else return fail(WIDE_ERR_INVALID_ARG, "unknown option '%s'", key);
   return ok();
@@ -656,6 +668,8 @@ wide_status_t wide_ffn_masked(wide_dtype_t dt, int64_t M, int32_t d_model, int32
     // every K-axis schedule, so its inactive blocks need no zeros.
     ma.reg[0] = wide::MN256Region{static_cast<const uint16_t*>(w_gate), static_cast<const uint16_t*>(w_up), h,
                                   Dff, G, 1, ng * ma.m_tiles * (G / 128), h_out == nullptr ? 1 : 0};
+    // (no tail split for gate/up: over seven rounds of tiles the chunks and
+    // their finishing kernel cost about what the last partial round saves)
     if ((e = wide::launch_mn256(ma, true, stream)) != hipSuccess) return hip_fail(e, "mn256 gate/up");
   } else {
     wide::MNArgs ma{};
@@ -754,8 +768,10 @@ wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M, i
   const bool rows_k = phase == WIDE_PHASE_O && kaxis_row_gathered(d.Nq, d.D, d.G);
   const bool need_reorder = idx == nullptr && (phase == WIDE_PHASE_QKV || kpath == 2 || rows_k);
   ReorderWS r;
+  float* tail_ws = nullptr;
   if (phase == WIDE_PHASE_QKV) {
     if (idx == nullptr) carve_reorder(c, M, ng, true, r);
+    if (qkv_big(d)) tail_ws = c.take<float>(wide::kMN256TailFloats);
   } else if (idx == nullptr && (kpath == 0 || kpath == 2 || rows_k)) {
     carve_reorder(c, M, ng, true, r);
   }
@@ -771,7 +787,7 @@ wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M, i
     const uint16_t* wq = static_cast<const uint16_t*>(w_q);
     const uint16_t* wk = static_cast<const uint16_t*>(w_k);
     const uint16_t* wv = static_cast<const uint16_t*>(w_v);
-    if (g_big_tiles && d.G % wide::kT256 == 0 && d.Nkv % wide::kT256 == 0) {
+    if (qkv_big(d)) {
       wide::MN256Args ma{};
     ma.order = (g_mn_order >> 1) & 1;
       ma.x = x;
@@ -791,6 +807,8 @@ wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M, i
                                          ma.m_tiles * (d.Nkv / T)};
       ma.reg[iq] = wide::MN256Region{wq, nullptr, static_cast<uint16_t*>(q), d.Nq, d.G, 1,
                                      ng * ma.m_tiles * (d.G / T)};
+      ma.tail = g_mn_tail && wide::mn256_tail_ok(ma, 256) ? 1 : 0;
+      ma.tail_ws = tail_ws;
       if ((e = wide::launch_mn256(ma, false, stream)) != hipSuccess) return hip_fail(e, "mn256 qkv");
       return ok();
     }

@@ -82,52 +82,32 @@ __device__ __forceinline__ void run_tile(uint16_t* smem, int nsteps, Src src, in
 }
 }  // namespace
 
-// --------------------------------------------------------------------- GEMM-MN
-template <bool SWIGLU, int BK>
-__global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
-  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
-  using Rg = RingMN<BK>;
-  constexpr int S = Rg::SLOTS;
-  constexpr int BNO = SWIGLU ? 128 : 256;  // output columns per tile
-  const uint16_t* zero = g_zero_blk;
+// Tile order inside an XCD's share of a region: group, then sorted m-tile,
+// then column tile inside the group, so the tiles an XCD runs together share
+// the group's weight panel in L2 (measured faster than blocking m-tiles
+// across groups).  A group wider than four column tiles (one group over a
+// whole projection, the M-axis case) goes column tile first: each XCD then
+// covers a slice of the weight once and re-reads the gathered rows, which
+// fit the last-level cache, instead of streaming the whole weight once per
+// m-tile.
+//
+// When an XCD's share is a whole number of groups ("ordered"), it runs the
+// full tiles of its groups first, then their partial last m-tiles, then the
+// empty ones, so its real tiles come first.
+template <int BNO>
+__device__ __forceinline__ bool mn256_ordered(const MN256Args& a, const MN256Region& R) {
+  const int share = mn256_share(R.tiles), per_group = R.gw / BNO * a.m_tiles;
+  return a.order && R.masked && R.gw / BNO <= 4 && 8 * share == R.tiles && share % per_group == 0;
+}
 
-  // Workgroups are dealt round-robin to the 8 XCDs.  Each region's tiles
-  // (padded to a multiple of 8) are cut into 8 contiguous shares and XCD x
-  // runs share x of every region in turn: a masked region whose tail tiles
-  // are mostly empty then loads the XCDs as evenly as the dense regions
-  // beside it (one contiguous range per XCD over all regions left the XCDs
-  // holding K and V with half again the work of the others).
-  const int xcd = blockIdx.x % 8;
-  int local = blockIdx.x / 8;
-  MN256Region R = a.reg[0];
-  if (a.n_regions > 1 && local >= mn256_share(a.reg[0].tiles)) {
-    local -= mn256_share(a.reg[0].tiles);
-    R = a.reg[1];
-    if (a.n_regions > 2 && local >= mn256_share(a.reg[1].tiles)) {
-      local -= mn256_share(a.reg[1].tiles);
-      R = a.reg[2];
-    }
-  }
+template <int BNO>
+__device__ __forceinline__ void mn256_coords(const MN256Args& a, const MN256Region& R, int xcd, int local,
+                                             int& g, int& m_tile, int& nt_in) {
   const int share = mn256_share(R.tiles);
   const int tile = xcd * share + local;
-  if (tile >= R.tiles) return;  // padding
-  // Tile order: group, then sorted m-tile, then column tile inside the
-  // group, so the tiles an XCD runs together share the group's weight panel
-  // in L2 (measured faster than blocking m-tiles across groups).  A group
-  // wider than four column tiles (one group over a whole projection, the
-  // M-axis case) goes column tile first: each XCD then covers a slice of the
-  // weight once and re-reads the gathered rows, which fit the last-level
-  // cache, instead of streaming the whole weight once per m-tile.
-  //
-  // When an XCD's share is a whole number of groups, it runs the full tiles
-  // of its groups first (in the order above), then their partial last
-  // m-tiles, then the empty ones: the tiles left for the final partial round
-  // of the XCD are the cheap ones (the partial tiles issue MFMAs only for
-  // their live fragments; the empty ones only write zeros, or nothing).
   const int ntpg = R.gw / BNO;  // tiles per group
   const int per_group = ntpg * a.m_tiles;
-  int g, nt_in, m_tile;
-  if (a.order && R.masked && ntpg <= 4 && 8 * share == R.tiles && share % per_group == 0) {
+  if (mn256_ordered<BNO>(a, R)) {
     const int gps = share / per_group, gb = xcd * gps, gl = gb + gps - 1;
     int n_full = 0, n_part = 0;
     for (int i = gb; i <= gl; ++i) {
@@ -172,6 +152,126 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
     }
     g = tile / per_group;
   }
+}
+
+__device__ __forceinline__ int mn256_shares(const MN256Args& a) {
+  int n = mn256_share(a.reg[0].tiles);
+  if (a.n_regions > 1) n += mn256_share(a.reg[1].tiles);
+  if (a.n_regions > 2) n += mn256_share(a.reg[2].tiles);
+  return n;
+}
+
+// The XCD's last partial round.  An XCD's 32 CUs run its real tiles in
+// rounds of 32; with T real tiles the last T % 32 would leave most CUs idle
+// for a whole tile's time (measured: 15-20% of Q/K/V, 7% of gate/up).  With
+// a.tail those n = T % 32 tiles are cut along k into split = 32 / n chunks,
+// run by 32 extra workgroups per XCD that write fp32 partial tiles; a second
+// kernel adds each tile's chunks in order and applies the epilogue.  Only
+// for launches whose regions are dense or ordered (real tiles first in every
+// share, so a tile's rank among the XCD's real tiles is known).
+struct MN256Tail {
+  int real[3], before[3];  // real tiles per region share; real tiles of earlier regions
+  int base, n, split;      // first tail rank, tail tiles, chunks per tail tile
+};
+
+template <int BNO>
+__device__ __forceinline__ int mn256_real(const MN256Args& a, const MN256Region& R, int xcd) {
+  const int share = mn256_share(R.tiles);
+  if (!R.masked) return max(0, min(share, R.tiles - xcd * share));
+  const int ntpg = R.gw / BNO, gps = share / (ntpg * a.m_tiles), gb = xcd * gps;
+  int n = 0;
+  for (int i = 0; i < gps; ++i) n += (a.cnt[gb + i] + BM - 1) / BM;
+  return n * ntpg;
+}
+
+template <int BNO>
+__device__ __forceinline__ MN256Tail mn256_tail(const MN256Args& a, int xcd) {
+  MN256Tail t;
+  t.real[0] = mn256_real<BNO>(a, a.reg[0], xcd);
+  t.real[1] = a.n_regions > 1 ? mn256_real<BNO>(a, a.reg[1], xcd) : 0;
+  t.real[2] = a.n_regions > 2 ? mn256_real<BNO>(a, a.reg[2], xcd) : 0;
+  t.before[0] = 0;
+  t.before[1] = t.real[0];
+  t.before[2] = t.real[0] + t.real[1];
+  const int total = t.before[2] + t.real[2];
+  t.base = total / kMN256TailJobs * kMN256TailJobs;
+  t.n = total - t.base;
+  // at most 8 chunks: each adds a 256 KB partial tile to write and read back
+  t.split = t.n ? min(kMN256TailJobs / t.n, kMN256TailMaxSplit) : 0;
+  if (!a.tail || t.split < 2) {  // nothing to gain: the tiles stay whole
+    t.base = total;
+    t.n = t.split = 0;
+  }
+  return t;
+}
+
+// Region and share-local index of tail tile k (rank base + k).
+__device__ __forceinline__ void mn256_tail_tile(const MN256Tail& t, int k, int& ri, int& local) {
+  const int rank = t.base + k;
+  ri = rank < t.before[1] ? 0 : rank < t.before[2] ? 1 : 2;
+  local = rank - (ri == 0 ? 0 : ri == 1 ? t.before[1] : t.before[2]);
+}
+
+// The k range of chunk c of n over K (in whole 64-wide units, so both ring
+// depths cut at the same k): steps [s0, s0 + ns) of a BK-deep ring.
+template <int BK>
+__device__ __forceinline__ void mn256_chunk_steps(int K, int c, int n, int& s0, int& ns) {
+  const int u = K / 64;
+  const int u0 = (int)((int64_t)u * c / n), u1 = (int)((int64_t)u * (c + 1) / n);
+  s0 = u0 * (64 / BK);
+  ns = (u1 - u0) * (64 / BK);
+}
+
+// --------------------------------------------------------------------- GEMM-MN
+template <bool SWIGLU, int BK>
+__global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+  using Rg = RingMN<BK>;
+  constexpr int S = Rg::SLOTS;
+  constexpr int BNO = SWIGLU ? 128 : 256;  // output columns per tile
+  const uint16_t* zero = g_zero_blk;
+
+  // Workgroups are dealt round-robin to the 8 XCDs.  Each region's tiles
+  // (padded to a multiple of 8) are cut into 8 contiguous shares and XCD x
+  // runs share x of every region in turn: a masked region whose tail tiles
+  // are mostly empty then loads the XCDs as evenly as the dense regions
+  // beside it (one contiguous range per XCD over all regions left the XCDs
+  // holding K and V with half again the work of the others).
+  const int xcd = blockIdx.x % 8;
+  int local = blockIdx.x / 8;
+  const int shares = mn256_shares(a);
+  int ri = 0, job = -1;   // region; tail job of a tail block
+  int chunk = 0, nchunks = 1;
+  if (local >= shares) {  // one of the 32 tail blocks per XCD
+    job = local - shares;
+    const MN256Tail t = mn256_tail<BNO>(a, xcd);
+    if (job >= t.n * t.split) return;
+    chunk = job % t.split;
+    nchunks = t.split;
+    mn256_tail_tile(t, job / t.split, ri, local);
+  } else {
+    ri = 0;
+    if (a.n_regions > 1 && local >= mn256_share(a.reg[0].tiles)) {
+      local -= mn256_share(a.reg[0].tiles);
+      ri = 1;
+      if (a.n_regions > 2 && local >= mn256_share(a.reg[1].tiles)) {
+        local -= mn256_share(a.reg[1].tiles);
+        ri = 2;
+      }
+    }
+    if (a.tail) {  // a tile of the XCD's last partial round is left to the tail blocks
+      const MN256Tail t = mn256_tail<BNO>(a, xcd);
+      const int real = ri == 0 ? t.real[0] : ri == 1 ? t.real[1] : t.real[2];  // no dynamic
+      const int before = ri == 0 ? 0 : ri == 1 ? t.before[1] : t.before[2];   // indexing
+      if (local < real && before + local >= t.base) return;
+    }
+  }
+  const MN256Region R = ri == 0 ? a.reg[0] : ri == 1 ? a.reg[1] : a.reg[2];
+  const int share = mn256_share(R.tiles);
+  const int tile = xcd * share + local;
+  if (tile >= R.tiles) return;  // padding
+  int g, nt_in, m_tile;
+  mn256_coords<BNO>(a, R, xcd, local, g, m_tile, nt_in);
   const int n0 = g * R.gw + nt_in * BNO;
   const int64_t M = a.M;
   const int K = a.K;
@@ -220,8 +320,10 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
 
   f32x16 acc[4][2];
   zero_acc(acc);
+  int s0 = 0, ns = K / BK;  // a tail chunk runs its share of the k steps
+  if (job >= 0) mn256_chunk_steps<BK>(K, chunk, nchunks, s0, ns);
   auto src = [&](int s, const uint16_t* (&ap)[S], const uint16_t* (&bp)[S]) {
-    const int k0 = s * BK;
+    const int k0 = (s0 + s) * BK;
 #pragma unroll
     for (int j = 0; j < S; ++j) {
       ap[j] = abase[j] ? abase[j] + k0 : zero;
@@ -229,8 +331,21 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
     }
   };
   int my_row = -1;
-  if (tid < BM && m0 + tid < M) my_row = rows ? rows[m0 + tid] : (int)(m0 + tid);
-  run_tile<Rg>(smem, K / BK, src, brow0, brow1, live, acc);
+  if (job < 0 && tid < BM && m0 + tid < M) my_row = rows ? rows[m0 + tid] : (int)(m0 + tid);
+  run_tile<Rg>(smem, ns, src, brow0, brow1, live, acc);
+
+  if (job >= 0) {  // tail chunk: fp32 partial tile [256 rows][256 B-tile rows]
+    float* P = a.tail_ws + ((int64_t)xcd * kMN256TailJobs + job) * (BM * BN);
+#pragma unroll
+    for (int fm = 0; fm < 4; ++fm)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int r = acc_row(fm, i);
+        P[r * BN + brow0] = acc[fm][0][i];
+        P[r * BN + brow1] = acc[fm][1][i];
+      }
+    return;
+  }
 
   // Epilogue: rows back to token order; rows past cnt hold +0 accumulators.
   const int* map = stage_row_map(smem, my_row);
@@ -249,6 +364,58 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
         o[wn * 64 + 32 + col] = f32_to_bf16_hw(acc[fm][1][i]);
       }
     }
+  }
+}
+
+// Finish the XCDs' tail tiles: add each tile's chunks in order, then the
+// mn256 epilogue (SwiGLU or plain, rows back to token order).  Workgroup
+// (xcd, k, rb) takes rows [16 rb, 16 rb + 16) of tail tile k; each thread
+// loads the chunks of its elements together (independent loads) and adds
+// them in chunk order.
+constexpr int kTailRows = 16;
+template <bool SWIGLU>
+__global__ __launch_bounds__(NT) void wide_mn256_tail(MN256Args a) {
+  constexpr int BNO = SWIGLU ? 128 : 256;
+  constexpr int PER = kTailRows * BNO / NT;  // elements per thread
+  __shared__ int map[kTailRows];
+  static_assert(kTailRows <= NT, "one thread per row for the row map");
+  const int rb = blockIdx.x % (BM / kTailRows);
+  const int k = (blockIdx.x / (BM / kTailRows)) % kMN256TailJobs;
+  const int xcd = blockIdx.x / (BM / kTailRows * kMN256TailJobs);
+  const MN256Tail t = mn256_tail<BNO>(a, xcd);
+  if (k >= t.n) return;
+  int ri, local, g, m_tile, nt_in;
+  mn256_tail_tile(t, k, ri, local);
+  const MN256Region R = ri == 0 ? a.reg[0] : ri == 1 ? a.reg[1] : a.reg[2];
+  mn256_coords<BNO>(a, R, xcd, local, g, m_tile, nt_in);
+  const int n0 = g * R.gw + nt_in * BNO;
+  const int32_t* rows = R.masked ? a.idx + (int64_t)g * a.M : nullptr;
+  const int64_t p0 = (int64_t)m_tile * BM + rb * kTailRows;
+  const int tid = threadIdx.x;
+  if (tid < kTailRows) map[tid] = p0 + tid < a.M ? (rows ? rows[p0 + tid] : (int)(p0 + tid)) : -1;
+  __syncthreads();
+  const float* P = a.tail_ws + ((int64_t)xcd * kMN256TailJobs + k * t.split) * (BM * BN);
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const int i = e * NT + tid;
+    const int r = i / BNO, c = i % BNO;
+    const int tok = map[r];
+    const float* Pe = P + (rb * kTailRows + r) * BN + c;
+    float v0[kMN256TailMaxSplit], v1[kMN256TailMaxSplit];
+#pragma unroll
+    for (int q = 0; q < kMN256TailMaxSplit; ++q) {
+      const bool on = q < t.split;
+      const float* Pq = Pe + (int64_t)(on ? q : 0) * (BM * BN);  // in range whether or not used
+      v0[q] = on ? Pq[0] : 0.f;
+      v1[q] = SWIGLU && on ? Pq[128] : 0.f;
+    }
+    float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+    for (int q = 0; q < kMN256TailMaxSplit; ++q) {  // chunk order
+      s0 += v0[q];
+      s1 += v1[q];
+    }
+    if (tok >= 0) R.out[(int64_t)tok * R.ldo + n0 + c] = f32_to_bf16_hw(SWIGLU ? silu(s0) * s1 : s0);
   }
 }
 
@@ -499,11 +666,29 @@ hipError_t launch_mn256(const MN256Args& a, bool swiglu, hipStream_t s) {
   int64_t total = 0;
   for (int i = 0; i < a.n_regions; ++i) total += 8 * (int64_t)mn256_share(a.reg[i].tiles);
   if (total == 0) return hipSuccess;
+  if (a.tail) total += 8 * kMN256TailJobs;  // the tail blocks of every XCD, dispatched last
   if (swiglu)
     WIDE_RING_LAUNCH("wide_mn256<true>", MN_SW, RingMN, (unsigned)total, s, a);
   else
     WIDE_RING_LAUNCH("wide_mn256<false>", MN_PL, RingMN, (unsigned)total, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !a.tail) return e;
+  const dim3 tg(8 * kMN256TailJobs * (BM / kTailRows));
+  if (swiglu)
+    WIDE_LAUNCH(wide_mn256_tail<true>, tg, dim3(NT), 0, s, a);
+  else
+    WIDE_LAUNCH(wide_mn256_tail<false>, tg, dim3(NT), 0, s, a);
   return hipGetLastError();
+}
+
+bool mn256_tail_ok(const MN256Args& a, int bno) {
+  for (int i = 0; i < a.n_regions; ++i) {
+    const MN256Region& R = a.reg[i];
+    if (!R.masked) continue;
+    const int share = mn256_share(R.tiles), per_group = R.gw / bno * a.m_tiles;
+    if (!(a.order && R.gw / bno <= 4 && 8 * share == R.tiles && share % per_group == 0)) return false;
+  }
+  return true;
 }
 
 hipError_t launch_kd256(const KArgs& a, hipStream_t s) {

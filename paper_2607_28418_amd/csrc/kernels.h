@@ -101,8 +101,16 @@ struct MN256Args {
   int m_tiles;
   int n_regions;
   int order;  // 1: each XCD runs its groups' full tiles, then the partial, then the empty ones
+  int tail;   // 1: split each XCD's last partial round of tiles along k (regions dense or ordered)
+  float* tail_ws;  // kMN256TailFloats floats when tail
   MN256Region reg[3];
 };
+constexpr int kMN256TailJobs = 32;  // tail workgroups per XCD (its CUs)
+constexpr int kMN256TailMaxSplit = 8;  // chunks per tail tile at most
+constexpr size_t kMN256TailFloats = (size_t)8 * kMN256TailJobs * 256 * 256;
+// Host view of the launch condition: every region dense, or masked with the
+// ordered tile order (bno: output columns per tile, 128 with SwiGLU else 256).
+bool mn256_tail_ok(const MN256Args& a, int bno);
 
 constexpr int kT256 = 256;
 hipError_t launch_mn256(const MN256Args& a, bool swiglu, hipStream_t s);

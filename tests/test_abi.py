@@ -107,7 +107,7 @@ def test_options():
         W.wide_set_option("k_path", 9)
     with pytest.raises(W.WideError):
         W.wide_set_option("nope", 1)
-    for key, default, bad in (("mn_order", 2, 4), ("kd_pattern", 1, 2), ("attn_qb", 1, 3)):
+    for key, default, bad in (("mn_order", 3, 4), ("kd_pattern", 1, 2), ("attn_qb", 1, 3), ("mn_tail", 1, 2)):
         assert W.wide_get_option(key) == default
         W.wide_set_option(key, 0 if key != "attn_qb" else 2)
         with pytest.raises(W.WideError):

@@ -31,7 +31,8 @@ def _options():
     W.wide_set_option("big_tiles", 1)
     W.wide_set_option("ring_bk", 64)
     W.wide_set_option("kd_pattern", 1)
-    W.wide_set_option("mn_order", 2)
+    W.wide_set_option("mn_order", 3)
+    W.wide_set_option("mn_tail", 1)
 
 
 def ffn_dev(c):
@@ -607,3 +608,36 @@ def test_ffn_kd256_group_counts(orc, Dff):
     torch.cuda.synchronize()
     rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, G, round_bf16=True)
     assert_close(y, ry, what="y", abs_allow=ffn_flip_allowance(rh, synth.as_f32(c.w_down)))
+
+
+@pytest.mark.parametrize("M,D,Dff", [(1000, 256, 2048), (3000, 512, 4096), (300, 256, 1024)])
+def test_ffn_tail_split_matches(orc, M, D, Dff):
+    """Each XCD's last partial round of gate/up tiles is cut along k into
+    chunks (fp32 partial tiles, added in order by a second kernel); with and
+    without the split the outputs match the oracle."""
+    say("ffn tail split", M, D, Dff)
+    W.wide_set_option("decode_max_m", 0)
+    G = 128
+    c = synth.ffn_case(M + D, M, D, Dff, G, mask="topk")
+    x, wg, wu, wd, m = ffn_dev(c)
+    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, G, round_bf16=True)
+    for tail in (1, 0):
+        W.wide_set_option("mn_tail", tail)
+        h = torch.full((M, Dff), 7.0, dtype=torch.bfloat16, device=dev())
+        y = W.wide_ffn_masked(x, wg, wu, wd, m, G, h_out=h)
+        torch.cuda.synchronize()
+        assert_close(h, rh, what=f"h tail={tail}")
+        assert_close(y, ry, what=f"y tail={tail}", abs_allow=ffn_flip_allowance(rh, synth.as_f32(c.w_down)))
+    W.wide_set_option("mn_tail", 1)
+
+
+@pytest.mark.parametrize("order", [2, 3])
+@pytest.mark.parametrize("M", [1000, 2600])
+def test_qkv_tail_split_matches(orc, M, order):
+    say("qkv tail split", M, order)
+    W.wide_set_option("mn_order", order)
+    c = synth.attn_case(M + 13, M, 512, 16, 4, 128, 256, mask="topk")
+    for tail in (1, 0):
+        W.wide_set_option("mn_tail", tail)
+        check_qkvo(orc, c, kpath=0)
+    W.wide_set_option("mn_tail", 1)
