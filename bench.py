@@ -674,11 +674,14 @@ def main():
             torch.cuda.synchronize()
             kf_ms, kf_n = W.wide_timing_query("wide_attn_fwd")
             kp_ms, kp_n = W.wide_timing_query("wide_attn_prep")
+            km_ms, km_n = W.wide_timing_query("wide_attn_merge")
             W.wide_timing_enable(False)
             fl = att_flops(ma)
             att_rows.append(dict(keep=keep, ms=round(t, 4), active_TFLOPs=round(fl / (t * 1e-3) / 1e12, 1),
                                  fwd_kernel_us=round(1e3 * kf_ms / kf_n, 2),
-                                 prep_kernel_us=round(1e3 * kp_ms / kp_n, 2), active_flops=fl))
+                                 prep_kernel_us=round(1e3 * kp_ms / kp_n, 2),
+                                 merge_kernel_us=round(1e3 * km_ms / km_n, 2) if km_n else None,
+                                 active_flops=fl))
         dense_fl = att_flops(np.ones((T, L.nga), np.uint8))
         ones_ms = att_rows[-1]["ms"]
         sdpa_ms = None

@@ -211,7 +211,15 @@ wide_status_t wide_router(wide_dtype_t dt, int64_t M, int32_t d_model, int32_t r
  *   o         [n_seq*T_q][n_q_heads*head_dim] out; every element is written
  *             (inactive (token, group) rows +0).
  *   ws        >= wide_attention_workspace_size(...) bytes (a transposed copy
- *             of V, per-sequence offsets, and the reorder when idx is NULL).
+ *             of V, per-sequence offsets, the reorder when idx is NULL, and,
+ *             for one sequence with 8..1024 key tiles of 64 while the
+ *             "attn_split" option is on, the key-range split's schedule and
+ *             fp32 partials: 138 MB).
+ * With few active query tiles (one causal sequence, at most "attn_split"
+ * tiles of 32 rows x a head block) the tiles' causal key ranges are cut into
+ * chunks run by separate workgroups; a third kernel combines each tile's
+ * chunks in chunk order (the result is deterministic, and differs from the
+ * unsplit run only in fp32 summation order).
  * Arithmetic: scores as fp32 sums of bf16 products; softmax in fp32 (online,
  * one running maximum and sum per query); the probabilities are rounded to
  * bf16 for the P.V product, which accumulates in fp32; o is rounded to bf16.
@@ -326,6 +334,13 @@ size_t wide_workspace_size(wide_op_t op, wide_dtype_t dt, int64_t M,
  *   "attn_qb"       32-query blocks per wave in the prefill attention kernel:
  *                   1 (default) or 2 (each K/V fragment feeds two MFMAs, one
  *                   wave per SIMD; measured slower).
+ *   "attn_split"    prefill attention key-range split: split when at most
+ *                   this many query tiles are active (0..1024, default 1024;
+ *                   0 never splits).  Only with attn_qb 1.  Changes the
+ *                   workspace size: query it again after setting this.
+ *   "attn_split_rounds"  chunks per resident workgroup slot the split aims at
+ *                   (1..8, default 1: the chunk length is the mean work per
+ *                   slot, so only the longer key ranges split).
  * Not synchronised with calls running on other host threads.
  */
 wide_status_t wide_set_option(const char* key, int64_t value);

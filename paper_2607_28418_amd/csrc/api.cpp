@@ -469,6 +469,17 @@ wide_status_t wide_set_option(const char* key, int64_t value) {
     wide::g_attn_qb = (int)value;
     return ok();
   }
+  if (!strcmp(key, "attn_split_rounds")) {
+    if (value < 1 || value > 8) return fail(WIDE_ERR_INVALID_ARG, "attn_split_rounds must be 1..8");
+    wide::g_attn_split_rounds = (int)value;
+    return ok();
+  }
+  if (!strcmp(key, "attn_split")) {
+    if (value < 0 || value > wide::kAttnMaxSplitTiles)
+      return fail(WIDE_ERR_INVALID_ARG, "attn_split must be 0..%d", wide::kAttnMaxSplitTiles);
+    wide::g_attn_split = (int)value;
+    return ok();
+  }
   return fail(WIDE_ERR_INVALID_ARG, "unknown option '%s'", key);
 }
 
@@ -486,6 +497,8 @@ wide_status_t wide_get_option(const char* key, int64_t* value) {
   else if (!strcmp(key, "mn_order")) *value = g_mn_order;
   else if (!strcmp(key, "mn_tail")) *value = g_mn_tail;
   else if (!strcmp(key, "attn_qb")) *value = wide::g_attn_qb;
+  else if (!strcmp(key, "attn_split")) *value = wide::g_attn_split;
+  else if (!strcmp(key, "attn_split_rounds")) *value = wide::g_attn_split_rounds;
   else return fail(WIDE_ERR_INVALID_ARG, "unknown option '%s'", key);
   return ok();
 }
@@ -890,6 +903,7 @@ namespace {
 struct AttnShape {
   int64_t M = 0, Mk = 0;
   int T_kp = 0, ng = 0, hpg = 0, qpk = 0;
+  int T_q = 0, T_k = 0, n_q = 0;
 };
 
 wide_status_t attention_shape(wide_dtype_t dt, int64_t n_seq, int T_q, int T_k, int nq, int nkv,
@@ -916,6 +930,9 @@ wide_status_t attention_shape(wide_dtype_t dt, int64_t n_seq, int T_q, int T_k, 
   s.T_kp = (int)((T_k + 63) / 64 * 64);
   s.hpg = G / hd;
   s.qpk = nq / nkv;
+  s.T_q = T_q;
+  s.T_k = T_k;
+  s.n_q = nq;
   return WIDE_OK;
 }
 
@@ -923,12 +940,20 @@ struct AttnWS {
   ReorderWS r;
   uint16_t* vt = nullptr;
   int32_t* seq_off = nullptr;
+  int split_tiles = 0;  // key-range split (0: none)
+  int32_t* sched = nullptr;
+  float* part = nullptr;
 };
 
 void carve_attention(Carve& c, int64_t n_seq, int nkv, const AttnShape& s, bool need_idx, AttnWS& w) {
   if (need_idx) carve_reorder(c, s.M, s.ng, true, w.r);
   w.vt = c.take<uint16_t>((size_t)n_seq * nkv * wide::kAttnHeadDim * (size_t)s.T_kp);
   w.seq_off = c.take<int32_t>((size_t)s.ng * (size_t)(n_seq + 1));
+  w.split_tiles = wide::attn_split_tiles(n_seq, s.T_q, s.T_k, s.n_q, s.hpg, s.qpk);
+  if (w.split_tiles > 0) {
+    w.sched = c.take<int32_t>(wide::attn_sched_ints(w.split_tiles));
+    w.part = c.take<float>(wide::attn_part_floats());
+  }
 }
 
 }  // namespace
@@ -1005,6 +1030,9 @@ wide_status_t wide_attention_masked(wide_dtype_t dt, int64_t n_seq, int32_t T_q,
   a.qpk = s.qpk;
   a.causal = causal;
   a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)head_dim));
+  a.sched = w.sched;
+  a.part = w.part;
+  a.split_tiles = w.split_tiles;
   if ((e = wide::launch_attention(a, static_cast<const uint16_t*>(v), w.seq_off, stream)) != hipSuccess)
     return hip_fail(e, "attention");
   return ok();

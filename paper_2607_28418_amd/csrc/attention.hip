@@ -40,9 +40,17 @@
 
 namespace wide {
 
-int g_attn_qb = 1;  // query blocks of 32 per wave in the prefill kernel (1 or 2)
+int g_attn_qb = 1;     // query blocks of 32 per wave in the prefill kernel (1 or 2)
+int g_attn_split_rounds = 1;
+int g_attn_split = 1024;  // key-range split when at most this many query tiles are active (0: never)
 
 namespace {
+
+__host__ __device__ inline int attn_hb_of(int hpg, int qpk) {
+  if (hpg % 4 == 0 && qpk % 4 == 0) return 4;
+  if (hpg % 2 == 0 && qpk % 2 == 0) return 2;
+  return 1;
+}
 
 using t256::gptr_t;
 using t256::lptr_t;
@@ -76,37 +84,71 @@ __global__ __launch_bounds__(kAT, QB == 1 ? 2 : 1) void wide_attn_fwd(AttnArgs a
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (2 * kKSub + kVt)];  // 64 KB
 
   const int per_hb = a.n_seq * a.n_slots;
-  const int lid = t256::xcd_remap(blockIdx.x, gridDim.x);
-  const int hbk = lid / per_hb;
-  const int rem = lid - hbk * per_hb;
-  const int b = rem / a.n_slots;
-  const int slot = a.n_slots - 1 - (rem - b * a.n_slots);  // long key ranges first
-  const int h0 = hbk * HB;
-  const int g = h0 / a.hpg, hkv = h0 / a.qpk;
-  const int64_t M = a.M;
-  const int32_t* idx_g = a.idx + (int64_t)g * M;
-  const int cnt_g = a.cnt[g];
-  int s0 = 0, s1 = cnt_g;
-  if (a.seq_off) {
-    s0 = a.seq_off[g * (a.n_seq + 1) + b];
-    s1 = a.seq_off[g * (a.n_seq + 1) + b + 1];
-  }
-  const int c = s1 - s0;  // active rows of (sequence b, group g)
+  const int n_classic = a.n_q / HB * per_hb;
   const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
   const int64_t ldq = (int64_t)a.n_q * kHd;
-  const int64_t seq0 = (int64_t)b * a.T_q;
+  const int64_t M = a.M;
+  int hbk, b, slot;
+  auto classic = [&](int lid) {
+    hbk = lid / per_hb;
+    const int rem = lid - hbk * per_hb;
+    b = rem / a.n_slots;
+    slot = a.n_slots - 1 - (rem - b * a.n_slots);  // long key ranges first
+  };
+  auto rows_of = [&](int hk, int bb, int& s0, int& s1) {  // active run of (sequence bb, group of hk)
+    const int gg = hk * HB / a.hpg;
+    s0 = 0;
+    s1 = a.cnt[gg];
+    if (a.seq_off) {
+      s0 = a.seq_off[gg * (a.n_seq + 1) + bb];
+      s1 = a.seq_off[gg * (a.n_seq + 1) + bb + 1];
+    }
+  };
 
-  // Inactive rows of this sequence sit at idx_g[cnt_g + (b*T_q - s0) ...];
-  // slot i clears rows [i*BMW, (i+1)*BMW) of that run for its HB heads.
-  {
+  // Inactive rows of a sequence sit at idx_g[cnt_g + (b*T_q - s0) ...]; slot
+  // i of the classic mapping clears rows [i*BMW, (i+1)*BMW) of that run for
+  // its HB heads.
+  if ((int)blockIdx.x < n_classic) {
+    classic(t256::xcd_remap(blockIdx.x, n_classic));
     constexpr int CPR = HB * kHd / 8;  // 16-byte chunks per row
-    const int64_t ib = (int64_t)cnt_g + (seq0 - s0);
-    const int r0 = slot * BMW, r1 = min(a.T_q - c, r0 + BMW);
+    int s0, s1;
+    rows_of(hbk, b, s0, s1);
+    const int gg = hbk * HB / a.hpg;
+    const int64_t ib = (int64_t)a.cnt[gg] + ((int64_t)b * a.T_q - s0);
+    const int r0 = slot * BMW, r1 = min(a.T_q - (s1 - s0), r0 + BMW);
+    const int32_t* ig = a.idx + (int64_t)gg * M;
     for (int i = tid; i < (r1 - r0) * CPR; i += kAT) {
-      const int64_t t = idx_g[ib + r0 + i / CPR];
-      stg16(a.o + t * ldq + (int64_t)h0 * kHd + (i % CPR) * 8, u32x4{0, 0, 0, 0});
+      const int64_t t = ig[ib + r0 + i / CPR];
+      stg16(a.o + t * ldq + (int64_t)(hbk * HB) * kHd + (i % CPR) * 8, u32x4{0, 0, 0, 0});
     }
   }
+  // The work unit: the classic (head block, sequence, slot), or, when the
+  // schedule pass split the key ranges, entry blockIdx.x of its list (a
+  // tile's key chunk; longest chunks first).
+  int chunk = 0, n_chunk = 1, part_unit = 0, chunk_tiles = 0;
+  if (QB == 1 && a.sched && a.sched[0] > 0) {
+    if ((int)blockIdx.x >= a.sched[0]) return;
+    const int e = a.sched[kAttnSchedHead + blockIdx.x];
+    const int rank = e / kAttnMaxChunks;
+    chunk = e - rank * kAttnMaxChunks;
+    const int32_t* tab = a.sched + kAttnSchedHead + kAttnMaxUnits;
+    hbk = tab[rank] >> 16;
+    slot = tab[rank] & 0xffff;
+    b = 0;
+    n_chunk = tab[a.split_tiles + rank];
+    part_unit = tab[2 * a.split_tiles + rank] + chunk;
+    chunk_tiles = a.sched[2];
+  } else {
+    if ((int)blockIdx.x >= n_classic) return;
+    classic(t256::xcd_remap(blockIdx.x, n_classic));
+  }
+  const int h0 = hbk * HB;
+  const int g = h0 / a.hpg, hkv = h0 / a.qpk;
+  const int32_t* idx_g = a.idx + (int64_t)g * M;
+  int s0, s1;
+  rows_of(hbk, b, s0, s1);
+  const int c = s1 - s0;  // active rows of (sequence b, group g)
+  const int64_t seq0 = (int64_t)b * a.T_q;
   const int m0 = slot * BMW;
   if (m0 >= c) return;  // l = 0: no active row in this tile
 
@@ -133,7 +175,10 @@ __global__ __launch_bounds__(kAT, QB == 1 ? 2 : 1) void wide_attn_fwd(AttnArgs a
   const int wmin = wave_live ? limit_of(idx_g[s0 + wr0]) : -1;
   const int wmax = wave_live ? limit_of(idx_g[s0 + wr1 - 1]) : -1;
   const int gmax = limit_of(idx_g[s0 + min(c, m0 + BMW) - 1]);
-  const int n_tiles = (gmax + kBN) / kBN;
+  // This unit's key tiles [jlo, jhi): the tile's whole causal range, or one
+  // chunk of it.
+  const int jlo = chunk * chunk_tiles;
+  const int n_tiles = n_chunk > 1 ? min((gmax + kBN) / kBN, jlo + chunk_tiles) : (gmax + kBN) / kBN;
 
   // Q^T fragments (B operand): d-step s holds dims 16s + 8*hi .. +8 of the row.
   u32x4 qf[QB][8];
@@ -300,22 +345,22 @@ __global__ __launch_bounds__(kAT, QB == 1 ? 2 : 1) void wide_attn_fwd(AttnArgs a
   };
 
   // Key tiles this wave sees at all (a prefix of the workgroup's range).
-  const int wtiles = wave_live ? (wmax + kBN) / kBN : 0;
+  const int wtiles = wave_live ? min(n_tiles, (wmax + kBN) / kBN) : 0;
   // Pipeline: iteration jt loads K of tile jt+2 and V of tile jt+1, computes
   // the scores of tile jt+1 and then the softmax and P.V of tile jt, so the
   // matrix core has independent work while the softmax runs.  Everything
   // issued in one iteration lands before the next one starts.
   if constexpr (QB == 1) {
     if (kwave) {
-      issue_k(0);
-      if (n_tiles > 1) issue_k(1);
+      issue_k(jlo);
+      if (jlo + 1 < n_tiles) issue_k(jlo + 1);
     } else {
-      issue_v(0);
+      issue_v(jlo);
     }
     t256::wait_vm<0>();
     t256::stage_barrier();
     f32x16 Sa[QB][2], Sb[QB][2];
-    if (wtiles > 0) qk(0, Sa);
+    if (jlo < wtiles) qk(jlo, Sa);
     auto step = [&](int jt, f32x16 (&Sc)[QB][2], f32x16 (&Sn)[QB][2]) {
       t256::wait_vm<0>();
       t256::stage_barrier();
@@ -327,7 +372,7 @@ __global__ __launch_bounds__(kAT, QB == 1 ? 2 : 1) void wide_attn_fwd(AttnArgs a
       if (jt + 1 < wtiles) qk(jt + 1, Sn);
       if (jt < wtiles) softmax_pv(jt, Sc);  // l = 2: tiles past the wave's rows issue no MFMA
     };
-    for (int jt = 0; jt < n_tiles; jt += 2) {
+    for (int jt = jlo; jt < n_tiles; jt += 2) {
       step(jt, Sa, Sb);
       if (jt + 1 < n_tiles) step(jt + 1, Sb, Sa);
     }
@@ -338,9 +383,9 @@ __global__ __launch_bounds__(kAT, QB == 1 ? 2 : 1) void wide_attn_fwd(AttnArgs a
     // Both rings run one tile ahead: iteration jt loads K and V of tile jt+1
     // into the stages tile jt-1 used.
     f32x16 S[QB][2];
-    if (kwave) issue_k(0);
-    else issue_v(0);
-    for (int jt = 0; jt < n_tiles; ++jt) {
+    if (kwave) issue_k(jlo);
+    else issue_v(jlo);
+    for (int jt = jlo; jt < n_tiles; ++jt) {
       t256::wait_vm<0>();
       t256::stage_barrier();
       if (jt + 1 < n_tiles) {
@@ -354,6 +399,26 @@ __global__ __launch_bounds__(kAT, QB == 1 ? 2 : 1) void wide_attn_fwd(AttnArgs a
     }
   }
 
+  if (QB == 1 && n_chunk > 1) {
+    // One chunk of a split key range: the unnormalised O^T registers, the
+    // running maximum and this lane half's sum go to the unit's partial
+    // slot, lane-major so that every store of the wave is 1 KB contiguous;
+    // wide_attn_merge combines the chunks.
+    float4* po = reinterpret_cast<float4*>(a.part) + ((int64_t)part_unit * 4 + w) * (QB * 16 * kWave);
+    float2* pm = reinterpret_cast<float2*>(a.part + (int64_t)kAttnMaxUnits * kAttnPartO) +
+                 ((int64_t)part_unit * 4 + w) * (QB * kWave);
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      pm[qb * kWave + lane] = make_float2(m[qb], z[qb]);
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          po[((qb * 4 + db) * 4 + j) * kWave + lane] =
+              make_float4(O[qb][db][4 * j], O[qb][db][4 * j + 1], O[qb][db][4 * j + 2], O[qb][db][4 * j + 3]);
+    }
+    return;
+  }
   // Epilogue: the two halves of a query's sum, normalise, scatter the row.
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
@@ -374,6 +439,194 @@ __global__ __launch_bounds__(kAT, QB == 1 ? 2 : 1) void wide_attn_fwd(AttnArgs a
   }
 }
 
+// Exclusive prefix sum, in place, of n <= 16 * 64 LDS values taken in the
+// order v[0], v[1], ... (or v[top], v[top - 1], ... when rev), by one wave;
+// returns the total.
+__device__ int wave_exscan(int* v, int n, bool rev, int top) {
+  const int lane = lane_id();
+  int x[16], s = 0;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const int i = lane * 16 + k;
+    x[k] = i < n ? v[rev ? top - i : i] : 0;
+    s += x[k];
+  }
+  int inc = s;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int y = __shfl_up(inc, o, kWave);
+    if (lane >= o) inc += y;
+  }
+  int ex = inc - s;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const int i = lane * 16 + k;
+    if (i < n) v[rev ? top - i : i] = ex;
+    ex += x[k];
+  }
+  return __shfl(inc, kWave - 1, kWave);
+}
+
+// Schedule of the key-range split (one workgroup; causal, one sequence).
+// The active query tiles are numbered head block by head block.  With W key
+// tiles of work over all of them, the chunk length is the smallest that
+// keeps a tile to kAttnMaxChunks chunks and the launch to kAttnMaxUnits
+// units, and at least W / (split_rounds * kAttnSlots), so that each resident
+// workgroup slot runs about split_rounds units.  A tile whose causal range
+// spans nt key tiles becomes ceil(nt / chunk) units (one, written straight
+// to the output, when nt <= chunk), listed by their number of key tiles,
+// largest first, so that the dispatcher hands out the long ones while every
+// CU is still busy.  More active tiles than split_tiles: no split (units = 0).
+__device__ void attn_schedule(const AttnArgs& a, int hb, int bmw) {
+  __shared__ int tpre[kAttnMaxSplitHB + 1];
+  __shared__ int hist[kAttnMaxChunkTiles + 1];
+  __shared__ int nt_of[kAttnMaxSplitTiles];
+  __shared__ int tsum[kAT];
+  __shared__ int work, chl, n_units;
+  const int tid = threadIdx.x, n_hb = a.n_q / hb;
+  int32_t* sched = a.sched;
+  int32_t* list = sched + kAttnSchedHead;
+  int32_t* tab = list + kAttnMaxUnits;
+  int32_t* nch = tab + a.split_tiles;
+  int32_t* ubase = nch + a.split_tiles;
+  if (tid < n_hb) tpre[tid] = (a.cnt[tid * hb / a.hpg] + bmw - 1) / bmw;  // n_hb <= kAT
+  if (tid == 0) work = 0;
+  __syncthreads();
+  if (tid < kWave) {
+    const int t = wave_exscan(tpre, n_hb, false, 0);
+    if (tid == 0) tpre[n_hb] = t;
+  }
+  __syncthreads();
+  const int total = tpre[n_hb];
+  if (total == 0 || total > a.split_tiles) {
+    if (tid == 0) {
+      sched[0] = 0;
+      sched[1] = 0;
+      sched[2] = 0;
+    }
+    return;
+  }
+  const int delta = a.T_k - a.T_q;
+  for (int i = tid; i < total; i += kAT) {
+    int h = 0;
+    while (tpre[h + 1] <= i) ++h;
+    const int slot = i - tpre[h], gg = h * hb / a.hpg;
+    const int last = min(a.cnt[gg], (slot + 1) * bmw) - 1;
+    const int nt = (a.idx[(int64_t)gg * a.M + last] + delta + kBN) / kBN;  // key tiles of the tile
+    nt_of[i] = nt;
+    tab[i] = h << 16 | slot;
+    atomicAdd(&work, nt);
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const int nkt = (a.T_k + kBN - 1) / kBN, per_round = a.split_rounds * kAttnSlots;
+    int ch = (nkt + kAttnMaxChunks - 1) / kAttnMaxChunks;
+    ch = max(ch, (work + per_round - 1) / per_round);
+    // sum of ceil(nt / ch) <= work / ch + total <= kAttnMaxUnits
+    ch = max(ch, (work + (kAttnMaxUnits - total) - 1) / (kAttnMaxUnits - total));
+    chl = ch;
+  }
+  for (int i = tid; i <= kAttnMaxChunkTiles; i += kAT) hist[i] = 0;
+  __syncthreads();
+  const int ch = chl;
+  // Each thread's contiguous run of tiles: chunk counts, their sum, the sizes.
+  const int per = (total + kAT - 1) / kAT, i0 = min(total, tid * per), i1 = min(total, i0 + per);
+  int mine = 0;
+  for (int i = i0; i < i1; ++i) {
+    const int nt = nt_of[i], nc = (nt + ch - 1) / ch;
+    nch[i] = nc;
+    mine += nc;
+    for (int c = 0; c < nc; ++c) atomicAdd(&hist[min(ch, nt - c * ch)], 1);
+  }
+  tsum[tid] = mine;
+  __syncthreads();
+  if (tid < kWave) {
+    n_units = wave_exscan(tsum, kAT, false, 0);
+  } else if (tid < 2 * kWave) {  // start of each size's run, largest size first
+    wave_exscan(hist + 1, ch, true, ch - 1);
+  }
+  __syncthreads();
+  if (tid == 0) {
+    sched[0] = n_units;
+    sched[1] = total;
+    sched[2] = ch;
+  }
+  int u = tsum[tid];
+  for (int i = i0; i < i1; ++i) {
+    const int nt = nt_of[i], nc = (nt + ch - 1) / ch;
+    ubase[i] = u;
+    u += nc;
+    for (int c = 0; c < nc; ++c) list[atomicAdd(&hist[min(ch, nt - c * ch)], 1)] = i * kAttnMaxChunks + c;
+  }
+}
+
+// Merge of a split tile's chunks: with m_c the chunks' running maxima (log2
+// units) and M their maximum, O = sum_c 2^(m_c - M) O_c and the sum likewise,
+// added in chunk order; then the epilogue of wide_attn_fwd.  One workgroup
+// per listed tile, its waves laid out as the attention kernel's.
+template <int HB>
+__global__ __launch_bounds__(kAT) void wide_attn_merge(AttnArgs a) {
+  constexpr int WR = 32, BMW = WR * (4 / HB);
+  const int rank = blockIdx.x;
+  if (rank >= a.sched[1]) return;
+  const int32_t* tab = a.sched + kAttnSchedHead + kAttnMaxUnits;
+  const int nc = tab[a.split_tiles + rank];
+  if (nc <= 1) return;
+  const int hbk = tab[rank] >> 16, slot = tab[rank] & 0xffff, u0 = tab[2 * a.split_tiles + rank];
+  const int lane = lane_id(), w = wave_id(), l32 = lane & 31, hi = lane >> 5;
+  const int rb = w / HB, h = hbk * HB + (w - rb * HB), g = hbk * HB / a.hpg;
+  const int myr = slot * BMW + rb * WR + l32;
+  const bool valid = myr < a.cnt[g];
+  const float4* po = reinterpret_cast<const float4*>(a.part);
+  const float2* pm = reinterpret_cast<const float2*>(a.part + (int64_t)kAttnMaxUnits * kAttnPartO);
+  float mc[kAttnMaxChunks], zc[kAttnMaxChunks];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int c = 0; c < kAttnMaxChunks; ++c) {
+    const float2 v = c < nc ? pm[((int64_t)(u0 + c) * 4 + w) * kWave + lane]
+                            : make_float2(-INFINITY, 0.0f);
+    mc[c] = v.x;
+    zc[c] = v.y;
+    mx = fmaxf(mx, v.x);
+  }
+  const float muse = mx == -INFINITY ? 0.0f : mx;  // a wave with no valid row
+  float4 o[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) o[i] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  float zs = 0.0f;
+#pragma unroll
+  for (int c = 0; c < kAttnMaxChunks; ++c) {
+    if (c >= nc) break;
+    const float wc = fast_exp2(mc[c] - muse);
+    zs += wc * zc[c];
+    const float4* src = po + ((int64_t)(u0 + c) * 4 + w) * (16 * kWave) + lane;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float4 v = src[i * kWave];
+      o[i].x += wc * v.x;
+      o[i].y += wc * v.y;
+      o[i].z += wc * v.z;
+      o[i].w += wc * v.w;
+    }
+  }
+  const float zt = zs + __shfl_xor(zs, 32);
+  if (!valid) return;
+  const float inv = 1.0f / zt;
+  const int64_t t = a.idx[(int64_t)g * a.M + myr];
+  uint16_t* orow = a.o + t * ((int64_t)a.n_q * kHd) + (int64_t)h * kHd + 4 * hi;
+#pragma unroll
+  for (int db = 0; db < 4; ++db) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float4 v = o[db * 4 + j];
+      uint2 u;
+      u.x = pack_bf16x2_hw(v.x * inv, v.y * inv);
+      u.y = pack_bf16x2_hw(v.z * inv, v.w * inv);
+      *reinterpret_cast<uint2*>(orow + 32 * db + 8 * j) = u;
+    }
+  }
+}
+
 // Prep: V [n_seq*T_k][n_kv*128] -> V^T [n_seq][n_kv][128][T_kp] (zero past
 // T_k), one workgroup per (sequence, KV head, 64 keys); then, when there is
 // more than one sequence, one wave per (group, sequence boundary) finds where
@@ -383,10 +636,19 @@ __global__ __launch_bounds__(kAT) void wide_attn_prep(AttnArgs a, const uint16_t
                                                       int n_vt_blocks) {
   __shared__ __attribute__((aligned(16))) uint16_t tile[64][kHd + 8];
   const int tid = threadIdx.x;
-  if ((int)blockIdx.x < n_vt_blocks) {
+  int blk = blockIdx.x;
+  if (a.sched) {  // block 0: the split's schedule, dispatched first
+    if (blk == 0) {
+      const int hb = attn_hb_of(a.hpg, a.qpk);
+      attn_schedule(a, hb, 32 * (4 / hb));
+      return;
+    }
+    --blk;
+  }
+  if (blk < n_vt_blocks) {
     const int nkt = a.T_kp / 64;
-    const int kt = blockIdx.x % nkt;
-    const int bh = blockIdx.x / nkt;  // b * n_kv + hkv
+    const int kt = blk % nkt;
+    const int bh = blk / nkt;  // b * n_kv + hkv
     const int b = bh / a.n_kv, hkv = bh - b * a.n_kv;
     const int64_t ldk = (int64_t)a.n_kv * kHd;
 #pragma unroll
@@ -413,7 +675,7 @@ __global__ __launch_bounds__(kAT) void wide_attn_prep(AttnArgs a, const uint16_t
     return;
   }
   // sequence offsets
-  const int wv = (blockIdx.x - n_vt_blocks) * (kAT / kWave) + wave_id();
+  const int wv = (blk - n_vt_blocks) * (kAT / kWave) + wave_id();
   const int nb = a.n_seq + 1;
   if (wv >= a.ng * nb) return;
   const int g = wv / nb, b = wv - g * nb;
@@ -444,27 +706,41 @@ __global__ __launch_bounds__(kAT) void wide_attn_prep(AttnArgs a, const uint16_t
 
 }  // namespace
 
-int attn_heads_per_block(int hpg, int qpk) {
-  if (hpg % 4 == 0 && qpk % 4 == 0) return 4;
-  if (hpg % 2 == 0 && qpk % 2 == 0) return 2;
-  return 1;
-}
+int attn_heads_per_block(int hpg, int qpk) { return attn_hb_of(hpg, qpk); }
 
 int attn_query_blocks() { return g_attn_qb; }
 
 int attn_slots(int T_q, int hb) { return (T_q + 32 * attn_query_blocks() * (4 / hb) - 1) / (32 * attn_query_blocks() * (4 / hb)); }
 
+int attn_split_tiles(int64_t n_seq, int T_q, int T_k, int n_q, int hpg, int qpk) {
+  const int hb = attn_hb_of(hpg, qpk);
+  const int nkt = (T_k + 63) / 64;
+  if (!g_attn_split || g_attn_qb != 1 || n_seq != 1 || nkt < 8 || nkt > kAttnMaxChunkTiles ||
+      n_q / hb > kAttnMaxSplitHB)
+    return 0;
+  return (int)std::min<int64_t>(g_attn_split, (int64_t)(n_q / hb) * attn_slots(T_q, hb));
+}
+
 hipError_t launch_attention(AttnArgs a, const uint16_t* v, int32_t* seq_off, hipStream_t s) {
   if (a.M == 0) return hipSuccess;
   const int hb = attn_heads_per_block(a.hpg, a.qpk);
   a.n_slots = attn_slots(a.T_q, hb);
+  if (!a.causal || !a.sched || !a.part || a.split_tiles <= 0) {
+    a.sched = nullptr;
+    a.part = nullptr;
+    a.split_tiles = 0;
+  }
+  a.split_rounds = g_attn_split_rounds;
   const int n_vt = a.n_seq * a.n_kv * (a.T_kp / 64);
   const int n_off = a.n_seq > 1 ? (a.ng * (a.n_seq + 1) + 3) / 4 : 0;
-  WIDE_LAUNCH(wide_attn_prep, dim3((unsigned)(n_vt + n_off)), dim3(kAT), 0, s, a, v, seq_off, n_vt);
+  WIDE_LAUNCH(wide_attn_prep, dim3((unsigned)(n_vt + n_off + (a.sched ? 1 : 0))), dim3(kAT), 0, s, a, v, seq_off,
+              n_vt);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   a.seq_off = a.n_seq > 1 ? seq_off : nullptr;
-  const dim3 grid((unsigned)((int64_t)(a.n_q / hb) * a.n_seq * a.n_slots));
+  const int64_t n_classic = (int64_t)(a.n_q / hb) * a.n_seq * a.n_slots;
+  const int64_t max_units = std::min<int64_t>(kAttnMaxUnits, (int64_t)a.split_tiles * kAttnMaxChunks);
+  const dim3 grid((unsigned)std::max<int64_t>(n_classic, a.sched ? max_units : 0));
   if (g_attn_qb == 2) {
     if (hb == 4) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<4, 2>), grid, dim3(kAT), 0, s, a);
     else if (hb == 2) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<2, 2>), grid, dim3(kAT), 0, s, a);
@@ -473,6 +749,13 @@ hipError_t launch_attention(AttnArgs a, const uint16_t* v, int32_t* seq_off, hip
     if (hb == 4) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<4, 1>), grid, dim3(kAT), 0, s, a);
     else if (hb == 2) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<2, 1>), grid, dim3(kAT), 0, s, a);
     else WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<1, 1>), grid, dim3(kAT), 0, s, a);
+  }
+  if (a.sched) {
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const dim3 mg((unsigned)a.split_tiles);
+    if (hb == 4) WIDE_LAUNCH_NAMED("wide_attn_merge", wide_attn_merge<4>, mg, dim3(kAT), 0, s, a);
+    else if (hb == 2) WIDE_LAUNCH_NAMED("wide_attn_merge", wide_attn_merge<2>, mg, dim3(kAT), 0, s, a);
+    else WIDE_LAUNCH_NAMED("wide_attn_merge", wide_attn_merge<1>, mg, dim3(kAT), 0, s, a);
   }
   return hipGetLastError();
 }

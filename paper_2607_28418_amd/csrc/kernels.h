@@ -198,11 +198,40 @@ struct AttnArgs {
   int n_q, n_kv, ng, hpg, qpk, causal;
   int n_slots;              // set by launch_attention
   float scale_log2;         // log2(e) / sqrt(128)
+  // Key-range split (causal, one sequence): null when off.  sched holds
+  // attn_sched_ints(split_tiles) ints, part attn_part_floats() floats.
+  int32_t* sched;
+  float* part;
+  int split_tiles;
+  int split_rounds;         // set by launch_attention
 };
+// The split: a launch whose active query tiles number at most split_tiles
+// cuts each tile's causal key range into chunks of equal length (at most
+// kAttnMaxChunks per tile, at most kAttnMaxUnits in all, about
+// g_attn_split_rounds units per resident workgroup slot; split_tiles is at
+// most half of kAttnMaxUnits, which leaves room for the chunks).  sched = {units,
+// tiles, chunk length, list[kAttnMaxUnits], (head block << 16 | slot),
+// chunks, first unit [split_tiles each]}.
+constexpr int kAttnMaxChunks = 8;
+constexpr int kAttnMaxUnits = 2048;
+constexpr int kAttnMaxSplitTiles = kAttnMaxUnits / 2;
+constexpr int kAttnSlots = 512;  // workgroups resident at once: 2 per CU on 256 CUs
+constexpr int kAttnMaxSplitHB = 256;
+constexpr int kAttnMaxChunkTiles = 1024;
+constexpr int kAttnSchedHead = 3;
+constexpr int kAttnPartO = 4 * 16 * 64 * 4;  // floats of one unit's O^T partial (4 waves)
+inline size_t attn_sched_ints(int split_tiles) {
+  return kAttnSchedHead + kAttnMaxUnits + (size_t)split_tiles * 3;
+}
+inline size_t attn_part_floats() { return (size_t)kAttnMaxUnits * (kAttnPartO + 4 * 64 * 2); }
+// Query tiles the split is sized for (0: no split for this shape or option).
+int attn_split_tiles(int64_t n_seq, int T_q, int T_k, int n_q, int hpg, int qpk);
 // seq_off: workspace of ng*(n_seq+1) ints (used when n_seq > 1).
 hipError_t launch_attention(AttnArgs a, const uint16_t* v, int32_t* seq_off, hipStream_t s);
 int attn_heads_per_block(int hpg, int qpk);
 int attn_slots(int T_q, int hb);
+extern int g_attn_split_rounds;  // units per resident workgroup slot the split aims at (1..8)
+extern int g_attn_split;  // split the causal key ranges when at most this many query tiles exist (0: never)
 extern int g_attn_qb;  // 32-query blocks per wave in the prefill attention kernel (1 or 2)
 
 // ---- masked attention, decode (attention_decode.hip)

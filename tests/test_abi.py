@@ -107,9 +107,10 @@ def test_options():
         W.wide_set_option("k_path", 9)
     with pytest.raises(W.WideError):
         W.wide_set_option("nope", 1)
-    for key, default, bad in (("mn_order", 3, 4), ("kd_pattern", 1, 2), ("attn_qb", 1, 3), ("mn_tail", 1, 2)):
+    for key, default, bad in (("mn_order", 3, 4), ("kd_pattern", 1, 2), ("attn_qb", 1, 3), ("mn_tail", 1, 2),
+                               ("attn_split", 1024, 1025), ("attn_split_rounds", 1, 9)):
         assert W.wide_get_option(key) == default
-        W.wide_set_option(key, 0 if key != "attn_qb" else 2)
+        W.wide_set_option(key, {"attn_qb": 2, "attn_split_rounds": 3}.get(key, 0))
         with pytest.raises(W.WideError):
             W.wide_set_option(key, bad)
         W.wide_set_option(key, default)
@@ -237,3 +238,27 @@ def test_single_group_is_accepted():
     assert ffn(Dff=14336, G=7168) == W.ERR_INVALID_ARG and "power of two" in err()
     assert ffn(Dff=1000, G=1000, D=256) == W.ERR_UNSUPPORTED and "128" in err()
     assert W.wide_workspace_size(W.OP_FFN, W.BF16, 8192, 4096, 14336, 14336) != W.SIZE_MAX
+
+
+def test_attention_workspace_holds_the_key_split_only_where_it_can_run():
+    """The key-range split's schedule and partials are carved only for one
+    causal-capable sequence with enough key tiles; switching the option off
+    shrinks the workspace back."""
+    T, n_q, n_kv, hd, G = 8192, 32, 8, 128, 512
+    with_split = W.wide_attention_workspace_size(1, T, T, n_q, n_kv, hd, G, False)
+    two_seq = W.wide_attention_workspace_size(2, T, T, n_q, n_kv, hd, G, False)
+    W.wide_set_option("attn_split", 0)
+    try:
+        without = W.wide_attention_workspace_size(1, T, T, n_q, n_kv, hd, G, False)
+    finally:
+        W.wide_set_option("attn_split", 1024)
+    # 2048 units x (16384 + 512) floats of partials, plus the schedule's ints
+    assert with_split - without >= 2048 * (16384 + 512) * 4
+    assert with_split - without < 2048 * (16384 + 512) * 4 + 64 * 1024
+    assert two_seq < 2 * with_split  # no split for two sequences: only V^T grows
+    short = W.wide_attention_workspace_size(1, 256, 256, n_q, n_kv, hd, G, False)
+    W.wide_set_option("attn_split", 0)
+    try:
+        assert W.wide_attention_workspace_size(1, 256, 256, n_q, n_kv, hd, G, False) == short
+    finally:
+        W.wide_set_option("attn_split", 1024)

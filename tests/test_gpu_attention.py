@@ -100,7 +100,7 @@ def test_attention_empty():
     assert o.shape == (0, 256)
 
 
-@pytest.mark.parametrize("keep", [0.5, 0.25])
+@pytest.mark.parametrize("keep", [0.5, 0.25, 0.125])
 def test_attention_llama3_8b_full_sampled(orc, keep):
     """Full size (one sequence of 8192 tokens, 32/8 heads, 8 groups), checked
     on sampled rows: the oracle computes a row at position p from keys 0..p."""
@@ -121,6 +121,61 @@ def test_attention_llama3_8b_full_sampled(orc, keep):
         ref = orc.attention(*args)
         bound = attention_bound(orc, *args, T_k=p + 1)
         check_rows(got[sl], ref, bound, c.mask[sl], G, f"row {p}")
+
+
+@pytest.fixture
+def attn_split_on():
+    yield
+    W.wide_set_option("attn_split", 1024)
+    W.wide_set_option("attn_split_rounds", 1)
+
+
+@pytest.mark.parametrize("T_q,T_k,n_q,n_kv,G,mask,keep", [
+    (1000, 1000, 8, 2, 512, "topk", 0.5),       # four heads per workgroup, 32-row tiles
+    (777, 1200, 32, 8, 512, "bernoulli", 0.3),  # queries after a 423-key prefix, ragged last key tile
+    (640, 640, 8, 2, 256, "topk", 0.25),        # two heads per workgroup, 64-row tiles
+    (700, 700, 4, 4, 128, "bernoulli", 0.5),    # one head per workgroup, 128-row tiles
+    (512, 512, 8, 2, 512, "ones", 1.0),         # every row active
+])
+def test_attention_key_split_matches_oracle(orc, attn_split_on, T_q, T_k, n_q, n_kv, G, mask, keep):
+    """One causal sequence with few query tiles: the key ranges are cut into
+    chunks whose partial results a merge kernel combines.  Both the split and
+    the unsplit run meet the bound, and the split really ran (its merge
+    kernel was launched)."""
+    for split, rounds in ((1024, 1), (1024, 8), (0, 1)):
+        say("attention key split", split, rounds, T_q, T_k, n_q, n_kv, G, mask, keep)
+        W.wide_set_option("attn_split", split)
+        W.wide_set_option("attn_split_rounds", rounds)
+        W.wide_timing_enable(True)
+        W.wide_timing_reset()
+        run_case(orc, 1, T_q, T_k, n_q, n_kv, G, True, mask=mask, keep=keep, seed=T_q + split)
+        _, n_merge = W.wide_timing_query("wide_attn_merge")
+        W.wide_timing_enable(False)
+        assert (n_merge > 0) == (split > 0)
+
+
+def test_attention_key_split_replays_in_hip_graph(attn_split_on):
+    say("attention key split graph replay")
+    hd, n_q, n_kv, G, T = 128, 8, 2, 512, 900
+    cp = synth.attn_prefill_case(8, 1, T, T, n_q, n_kv, hd, n_q * hd // G, mask="topk", keep=0.25)
+    q, k, v, m = (to_dev(a) for a in (cp.q, cp.k, cp.v, cp.mask))
+    o = torch.empty_like(q)
+    ws = torch.empty(W.wide_attention_workspace_size(1, T, T, n_q, n_kv, hd, G, True),
+                     dtype=torch.uint8, device=dev())
+    step = lambda: W.wide_attention_masked(q, k, v, m, 1, n_q, n_kv, hd, G, True, o=o, ws=ws)
+    step()
+    torch.cuda.synchronize()
+    ref = o.clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for _ in range(3):
+        o.fill_(7.0)
+        ws.fill_(0x5A)   # stale schedule and partials must not matter
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(o.view(torch.int16), ref.view(torch.int16))
 
 
 @pytest.mark.parametrize("n_seq,T_q,T_k,n_q,n_kv,G,causal", [
