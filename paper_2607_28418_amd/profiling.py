@@ -27,6 +27,7 @@ import re
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
+CALIBRATION_COPIES = 2  # bench.py --calibration-copy ends with two copies of copy_bytes
 
 
 def source_digest() -> str:
@@ -54,16 +55,30 @@ def kernel_key(name: str) -> str:
 def counter_means(path: str) -> dict:
     """{kernel key: {counter: mean value per dispatch, 'dispatches': n}}.
 
-    Small device copies made by the runtime also run the copy kernel; only its
-    dispatches with the largest grid (the calibration copies) are kept."""
+    Other device copies of the program (the runtime's, torch's) also run the
+    copy kernel, some with the calibration copies' grid; the calibration
+    copies are the program's last CALIBRATION_COPIES dispatches of it with
+    the largest grid, and only those are kept for it (in dispatch order when the dump numbers the
+    dispatches, else in file order)."""
     acc = collections.defaultdict(lambda: collections.defaultdict(list))
     with open(path) as f:
         rows = list(csv.DictReader(f))
-    copy_grid = max((int(r.get("Grid_Size") or 0) for r in rows
-                     if kernel_key(r["Kernel_Name"]) == COPY_KERNEL), default=0)
-    for r in rows:
+    order = lambda i: (int(rows[i]["Dispatch_Id"]) if rows[i].get("Dispatch_Id") else i, i)
+    grid = lambda r: int(r.get("Grid_Size") or 0)
+    copy_grid = max((grid(r) for r in rows if kernel_key(r["Kernel_Name"]) == COPY_KERNEL), default=0)
+    copies = sorted((i for i, r in enumerate(rows)
+                     if kernel_key(r["Kernel_Name"]) == COPY_KERNEL and grid(r) == copy_grid), key=order)
+    ids = []
+    for i in reversed(copies):  # one row per (dispatch, counter): keep the last dispatches' rows
+        d = rows[i].get("Dispatch_Id") or i
+        if d not in ids:
+            if len(ids) == CALIBRATION_COPIES:
+                break
+            ids.append(d)
+    keep = {i for i in copies if (rows[i].get("Dispatch_Id") or i) in ids}
+    for i, r in enumerate(rows):
         k = kernel_key(r["Kernel_Name"])
-        if k == COPY_KERNEL and int(r.get("Grid_Size") or 0) != copy_grid:
+        if k == COPY_KERNEL and i not in keep:
             continue
         acc[k][r["Counter_Name"]].append(float(r["Counter_Value"]))
     out = {}

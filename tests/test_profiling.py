@@ -33,6 +33,20 @@ def test_summary_scales_by_copy_and_guards_sources(tmp_path):
     assert profiling.traffic_for(str(p), "wide_mn256<true>") is None
 
 
+def test_calibration_is_the_last_two_copies(tmp_path):
+    """Earlier copies of the program run the copy kernel with the same grid;
+    only the last two dispatches (the calibration copies) set the scale."""
+    k = "void wide::wide_attn_fwd<4, 1>(wide::AttnArgs)"
+    c = profiling.COPY_KERNEL
+    _dump(tmp_path / "f.csv", "FETCH_SIZE", [(c, 16.0, 131072), (k, 10.0), (c, 57.0, 131072), (c, 3.0, 512),
+                                             (c, 512.0, 131072), (c, 512.0, 131072)])
+    _dump(tmp_path / "w.csv", "WRITE_SIZE", [(c, 16.0, 131072), (k, 10.0), (c, 57.0, 131072), (c, 3.0, 512),
+                                             (c, 1024.0, 131072), (c, 1024.0, 131072)])
+    s = profiling.summarize(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), 1024 * 1024, "cmd")
+    assert s["fetch_scale"] == 2.0 and s["write_scale"] == 1.0
+    assert profiling.counter_means(str(tmp_path / "f.csv"))[c]["dispatches"] == 2
+
+
 def test_label_matching():
     m = profiling.label_matches
     assert m("wide_kd256<64>", "wide_kd256")
