@@ -12,7 +12,8 @@ router logits at 50% sparsity.  One step is the whole hot path twice:
 
 Outside the timed step the line also reports the masked causal attention
 that sits between the Q/K/V and O projections (same tokens and attention
-mask; 25/75/100% keep; torch's fused SDPA as the dense reference).
+mask; 25/75/100% keep; torch's fused SDPA as the dense reference) and the
+bottleneck router (rank 32) over the same tokens.
 
 value = active FLOPs of the step (FLOPs of the executed groups only, the
 paper's accounting) / step time, in TFLOP/s.  The JSON line also carries the
@@ -56,6 +57,8 @@ def parse():
                     help="skip the masked-attention figures (prefill, outside the timed step)")
     ap.add_argument("--no-sweeps", action="store_true",
                     help="skip the decode batch sweep and the prefill keep sweep")
+    ap.add_argument("--no-router", action="store_true",
+                    help="skip the router figures (outside the timed step)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="end with two 1 GiB device copies (counter calibration under rocprofv3)")
     ap.add_argument("--decode-bytes-case", type=int, default=0, metavar="B",
@@ -841,6 +844,58 @@ def main():
             vs_group_size=g_rows)
         del qd, kd, vd, od, wsd, caches
 
+    # ---- bottleneck router (outside the timed region) --------------------------------
+    # R = X W1 W2 at rank 32 with random weights, for the layer's FFN (112
+    # groups) and attention (8 groups) routers, over the prefill tokens and the
+    # decode batch.  Bound by HBM: the bytes are X read once, W1, W2 and the
+    # mask written.
+    router = None
+    if not args.no_router:
+        gr = torch.Generator(device=dev)
+        gr.manual_seed(13)
+        rank = 32
+        router_rows = []
+        for nm in ("prefill", "decode"):
+            xr = bd[nm]["x_ffn"]
+            M = xr.shape[0]
+            for which, ngr in (("ffn", L.ng), ("attention", L.nga)):
+                w1 = (torch.randn(rank, L.D, device=dev, generator=gr) * 0.02).to(torch.bfloat16)
+                w2 = (torch.randn(2 * ngr, rank, device=dev, generator=gr) * 0.3).to(torch.bfloat16)
+                mr = torch.empty((M, ngr), dtype=torch.uint8, device=dev)
+                call = lambda: W.wide_router(xr, w1, w2, mask=mr)
+                for _ in range(3):
+                    call()
+                torch.cuda.synchronize()
+                s0, s1 = ev(), ev()
+                s0.record(stream)
+                for _ in range(20):
+                    call()
+                s1.record(stream)
+                torch.cuda.synchronize()
+                ms = s0.elapsed_time(s1) / 20
+                W.wide_timing_enable(True)
+                W.wide_timing_reset()
+                for _ in range(10):
+                    call()
+                torch.cuda.synchronize()
+                k_ms, k_n = W.wide_timing_query("wide_router")
+                W.wide_timing_enable(False)
+                by = 2 * M * L.D + 2 * rank * L.D + 2 * 2 * ngr * rank + M * ngr
+                k_us = 1e3 * k_ms / k_n
+                router_rows.append(dict(tokens=M, router=which, groups=ngr, rank=rank, ms=round(ms, 4),
+                                        kernel_us=round(k_us, 2), bytes=by,
+                                        GBps=round(by / (k_us * 1e-6) / 1e9, 1),
+                                        frac_hbm=round(by / (k_us * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4)))
+        main_r = router_rows[0]
+        router = dict(
+            workload="bottleneck router R = X W1 W2 (rank 32, random weights), d_model %d; FFN (%d groups) "
+                     "and attention (%d groups) routers over %d prefill tokens and a decode batch of %d"
+                     % (L.D, L.ng, L.nga, args.prefill_tokens, args.decode_batch),
+            rows=router_rows,
+            roofline=dict(kernel="wide_router", bound="hbm", achieved=main_r["GBps"], peak=PEAK_HBM_GBPS,
+                          unit="GB/s", frac=main_r["frac_hbm"], tokens=main_r["tokens"],
+                          algorithmic_bytes_per_launch=main_r["bytes"], avg_launch_us=main_r["kernel_us"]))
+
     # ---- CPU oracle on a bounded sample --------------------------------------------
     cpu = None
     if not args.no_cpu_baseline:
@@ -888,6 +943,7 @@ def main():
         "cpu_baseline": cpu,
         "sweeps": sweeps,
         "attention": attention,
+        "router": router,
     }
     print(json.dumps(out), flush=True)
     if args.calibration_copy:
