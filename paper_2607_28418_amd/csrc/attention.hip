@@ -507,15 +507,29 @@ __device__ void attn_schedule(const AttnArgs& a, int hb, int bmw) {
     return;
   }
   const int delta = a.T_k - a.T_q;
-  for (int i = tid; i < total; i += kAT) {
-    int h = 0;
-    while (tpre[h + 1] <= i) ++h;
-    const int slot = i - tpre[h], gg = h * hb / a.hpg;
-    const int last = min(a.cnt[gg], (slot + 1) * bmw) - 1;
-    const int nt = (a.idx[(int64_t)gg * a.M + last] + delta + kBN) / kBN;  // key tiles of the tile
-    nt_of[i] = nt;
-    tab[i] = h << 16 | slot;
-    atomicAdd(&work, nt);
+  static_assert(kAttnMaxSplitTiles <= 4 * kAT, "four tiles per thread");
+  int last_tok[4];  // each tile's last row: four independent loads in flight
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int i = tid + q * kAT;
+    last_tok[q] = 0;
+    if (i < total) {
+      int h = 0;
+      while (tpre[h + 1] <= i) ++h;
+      const int slot = i - tpre[h], gg = h * hb / a.hpg;
+      const int last = min(a.cnt[gg], (slot + 1) * bmw) - 1;
+      last_tok[q] = a.idx[(int64_t)gg * a.M + last];
+      tab[i] = h << 16 | slot;
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int i = tid + q * kAT;
+    if (i < total) {
+      const int nt = (last_tok[q] + delta + kBN) / kBN;  // key tiles of the tile
+      nt_of[i] = nt;
+      atomicAdd(&work, nt);
+    }
   }
   __syncthreads();
   if (tid == 0) {
@@ -634,7 +648,6 @@ __global__ __launch_bounds__(kAT) void wide_attn_merge(AttnArgs a) {
 // list).
 __global__ __launch_bounds__(kAT) void wide_attn_prep(AttnArgs a, const uint16_t* v, int32_t* seq_off,
                                                       int n_vt_blocks) {
-  __shared__ __attribute__((aligned(16))) uint16_t tile[64][kHd + 8];
   const int tid = threadIdx.x;
   int blk = blockIdx.x;
   if (a.sched) {  // block 0: the split's schedule, dispatched first
@@ -646,31 +659,33 @@ __global__ __launch_bounds__(kAT) void wide_attn_prep(AttnArgs a, const uint16_t
     --blk;
   }
   if (blk < n_vt_blocks) {
+    // Thread (kc, dc) of the first 128 moves the 8 x 8 block of keys
+    // kt*64 + 8kc.. and dims 8dc..: eight 16-byte row loads, a transpose in
+    // registers, eight 16-byte stores.  A wave's loads cover 8 key rows x 128
+    // contiguous bytes, its stores 8 dim rows x 128 contiguous bytes.
+    if (tid >= 128) return;
     const int nkt = a.T_kp / 64;
     const int kt = blk % nkt;
     const int bh = blk / nkt;  // b * n_kv + hkv
     const int b = bh / a.n_kv, hkv = bh - b * a.n_kv;
     const int64_t ldk = (int64_t)a.n_kv * kHd;
+    const int kc = tid & 7, dc = tid >> 3;
+    const int k0 = kt * 64 + kc * 8;
+    u32x4 in[8];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int cidx = tid + kAT * u;
-      const int r = cidx >> 4, cc = cidx & 15;
-      const int key = kt * 64 + r;
-      u32x4 d = {0, 0, 0, 0};
-      if (key < a.T_k) d = ldg16(v + ((int64_t)b * a.T_k + key) * ldk + hkv * kHd + cc * 8);
-      *reinterpret_cast<u32x4*>(&tile[r][cc * 8]) = d;
-    }
-    __syncthreads();
-    uint16_t* vt = a.vt + (int64_t)bh * kHd * a.T_kp;
+    for (int i = 0; i < 8; ++i)
+      in[i] = k0 + i < a.T_k ? ldg16(v + ((int64_t)b * a.T_k + k0 + i) * ldk + hkv * kHd + dc * 8)
+                             : u32x4{0, 0, 0, 0};
+    uint16_t* vt = a.vt + (int64_t)bh * kHd * a.T_kp + k0;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int cidx = tid + kAT * u;
-      const int d = cidx >> 3, kc = cidx & 7;
+    for (int e = 0; e < 8; ++e) {  // dim 8dc + e: keys k0 .. k0 + 7, two per word
       u32x4 o;
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        o[e] = (uint32_t)tile[kc * 8 + 2 * e][d] | ((uint32_t)tile[kc * 8 + 2 * e + 1][d] << 16);
-      stg16(vt + (int64_t)d * a.T_kp + kt * 64 + kc * 8, o);
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t lo = in[2 * j][e >> 1], hi = in[2 * j + 1][e >> 1];
+        o[j] = (e & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+      }
+      stg16(vt + (int64_t)(dc * 8 + e) * a.T_kp, o);
     }
     return;
   }
