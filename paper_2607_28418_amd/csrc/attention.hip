@@ -472,7 +472,8 @@ __device__ int wave_exscan(int* v, int n, bool rev, int top) {
 // tiles of work over all of them, the chunk length is the smallest that
 // keeps a tile to kAttnMaxChunks chunks and the launch to kAttnMaxUnits
 // units, and at least W / (split_rounds * kAttnSlots), so that each resident
-// workgroup slot runs about split_rounds units.  A tile whose causal range
+// workgroup slot runs about split_rounds units; at most the key tiles of the
+// whole range (no tile spans more).  A tile whose causal range
 // spans nt key tiles becomes ceil(nt / chunk) units (one, written straight
 // to the output, when nt <= chunk), listed by their number of key tiles,
 // largest first, so that the dispatcher hands out the long ones while every
@@ -538,7 +539,9 @@ __device__ void attn_schedule(const AttnArgs& a, int hb, int bmw) {
     ch = max(ch, (work + per_round - 1) / per_round);
     // sum of ceil(nt / ch) <= work / ch + total <= kAttnMaxUnits
     ch = max(ch, (work + (kAttnMaxUnits - total) - 1) / (kAttnMaxUnits - total));
-    chl = ch;
+    // No tile spans more than nkt key tiles: a longer chunk splits nothing,
+    // and nkt <= kAttnMaxChunkTiles bounds the size histogram.
+    chl = min(ch, nkt);
   }
   for (int i = tid; i <= kAttnMaxChunkTiles; i += kAT) hist[i] = 0;
   __syncthreads();

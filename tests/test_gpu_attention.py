@@ -178,6 +178,30 @@ def test_attention_key_split_replays_in_hip_graph(attn_split_on):
         assert torch.equal(o.view(torch.int16), ref.view(torch.int16))
 
 
+def test_attention_key_split_long_keys_sampled(orc):
+    """3360 queries after a 56640-key prefix (T_k = 60000, 938 key tiles):
+    with 840 active query tiles the work term alone asks for chunks longer
+    than any tile's range; the schedule caps the chunk at the key tiles of
+    the whole range (no split) and every row is still right.  Sampled rows
+    against the oracle."""
+    T_q, T_k, n_q, n_kv, G, hd = 3360, 60000, 32, 8, 512, 128
+    say("attention long keys", T_q, T_k)
+    c = synth.attn_prefill_case(31, 1, T_q, T_k, n_q, n_kv, hd, n_q * hd // G, mask="ones")
+    q, k, v, m = (to_dev(a) for a in (c.q, c.k, c.v, c.mask))
+    o = torch.full_like(q, float("nan"))
+    W.wide_attention_masked(q, k, v, m, 1, n_q, n_kv, hd, G, True, o=o)
+    torch.cuda.synchronize()
+    got = to_np64(o)
+    assert np.isfinite(got).all()
+    delta = T_k - T_q
+    for p in (0, 1777, T_q - 1):
+        sl = slice(p, p + 1)
+        args = (c.q[sl], c.k[:delta + p + 1], c.v[:delta + p + 1], c.mask[sl], 1, n_q, n_kv, hd, True)
+        ref = orc.attention(*args)
+        bound = attention_bound(orc, *args, T_k=delta + p + 1)
+        check_rows(got[sl], ref, bound, c.mask[sl], G, f"row {p}")
+
+
 @pytest.mark.parametrize("n_seq,T_q,T_k,n_q,n_kv,G,causal", [
     (2, 300, 300, 8, 2, 512, True), (3, 70, 133, 8, 2, 256, True), (1, 200, 90, 4, 4, 128, False)])
 def test_attention_zero_queries_are_exact_means(orc, n_seq, T_q, T_k, n_q, n_kv, G, causal):
