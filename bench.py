@@ -107,7 +107,7 @@ def log(*a):
 class Layer:
     """Synthetic inputs of one decoder layer's projections (host bf16 bits)."""
 
-    def __init__(self, seed, T, B, keep):
+    def __init__(self, seed, T, B, keep, weights=True):
         from paper_2607_28418_amd import synth
         p = synth.WORKLOADS["layer_llama3_8b"].params
         self.D, self.Dff, self.G = p["D"], p["Dff"], p["G"]
@@ -117,10 +117,12 @@ class Layer:
         g = synth.rng(seed)
         D, Dff, Nq, Nkv = self.D, self.Dff, self.Nq, self.Nkv
         n = synth.normal
-        self.w = dict(w_q=n(g, (Nq, D), 0.02, "bf16"), w_k=n(g, (Nkv, D), 0.02, "bf16"),
-                      w_v=n(g, (Nkv, D), 0.02, "bf16"), w_o=n(g, (D, Nq), 0.02, "bf16"),
-                      w_gate=n(g, (Dff, D), 0.02, "bf16"), w_up=n(g, (Dff, D), 0.02, "bf16"),
-                      w_down=n(g, (D, Dff), 0.02, "bf16"))
+        self.w = None
+        if weights:   # (False: masks and FLOP accounting only)
+            self.w = dict(w_q=n(g, (Nq, D), 0.02, "bf16"), w_k=n(g, (Nkv, D), 0.02, "bf16"),
+                          w_v=n(g, (Nkv, D), 0.02, "bf16"), w_o=n(g, (D, Nq), 0.02, "bf16"),
+                          w_gate=n(g, (Dff, D), 0.02, "bf16"), w_up=n(g, (Dff, D), 0.02, "bf16"),
+                          w_down=n(g, (D, Dff), 0.02, "bf16"))
         self.batches = {}
         for name, M in (("prefill", T), ("decode", B)):
             xa = n(g, (M, D), 1.0, "bf16")
@@ -147,6 +149,12 @@ class Layer:
     def dense_flops(self, name):
         M = self.batches[name]["mask_attn"].shape[0]
         return 2.0 * M * self.D * (2 * self.Nq + 2 * self.Nkv + 3 * self.Dff)
+
+    def dense_flops_per_op(self, name):
+        M = self.batches[name]["mask_attn"].shape[0]
+        D = self.D
+        return dict(q=2.0 * M * D * self.Nq, kv=2.0 * 2 * M * D * self.Nkv, o=2.0 * M * D * self.Nq,
+                    gate_up=2.0 * 2 * M * D * self.Dff, down=2.0 * M * D * self.Dff)
 
     def decode_bytes(self):
         """Weight bytes the decode batch must read: dense K/V plus the union groups."""

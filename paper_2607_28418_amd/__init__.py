@@ -116,9 +116,13 @@ def _dtype_code(t) -> int:
 def _mask_bytes(mask):
     torch = _torch()
     if mask.dtype == torch.bool:
-        return mask.view(torch.uint8)
+        mask = mask.view(torch.uint8)
     if mask.dtype != torch.uint8:
         raise TypeError("mask must be uint8 or bool")
+    if mask.numel() and mask.data_ptr() % 16:
+        # the library reads mask rows with 16-byte loads and requires a
+        # 16-byte aligned mask (a row slice of a mask may not be): copy it
+        mask = mask.clone()
     return mask
 
 
@@ -288,6 +292,7 @@ def wide_attention_masked(q, k, v, mask, n_seq, n_q, n_kv, head_dim, group_size,
     idx/counts optional (a reorder of `mask`).  Returns o, same shape as q."""
     torch = _torch()
     _contig(q, k, v, mask, idx, counts, o)
+    mask = _mask_bytes(mask)
     if n_seq > 0 and (q.shape[0] % n_seq or k.shape[0] % n_seq):
         raise ValueError("q and k rows must split evenly into n_seq sequences")
     T_q = q.shape[0] // n_seq if n_seq > 0 else 0
@@ -319,6 +324,7 @@ def wide_attention_decode(q, k_cache, v_cache, mask, n_q, n_kv, head_dim, group_
     mask [B][n_groups] uint8; kv_len optional int32 [B].  Returns o, same
     shape as q."""
     _contig(q, k_cache, v_cache, mask, kv_len, o)
+    mask = _mask_bytes(mask)
     B = q.shape[0]
     if head_major:
         L = k_cache.shape[2] if k_cache.dim() == 4 else 0

@@ -194,12 +194,21 @@ wide_status_t ffn_shape(wide_dtype_t dt, int64_t M, int D, int Dff, int G) {
     if (D % 16 || Dff % 16) return fail(WIDE_ERR_UNSUPPORTED, "fp32 path needs d_model, d_ff multiples of 16");
   } else {
     if (D % 256) return fail(WIDE_ERR_UNSUPPORTED, "bf16 path needs d_model %% 256 == 0 (got %d)", D);
-    if (G < 64) return fail(WIDE_ERR_UNSUPPORTED, "bf16 path needs group_size >= 64 (got %d)", G);
+    if (G < wide::kKMergeWidth && (Dff % 128 || Dff / wide::kKMergeWidth > wide::kKd256MaxGroups))
+      return fail(WIDE_ERR_UNSUPPORTED, "bf16 path with group_size < 64 needs d_ff %% 128 == 0 and d_ff <= %d",
+                  wide::kKd256MaxGroups * wide::kKMergeWidth);
     if (G == Dff && !is_pow2(G) && G % 128)
       return fail(WIDE_ERR_UNSUPPORTED, "bf16 single-group path needs d_ff %% 128 == 0 (got %d)", G);
   }
   return WIDE_OK;
 }
+
+// Groups narrower than the K axis's 64-wide k step (bf16 prefill): the
+// N axis runs on 256-row tiles in token order and stores +0 for inactive
+// (token, group) blocks; the K axis then works on 64-wide merged blocks (a
+// block is active for a token when any of its groups is, and the inactive
+// groups inside it contribute the zeros H holds).
+bool small_groups(wide_dtype_t dt, int G) { return dt == WIDE_BF16 && G < wide::kKMergeWidth; }
 
 size_t ffn_ws_bytes(wide_dtype_t dt, int64_t M, int D, int Dff, int G, bool need_idx, bool need_h,
                     int kpath) {
@@ -215,6 +224,11 @@ size_t ffn_ws_bytes(wide_dtype_t dt, int64_t M, int D, int Dff, int G, bool need
     if (pn) c.take<float>(pn);
     const int ks = wide::gemv_k_split(D);
     if (ks > 1) c.take<float>((size_t)ks * M * D);
+  } else if (small_groups(dt, G)) {
+    const int nm = Dff / wide::kKMergeWidth;
+    c.take<uint8_t>((size_t)M * nm);  // merged mask
+    KWS k;
+    carve_kaxis(c, M, D, nm, 1, k);
   } else {
     ReorderWS r;
     carve_reorder(c, M, ng, need_idx, r);
@@ -245,7 +259,12 @@ wide_status_t attn_shape(wide_dtype_t dt, int64_t M, int D, int nq, int nkv, int
       return fail(WIDE_ERR_UNSUPPORTED, "fp32 path needs d_model, n_kv*head_dim, group_size multiples of 16");
   } else {
     if (D % 256) return fail(WIDE_ERR_UNSUPPORTED, "bf16 path needs d_model %% 256 == 0");
-    if (G % 128) return fail(WIDE_ERR_UNSUPPORTED, "bf16 path needs group_size %% 128 == 0");
+    if (G == 64) {  // Q on token-order 256-wide tiles
+      if (Nq % 256 || Nkv % 256)
+        return fail(WIDE_ERR_UNSUPPORTED, "bf16 path with group_size 64 needs n_q*head_dim and n_kv*head_dim %% 256 == 0");
+    } else if (G % 128) {
+      return fail(WIDE_ERR_UNSUPPORTED, "bf16 path needs group_size 64 or a multiple of 128");
+    }
     if (Nkv % 128) return fail(WIDE_ERR_UNSUPPORTED, "bf16 path needs n_kv*head_dim %% 128 == 0");
   }
   d = AttnDims{D, nq, nkv, hd, G, Nq, Nkv, Nq / G};
@@ -274,8 +293,13 @@ wide::GVNArgs qkv_gvn(int64_t M, const AttnDims& d, const uint8_t* mask, const v
   return na;
 }
 
+// Q groups narrower than 128 columns: Q runs on 256-wide tiles in token order
+// (every output computed, +0 stored where the group is inactive).
+bool qkv_token_order(const AttnDims& d) { return d.G < 128; }
 // Q/K/V on 256x256 tiles (else the 128-tile kernel)
-bool qkv_big(const AttnDims& d) { return g_big_tiles && d.G % wide::kT256 == 0 && d.Nkv % wide::kT256 == 0; }
+bool qkv_big(const AttnDims& d) {
+  return qkv_token_order(d) || (g_big_tiles && d.G % wide::kT256 == 0 && d.Nkv % wide::kT256 == 0);
+}
 
 size_t attn_ws_bytes(wide_phase_t ph, wide_dtype_t dt, int64_t M, const AttnDims& d, bool need_idx,
                      int kpath) {
@@ -300,7 +324,8 @@ size_t attn_ws_bytes(wide_phase_t ph, wide_dtype_t dt, int64_t M, const AttnDims
     ReorderWS r;
     if (need_idx) carve_reorder(c, M, d.ng, true, r);
     // Q/K/V tail tiles (a sizing query without n_kv assumes the 256 tiles)
-    if (d.Nkv < 0 ? g_big_tiles && d.G % wide::kT256 == 0 : qkv_big(d)) c.take<float>(wide::kMN256TailFloats);
+    if (d.Nkv < 0 ? d.G < 128 || (g_big_tiles && d.G % wide::kT256 == 0) : qkv_big(d))
+      c.take<float>(wide::kMN256TailFloats);
   } else {
     ReorderWS r;
     const int path = kpath;
@@ -544,7 +569,7 @@ wide_status_t wide_mask_reorder(const uint8_t* mask, int64_t M, int32_t n_groups
   if (n_groups < 1 || n_groups > 4096) return fail(WIDE_ERR_INVALID_ARG, "n_groups must be in [1, 4096]");
   CHECK(check_ptr(counts, "counts", false));
   if (M > 0) {
-    CHECK(check_ptr(mask, "mask", false));
+    CHECK(check_ptr(mask, "mask"));
     CHECK(check_ptr(idx, "idx", false));
   }
   Carve c0(nullptr);
@@ -580,7 +605,7 @@ wide_status_t wide_router(wide_dtype_t dt, int64_t M, int32_t d_model, int32_t r
     return e == hipSuccess ? ok() : hip_fail(e, "router counts");
   }
   CHECK(check_ptr(x, "x"));
-  CHECK(check_ptr(mask, "mask", false));
+  CHECK(check_ptr(mask, "mask"));
   if (logits) CHECK(check_ptr(logits, "logits", false));
   if (idx) {
     CHECK(check_ptr(idx, "idx", false));
@@ -617,7 +642,7 @@ wide_status_t wide_ffn_masked(wide_dtype_t dt, int64_t M, int32_t d_model, int32
   CHECK(check_ptr(w_down, "w_down"));
   if (h_out) CHECK(check_ptr(h_out, "h_out"));
   if (M == 0) return ok();
-  CHECK(check_ptr(mask, "mask", false));
+  CHECK(check_ptr(mask, "mask"));
   CHECK(check_ptr(x, "x"));
   CHECK(check_ptr(y, "y"));
   if (idx) {
@@ -649,12 +674,38 @@ wide_status_t wide_ffn_masked(wide_dtype_t dt, int64_t M, int32_t d_model, int32
     if ((e = wide::launch_gemv_n(na, true, stream)) != hipSuccess) return hip_fail(e, "gemv gate/up");
     const int ks = wide::gemv_k_split(D);
     float* part = ks > 1 ? c.take<float>((size_t)ks * M * D) : nullptr;
+    // groups narrower than 64 are walked as merged 64-wide groups
+    const int mg = std::max(1, wide::kKMergeWidth / G);
     wide::GVKArgs ka{h, static_cast<const uint16_t*>(w_down), mask, static_cast<uint16_t*>(y),
-                     (int)M, Dff, D, G, ng, ks, part};
+                     (int)M, Dff, D, G * mg, ng / mg, ks, part, mg};
     if ((e = wide::launch_gemv_k(ka, stream)) != hipSuccess) return hip_fail(e, "gemv down");
     return ok();
   }
 
+  if (small_groups(dt, G)) {
+    const int nm = Dff / wide::kKMergeWidth;
+    uint8_t* merged = c.take<uint8_t>((size_t)M * nm);
+    KWS kws;
+    carve_kaxis(c, M, D, nm, 1, kws);
+    wide::MN256Args ma{};
+    ma.x = static_cast<const uint16_t*>(x);
+    ma.M = M;
+    ma.K = D;
+    ma.m_tiles = (int)((M + wide::kT256 - 1) / wide::kT256);
+    ma.n_regions = 1;
+    ma.mask = mask;
+    ma.mask_ng = ng;
+    ma.mask_G = G;
+    // every H block is written (+0 where inactive): the merged K axis reads them
+    ma.reg[0] = wide::MN256Region{static_cast<const uint16_t*>(w_gate), static_cast<const uint16_t*>(w_up), h,
+                                  Dff, Dff, wide::kMN256TokenOrder, ma.m_tiles * (Dff / 128), 0};
+    if ((e = wide::launch_mn256(ma, true, stream)) != hipSuccess) return hip_fail(e, "mn256 gate/up");
+    if ((e = wide::launch_mask_merge(mask, M, ng, wide::kKMergeWidth / G, merged, stream)) != hipSuccess)
+      return hip_fail(e, "mask merge");
+    CHECK(run_kaxis(h, static_cast<const uint16_t*>(w_down), merged, nullptr, nullptr, static_cast<uint16_t*>(y), M,
+                    Dff, D, wide::kKMergeWidth, 1, kws, stream));
+    return ok();
+  }
   ReorderWS r;
   carve_reorder(c, M, ng, idx == nullptr, r);
   KWS kws;
@@ -723,7 +774,7 @@ wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M, i
     CHECK(check_ptr(w_o, "w_o"));
   }
   if (M == 0) return ok();
-  CHECK(check_ptr(mask, "mask", false));
+  CHECK(check_ptr(mask, "mask"));
   CHECK(check_ptr(in, "in"));
   if (phase == WIDE_PHASE_QKV) {
     CHECK(check_ptr(q, "q"));
@@ -772,14 +823,15 @@ wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M, i
       const int ks = wide::gemv_k_split(d.D);
       float* part = ks > 1 ? c.take<float>((size_t)ks * M * d.D) : nullptr;
       wide::GVKArgs ka{x, static_cast<const uint16_t*>(w_o), mask, static_cast<uint16_t*>(y), (int)M, d.Nq,
-                       d.D, d.G, ng, ks, part};
+                       d.D, d.G, ng, ks, part, 1};
       if ((e = wide::launch_gemv_k(ka, stream)) != hipSuccess) return hip_fail(e, "gemv o");
     }
     return ok();
   }
 
   const bool rows_k = phase == WIDE_PHASE_O && kaxis_row_gathered(d.Nq, d.D, d.G);
-  const bool need_reorder = idx == nullptr && (phase == WIDE_PHASE_QKV || kpath == 2 || rows_k);
+  const bool need_reorder =
+      idx == nullptr && ((phase == WIDE_PHASE_QKV && !qkv_token_order(d)) || kpath == 2 || rows_k);
   ReorderWS r;
   float* tail_ws = nullptr;
   if (phase == WIDE_PHASE_QKV) {
@@ -818,8 +870,16 @@ wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M, i
                                      ma.m_tiles * (d.Nkv / T)};
       ma.reg[ik + 1] = wide::MN256Region{wv, nullptr, static_cast<uint16_t*>(v), d.Nkv, d.Nkv, 0,
                                          ma.m_tiles * (d.Nkv / T)};
-      ma.reg[iq] = wide::MN256Region{wq, nullptr, static_cast<uint16_t*>(q), d.Nq, d.G, 1,
-                                     ng * ma.m_tiles * (d.G / T)};
+      if (qkv_token_order(d)) {
+        ma.mask = mask;
+        ma.mask_ng = ng;
+        ma.mask_G = d.G;
+        ma.reg[iq] = wide::MN256Region{wq, nullptr, static_cast<uint16_t*>(q), d.Nq, d.Nq, wide::kMN256TokenOrder,
+                                       ma.m_tiles * (d.Nq / T)};
+      } else {
+        ma.reg[iq] = wide::MN256Region{wq, nullptr, static_cast<uint16_t*>(q), d.Nq, d.G, wide::kMN256Sorted,
+                                       ng * ma.m_tiles * (d.G / T)};
+      }
       ma.tail = g_mn_tail && wide::mn256_tail_ok(ma, 256) ? 1 : 0;
       ma.tail_ws = tail_ws;
       if ((e = wide::launch_mn256(ma, false, stream)) != hipSuccess) return hip_fail(e, "mn256 qkv");
@@ -985,7 +1045,7 @@ wide_status_t wide_attention_masked(wide_dtype_t dt, int64_t n_seq, int32_t T_q,
   if ((idx == nullptr) != (counts == nullptr))
     return fail(WIDE_ERR_INVALID_ARG, "idx and counts must both be given or both be NULL");
   if (s.M == 0) return ok();
-  CHECK(check_ptr(mask, "mask", false));
+  CHECK(check_ptr(mask, "mask"));
   CHECK(check_ptr(q, "q"));
   CHECK(check_ptr(k, "k"));
   CHECK(check_ptr(v, "v"));
@@ -1093,7 +1153,7 @@ wide_status_t wide_attention_decode(wide_dtype_t dt, int64_t batch, int32_t L, i
   if (kv_layout != WIDE_KV_TOKEN_MAJOR && kv_layout != WIDE_KV_HEAD_MAJOR)
     return fail(WIDE_ERR_INVALID_ARG, "kv_layout must be WIDE_KV_TOKEN_MAJOR or WIDE_KV_HEAD_MAJOR");
   if (batch == 0) return ok();
-  CHECK(check_ptr(mask, "mask", false));
+  CHECK(check_ptr(mask, "mask"));
   if (kv_len) CHECK(check_ptr(kv_len, "kv_len", false));
   CHECK(check_ptr(q, "q"));
   CHECK(check_ptr(k_cache, "k_cache"));

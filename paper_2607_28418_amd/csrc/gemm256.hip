@@ -37,10 +37,14 @@ using RingKD = Ring<BK, BK == 64 ? 2 : 4>;
 // put one dependent global load in front of every store.  Instead, thread
 // r < 256 fetches tile row r's token (-1 past the end) before the k loop,
 // and after it the map goes through the then idle ring LDS.
-__device__ __forceinline__ const int* stage_row_map(uint16_t* smem, int my_row) {
+// `extra` (a row's mask bits, token-order regions) goes to map[BM + r].
+__device__ __forceinline__ const int* stage_row_map(uint16_t* smem, int my_row, int extra = 0) {
   int* map = reinterpret_cast<int*>(smem);
   __syncthreads();  // every wave is done with the ring
-  if (threadIdx.x < BM) map[threadIdx.x] = my_row;
+  if (threadIdx.x < BM) {
+    map[threadIdx.x] = my_row;
+    map[BM + threadIdx.x] = extra;
+  }
   __syncthreads();
   return map;
 }
@@ -97,7 +101,8 @@ __device__ __forceinline__ void run_tile(uint16_t* smem, int nsteps, Src src, in
 template <int BNO>
 __device__ __forceinline__ bool mn256_ordered(const MN256Args& a, const MN256Region& R) {
   const int share = mn256_share(R.tiles), per_group = R.gw / BNO * a.m_tiles;
-  return a.order && R.masked && R.gw / BNO <= 4 && 8 * share == R.tiles && share % per_group == 0;
+  return a.order && R.masked == kMN256Sorted && R.gw / BNO <= 4 && 8 * share == R.tiles &&
+         share % per_group == 0;
 }
 
 template <int BNO>
@@ -177,7 +182,7 @@ struct MN256Tail {
 template <int BNO>
 __device__ __forceinline__ int mn256_real(const MN256Args& a, const MN256Region& R, int xcd) {
   const int share = mn256_share(R.tiles);
-  if (!R.masked) return max(0, min(share, R.tiles - xcd * share));
+  if (R.masked != kMN256Sorted) return max(0, min(share, R.tiles - xcd * share));
   const int ntpg = R.gw / BNO, gps = share / (ntpg * a.m_tiles), gb = xcd * gps;
   int n = 0;
   for (int i = 0; i < gps; ++i) n += (a.cnt[gb + i] + BM - 1) / BM;
@@ -275,12 +280,36 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
   const int n0 = g * R.gw + nt_in * BNO;
   const int64_t M = a.M;
   const int K = a.K;
-  const int32_t* rows = R.masked ? a.idx + (int64_t)g * M : nullptr;
-  const int64_t cnt = R.masked ? (int64_t)a.cnt[g] : M;
+  const bool sorted = R.masked == kMN256Sorted;
+  const int32_t* rows = sorted ? a.idx + (int64_t)g * M : nullptr;
+  const int64_t cnt = sorted ? (int64_t)a.cnt[g] : M;
   const int64_t m0 = (int64_t)m_tile * BM;
   const int tid = threadIdx.x;
 
-  if (m0 >= cnt) {  // l = 0: the whole tile is inactive for group g
+  // Token-order region: thread r < 256 holds row r's mask bits over the
+  // tile's groups (bit i: group n0 / mask_G + i), for the epilogue.
+  const bool tok_order = R.masked == kMN256TokenOrder;
+  uint32_t rbits = 0;
+  bool empty = m0 >= cnt;  // l = 0: the whole tile is inactive for group g
+  if (tok_order) {
+    const int gpt = BNO / a.mask_G;
+    if (tid < BM && m0 + tid < M) {
+      const uint8_t* mr = a.mask + (m0 + tid) * a.mask_ng + n0 / a.mask_G;
+      for (int i = 0; i < gpt; ++i) rbits |= (uint32_t)(mr[i] != 0) << i;
+    }
+    // l = 0: no (row, group) of the tile is active.  (The flag lives in the
+    // ring's LDS, not yet in use: a block-wide vote would take static LDS,
+    // which the five-stage ring leaves none of.)
+    int* flag = reinterpret_cast<int*>(smem);
+    if (tid == 0) *flag = 0;
+    __syncthreads();
+    if (rbits) *flag = 1;
+    __syncthreads();
+    empty = *flag == 0;
+    __syncthreads();  // before the ring's loads overwrite the flag
+  }
+
+  if (empty) {
     if (R.skip_zero) return;
     constexpr int CH = BNO / 8;
     int my_row = -1;
@@ -348,20 +377,28 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
   }
 
   // Epilogue: rows back to token order; rows past cnt hold +0 accumulators.
-  const int* map = stage_row_map(smem, my_row);
+  // A token-order region stores +0 where the row's group is inactive.
+  const int* map = stage_row_map(smem, my_row, (int)rbits);
   const int col = acc_col();
+  const int gsh = tok_order ? __builtin_ctz(a.mask_G) : 0;
+  const int c0 = SWIGLU ? wn * 32 + col : wn * 64 + col;  // tile columns of the two fragments
+  const int c1 = SWIGLU ? c0 : c0 + 32;
 #pragma unroll
   for (int fm = 0; fm < 4; ++fm) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const int t = map[acc_row(fm, i)];
+      const int r = acc_row(fm, i);
+      const int t = map[r];
       if (t < 0) continue;
+      const int rb = tok_order ? map[BM + r] : 0;
+      const bool on0 = !tok_order || ((rb >> (c0 >> gsh)) & 1);
+      const bool on1 = !tok_order || ((rb >> (c1 >> gsh)) & 1);
       uint16_t* o = R.out + (int64_t)t * R.ldo + n0;
       if (SWIGLU) {
-        o[wn * 32 + col] = f32_to_bf16_hw(silu(acc[fm][0][i]) * acc[fm][1][i]);
+        o[c0] = f32_to_bf16_hw(on0 ? silu(acc[fm][0][i]) * acc[fm][1][i] : 0.f);
       } else {
-        o[wn * 64 + col] = f32_to_bf16_hw(acc[fm][0][i]);
-        o[wn * 64 + 32 + col] = f32_to_bf16_hw(acc[fm][1][i]);
+        o[c0] = f32_to_bf16_hw(on0 ? acc[fm][0][i] : 0.f);
+        o[c1] = f32_to_bf16_hw(on1 ? acc[fm][1][i] : 0.f);
       }
     }
   }
@@ -415,7 +452,9 @@ __global__ __launch_bounds__(NT) void wide_mn256_tail(MN256Args a) {
       s0 += v0[q];
       s1 += v1[q];
     }
-    if (tok >= 0) R.out[(int64_t)tok * R.ldo + n0 + c] = f32_to_bf16_hw(SWIGLU ? silu(s0) * s1 : s0);
+    if (tok < 0) continue;
+    const bool on = R.masked != kMN256TokenOrder || a.mask[(int64_t)tok * a.mask_ng + (n0 + c) / a.mask_G] != 0;
+    R.out[(int64_t)tok * R.ldo + n0 + c] = f32_to_bf16_hw(on ? (SWIGLU ? silu(s0) * s1 : s0) : 0.f);
   }
 }
 
@@ -684,7 +723,7 @@ hipError_t launch_mn256(const MN256Args& a, bool swiglu, hipStream_t s) {
 bool mn256_tail_ok(const MN256Args& a, int bno) {
   for (int i = 0; i < a.n_regions; ++i) {
     const MN256Region& R = a.reg[i];
-    if (!R.masked) continue;
+    if (R.masked != kMN256Sorted) continue;  // dense and token-order regions: every tile is real
     const int share = mn256_share(R.tiles), per_group = R.gw / bno * a.m_tiles;
     if (!(a.order && R.gw / bno <= 4 && 8 * share == R.tiles && share % per_group == 0)) return false;
   }

@@ -277,8 +277,11 @@ __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
   const int w = wave_id(), lane = lane_id();
   for (int i = tid; i < ng; i += NT) s_act[i] = 0ull;
   __syncthreads();
-  for (int i = tid; i < B * ng; i += NT)
-    if (a.mask[i] != 0) atomicOr(&s_act[i % ng], 1ull << (i / ng));
+  // (groups narrower than 64 arrive merged: a.merge mask columns per group
+  // of G; the inactive ones inside an active merged group hold exact zeros)
+  const int rng = ng * a.merge;
+  for (int i = tid; i < B * rng; i += NT)
+    if (a.mask[i] != 0) atomicOr(&s_act[(i % rng) / a.merge], 1ull << (i / rng));
   if (tid == 0) n_union = 0;
   __syncthreads();
   // Union of the batch's active groups, compacted in ascending order.
@@ -385,18 +388,41 @@ __global__ __launch_bounds__(256) void wide_gemv_k_finish(const float* __restric
 }
 
 namespace {
+// Timing labels name the variant: "wide_gemv_n<true>/ntb2_ncb4" is
+// wide_gemv_n<true, 2, 4> (queries of "wide_gemv_n<true>" cover them all).
+#define WIDE_GV_LABEL(BASE, NTB, NCB) BASE "/ntb" #NTB "_ncb" #NCB
+
+template <bool SW, int NTB, int NCB>
+constexpr const char* gemv_n_label() {
+  if constexpr (SW) {
+    if constexpr (NTB == 1) return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_n<true>", 1, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_n<true>", 1, 2) : WIDE_GV_LABEL("wide_gemv_n<true>", 1, 4);
+    if constexpr (NTB == 2) return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_n<true>", 2, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_n<true>", 2, 2) : WIDE_GV_LABEL("wide_gemv_n<true>", 2, 4);
+    return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_n<true>", 4, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_n<true>", 4, 2) : WIDE_GV_LABEL("wide_gemv_n<true>", 4, 4);
+  } else {
+    if constexpr (NTB == 1) return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_n<false>", 1, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_n<false>", 1, 2) : WIDE_GV_LABEL("wide_gemv_n<false>", 1, 4);
+    if constexpr (NTB == 2) return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_n<false>", 2, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_n<false>", 2, 2) : WIDE_GV_LABEL("wide_gemv_n<false>", 2, 4);
+    return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_n<false>", 4, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_n<false>", 4, 2) : WIDE_GV_LABEL("wide_gemv_n<false>", 4, 4);
+  }
+}
+
+template <int NTB, int NCB>
+constexpr const char* gemv_k_label() {
+  if constexpr (NTB == 1) return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_k", 1, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_k", 1, 2) : WIDE_GV_LABEL("wide_gemv_k", 1, 4);
+  if constexpr (NTB == 2) return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_k", 2, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_k", 2, 2) : WIDE_GV_LABEL("wide_gemv_k", 2, 4);
+  return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_k", 4, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_k", 4, 2) : WIDE_GV_LABEL("wide_gemv_k", 4, 4);
+}
+
 template <bool SW, int NCB>
 hipError_t gemv_n_launch(const GVNArgs& a, int nb, hipStream_t s) {
-  const char* name = SW ? "wide_gemv_n<true>" : "wide_gemv_n<false>";
   const int grid = nb / NCB * a.k_split;
   if (a.B <= 16)
-    WIDE_LAUNCH_NAMED(name, (wide_gemv_n<SW, 1, NCB>), dim3(grid), dim3(NT), 0, s, a);
+    WIDE_LAUNCH_NAMED((gemv_n_label<SW, 1, NCB>()), (wide_gemv_n<SW, 1, NCB>), dim3(grid), dim3(NT), 0, s, a);
   else if (a.B <= 32)
-    WIDE_LAUNCH_NAMED(name, (wide_gemv_n<SW, 2, NCB>), dim3(grid), dim3(NT), 0, s, a);
+    WIDE_LAUNCH_NAMED((gemv_n_label<SW, 2, NCB>()), (wide_gemv_n<SW, 2, NCB>), dim3(grid), dim3(NT), 0, s, a);
   else if constexpr (SW && NCB == 4)
     return hipErrorInvalidValue;  // not instantiated: gemv_n_ncb never picks it
   else
-    WIDE_LAUNCH_NAMED(name, (wide_gemv_n<SW, 4, NCB>), dim3(grid), dim3(NT), 0, s, a);
+    WIDE_LAUNCH_NAMED((gemv_n_label<SW, 4, NCB>()), (wide_gemv_n<SW, 4, NCB>), dim3(grid), dim3(NT), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.k_split == 1) return e;
   const int64_t n = (int64_t)a.B * gv_total_cols(a);
@@ -412,11 +438,11 @@ template <int NCB>
 hipError_t gemv_k_launch(const GVKArgs& a, hipStream_t s) {
   const int grid = a.N / (16 * NCB) * a.k_split;
   if (a.B <= 16)
-    WIDE_LAUNCH_NAMED("wide_gemv_k", (wide_gemv_k<1, NCB>), dim3(grid), dim3(NT), 0, s, a);
+    WIDE_LAUNCH_NAMED((gemv_k_label<1, NCB>()), (wide_gemv_k<1, NCB>), dim3(grid), dim3(NT), 0, s, a);
   else if (a.B <= 32)
-    WIDE_LAUNCH_NAMED("wide_gemv_k", (wide_gemv_k<2, NCB>), dim3(grid), dim3(NT), 0, s, a);
+    WIDE_LAUNCH_NAMED((gemv_k_label<2, NCB>()), (wide_gemv_k<2, NCB>), dim3(grid), dim3(NT), 0, s, a);
   else
-    WIDE_LAUNCH_NAMED("wide_gemv_k", (wide_gemv_k<4, NCB>), dim3(grid), dim3(NT), 0, s, a);
+    WIDE_LAUNCH_NAMED((gemv_k_label<4, NCB>()), (wide_gemv_k<4, NCB>), dim3(grid), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 }  // namespace

@@ -18,6 +18,10 @@ constexpr int kPatternMaxGroups = 8;
 size_t pattern_scratch_ints(int64_t M);
 hipError_t launch_pattern_order(const uint8_t* mask, int64_t M, int n_groups, int32_t* perm, int32_t* scratch,
                                 hipStream_t s);
+// out [M][n_groups / r] uint8: 1 where any of r consecutive groups is active.
+hipError_t launch_mask_merge(const uint8_t* mask, int64_t M, int n_groups, int r, uint8_t* out, hipStream_t s);
+// Groups narrower than this run the K axis on merged blocks of this width.
+constexpr int kKMergeWidth = 64;
 
 // ---- prefill N-axis GEMM ---------------------------------------------------
 // A region is a run of output tiles sharing one weight (or gate/up pair) and
@@ -81,6 +85,12 @@ hipError_t launch_tile_union(const uint8_t* mask, int64_t M, int n_groups, int t
 // A region of the large-tile GEMM-MN: output columns [0, N) of one tensor cut
 // into groups of `gw` columns (gw = G for a masked region, gw = N for a dense
 // one); tiles = (N / gw) * m_tiles * (gw / tile_cols).
+// masked: 0 dense; 1 (kMN256Sorted) rows of a tile follow the reorder of its
+// group (gw = G, a multiple of the tile width); 2 (kMN256TokenOrder) groups
+// narrower than a tile: rows in token order, every output (t, n) written
+// as the product when group n / mask_G is active for t, else +0 (gw = N, as
+// for a dense region).
+constexpr int kMN256Sorted = 1, kMN256TokenOrder = 2;
 struct MN256Region {
   const uint16_t* w0;
   const uint16_t* w1;
@@ -103,6 +113,8 @@ struct MN256Args {
   int order;  // 1: each XCD runs its groups' full tiles, then the partial, then the empty ones
   int tail;   // 1: split each XCD's last partial round of tiles along k (regions dense or ordered)
   float* tail_ws;  // kMN256TailFloats floats when tail
+  const uint8_t* mask;  // [M][mask_ng]: the routing mask (token-order regions only)
+  int mask_ng, mask_G;
   MN256Region reg[3];
 };
 constexpr int kMN256TailJobs = 32;  // tail workgroups per XCD (its CUs)
@@ -152,9 +164,10 @@ struct GVKArgs {
   const uint16_t* w;   // [N][K]
   const uint8_t* mask; // [B][K/G]
   uint16_t* y;         // [B][N]
-  int B, K, N, G, n_groups;
+  int B, K, N, G, n_groups;  // G >= 64; n_groups = K / G
   int k_split;         // workgroups sharing one row block's union steps
   float* part;         // [k_split][B][N] partial sums when k_split > 1
+  int merge;           // mask columns per group of G (> 1: routing groups of G / merge merged)
 };
 // Decode K-axis: output rows per workgroup (16 * gemv_k_ncb) and the split of
 // the union steps over workgroups (see gemv.hip).

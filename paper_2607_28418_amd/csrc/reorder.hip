@@ -410,4 +410,28 @@ size_t reorder_scratch_ints(int64_t M, int n_groups) {
   return (size_t)(n_chunks * n_groups);
 }
 
+// Routing columns merged r at a time: out[t][b] = 1 when any of groups
+// [b r, (b+1) r) is active for token t, else 0.  The K axis of groups
+// narrower than its 64-wide k step works on these blocks (the inactive
+// groups inside an active block hold exact zeros in H).
+__global__ __launch_bounds__(256) void wide_mask_merge(const uint8_t* __restrict__ mask, int64_t M, int ng, int r,
+                                                       uint8_t* __restrict__ out) {
+  const int nb = ng / r;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= M * nb) return;
+  const int64_t t = i / nb;
+  const int b = (int)(i % nb);
+  const uint8_t* p = mask + t * ng + (int64_t)b * r;
+  int on = 0;
+  for (int j = 0; j < r; ++j) on |= p[j];
+  out[i] = on != 0;
+}
+
+hipError_t launch_mask_merge(const uint8_t* mask, int64_t M, int n_groups, int r, uint8_t* out, hipStream_t s) {
+  const int64_t n = M * (n_groups / r);
+  if (n == 0) return hipSuccess;
+  WIDE_LAUNCH(wide_mask_merge, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, mask, M, n_groups, r, out);
+  return hipGetLastError();
+}
+
 }  // namespace wide

@@ -2,6 +2,8 @@
 import numpy as np
 import torch
 
+from paper_2607_28418_amd import synth
+
 # Parity bar for the bf16 path against the storage-matched fp64 oracle
 # (bf16 rounding of H and of every output, as the kernels store them):
 #   mean |got - ref| <= 1e-3  and  max |got - ref| / max(|ref|, 0.1 rms(ref)) <= 2e-2.
@@ -28,11 +30,12 @@ def to_np64(t) -> np.ndarray:
     return t.detach().float().cpu().numpy().astype(np.float64)
 
 
-def parity_stats(got: np.ndarray, ref: np.ndarray, abs_allow: float = 0.0):
+def parity_stats(got: np.ndarray, ref: np.ndarray, abs_allow=0.0):
     """(mean abs error, max relative error); the relative error of an element
-    is (|got-ref| - abs_allow)+ / max(|ref|, 0.1 rms(ref))."""
-    err = np.maximum(np.abs(got - ref) - abs_allow, 0.0) if abs_allow else np.abs(got - ref)
+    is (|got-ref| - abs_allow)+ / max(|ref|, 0.1 rms(ref)).  abs_allow is a
+    scalar or an array of ref's shape (a per-element allowance)."""
     mae_err = np.abs(got - ref)
+    err = np.maximum(mae_err - abs_allow, 0.0)
     rms = float(np.sqrt(np.mean(ref ** 2))) if ref.size else 0.0
     floor = np.maximum(np.abs(ref), 0.1 * rms)
     with np.errstate(divide="ignore", invalid="ignore"):
@@ -40,24 +43,7 @@ def parity_stats(got: np.ndarray, ref: np.ndarray, abs_allow: float = 0.0):
     return float(mae_err.mean()) if err.size else 0.0, float(rel.max()) if rel.size else 0.0
 
 
-def bf16_ulp(v: float) -> float:
-    """Spacing of bf16 values at magnitude v (8 significant bits)."""
-    return 2.0 ** (np.floor(np.log2(v)) - 7) if v > 0 else 0.0
-
-
-def ffn_flip_allowance(h_ref: np.ndarray, w_down: np.ndarray) -> float:
-    """Absolute allowance for the FFN output on the bf16 path.
-
-    H is stored in bf16, so a kernel whose fp32 sums differ from fp64 in the
-    last bits rounds a few H entries to the neighbouring bf16 value (a one-ulp
-    flip; about 1e-4 of the entries).  Each flip moves one output by
-    ulp(h) * |w_down|, whatever the size of that output, so near-zero outputs
-    need an absolute allowance: two flips of the largest |h| times the largest
-    |w_down|.  Computed from oracle values and inputs only."""
-    return 2.0 * bf16_ulp(float(np.abs(h_ref).max())) * float(np.abs(w_down).max())
-
-
-def assert_close(got, ref: np.ndarray, kind: str = "bf16", what: str = "", abs_allow: float = 0.0):
+def assert_close(got, ref: np.ndarray, kind: str = "bf16", what: str = "", abs_allow=0.0):
     g = to_np64(got) if isinstance(got, torch.Tensor) else got
     assert g.shape == ref.shape, (what, g.shape, ref.shape)
     assert np.isfinite(g).all(), f"{what}: non-finite output"
@@ -98,3 +84,67 @@ def check_attention_rows(got, ref, bound, mask_rows, hpg_feat, what):
     mae = float(err.mean()) if err.size else 0.0
     assert mae <= 1e-3, f"{what}: mae {mae:.3g}"
     return mae
+
+
+# ---- bf16 projections: rounding bands (tests/_bounds) plus the parity bar -----------
+
+def _rows_np(t, rows):
+    if isinstance(t, np.ndarray):
+        return np.asarray(t if rows is None else t[rows], np.float64)
+    if rows is None:
+        return to_np64(t)
+    return to_np64(t[torch.as_tensor(rows, device=t.device)])
+
+
+def _sel(a, rows):
+    return a if rows is None else a[rows]
+
+
+def check_ffn(orc, c, y, h=None, rows=None, what="ffn"):
+    """bf16 masked FFN against the oracle on token rows `rows` (all if None).
+
+    H and y must lie in their rounding bands (bit-exact outside a narrow band
+    around bf16 rounding boundaries, one bf16 step inside it; skipped H
+    blocks and all-inactive rows exactly +0), and y must meet the parity bar
+    (mean |err| <= 1e-3, max relative error <= 2e-2 with the 0.1 rms floor)
+    after the per-element allowance for H values the kernel may round to the
+    neighbouring bf16 value."""
+    from tests import _bounds as B
+    x, mask = _sel(c.x, rows), _sel(c.mask, rows)
+    rh, ry = orc.ffn(x, c.w_gate, c.w_up, c.w_down, mask, c.G, round_bf16=True)
+    h64, _ = orc.ffn(x, c.w_gate, c.w_up, c.w_down, mask, c.G)
+    y64 = orc.kproj(synth.f32_to_bf16_bits(rh.astype(np.float32)), c.w_down, mask, c.G)
+    A_h, A_flip, A_y = B.ffn_bands(x, c.w_gate, c.w_up, c.w_down, mask, c.G, h64, rh)
+    if h is not None:
+        B.check_band(_rows_np(h, rows), h64, A_h, f"{what} h", zero=~B.expand(mask, c.G))
+    yg = _rows_np(y, rows)
+    B.check_band(yg, y64, A_y, f"{what} y", zero=np.broadcast_to(~mask.any(1)[:, None], yg.shape))
+    return assert_close(yg, ry, what=f"{what} y", abs_allow=A_flip)
+
+
+def check_nproj(orc, x, w, mask, G, got, rows=None, what="q"):
+    """bf16 N-axis projection (mask None: dense) against the oracle: rounding
+    band, +0 at inactive blocks, and the parity bar."""
+    from tests import _bounds as B
+    x = _sel(x, rows)
+    if mask is None:
+        v, ref, zero = orc.linear(x, w), orc.linear(x, w, round_bf16=True), None
+    else:
+        mask = _sel(mask, rows)
+        v, ref = orc.nproj(x, w, mask, G), orc.nproj(x, w, mask, G, round_bf16=True)
+        zero = ~B.expand(mask, G)
+    g = _rows_np(got, rows)
+    B.check_band(g, v, B.nproj_band(x, w, mask, G), what, zero=zero)
+    return assert_close(g, ref, what=what)
+
+
+def check_kproj(orc, a, w, mask, G, got, rows=None, what="o"):
+    """bf16 K-axis projection against the oracle: rounding band, +0 rows for
+    tokens with no active group, and the parity bar."""
+    from tests import _bounds as B
+    a, mask = _sel(a, rows), _sel(mask, rows)
+    v, ref = orc.kproj(a, w, mask, G), orc.kproj(a, w, mask, G, round_bf16=True)
+    g = _rows_np(got, rows)
+    B.check_band(g, v, B.kproj_band(a, w, mask, G), what,
+                 zero=np.broadcast_to(~mask.any(1)[:, None], g.shape))
+    return assert_close(g, ref, what=what)

@@ -44,7 +44,8 @@ def err():
     (dict(G=48), W.ERR_INVALID_ARG, "power of two"),
     (dict(G=8), W.ERR_INVALID_ARG, "power of two"),
     (dict(Dff=11000), W.ERR_INVALID_ARG, "does not divide"),
-    (dict(G=32, Dff=1024), W.ERR_UNSUPPORTED, "group_size >= 64"),
+    (dict(G=32, Dff=1056), W.ERR_UNSUPPORTED, "group_size < 64"),
+    (dict(mask=MIS), W.ERR_INVALID_ARG, "mask is not 16-byte aligned"),
     (dict(D=4000), W.ERR_UNSUPPORTED, "256"),
     (dict(M=-1), W.ERR_INVALID_ARG, "out of range"),
     (dict(dt=7), W.ERR_INVALID_ARG, "dtype"),
@@ -80,13 +81,21 @@ def test_qkvo_validation():
     assert call(phase=5) == W.ERR_INVALID_ARG
     assert call(wq=None) == W.ERR_INVALID_ARG and "w_q" in err()
     assert call(phase=W.PHASE_O, wo=None) == W.ERR_INVALID_ARG and "w_o" in err()
-    assert call(hd=64, G=64, dt=W.BF16) == W.ERR_UNSUPPORTED
+    assert call(hd=64, G=64, nkv=2) == W.ERR_UNSUPPORTED and "group_size 64" in err()
+    assert call(mask=MIS) == W.ERR_INVALID_ARG and "mask is not 16-byte aligned" in err()
+    assert call(phase=W.PHASE_O, mask=MIS) == W.ERR_INVALID_ARG
     assert call(M=0, inp=None, mask=None, q=None, k=None, v=None) == W.OK
 
 
 def test_workspace_sizes():
     s = W.wide_workspace_size
     assert s(W.OP_FFN, W.BF16, 4096, 4096, 11008, 48) == W.SIZE_MAX
+    # groups of 16 and 32 (Section 3.1: {2^k, k >= 4}): a merged mask instead of a reorder
+    for G in (16, 32):
+        small = s(W.OP_FFN, W.BF16, 8192, 4096, 14336, G)
+        assert small != W.SIZE_MAX and small >= 8192 * 14336 * 2 + 8192 * (14336 // 64)
+        assert s(W.OP_FFN, W.BF16, 16, 4096, 14336, G) != W.SIZE_MAX
+    assert s(W.OP_FFN, W.BF16, 8192, 4096, 1056, 32) == W.SIZE_MAX
     pre = s(W.OP_FFN, W.BF16, 4096, 4096, 11008, 128)
     # H (bf16) + fp32 K-axis buffer + reorder index at least
     assert pre >= 4096 * 11008 * 2 + 4096 * 4096 * 4 + 86 * 4096 * 4

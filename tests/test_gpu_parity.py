@@ -5,6 +5,7 @@ Sizes: small cases span several tiles with ragged tails and are checked
 element by element; full-size cases run the whole problem on the GPU and
 check sampled token rows against the oracle (rows are independent).
 """
+import dataclasses
 import sys
 
 import numpy as np
@@ -13,7 +14,7 @@ import torch
 
 import paper_2607_28418_amd as W
 from paper_2607_28418_amd import synth
-from tests._helpers import assert_close, dev, ffn_flip_allowance, to_dev, to_np64
+from tests._helpers import assert_close, check_ffn, check_kproj, check_nproj, dev, to_dev, to_np64
 
 pytestmark = pytest.mark.gpu
 
@@ -89,9 +90,7 @@ def test_ffn_bf16_prefill_small(orc, M, D, Dff, G, kind, kpath, big):
     h = torch.empty((M, Dff), dtype=torch.bfloat16, device=dev())
     y = W.wide_ffn_masked(x, wg, wu, wd, m, G, h_out=h)
     torch.cuda.synchronize()
-    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, G, round_bf16=True)
-    assert_close(h, rh, what="h")
-    assert_close(y, ry, what="y", abs_allow=ffn_flip_allowance(rh, synth.as_f32(c.w_down)))
+    check_ffn(orc, c, y, h)
 
 
 @pytest.mark.parametrize("M,D,Dff,G,kpath", [
@@ -105,9 +104,7 @@ def test_ffn_bf16_prefill_ring32(orc, M, D, Dff, G, kpath):
     h = torch.empty((M, Dff), dtype=torch.bfloat16, device=dev())
     y = W.wide_ffn_masked(x, wg, wu, wd, m, G, h_out=h)
     torch.cuda.synchronize()
-    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, G, round_bf16=True)
-    assert_close(h, rh, what="h")
-    assert_close(y, ry, what="y", abs_allow=ffn_flip_allowance(rh, synth.as_f32(c.w_down)))
+    check_ffn(orc, c, y, h)
 
 
 @pytest.mark.parametrize("M,D,Dff,G", [(513, 256, 1024, 512), (700, 512, 768, 128), (300, 4096, 1024, 128)])
@@ -146,9 +143,7 @@ def test_ffn_bf16_decode_small(orc, B):
     h = torch.empty((B, 1024), dtype=torch.bfloat16, device=dev())
     y = W.wide_ffn_masked(x, wg, wu, wd, m, 128, h_out=h)
     torch.cuda.synchronize()
-    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, 128, round_bf16=True)
-    assert_close(h, rh, what="h")
-    assert_close(y, ry, what="y", abs_allow=ffn_flip_allowance(rh, synth.as_f32(c.w_down)))
+    check_ffn(orc, c, y, h)
 
 
 def test_ffn_decode_equals_prefill_rows(orc):
@@ -160,10 +155,8 @@ def test_ffn_decode_equals_prefill_rows(orc):
     y_pre = W.wide_ffn_masked(x, wg, wu, wd, m, 128)
     y_dec = W.wide_ffn_masked(x[:16].contiguous(), wg, wu, wd, m[:16].contiguous(), 128)
     torch.cuda.synchronize()
-    rh, ry = orc.ffn(c.x[:16], c.w_gate, c.w_up, c.w_down, c.mask[:16], 128, round_bf16=True)
-    tol = ffn_flip_allowance(rh, synth.as_f32(c.w_down))
-    assert_close(y_pre[:16], ry, what="prefill rows", abs_allow=tol)
-    assert_close(y_dec, ry, what="decode rows", abs_allow=tol)
+    check_ffn(orc, c, y_pre, rows=np.arange(16), what="prefill rows")
+    check_ffn(orc, dataclasses.replace(c, x=c.x[:16], mask=c.mask[:16]), y_dec, what="decode rows")
 
 
 @pytest.mark.parametrize("kind", ["zeros", "ones"])
@@ -181,9 +174,7 @@ def test_ffn_degenerate_masks(orc, kind, M):
         assert not to_np64(y).any() and not to_np64(h).any()
         assert not torch.signbit(y.float()).any()
     else:
-        rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, G, round_bf16=True)
-        assert_close(h, rh, what="h")
-        assert_close(y, ry, what="y")
+        check_ffn(orc, c, y, h)
 
 
 def test_ffn_m_zero_is_noop():
@@ -212,10 +203,8 @@ def test_ffn_poisoned_unused_groups(orc, M, kpath):
     y1 = W.wide_ffn_masked(x, wg, wu, wd, m, 128)
     torch.cuda.synchronize()
     assert torch.isfinite(y1.float()).all()
-    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, 128, round_bf16=True)
-    tol = ffn_flip_allowance(rh, synth.as_f32(c.w_down))
-    assert_close(y0, ry, what="clean", abs_allow=tol)
-    assert_close(y1, ry, what="poisoned", abs_allow=tol)
+    check_ffn(orc, c, y0, what="clean")
+    check_ffn(orc, c, y1, what="poisoned")
 
 
 def test_ffn_reuses_given_reorder(orc):
@@ -238,9 +227,7 @@ def test_ffn_bf16_prefill_full_llama7b_sampled(orc, keep):
     y = W.wide_ffn_masked(x, wg, wu, wd, m, 128)
     torch.cuda.synchronize()
     rows = np.unique(np.concatenate([[0, 4095], synth.rng(0).integers(0, 4096, 14)]))
-    rh, ry = orc.ffn(c.x[rows], c.w_gate, c.w_up, c.w_down, c.mask[rows], 128, round_bf16=True)
-    assert_close(y[torch.from_numpy(rows).to(dev())], ry, what="sampled rows",
-                 abs_allow=ffn_flip_allowance(rh, synth.as_f32(c.w_down)))
+    check_ffn(orc, c, y, rows=rows, what="sampled rows")
 
 
 @pytest.mark.parametrize("B", [1, 4, 16, 64])
@@ -250,10 +237,7 @@ def test_ffn_bf16_decode_full_llama7b(orc, B):
     x, wg, wu, wd, m = ffn_dev(c)
     y = W.wide_ffn_masked(x, wg, wu, wd, m, 128)
     torch.cuda.synchronize()
-    rows = np.arange(B) if B <= 16 else np.unique(synth.rng(1).integers(0, B, 16))
-    rh, ry = orc.ffn(c.x[rows], c.w_gate, c.w_up, c.w_down, c.mask[rows], 128, round_bf16=True)
-    assert_close(y[torch.from_numpy(rows).to(dev())], ry, what="decode rows",
-                 abs_allow=ffn_flip_allowance(rh, synth.as_f32(c.w_down)))
+    check_ffn(orc, c, y, what="decode rows")
 
 
 # ------------------------------------------------------------------ FFN fp32
@@ -283,11 +267,16 @@ def check_qkvo(orc, c, kind="bf16", kpath=0):
                                  w_q=d["w_q"], w_k=d["w_k"], w_v=d["w_v"])
     y = W.wide_qkvo_masked(W.PHASE_O, d["a"], d["mask"], c.G, c.n_q, c.n_kv, c.hd, w_o=d["w_o"])
     torch.cuda.synchronize()
-    rnd = kind == "bf16"
-    assert_close(q, orc.nproj(c.x, c.w_q, c.mask, c.G, round_bf16=rnd), kind, "q")
-    assert_close(k, orc.linear(c.x, c.w_k, round_bf16=rnd), kind, "k")
-    assert_close(v, orc.linear(c.x, c.w_v, round_bf16=rnd), kind, "v")
-    assert_close(y, orc.kproj(c.a, c.w_o, c.mask, c.G, round_bf16=rnd), kind, "o")
+    if kind == "bf16":
+        check_nproj(orc, c.x, c.w_q, c.mask, c.G, q, what="q")
+        check_nproj(orc, c.x, c.w_k, None, 0, k, what="k")
+        check_nproj(orc, c.x, c.w_v, None, 0, v, what="v")
+        check_kproj(orc, c.a, c.w_o, c.mask, c.G, y, what="o")
+        return
+    assert_close(q, orc.nproj(c.x, c.w_q, c.mask, c.G), kind, "q")
+    assert_close(k, orc.linear(c.x, c.w_k), kind, "k")
+    assert_close(v, orc.linear(c.x, c.w_v), kind, "v")
+    assert_close(y, orc.kproj(c.a, c.w_o, c.mask, c.G), kind, "o")
 
 
 @pytest.mark.parametrize("big", [1, 0])
@@ -319,7 +308,7 @@ def test_o_poisoned_inactive_blocks(orc):
         a[inactive] = float("nan")
         y = W.wide_qkvo_masked(W.PHASE_O, a, d["mask"], c.G, 8, 2, 128, w_o=d["w_o"])
         torch.cuda.synchronize()
-        assert_close(y, orc.kproj(c.a, c.w_o, c.mask, c.G, round_bf16=True), what="o poisoned")
+        check_kproj(orc, c.a, c.w_o, c.mask, c.G, y, what="o poisoned")
 
 
 @pytest.mark.parametrize("name", ["attn_proj_mha", "layer_llama3_8b"])
@@ -335,10 +324,10 @@ def test_qkvo_bf16_full_sampled(orc, name):
     y = W.wide_qkvo_masked(W.PHASE_O, d["a"], d["mask"], c.G, c.n_q, c.n_kv, c.hd, w_o=d["w_o"])
     torch.cuda.synchronize()
     rows = np.unique(np.concatenate([[0, M - 1], synth.rng(2).integers(0, M, 10)]))
-    r = torch.from_numpy(rows).to(dev())
-    assert_close(q[r], orc.nproj(c.x[rows], c.w_q, c.mask[rows], c.G, round_bf16=True), what="q")
-    assert_close(k[r], orc.linear(c.x[rows], c.w_k, round_bf16=True), what="k")
-    assert_close(y[r], orc.kproj(c.a[rows], c.w_o, c.mask[rows], c.G, round_bf16=True), what="o")
+    check_nproj(orc, c.x, c.w_q, c.mask, c.G, q, rows=rows, what="q")
+    check_nproj(orc, c.x, c.w_k, None, 0, k, rows=rows, what="k")
+    check_nproj(orc, c.x, c.w_v, None, 0, v, rows=rows, what="v")
+    check_kproj(orc, c.a, c.w_o, c.mask, c.G, y, rows=rows, what="o")
 
 
 # ------------------------------------------------------------------ graphs
@@ -383,8 +372,7 @@ def test_calls_replay_in_hip_graph(orc, M):
         torch.cuda.synchronize()
         for got, want in zip((y, q, kk, vv, yo), ref):
             assert torch.equal(got, want)
-    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, 128, round_bf16=True)
-    assert_close(y, ry, what="y", abs_allow=ffn_flip_allowance(rh, synth.as_f32(c.w_down)))
+    check_ffn(orc, c, y)
 
 
 # ------------------------------------------------------------------ errors, timing
@@ -499,10 +487,8 @@ def test_ffn_single_group_m_axis(orc, M, big, decode):
     h = torch.empty((M, Dff), dtype=torch.bfloat16, device=dev())
     y = W.wide_ffn_masked(x, wg, wu, wd, m, Dff, h_out=h)
     torch.cuda.synchronize()
-    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, Dff, round_bf16=True)
     assert 0 < c.mask.mean() < 1
-    assert_close(h, rh, what="h")
-    assert_close(y, ry, what="y", abs_allow=ffn_flip_allowance(rh, synth.as_f32(c.w_down)))
+    check_ffn(orc, c, y, h)
     yn = to_np64(y)
     assert not yn[c.mask[:, 0] == 0].any()
 
@@ -543,8 +529,7 @@ def test_o_pattern_order_is_bitwise_same(orc, M, n_q, n_kv, G, kind):
     torch.cuda.synchronize()
     assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
     rows = np.arange(M) if M <= 1000 else np.sort(synth.rng(M).choice(M, 64, replace=False))
-    assert_close(outs[0][torch.as_tensor(rows, device=outs[0].device)],
-                 orc.kproj(c.a[rows], c.w_o, c.mask[rows], G, round_bf16=True), what="o")
+    check_kproj(orc, c.a, c.w_o, c.mask, G, outs[0], rows=rows, what="o")
 
 
 def _edge_count_mask(g, M, ng):
@@ -575,9 +560,7 @@ def test_ffn_tile_order_edge_counts(orc, M, ng, order):
     y = W.wide_ffn_masked(x, wg, wu, wd, m, G, h_out=h)
     y2 = W.wide_ffn_masked(x, wg, wu, wd, m, G)  # H kept in the workspace
     torch.cuda.synchronize()
-    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, G, round_bf16=True)
-    assert_close(h, rh, what="h")
-    assert_close(y, ry, what="y", abs_allow=ffn_flip_allowance(rh, synth.as_f32(c.w_down)))
+    check_ffn(orc, c, y, h)
     assert torch.equal(y.view(torch.int16), y2.view(torch.int16))
 
 
@@ -606,8 +589,7 @@ def test_ffn_kd256_group_counts(orc, Dff):
     x, wg, wu, wd, m = ffn_dev(c)
     y = W.wide_ffn_masked(x, wg, wu, wd, m, G)
     torch.cuda.synchronize()
-    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, G, round_bf16=True)
-    assert_close(y, ry, what="y", abs_allow=ffn_flip_allowance(rh, synth.as_f32(c.w_down)))
+    check_ffn(orc, c, y)
 
 
 @pytest.mark.parametrize("M,D,Dff", [(1000, 256, 2048), (3000, 512, 4096), (300, 256, 1024)])
@@ -620,14 +602,12 @@ def test_ffn_tail_split_matches(orc, M, D, Dff):
     G = 128
     c = synth.ffn_case(M + D, M, D, Dff, G, mask="topk")
     x, wg, wu, wd, m = ffn_dev(c)
-    rh, ry = orc.ffn(c.x, c.w_gate, c.w_up, c.w_down, c.mask, G, round_bf16=True)
     for tail in (1, 0):
         W.wide_set_option("mn_tail", tail)
         h = torch.full((M, Dff), 7.0, dtype=torch.bfloat16, device=dev())
         y = W.wide_ffn_masked(x, wg, wu, wd, m, G, h_out=h)
         torch.cuda.synchronize()
-        assert_close(h, rh, what=f"h tail={tail}")
-        assert_close(y, ry, what=f"y tail={tail}", abs_allow=ffn_flip_allowance(rh, synth.as_f32(c.w_down)))
+        check_ffn(orc, c, y, h, what=f"tail={tail}")
     W.wide_set_option("mn_tail", 1)
 
 
