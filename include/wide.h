@@ -127,6 +127,34 @@ wide_status_t wide_ffn_masked(wide_dtype_t dt, int64_t M, int32_t d_model,
                               void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * wide_ffn_masked without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments, semantics and errors as
+ * wide_ffn_masked minus ws/ws_bytes; the scratch it needs (the reorder, H
+ * when h_out is NULL, the K-axis scratch) lives in a device array inside the
+ * library of wide_static_scratch_bytes() bytes (32 MiB) per GPU, held from the
+ * first call on that GPU until the process ends.  A call needing more scratch
+ * than that (wide_workspace_size(WIDE_OP_FFN, ...) > 32 MiB, e.g. a long
+ * prefill with h_out NULL) returns WIDE_ERR_WORKSPACE before enqueuing
+ * anything.  Nothing is allocated and no library routine that allocates is
+ * called.  The first call on a device looks up the array's address on that
+ * device (make it outside graph capture, with that device current).
+ * Every call on one GPU shares that GPU's scratch: calls that overlap on one
+ * GPU (concurrent streams, other host threads) race and must be ordered by
+ * the caller (e.g. issued on one stream).
+ */
+wide_status_t wide_ffn_masked_noalloc(wide_dtype_t dt, int64_t M, int32_t d_model,
+                                      int32_t d_ff, int32_t group_size,
+                                      const uint8_t* mask, const int32_t* idx,
+                                      const int32_t* counts, const void* x,
+                                      const void* w_gate, const void* w_up,
+                                      const void* w_down, void* h_out, void* y,
+                                      hipStream_t stream);
+
+/* Bytes of the per-GPU scratch of wide_ffn_masked_noalloc (32 MiB). */
+size_t wide_static_scratch_bytes(void);
+
+/*
  * Head-group masked attention projections (WIDE Section 3.1, equations
  * (1)-(2) and Figure 1): W_q is pruned over its out-features and W_o over its
  * in-features in groups of G = group_size features (whole heads, contiguous:

@@ -16,7 +16,7 @@ __all__ = [
     "WideError", "lib", "wide_mask_reorder", "wide_ffn_masked", "wide_qkvo_masked", "wide_router",
     "wide_attention_masked", "wide_attention_workspace_size", "wide_attention_decode",
     "wide_attention_decode_workspace_size", "wide_workspace_size", "wide_set_option", "wide_get_option", "wide_timing_enable",
-    "wide_timing_reset", "wide_timing_query", "LIB_PATH",
+    "wide_timing_reset", "wide_timing_query", "wide_ffn_masked_noalloc", "wide_static_scratch_bytes", "LIB_PATH",
     "OP_REORDER", "OP_FFN", "OP_QKV", "OP_O", "OP_ROUTER", "PHASE_QKV", "PHASE_O", "F32", "BF16",
 ]
 
@@ -53,6 +53,10 @@ def lib() -> ctypes.CDLL:
         L.wide_ffn_masked.restype = ci
         L.wide_ffn_masked.argtypes = [ci, i64, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                       vp, sz, vp]
+        L.wide_ffn_masked_noalloc.restype = ci
+        L.wide_ffn_masked_noalloc.argtypes = [ci, i64, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.wide_static_scratch_bytes.restype = sz
+        L.wide_static_scratch_bytes.argtypes = []
         L.wide_qkvo_masked.restype = ci
         L.wide_qkvo_masked.argtypes = [ci, ci, i64, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp,
                                        vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
@@ -210,6 +214,27 @@ def wide_ffn_masked(x, w_gate, w_up, w_down, mask, group_size, idx=None, counts=
         dt, M, D, Dff, group_size, _p(mask), _p(idx), _p(counts), _p(x), _p(w_gate), _p(w_up),
         _p(w_down), _p(h_out), _p(y), _p(ws), nbytes, _stream(x)))
     return y
+
+
+def wide_ffn_masked_noalloc(x, w_gate, w_up, w_down, mask, group_size, idx=None, counts=None,
+                            h_out=None, y=None):
+    """wide_ffn_masked with the library's static per-GPU scratch instead of a
+    workspace (for callers that cannot allocate: pass y, and h_out for long
+    prefills, and the call allocates nothing)."""
+    torch = _torch()
+    mask = _mask_bytes(mask)
+    _contig(x, w_gate, w_up, w_down, mask, idx, counts, h_out, y)
+    M, D = x.shape
+    if y is None:
+        y = torch.empty((M, D), dtype=x.dtype, device=x.device)
+    _check("wide_ffn_masked_noalloc", lib().wide_ffn_masked_noalloc(
+        _dtype_code(x), M, D, w_gate.shape[0], group_size, _p(mask), _p(idx), _p(counts), _p(x), _p(w_gate),
+        _p(w_up), _p(w_down), _p(h_out), _p(y), _stream(x)))
+    return y
+
+
+def wide_static_scratch_bytes() -> int:
+    return int(lib().wide_static_scratch_bytes())
 
 
 def wide_qkvo_masked(phase, inp, mask, group_size, n_q_heads, n_kv_heads, head_dim,

@@ -754,6 +754,60 @@ wide_status_t wide_ffn_masked(wide_dtype_t dt, int64_t M, int32_t d_model, int32
   return ok();
 }
 
+// ---- allocation-free FFN ------------------------------------------------------------
+// For callers that cannot allocate (graph capture, serving loops): the
+// workspace of wide_ffn_masked lives in a file-scope device array instead of
+// the caller's buffer.  Host code never uses the array's name as an address
+// (it is a host-side stand-in there): each device's address comes from
+// hipGetSymbolAddress, looked up once per device with that device current.
+namespace {
+constexpr size_t kStaticScratchBytes = size_t(32) << 20;
+__device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};  // device address of `scratch`, per device
+
+wide_status_t scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(WIDE_ERR_UNSUPPORTED, "device ordinal %d out of range", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(WIDE_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return WIDE_OK;
+}
+}  // namespace
+
+size_t wide_static_scratch_bytes(void) { return kStaticScratchBytes; }
+
+wide_status_t wide_ffn_masked_noalloc(wide_dtype_t dt, int64_t M, int32_t d_model, int32_t d_ff,
+                                      int32_t group_size, const uint8_t* mask, const int32_t* idx,
+                                      const int32_t* counts, const void* x, const void* w_gate, const void* w_up,
+                                      const void* w_down, void* h_out, void* y, hipStream_t stream) {
+  CHECK(ffn_shape(dt, M, d_model, d_ff, group_size));
+  if ((idx == nullptr) != (counts == nullptr))
+    return fail(WIDE_ERR_INVALID_ARG, "idx and counts must both be given or both be NULL");
+  const size_t need = ffn_ws_bytes(dt, M, d_model, d_ff, group_size, idx == nullptr, h_out == nullptr,
+                                   k_path_for(group_size));
+  if (need > kStaticScratchBytes)
+    return fail(WIDE_ERR_WORKSPACE,
+                "this call needs %zu bytes of scratch; the static scratch holds %zu (pass h_out, or use "
+                "wide_ffn_masked with a workspace)", need, kStaticScratchBytes);
+  if (M == 0) return wide_ffn_masked(dt, M, d_model, d_ff, group_size, mask, idx, counts, x, w_gate, w_up,
+                                     w_down, h_out, y, nullptr, 0, stream);
+  void* ws = nullptr;
+  if (need) CHECK(scratch_address(&ws));
+  return wide_ffn_masked(dt, M, d_model, d_ff, group_size, mask, idx, counts, x, w_gate, w_up, w_down, h_out, y,
+                         ws, need ? kStaticScratchBytes : 0, stream);
+}
+
 wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M, int32_t d_model,
                                int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
                                int32_t group_size, const uint8_t* mask, const int32_t* idx,

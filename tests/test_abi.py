@@ -271,3 +271,14 @@ def test_attention_workspace_holds_the_key_split_only_where_it_can_run():
         assert W.wide_attention_workspace_size(1, 256, 256, n_q, n_kv, hd, G, False) == short
     finally:
         W.wide_set_option("attn_split", 1024)
+
+
+def test_noalloc_refuses_sizes_beyond_its_scratch_before_any_device_call():
+    """The allocation-free FFN checks its scratch need on the host first: a
+    prefill whose H would have to sit in the 32 MiB array is refused."""
+    L = W.lib()
+    assert L.wide_static_scratch_bytes() == 32 << 20
+    st = L.wide_ffn_masked_noalloc(W.BF16, 8192, 4096, 14336, 128, A, None, None, A, A, A, A, None, A, None)
+    assert st == W.ERR_WORKSPACE and "static scratch" in err()
+    st = L.wide_ffn_masked_noalloc(W.BF16, 8, 4096, 14336, 48, A, None, None, A, A, A, A, None, A, None)
+    assert st == W.ERR_INVALID_ARG and "power of two" in err()
