@@ -115,6 +115,7 @@ class Layer:
         self.Nq, self.Nkv = self.nq * self.hd, self.nkv * self.hd
         self.ng, self.nga = self.Dff // self.G, self.Nq // self.Ga
         g = synth.rng(seed)
+        self.keep = keep
         D, Dff, Nq, Nkv = self.D, self.Dff, self.Nq, self.Nkv
         n = synth.normal
         self.w = None
@@ -166,6 +167,51 @@ class Layer:
         ffn = 2 * (3 * uf * self.G * D)
         dense = 2 * D * (2 * self.Nq + 2 * self.Nkv + 3 * self.Dff)
         return int(attn + ffn), int(dense), int(ua), int(uf)
+
+
+def host_info():
+    """CPU model and core counts of the host (the oracle's baseline runs here)."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return dict(cpu_model=model, nproc=os.cpu_count(), usable_cores=len(os.sched_getaffinity(0)))
+
+
+def cpu_one_core(L, n_rows):
+    """The oracle on one core (a child process with OMP_NUM_THREADS=1): the
+    first n_rows prefill tokens through the layer's projections."""
+    import subprocess
+    code = (
+        "import sys, time, numpy as np\n"
+        f"sys.path.insert(0, {ROOT!r})\n"
+        "import bench, oracle\n"
+        f"L = bench.Layer(5, {L.batches['prefill']['x_attn'].shape[0]}, {L.batches['decode']['x_attn'].shape[0]}, "
+        f"{float(L.keep)})\n"
+        f"r = np.arange({n_rows}); b = L.batches['prefill']\n"
+        "t = time.time()\n"
+        "oracle.nproj(b['x_attn'][r], L.w['w_q'], b['mask_attn'][r], L.Ga, round_bf16=True)\n"
+        "oracle.linear(b['x_attn'][r], L.w['w_k'], round_bf16=True)\n"
+        "oracle.linear(b['x_attn'][r], L.w['w_v'], round_bf16=True)\n"
+        "oracle.kproj(b['a'][r], L.w['w_o'], b['mask_attn'][r], L.Ga, round_bf16=True)\n"
+        "oracle.ffn(b['x_ffn'][r], L.w['w_gate'], L.w['w_up'], L.w['w_down'], b['mask_ffn'][r], L.G, "
+        "round_bf16=True, want_h=False)\n"
+        "dt = time.time() - t\n"
+        "print(dt, L.active_flops('prefill', r)['total'], oracle.num_threads())\n")
+    env = dict(os.environ, OMP_NUM_THREADS="1", HIP_VISIBLE_DEVICES="", ROCR_VISIBLE_DEVICES="")
+    try:
+        out = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=600)
+        dt, fl, nt = out.stdout.split()[-3:]
+        dt, fl = float(dt), float(fl)
+        return dict(value=round(fl / dt / 1e12, 7), unit="TFLOP/s", cores=int(nt), seconds=round(dt, 2),
+                    sample=f"the first {n_rows} prefill tokens, same projections")
+    except Exception as e:  # the baseline is context: report why it is missing
+        return dict(error=str(e)[:200])
 
 
 def main():
@@ -515,24 +561,36 @@ def main():
         def rnd(*shape, std=0.02):
             return (torch.randn(*shape, device=dev, generator=gen) * std).to(torch.bfloat16)
 
-        wg7, wu7, wd7 = rnd(F7, D7), rnd(F7, D7), rnd(D7, F7)
+        # Four weight copies (1.08 GB), one call on each per graph replay: no
+        # call finds its weights in the 256 MB last-level cache, so every
+        # figure is an HBM figure.
+        n_copies = 4
+        w7 = [(rnd(F7, D7), rnd(F7, D7), rnd(D7, F7)) for _ in range(n_copies)]
         dec_rows = []
         for bq in (1, 4, 16, 64):
             mk = synth.mask_beta_groups(synth.rng(100 + bq), bq, F7 // G7, 0.5)
             xq, mq = rnd(bq, D7, std=1.0), to_dev(mk)
+            ones_q = torch.ones_like(mq)
             yq = torch.empty(bq, D7, dtype=torch.bfloat16, device=dev)
             wsq = torch.empty(max(W.wide_workspace_size(W.OP_FFN, W.BF16, bq, D7, F7, G7), 256),
                               dtype=torch.uint8, device=dev)
-            t_w = graph_ms(lambda: W.wide_ffn_masked(xq, wg7, wu7, wd7, mq, G7, y=yq, ws=wsq))
-            t_d = graph_ms(lambda: F.linear(F.silu(F.linear(xq, wg7)) * F.linear(xq, wu7), wd7))
+
+            def rot(call):
+                return lambda: [call(*wc) for wc in w7]
+
+            t_w = graph_ms(rot(lambda g_, u_, d_: W.wide_ffn_masked(xq, g_, u_, d_, mq, G7, y=yq, ws=wsq))) / n_copies
+            t_d = graph_ms(rot(lambda g_, u_, d_: F.linear(F.silu(F.linear(xq, g_)) * F.linear(xq, u_), d_))) / n_copies
+            t_1 = graph_ms(rot(lambda g_, u_, d_: W.wide_ffn_masked(xq, g_, u_, d_, ones_q, G7, y=yq, ws=wsq))) / n_copies
             u = int(mk.any(0).sum())
             ub = 3 * u * G7 * D7 * 2
-            dec_rows.append(dict(batch=bq, ms=round(t_w, 4), hipblaslt_ms=round(t_d, 4), union_groups=u,
-                                 union_bytes=ub, GBps=round(ub / (t_w * 1e-3) / 1e9, 1),
+            ideal = (F7 // G7) / u
+            best = min(t_d, t_1)
+            dec_rows.append(dict(batch=bq, ms=round(t_w, 4), hipblaslt_ms=round(t_d, 4), ones_mask_ms=round(t_1, 4),
+                                 union_groups=u, union_bytes=ub, GBps=round(ub / (t_w * 1e-3) / 1e9, 1),
                                  frac_hbm=round(ub / (t_w * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
-                                 speedup_vs_dense=round(t_d / t_w, 3),
-                                 ideal_speedup=round((F7 // G7) / u, 3)))
-        del wg7, wu7, wd7
+                                 speedup_vs_dense=round(best / t_w, 3), ideal_speedup=round(ideal, 3),
+                                 frac_of_ideal=round(best / t_w / ideal, 3), weight_copies=n_copies))
+        del w7
         # prefill of the layer at other keep fractions (same tokens, new top-k masks)
         pre_rows = []
         bp = L.batches["prefill"]
@@ -919,10 +977,12 @@ def main():
                    L.G, round_bf16=True, want_h=False)
         dt = time.time() - t1
         fl = L.active_flops("prefill", rows)["total"]
+        one = cpu_one_core(L, 64)
         cpu = dict(value=round(fl / dt / 1e12, 6), unit="TFLOP/s", cores=oracle.num_threads(),
                    kind="oracle", seconds=round(dt, 2),
                    sample=f"the full layer's projections (Q, K, V, O, gate/up, down) for the first "
-                          f"{len(rows)} of the {args.prefill_tokens} prefill tokens, fp64, same inputs")
+                          f"{len(rows)} of the {args.prefill_tokens} prefill tokens, fp64, same inputs",
+                   host=host_info(), one_core=one)
 
     out = {
         "metric": "speedup vs dense at 50% sparsity; prefill TFLOP/s, decode HBM GB/s",

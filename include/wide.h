@@ -345,6 +345,10 @@ size_t wide_workspace_size(wide_op_t op, wide_dtype_t dt, int64_t M,
  *                   three small kernels order the tokens by mask pattern so a
  *                   tile skips every group none of its rows uses; 0 keeps
  *                   token order.  Outputs are bitwise equal either way.
+ *   "ks_pack"       scatter schedule on 256x256 tiles: K-groups one workgroup
+ *                   runs in turn (Appendix B, Algorithm 3's outer loop; default
+ *                   1); the column tiles are dealt so that all adds into one
+ *                   256-column slab come from one XCD.
  *   "big_tiles"     1 (default): prefill GEMMs use 256x256 tiles where the
  *                   shape allows; 0: always the 128x128 tiles.
  *   "ring_bk"       k depth of a 256x256 pipeline stage: 64 (two stages,

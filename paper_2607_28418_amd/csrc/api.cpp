@@ -49,6 +49,7 @@ int g_big_tiles = 1;          // 1: 256x256 tile kernels where the shape allows
 int g_mn_tail = 1;            // 1: 256-tile N-axis launches split each XCD's last partial round along k
 int g_mn_order = 3;           // bit 0: Q/K/V launch K and V before Q; bit 1: full tiles before partial ones
 int g_kd_pattern = 1;         // 1: dense-masked K axis reads rows in mask-pattern order (<= 8 groups)
+int g_ks_pack = 1;            // scatter K axis (256 tiles): K-groups per workgroup
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
@@ -354,6 +355,7 @@ wide_status_t run_kaxis(const uint16_t* a, const uint16_t* w, const uint8_t* mas
   ka.K = K;
   ka.N = N;
   ka.G = G;
+  ka.pack = g_ks_pack;
   hipError_t e;
   const bool big = g_big_tiles && N % wide::kT256 == 0;
   if (kaxis_row_gathered(K, N, G)) {
@@ -484,6 +486,11 @@ wide_status_t wide_set_option(const char* key, int64_t value) {
     g_mn_order = (int)value;
     return ok();
   }
+  if (!strcmp(key, "ks_pack")) {
+    if (value < 1 || value > 4096) return fail(WIDE_ERR_INVALID_ARG, "ks_pack must be 1..4096");
+    g_ks_pack = (int)value;
+    return ok();
+  }
   if (!strcmp(key, "kd_pattern")) {
     if (value < 0 || value > 1) return fail(WIDE_ERR_INVALID_ARG, "kd_pattern must be 0 or 1");
     g_kd_pattern = (int)value;
@@ -519,6 +526,7 @@ wide_status_t wide_get_option(const char* key, int64_t* value) {
   else if (!strcmp(key, "gemv_k_ncb")) *value = wide::decode_tuning().k_ncb;
   else if (!strcmp(key, "gemv_k_split")) *value = wide::decode_tuning().k_split;
   else if (!strcmp(key, "kd_pattern")) *value = g_kd_pattern;
+  else if (!strcmp(key, "ks_pack")) *value = g_ks_pack;
   else if (!strcmp(key, "mn_order")) *value = g_mn_order;
   else if (!strcmp(key, "mn_tail")) *value = g_mn_tail;
   else if (!strcmp(key, "attn_qb")) *value = wide::g_attn_qb;

@@ -595,6 +595,12 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
 }
 
 // -------------------------------------------------------------- K-axis, scatter
+// One workgroup owns (sorted-position tile, 256 output columns, a run of
+// a.pack K-groups) and runs the groups in turn, each with its own pipeline
+// prologue and accumulator (Appendix B, Algorithm 3 and its outer loop that
+// packs K-groups into one CTA).  When the column tiles divide among the 8
+// XCDs, workgroup ids are dealt so that every workgroup adding into a column
+// slab runs on the same XCD.
 template <int BK>
 __global__ __launch_bounds__(NT, 1) void wide_ks256(KArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
@@ -603,62 +609,75 @@ __global__ __launch_bounds__(NT, 1) void wide_ks256(KArgs a) {
   const uint16_t* zero = g_zero_blk;
   const int n_tiles = a.N / BN;
   const int m_tiles = (int)((a.M + BM - 1) / BM);
-  const int tile = xcd_remap(blockIdx.x, gridDim.x);
-  const int n_tile = tile % n_tiles;
-  const int m_tile = (tile / n_tiles) % m_tiles;
-  const int g = tile / (n_tiles * m_tiles);
-  const int64_t cnt = a.cnt[g];
-  const int64_t m0 = (int64_t)m_tile * BM;
-  if (m0 >= cnt) return;  // l = 0
-  const int n0 = n_tile * BN;
-  const int32_t* rows = a.idx + (int64_t)g * a.M;
-
-  const uint16_t* abase[S];
-  const uint16_t* bbase[S];
-#pragma unroll
-  for (int j = 0; j < S; ++j) {
-    const int rr = Rg::slot_row(j);
-    const int c8 = Rg::slot_chunk(j) * 8;
-    const int64_t p = m0 + rr;
-    abase[j] = p < cnt ? a.a + (int64_t)rows[p] * a.K + c8 : nullptr;  // l = 1
-    bbase[j] = a.w + (int64_t)(n0 + rr) * a.K + c8;
+  const int ng = a.K / a.G;
+  const int n_splits = (ng + a.pack - 1) / a.pack;
+  int n_tile, m_tile, split;
+  if (n_tiles % 8 == 0) {  // column slab of the workgroup's XCD (dispatch is round-robin over XCDs)
+    const int xcd = blockIdx.x % 8, local = blockIdx.x / 8, per = n_tiles / 8;
+    n_tile = xcd * per + local % per;
+    m_tile = (local / per) % m_tiles;
+    split = local / per / m_tiles;
+  } else {
+    const int tile = xcd_remap(blockIdx.x, gridDim.x);
+    n_tile = tile % n_tiles;
+    m_tile = (tile / n_tiles) % m_tiles;
+    split = tile / (n_tiles * m_tiles);
   }
+  if (split >= n_splits) return;
+  const int g_end = min(ng, (split + 1) * a.pack);
+  const int64_t m0 = (int64_t)m_tile * BM;
+  const int n0 = n_tile * BN;
   const int lane = lane_id(), w = wave_id();
   const int wm = w >> 2, wn = w & 3;
   const int l32 = lane & 31;
   const int brow0 = wn * 64 + l32, brow1 = wn * 64 + 32 + l32;
-  int live = 0;  // l = 2
-#pragma unroll
-  for (int fm = 0; fm < 4; ++fm)
-    if (m0 + wm * 128 + fm * 32 < cnt) live |= 1 << fm;
-
-  f32x16 acc[4][2];
-  zero_acc(acc);
-  const int kbeg = g * a.G;
-  auto src = [&](int s, const uint16_t* (&ap)[S], const uint16_t* (&bp)[S]) {
-    const int k0 = kbeg + s * BK;
+  const int col = acc_col();
+  const int* map = reinterpret_cast<const int*>(smem);
+  for (int g = split * a.pack; g < g_end; ++g) {
+    const int64_t cnt = a.cnt[g];
+    if (m0 >= cnt) continue;  // l = 0 for this group
+    const int32_t* rows = a.idx + (int64_t)g * a.M;
+    const uint16_t* abase[S];
+    const uint16_t* bbase[S];
 #pragma unroll
     for (int j = 0; j < S; ++j) {
-      ap[j] = abase[j] ? abase[j] + k0 : zero;
-      bp[j] = bbase[j] + k0;
+      const int rr = Rg::slot_row(j);
+      const int c8 = Rg::slot_chunk(j) * 8;
+      const int64_t p = m0 + rr;
+      abase[j] = p < cnt ? a.a + (int64_t)rows[p] * a.K + c8 : nullptr;  // l = 1
+      bbase[j] = a.w + (int64_t)(n0 + rr) * a.K + c8;
     }
-  };
-  int my_row = -1;
-  if ((int)threadIdx.x < BM && m0 + (int)threadIdx.x < cnt) my_row = rows[m0 + threadIdx.x];
-  run_tile<Rg>(smem, a.G / BK, src, brow0, brow1, live, acc);
-
-  const int* map = stage_row_map(smem, my_row);
-  const int col = acc_col();
+    int live = 0;  // l = 2
 #pragma unroll
-  for (int fm = 0; fm < 4; ++fm) {
-    if (!(live & (1 << fm))) continue;
+    for (int fm = 0; fm < 4; ++fm)
+      if (m0 + wm * 128 + fm * 32 < cnt) live |= 1 << fm;
+    f32x16 acc[4][2];
+    zero_acc(acc);
+    const int kbeg = g * a.G;
+    auto src = [&](int s, const uint16_t* (&ap)[S], const uint16_t* (&bp)[S]) {
+      const int k0 = kbeg + s * BK;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int t = map[acc_row(fm, i)];
-      if (t < 0) continue;
-      float* o = a.acc32 + (int64_t)t * a.N + n0 + wn * 64;
-      unsafeAtomicAdd(o + col, acc[fm][0][i]);
-      unsafeAtomicAdd(o + 32 + col, acc[fm][1][i]);
+      for (int j = 0; j < S; ++j) {
+        ap[j] = abase[j] ? abase[j] + k0 : zero;
+        bp[j] = bbase[j] + k0;
+      }
+    };
+    int my_row = -1;
+    if ((int)threadIdx.x < BM && m0 + (int)threadIdx.x < cnt) my_row = rows[m0 + threadIdx.x];
+    __syncthreads();  // the previous group's epilogue is done with the row map in the ring
+    run_tile<Rg>(smem, a.G / BK, src, brow0, brow1, live, acc);
+    stage_row_map(smem, my_row);
+#pragma unroll
+    for (int fm = 0; fm < 4; ++fm) {
+      if (!(live & (1 << fm))) continue;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int t = map[acc_row(fm, i)];
+        if (t < 0) continue;
+        float* o = a.acc32 + (int64_t)t * a.N + n0 + wn * 64;
+        unsafeAtomicAdd(o + col, acc[fm][0][i]);
+        unsafeAtomicAdd(o + 32 + col, acc[fm][1][i]);
+      }
     }
   }
 }
@@ -747,7 +766,9 @@ hipError_t launch_kd256(const KArgs& a, hipStream_t s) {
 
 hipError_t launch_ks256(const KArgs& a, hipStream_t s) {
   const int64_t m_tiles = (a.M + BM - 1) / BM;
-  const int64_t total = (int64_t)(a.K / a.G) * m_tiles * (a.N / BN);
+  const int pack = a.pack > 0 ? a.pack : 1;
+  const int64_t splits = (a.K / a.G + pack - 1) / pack;
+  const int64_t total = splits * m_tiles * (a.N / BN);
   if (total == 0) return hipSuccess;
   WIDE_RING_LAUNCH("wide_ks256", KS, RingMN, (unsigned)total, s, a);
   return hipGetLastError();

@@ -67,6 +67,7 @@ struct KArgs {
   const int32_t* perm; // optional [M]: tile rows are tokens perm[m0 + r] (256-tile dense-masked)
   int64_t M;
   int K, N, G;
+  int pack;            // 256-tile scatter: K-groups run in turn by one workgroup (>= 1)
 };
 
 constexpr int kKTileM = 128;

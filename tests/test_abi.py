@@ -117,9 +117,9 @@ def test_options():
     with pytest.raises(W.WideError):
         W.wide_set_option("nope", 1)
     for key, default, bad in (("mn_order", 3, 4), ("kd_pattern", 1, 2), ("attn_qb", 1, 3), ("mn_tail", 1, 2),
-                               ("attn_split", 1024, 1025), ("attn_split_rounds", 1, 9)):
+                               ("attn_split", 1024, 1025), ("attn_split_rounds", 1, 9), ("ks_pack", 1, 0)):
         assert W.wide_get_option(key) == default
-        W.wide_set_option(key, {"attn_qb": 2, "attn_split_rounds": 3}.get(key, 0))
+        W.wide_set_option(key, {"attn_qb": 2, "attn_split_rounds": 3, "ks_pack": 4}.get(key, 0))
         with pytest.raises(W.WideError):
             W.wide_set_option(key, bad)
         W.wide_set_option(key, default)

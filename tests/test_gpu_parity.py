@@ -207,6 +207,25 @@ def test_ffn_poisoned_unused_groups(orc, M, kpath):
     check_ffn(orc, c, y1, what="poisoned")
 
 
+@pytest.mark.parametrize("pack", [3, 8])
+def test_ffn_scatter_packs_groups_per_workgroup(orc, pack):
+    """The atomic K-axis schedule with several K-groups run in turn by one
+    workgroup (Appendix B, Algorithm 3's outer loop); 11 groups, so the last
+    workgroup of a column tile gets fewer."""
+    say("ffn scatter pack", pack)
+    W.wide_set_option("decode_max_m", 0)
+    W.wide_set_option("k_path", 2)
+    W.wide_set_option("ks_pack", pack)
+    try:
+        c = synth.ffn_case(17 + pack, 700, 512, 11 * 128, 128, mask="topk")
+        x, wg, wu, wd, m = ffn_dev(c)
+        y = W.wide_ffn_masked(x, wg, wu, wd, m, 128)
+        torch.cuda.synchronize()
+        check_ffn(orc, c, y, what=f"pack {pack}")
+    finally:
+        W.wide_set_option("ks_pack", 1)
+
+
 def test_ffn_reuses_given_reorder(orc):
     say("ffn given idx")
     c = synth.ffn_case(5, 400, 256, 512, 128, mask="bernoulli")
