@@ -71,7 +71,7 @@ def _load():
         lib.oracle_kproj.argtypes = [ci, ci, i64, i32, i32, i32, vp, vp, vp, vp]
         lib.oracle_ffn.argtypes = [ci, ci, i64, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
         lib.oracle_router.argtypes = [ci, i64, i32, i32, i32, vp, vp, vp, vp, vp]
-        lib.oracle_attention.argtypes = [ci, ci, i64, i32, i32, i32, i32, i32, i32, ci, vp, vp, vp, vp, vp]
+        lib.oracle_attention.argtypes = [ci, ci, i64, i32, i32, i32, i32, i32, i32, ci, vp, vp, vp, vp, vp, vp]
         lib.oracle_num_threads.restype = ci
         _lib = lib
     return _lib
@@ -189,11 +189,12 @@ def router(x, w1, w2):
     return logits, mask
 
 
-def attention(q, k, v, mask, n_seq, n_q, n_kv, d, causal, round_bf16=False):
+def attention(q, k, v, mask, n_seq, n_q, n_kv, d, causal, round_bf16=False, leftpad=None):
     """Head-group masked attention (prefill).  q [n_seq*T_q][n_q*d],
     k/v [n_seq*T_k][n_kv*d], mask [n_seq*T_q][n_groups]; with causal masking
-    the queries are the last T_q of each sequence's T_k positions.  Returns
-    o float64 [n_seq*T_q][n_q*d]."""
+    the queries are the last T_q of each sequence's T_k positions; leftpad
+    (optional int [n_seq]) hides keys j < leftpad[b] of sequence b (a query
+    left with no key gets zeros).  Returns o float64 [n_seq*T_q][n_q*d]."""
     dt, (q, k, v) = _same_dtype(q, k, v)
     mask = _mask(mask)
     Mq, Mk = q.shape[0], k.shape[0]
@@ -203,7 +204,11 @@ def attention(q, k, v, mask, n_seq, n_q, n_kv, d, causal, round_bf16=False):
     assert not causal or T_k >= T_q
     ng = mask.shape[1]
     assert mask.shape[0] == Mq and n_q % ng == 0 and n_q % n_kv == 0
+    lp = None
+    if leftpad is not None:
+        lp = np.ascontiguousarray(leftpad, dtype=np.int32)
+        assert lp.shape == (n_seq,) and (lp >= 0).all() and (lp <= T_k).all()
     o = np.empty((Mq, n_q * d), np.float64)
     _load().oracle_attention(dt, int(round_bf16), n_seq, T_q, T_k, n_q, n_kv, d, ng, int(causal),
-                             _p(mask), _p(q), _p(k), _p(v), _p(o))
+                             _p(mask), _p(q), _p(k), _p(v), _p(lp) if lp is not None else None, _p(o))
     return o

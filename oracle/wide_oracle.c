@@ -241,12 +241,16 @@ void oracle_router(int dtype, int64_t M, int32_t D, int32_t r, int32_t n_groups,
  * o[t][h] = sum_j softmax_j(q[t][h] . k[j][hkv] / sqrt(d)) v[j][hkv] over the
  * keys of sequence b, and with causal masking only those with
  * j <= p + (T_k - T_q) (queries are the last T_q positions of the sequence);
- * for an inactive one o[t][h] = 0.  The softmax is the textbook one: subtract
- * the row maximum, exponentiate, divide by the sum, all in fp64.  Layouts:
- * q/o [n_seq*T_q][n_q*d], k/v [n_seq*T_k][n_kv*d], mask [n_seq*T_q][n_groups]. */
+ * for an inactive one o[t][h] = 0.  With left padding (leftpad not NULL,
+ * Algorithm 4's first key j_min = leftpad(b)) the keys j < leftpad[b] of
+ * sequence b are not visible either; a query that sees no key gets o = 0.
+ * The softmax is the textbook one: subtract the row maximum, exponentiate,
+ * divide by the sum, all in fp64.  Layouts: q/o [n_seq*T_q][n_q*d],
+ * k/v [n_seq*T_k][n_kv*d], mask [n_seq*T_q][n_groups], leftpad [n_seq]. */
 void oracle_attention(int dtype, int round_bf16, int64_t n_seq, int32_t T_q, int32_t T_k,
                       int32_t n_q, int32_t n_kv, int32_t d, int32_t n_groups, int causal,
-                      const uint8_t* mask, const void* q, const void* k, const void* v, double* o) {
+                      const uint8_t* mask, const void* q, const void* k, const void* v,
+                      const int32_t* leftpad, double* o) {
   const int64_t M = n_seq * T_q;
   const int32_t hpg = n_q / n_groups, qpk = n_q / n_kv;
   const int64_t delta = (int64_t)T_k - T_q;
@@ -258,17 +262,18 @@ void oracle_attention(int dtype, int round_bf16, int64_t n_seq, int32_t T_q, int
 #pragma omp for schedule(static)
     for (int64_t t = 0; t < M; ++t) {
       const int64_t b = t / T_q, p = t % T_q;
-      const int64_t nk = causal ? p + delta + 1 : T_k; /* keys 0 .. nk-1 are visible */
+      const int64_t nk = causal ? p + delta + 1 : T_k; /* keys j0 .. nk-1 are visible */
+      const int64_t j0 = leftpad ? leftpad[b] : 0;
       const int64_t kr0 = b * T_k;                     /* first key row of sequence b */
       for (int32_t h = 0; h < n_q; ++h) {
         double* out = o + t * (int64_t)n_q * d + (int64_t)h * d;
-        if (mask[t * n_groups + h / hpg] == 0) {
+        if (mask[t * n_groups + h / hpg] == 0 || j0 >= nk) {
           for (int32_t e = 0; e < d; ++e) out[e] = 0.0;
           continue;
         }
         const int32_t hk = h / qpk;
         double mx = -INFINITY;
-        for (int64_t j = 0; j < nk; ++j) {
+        for (int64_t j = j0; j < nk; ++j) {
           double dot = 0.0;
           for (int32_t e = 0; e < d; ++e)
             dot += load_elem(q, dtype, t * (int64_t)n_q * d + (int64_t)h * d + e) *
@@ -277,12 +282,12 @@ void oracle_attention(int dtype, int round_bf16, int64_t n_seq, int32_t T_q, int
           if (s[j] > mx) mx = s[j];
         }
         double z = 0.0;
-        for (int64_t j = 0; j < nk; ++j) {
+        for (int64_t j = j0; j < nk; ++j) {
           s[j] = exp(s[j] - mx);
           z += s[j];
         }
         for (int32_t e = 0; e < d; ++e) acc[e] = 0.0;
-        for (int64_t j = 0; j < nk; ++j)
+        for (int64_t j = j0; j < nk; ++j)
           for (int32_t e = 0; e < d; ++e)
             acc[e] += s[j] * load_elem(v, dtype, (kr0 + j) * (int64_t)n_kv * d + (int64_t)hk * d + e);
         for (int32_t e = 0; e < d; ++e) out[e] = store_round(acc[e] / z, round_bf16);

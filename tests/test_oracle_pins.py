@@ -504,3 +504,72 @@ def test_attention_bf16_storage_rounding(orc):
     o = orc.attention(c.q, c.k, c.v, c.mask, 1, 4, 2, 8, True)
     ob = orc.attention(c.q, c.k, c.v, c.mask, 1, 4, 2, 8, True, round_bf16=True)
     assert np.array_equal(ob, torch_bf16(o))
+
+
+# ---- left padding (Algorithm 4: the first visible key j_min = leftpad(b)) ---------
+
+def _sdpa_leftpad(c, causal, lp):
+    """torch SDPA in fp64 with an explicit visibility mask: key j of sequence b
+    is visible to query p when j >= lp[b] and (not causal or j <= p + T_k - T_q).
+    Returns (o, seen) where rows that see no key are left at 0."""
+    import torch.nn.functional as F
+    qpk = c.n_q // c.n_kv
+    out, seen = [], []
+    for b in range(c.n_seq):
+        q = torch.from_numpy(f64(c.q[b * c.T_q:(b + 1) * c.T_q])).view(c.T_q, c.n_q, c.hd).transpose(0, 1)
+        k = torch.from_numpy(f64(c.k[b * c.T_k:(b + 1) * c.T_k])).view(c.T_k, c.n_kv, c.hd).transpose(0, 1)
+        v = torch.from_numpy(f64(c.v[b * c.T_k:(b + 1) * c.T_k])).view(c.T_k, c.n_kv, c.hd).transpose(0, 1)
+        k, v = k.repeat_interleave(qpk, 0), v.repeat_interleave(qpk, 0)
+        j = torch.arange(c.T_k)[None, :]
+        p = torch.arange(c.T_q)[:, None]
+        vis = (j >= int(lp[b])) & (p >= 0)   # [T_q][T_k]
+        if causal:
+            vis = vis & (j <= p + c.T_k - c.T_q)
+        any_vis = vis.any(1)
+        o = torch.zeros(c.n_q, c.T_q, c.hd, dtype=torch.float64)
+        if any_vis.any():
+            o[:, any_vis] = F.scaled_dot_product_attention(q[:, any_vis], k, v, attn_mask=vis[any_vis])
+        out.append(o.transpose(0, 1).reshape(c.T_q, c.n_q * c.hd).numpy())
+        seen.append(any_vis.numpy())
+    return np.concatenate(out), np.concatenate(seen)
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_attention_leftpad_is_sdpa_with_padding_mask(orc, causal):
+    c = synth.attn_prefill_case(21, 3, 10, 13, 4, 2, 8, 2, mask="ones", qk_std=1.5)
+    lp = np.array([0, 5, 12], np.int32)   # none, some, all but one key
+    o = orc.attention(c.q, c.k, c.v, c.mask, 3, 4, 2, 8, causal, leftpad=lp)
+    ref, seen = _sdpa_leftpad(c, causal, lp)
+    assert rel_err(o, ref) < 1e-12
+    assert not o[~seen].any() and not np.signbit(o[~seen]).any()
+    if causal:
+        assert (~seen).any()          # padding queries that see no key exist in this case
+
+
+def test_attention_leftpad_equals_sliced_keys(orc):
+    # left padding L is the same problem on keys L.. with the queries that
+    # still see one (causal offset T_k - T_q shrinks with the slice)
+    c = synth.attn_prefill_case(22, 1, 9, 16, 4, 1, 8, 2, mask="topk", keep=0.5)
+    for L in (0, 3, 7, 10, 15):
+        for causal in (True, False):
+            o = orc.attention(c.q, c.k, c.v, c.mask, 1, 4, 1, 8, causal, leftpad=[L])
+            first = max(0, L - (16 - 9)) if causal else 0      # first query that sees key L
+            rows = np.arange(first, 9)
+            ref = orc.attention(c.q[rows], c.k[L:], c.v[L:], c.mask[rows], 1, 4, 1, 8, causal)
+            assert np.array_equal(o[rows], ref), (L, causal)
+            assert not o[:first].any()
+    # leftpad 0 is no padding, bit for bit
+    base = orc.attention(c.q, c.k, c.v, c.mask, 1, 4, 1, 8, True)
+    assert np.array_equal(orc.attention(c.q, c.k, c.v, c.mask, 1, 4, 1, 8, True, leftpad=[0]), base)
+
+
+def test_attention_leftpad_last_key_only(orc):
+    g = synth.rng(23)
+    T = 5
+    q = g.standard_normal((T, 8)).astype(np.float32)
+    k = g.standard_normal((T, 8)).astype(np.float32)
+    v = g.standard_normal((T, 8)).astype(np.float32)
+    o = orc.attention(q, k, v, np.ones((T, 1), np.uint8), 1, 1, 1, 8, False, leftpad=[T - 1])
+    assert np.array_equal(o, np.tile(v[T - 1:].astype(np.float64), (T, 1)))
+    o = orc.attention(q, k, v, np.ones((T, 1), np.uint8), 1, 1, 1, 8, True, leftpad=[T - 1])
+    assert np.array_equal(o[T - 1], v[T - 1].astype(np.float64)) and not o[:T - 1].any()
