@@ -224,10 +224,15 @@ wide_status_t wide_router(wide_dtype_t dt, int64_t M, int32_t d_model, int32_t r
  *             v[b*T_k + j, h_kv]     if mask[t][g] != 0, else +0,
  * with h_kv = h / (n_q_heads/n_kv_heads), over the keys j of sequence b;
  * with causal = 1 only keys j <= p + (T_k - T_q) (the queries are the last
- * T_q of the sequence's T_k positions, as after a cached prefix).
+ * T_q of the sequence's T_k positions, as after a cached prefix), and with
+ * left padding only keys j >= leftpad[b] (Algorithm 4's first key
+ * leftpad(b)); a query that sees no key at all gets +0.
  *   dt        WIDE_BF16 (WIDE_ERR_UNSUPPORTED otherwise).
  *   n_seq, T_q, T_k   sequences and their query / key lengths; causal needs
  *             T_k >= T_q, and T_k >= 1 whenever there are queries.
+ *   leftpad   optional int32 [n_seq] (device): the first non-padding key of
+ *             each sequence, in [0, T_k] (values outside are clamped); NULL
+ *             means no padding.  With padding the key-range split is off.
  *   n_q_heads, n_kv_heads, head_dim (128 only, else WIDE_ERR_UNSUPPORTED),
  *   group_size  as for wide_qkvo_masked (a multiple of head_dim dividing
  *             n_q_heads*head_dim; group g holds contiguous heads).
@@ -255,10 +260,11 @@ wide_status_t wide_router(wide_dtype_t dt, int64_t M, int32_t d_model, int32_t r
  */
 wide_status_t wide_attention_masked(wide_dtype_t dt, int64_t n_seq, int32_t T_q, int32_t T_k,
                                     int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
-                                    int32_t group_size, int32_t causal, const uint8_t* mask,
-                                    const int32_t* idx, const int32_t* counts, const void* q,
-                                    const void* k, const void* v, void* o, void* ws,
-                                    size_t ws_bytes, hipStream_t stream);
+                                    int32_t group_size, int32_t causal, const int32_t* leftpad,
+                                    const uint8_t* mask, const int32_t* idx,
+                                    const int32_t* counts, const void* q, const void* k,
+                                    const void* v, void* o, void* ws, size_t ws_bytes,
+                                    hipStream_t stream);
 
 /*
  * Head-group masked attention, decode (WIDE Section 3.1, equations (1)-(2);

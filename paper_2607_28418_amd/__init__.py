@@ -64,7 +64,7 @@ def lib() -> ctypes.CDLL:
         L.wide_router.argtypes = [ci, i64, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.wide_attention_masked.restype = ci
         L.wide_attention_masked.argtypes = [ci, i64, i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp,
-                                            vp, vp, vp, vp, sz, vp]
+                                            vp, vp, vp, vp, vp, sz, vp]
         L.wide_attention_workspace_size.restype = sz
         L.wide_attention_workspace_size.argtypes = [i64, i32, i32, i32, i32, i32, i32, i32]
         L.wide_attention_decode.restype = ci
@@ -311,12 +311,14 @@ def wide_attention_workspace_size(n_seq, T_q, T_k, n_q, n_kv, head_dim, group_si
 
 
 def wide_attention_masked(q, k, v, mask, n_seq, n_q, n_kv, head_dim, group_size, causal=True,
-                          idx=None, counts=None, o=None, ws=None):
+                          idx=None, counts=None, o=None, ws=None, leftpad=None):
     """Head-group masked attention (prefill).  q [n_seq*T_q][n_q*head_dim],
     k, v [n_seq*T_k][n_kv*head_dim], mask [n_seq*T_q][n_groups] uint8;
-    idx/counts optional (a reorder of `mask`).  Returns o, same shape as q."""
+    idx/counts optional (a reorder of `mask`); leftpad optional int32
+    [n_seq] (the first non-padding key of each sequence).  Returns o, same
+    shape as q."""
     torch = _torch()
-    _contig(q, k, v, mask, idx, counts, o)
+    _contig(q, k, v, mask, idx, counts, o, leftpad)
     mask = _mask_bytes(mask)
     if n_seq > 0 and (q.shape[0] % n_seq or k.shape[0] % n_seq):
         raise ValueError("q and k rows must split evenly into n_seq sequences")
@@ -330,7 +332,7 @@ def wide_attention_masked(q, k, v, mask, n_seq, n_q, n_kv, head_dim, group_size,
         ws = None if need == SIZE_MAX else _workspace(need, q.device)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check("wide_attention_masked", lib().wide_attention_masked(
-        _dtype_code(q), n_seq, T_q, T_k, n_q, n_kv, head_dim, group_size, int(bool(causal)),
+        _dtype_code(q), n_seq, T_q, T_k, n_q, n_kv, head_dim, group_size, int(bool(causal)), _p(leftpad),
         _p(mask), _p(idx), _p(counts), _p(q), _p(k), _p(v), _p(o), _p(ws), nbytes, _stream(q)))
     return o
 

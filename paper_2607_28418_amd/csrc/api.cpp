@@ -1098,10 +1098,10 @@ size_t wide_attention_workspace_size(int64_t n_seq, int32_t T_q, int32_t T_k, in
 
 wide_status_t wide_attention_masked(wide_dtype_t dt, int64_t n_seq, int32_t T_q, int32_t T_k,
                                     int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
-                                    int32_t group_size, int32_t causal, const uint8_t* mask,
-                                    const int32_t* idx, const int32_t* counts, const void* q,
-                                    const void* k, const void* v, void* o, void* ws, size_t ws_bytes,
-                                    hipStream_t stream) {
+                                    int32_t group_size, int32_t causal, const int32_t* leftpad,
+                                    const uint8_t* mask, const int32_t* idx, const int32_t* counts,
+                                    const void* q, const void* k, const void* v, void* o, void* ws,
+                                    size_t ws_bytes, hipStream_t stream) {
   AttnShape s;
   CHECK(attention_shape(dt, n_seq, T_q, T_k, n_q_heads, n_kv_heads, head_dim, group_size, causal, s));
   if ((idx == nullptr) != (counts == nullptr))
@@ -1116,6 +1116,7 @@ wide_status_t wide_attention_masked(wide_dtype_t dt, int64_t n_seq, int32_t T_q,
     CHECK(check_ptr(idx, "idx", false));
     CHECK(check_ptr(counts, "counts", false));
   }
+  if (leftpad) CHECK(check_ptr(leftpad, "leftpad", false));
   {
     Carve c0(nullptr);
     AttnWS w0;
@@ -1155,6 +1156,7 @@ wide_status_t wide_attention_masked(wide_dtype_t dt, int64_t n_seq, int32_t T_q,
   a.sched = w.sched;
   a.part = w.part;
   a.split_tiles = w.split_tiles;
+  a.leftpad = leftpad;
   if ((e = wide::launch_attention(a, static_cast<const uint16_t*>(v), w.seq_off, stream)) != hipSuccess)
     return hip_fail(e, "attention");
   return ok();

@@ -32,7 +32,9 @@
 // key range of a tile stops at its last row's position (rows are sorted);
 // a wave whose rows see none of a key tile issues no MFMA for it (l = 2);
 // only key tiles crossing a row's causal limit evaluate the per-element
-// mask.
+// mask.  With left padding (Algorithm 4's first key leftpad(b)) a tile's key
+// range starts at the tile holding key leftpad(b), that tile masks the keys
+// before it, and a query that sees no key at all stores +0.
 #include "common.h"
 #include "kernels.h"
 #include "launch.h"
@@ -175,9 +177,11 @@ __global__ __launch_bounds__(kAT, QB == 1 ? 2 : 1) void wide_attn_fwd(AttnArgs a
   const int wmin = wave_live ? limit_of(idx_g[s0 + wr0]) : -1;
   const int wmax = wave_live ? limit_of(idx_g[s0 + wr1 - 1]) : -1;
   const int gmax = limit_of(idx_g[s0 + min(c, m0 + BMW) - 1]);
-  // This unit's key tiles [jlo, jhi): the tile's whole causal range, or one
-  // chunk of it.
-  const int jlo = chunk * chunk_tiles;
+  // First visible key of the sequence (left padding; clamped into [0, T_k]).
+  const int lp = a.leftpad ? min(max(a.leftpad[b], 0), a.T_k) : 0;
+  // This unit's key tiles [jlo, jhi): the tile's whole causal range (from
+  // the tile of the first visible key), or one chunk of it.
+  const int jlo = n_chunk > 1 ? chunk * chunk_tiles : lp / kBN;
   const int n_tiles = n_chunk > 1 ? min((gmax + kBN) / kBN, jlo + chunk_tiles) : (gmax + kBN) / kBN;
 
   // Q^T fragments (B operand): d-step s holds dims 16s + 8*hi .. +8 of the row.
@@ -276,17 +280,20 @@ __global__ __launch_bounds__(kAT, QB == 1 ? 2 : 1) void wide_attn_fwd(AttnArgs a
   // row maximum, then the exponentials and the rescale) and O^T += V^T P^T.
   auto softmax_pv = [&](int jt, f32x16 (&S)[QB][2]) {
     const int j0 = jt * kBN;
-    // Per-element mask only where the tile crosses some row's limit; every
-    // other tile is fully visible to the wave.
-    if (j0 + kBN - 1 > wmin) {
+    // Per-element mask only where the tile crosses some row's limit or holds
+    // the first visible key; every other tile is fully visible to the wave.
+    if (j0 + kBN - 1 > wmin || j0 < lp) {
+      const int lo = lp - j0 - 8 * hi;  // key offsets below this are padding
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
         const int lim = plim[qb] - j0 - 8 * hi;  // key offset past which this row sees nothing
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            S[qb][kb][r] = 32 * kb + 16 * (r >> 3) + (r & 7) > lim ? -INFINITY : S[qb][kb][r];
+          for (int r = 0; r < 16; ++r) {
+            const int ko = 32 * kb + 16 * (r >> 3) + (r & 7);
+            S[qb][kb][r] = ko > lim || ko < lo ? -INFINITY : S[qb][kb][r];
+          }
       }
     }
     float alpha[QB];
@@ -350,7 +357,9 @@ __global__ __launch_bounds__(kAT, QB == 1 ? 2 : 1) void wide_attn_fwd(AttnArgs a
   // the scores of tile jt+1 and then the softmax and P.V of tile jt, so the
   // matrix core has independent work while the softmax runs.  Everything
   // issued in one iteration lands before the next one starts.
-  if constexpr (QB == 1) {
+  if (jlo >= n_tiles) {
+    // left padding hides every key of this tile's rows: nothing to stream
+  } else if constexpr (QB == 1) {
     if (kwave) {
       issue_k(jlo);
       if (jlo + 1 < n_tiles) issue_k(jlo + 1);
@@ -424,7 +433,7 @@ __global__ __launch_bounds__(kAT, QB == 1 ? 2 : 1) void wide_attn_fwd(AttnArgs a
   for (int qb = 0; qb < QB; ++qb) {
     const float zt = z[qb] + __shfl_xor(z[qb], 32);
     if (!valid[qb]) continue;
-    const float inv = 1.0f / zt;
+    const float inv = zt > 0.0f ? 1.0f / zt : 0.0f;  // no visible key (left padding): +0
     uint16_t* orow = a.o + t[qb] * ldq + (int64_t)h * kHd + 4 * hi;
 #pragma unroll
     for (int db = 0; db < 4; ++db) {
@@ -743,7 +752,7 @@ hipError_t launch_attention(AttnArgs a, const uint16_t* v, int32_t* seq_off, hip
   if (a.M == 0) return hipSuccess;
   const int hb = attn_heads_per_block(a.hpg, a.qpk);
   a.n_slots = attn_slots(a.T_q, hb);
-  if (!a.causal || !a.sched || !a.part || a.split_tiles <= 0) {
+  if (!a.causal || !a.sched || !a.part || a.split_tiles <= 0 || a.leftpad) {
     a.sched = nullptr;
     a.part = nullptr;
     a.split_tiles = 0;

@@ -217,6 +217,7 @@ struct AttnArgs {
   int32_t* sched;
   float* part;
   int split_tiles;
+  const int32_t* leftpad;   // optional [n_seq]: keys j < leftpad[b] of sequence b are hidden (no split then)
   int split_rounds;         // set by launch_attention
 };
 // The split: a launch whose active query tiles number at most split_tiles

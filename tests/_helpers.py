@@ -61,14 +61,14 @@ def bf16_ulp_arr(x):
     return np.where(a > 0, 2.0 ** (e - 7), 0.0)
 
 
-def attention_bound(orc, q, k, v, mask, n_seq, n_q, n_kv, hd, causal, T_k):
+def attention_bound(orc, q, k, v, mask, n_seq, n_q, n_kv, hd, causal, T_k, leftpad=None):
     """Per-element error bound of the bf16 attention path (probabilities
     rounded to bf16 for P.V: unit roundoff 2^-8 times attention applied to
     |V|; fp32 scores, exponentials and sums: (2^-12 + T_k 2^-24) of the
     same); the stored output's own bf16 rounding is added by the check."""
-    from paper_2607_28418_amd import synth
     vabs = np.abs(synth.as_f32(v)).astype(np.float32)
-    a_abs = orc.attention(synth.as_f32(q), synth.as_f32(k), vabs, mask, n_seq, n_q, n_kv, hd, causal)
+    a_abs = orc.attention(synth.as_f32(q), synth.as_f32(k), vabs, mask, n_seq, n_q, n_kv, hd, causal,
+                          leftpad=leftpad)
     return (2.0 ** -8 + 2.0 ** -12 + T_k * 2.0 ** -24) * a_abs
 
 

@@ -163,7 +163,7 @@ def test_router_workspace_size():
 
 def attention(dt=W.BF16, n_seq=1, T_q=256, T_k=256, nq=32, nkv=8, hd=128, G=512, causal=1, mask=A, idx=None,
               cnt=None, q=A, k=A, v=A, o=A, ws=A, ws_bytes=1 << 40):
-    return W.lib().wide_attention_masked(dt, n_seq, T_q, T_k, nq, nkv, hd, G, causal, mask, idx, cnt, q, k, v,
+    return W.lib().wide_attention_masked(dt, n_seq, T_q, T_k, nq, nkv, hd, G, causal, None, mask, idx, cnt, q, k, v,
                                          o, ws, ws_bytes, None)
 
 

@@ -28,7 +28,7 @@ def say(*a):
 
 
 def run_case(orc, n_seq, T_q, T_k, n_q, n_kv, G, causal, mask="topk", keep=0.5, qk_std=1.0, seed=0,
-             given_reorder=False):
+             given_reorder=False, leftpad=None):
     hd = 128
     ng = n_q * hd // G
     c = synth.attn_prefill_case(seed, n_seq, T_q, T_k, n_q, n_kv, hd, ng, mask=mask, keep=keep,
@@ -38,11 +38,12 @@ def run_case(orc, n_seq, T_q, T_k, n_q, n_kv, G, causal, mask="topk", keep=0.5, 
     idx = cnt = None
     if given_reorder:
         idx, cnt = W.wide_mask_reorder(m)
-    W.wide_attention_masked(q, k, v, m, n_seq, n_q, n_kv, hd, G, causal, idx=idx, counts=cnt, o=o)
+    lp = None if leftpad is None else to_dev(np.asarray(leftpad, np.int32))
+    W.wide_attention_masked(q, k, v, m, n_seq, n_q, n_kv, hd, G, causal, idx=idx, counts=cnt, o=o, leftpad=lp)
     torch.cuda.synchronize()
     got = to_np64(o)
-    ref = orc.attention(c.q, c.k, c.v, c.mask, n_seq, n_q, n_kv, hd, causal)
-    bound = attention_bound(orc, c.q, c.k, c.v, c.mask, n_seq, n_q, n_kv, hd, causal, T_k)
+    ref = orc.attention(c.q, c.k, c.v, c.mask, n_seq, n_q, n_kv, hd, causal, leftpad=leftpad)
+    bound = attention_bound(orc, c.q, c.k, c.v, c.mask, n_seq, n_q, n_kv, hd, causal, T_k, leftpad=leftpad)
     check_rows(got, ref, bound, c.mask, G, f"attention {n_seq}x{T_q}/{T_k} {n_q}/{n_kv} G={G}")
     return c, got
 
@@ -61,6 +62,25 @@ def run_case(orc, n_seq, T_q, T_k, n_q, n_kv, G, causal, mask="topk", keep=0.5, 
 def test_attention_matches_oracle(orc, n_seq, T_q, T_k, n_q, n_kv, G, causal, mask, qk_std):
     say("attention", n_seq, T_q, T_k, n_q, n_kv, G, causal, mask, qk_std)
     run_case(orc, n_seq, T_q, T_k, n_q, n_kv, G, causal, mask=mask, qk_std=qk_std, seed=T_q + n_q)
+
+
+@pytest.mark.parametrize("n_seq,T_q,T_k,n_q,n_kv,G,causal,leftpad", [
+    (3, 200, 200, 8, 2, 512, True, [0, 37, 130]),       # padding queries see no key: +0
+    (2, 70, 130, 8, 2, 256, True, [60, 129]),           # after a prefix; the tile of key 129 only
+    (2, 100, 100, 4, 4, 128, False, [5, 99]),
+    (2, 257, 257, 32, 8, 512, True, [64, 200]),         # a tile-aligned first key; Llama-3-8B heads
+    (2, 64, 64, 8, 2, 512, True, [64, 0]),              # every key hidden in one sequence
+    (1, 1000, 1000, 8, 2, 512, True, [300]),            # one sequence: the key-range split is off
+])
+def test_attention_left_padding(orc, n_seq, T_q, T_k, n_q, n_kv, G, causal, leftpad):
+    """Algorithm 4's first key leftpad(b): keys before it are hidden."""
+    say("attention leftpad", n_seq, T_q, T_k, n_q, n_kv, G, causal, leftpad)
+    c, got = run_case(orc, n_seq, T_q, T_k, n_q, n_kv, G, causal, mask="bernoulli", keep=0.7,
+                      seed=T_q + sum(leftpad), leftpad=leftpad)
+    if causal:   # queries before the padding's end see nothing: exactly +0
+        for b, lp in enumerate(leftpad):
+            first = max(0, lp - (T_k - T_q))
+            assert not got[b * T_q:b * T_q + first].any()
 
 
 @pytest.mark.parametrize("kind", ["zeros", "ones"])
