@@ -223,7 +223,7 @@ size_t ffn_ws_bytes(wide_dtype_t dt, int64_t M, int D, int Dff, int G, bool need
   if (use_decode(dt, M)) {
     const size_t pn = wide::gemv_n_part_floats(ffn_gvn(M, D, Dff, G, nullptr, nullptr, nullptr, nullptr, nullptr), true);
     if (pn) c.take<float>(pn);
-    const int ks = wide::gemv_k_split(D);
+    const int ks = wide::gemv_k_split(D, (int)M, Dff);
     if (ks > 1) c.take<float>((size_t)ks * M * D);
   } else if (small_groups(dt, G)) {
     const int nm = Dff / wide::kKMergeWidth;
@@ -316,7 +316,7 @@ size_t attn_ws_bytes(wide_phase_t ph, wide_dtype_t dt, int64_t M, const AttnDims
                                                              false);
       if (pn) c.take<float>(pn);
     } else {
-      const int ks = wide::gemv_k_split(d.D);
+      const int ks = wide::gemv_k_split(d.D, (int)M, d.Nq);
       if (ks > 1) c.take<float>((size_t)ks * M * d.D);
     }
     return c.off;
@@ -464,8 +464,8 @@ wide_status_t wide_set_option(const char* key, int64_t value) {
   }
   for (const char* k : {"gemv_n_ncb", "gemv_k_ncb"})
     if (!strcmp(key, k)) {
-      if (value != 0 && value != 1 && value != 2 && value != 4)
-        return fail(WIDE_ERR_INVALID_ARG, "%s must be 0, 1, 2 or 4", key);
+      if (value != 0 && value != 1 && value != 2 && value != 4 && value != 8)
+        return fail(WIDE_ERR_INVALID_ARG, "%s must be 0, 1, 2, 4 or 8", key);
       (key[5] == 'n' ? wide::decode_tuning().n_ncb : wide::decode_tuning().k_ncb) = (int)value;
       return ok();
     }
@@ -680,7 +680,7 @@ wide_status_t wide_ffn_masked(wide_dtype_t dt, int64_t M, int32_t d_model, int32
     const size_t pn = wide::gemv_n_part_floats(na, true);
     na.part = pn ? c.take<float>(pn) : nullptr;
     if ((e = wide::launch_gemv_n(na, true, stream)) != hipSuccess) return hip_fail(e, "gemv gate/up");
-    const int ks = wide::gemv_k_split(D);
+    const int ks = wide::gemv_k_split(D, (int)M, Dff);
     float* part = ks > 1 ? c.take<float>((size_t)ks * M * D) : nullptr;
     // groups narrower than 64 are walked as merged 64-wide groups
     const int mg = std::max(1, wide::kKMergeWidth / G);
@@ -882,7 +882,7 @@ wide_status_t wide_qkvo_masked(wide_phase_t phase, wide_dtype_t dt, int64_t M, i
       na.part = pn ? c.take<float>(pn) : nullptr;
       if ((e = wide::launch_gemv_n(na, false, stream)) != hipSuccess) return hip_fail(e, "gemv qkv");
     } else {
-      const int ks = wide::gemv_k_split(d.D);
+      const int ks = wide::gemv_k_split(d.D, (int)M, d.Nq);
       float* part = ks > 1 ? c.take<float>((size_t)ks * M * d.D) : nullptr;
       wide::GVKArgs ka{x, static_cast<const uint16_t*>(w_o), mask, static_cast<uint16_t*>(y), (int)M, d.Nq,
                        d.D, d.G, ng, ks, part, 1};

@@ -88,6 +88,12 @@ __device__ __forceinline__ u32x4 buf_ld16(bufview_t v, uint32_t byte_off) {
   return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(v, (int)byte_off, 0, 0));
 }
 
+// The same with a workgroup-uniform part of the offset in a scalar register
+// (no range check applies to it: the sum must lie inside the view).
+__device__ __forceinline__ u32x4 buf_ld16s(bufview_t v, uint32_t byte_off, uint32_t uniform_off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(v, (int)byte_off, (int)uniform_off, 0));
+}
+
 __device__ __forceinline__ uint16_t buf_ld2(bufview_t v, uint32_t byte_off) {
   return __builtin_bit_cast(uint16_t, __builtin_amdgcn_raw_buffer_load_b16(v, (int)byte_off, 0, 0));
 }

@@ -114,12 +114,22 @@ __device__ __host__ __forceinline__ int gv_total_cols(const GVNArgs& a) {
 }  // namespace
 
 // Sum the k_split partials of every (token, column) in a fixed order, apply
-// SwiGLU (gate/up pair) and the mask, store bf16.
-template <bool SWIGLU>
+// SwiGLU (gate/up pair) and the mask, store bf16.  A thread takes four
+// adjacent columns (the column count is a multiple of 16, so they share a
+// row, a region and a group); its k_split loads are all issued before the
+// first add.
+__device__ __forceinline__ f32x4 ld4f(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+__device__ __forceinline__ void st4bf(uint16_t* p, f32x4 v) {
+  const uint32_t lo = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
+  const uint32_t hi = (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
+  *reinterpret_cast<uint2*>(p) = uint2{lo, hi};
+}
+
+template <bool SWIGLU, int KS>
 __global__ __launch_bounds__(256) void wide_gemv_n_finish(GVNArgs a) {
   constexpr int NV = SWIGLU ? 2 : 1;
   const int ncols = gv_total_cols(a);
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (i >= (int64_t)a.B * ncols) return;
   const int b = (int)(i / ncols);
   int col = (int)(i % ncols);
@@ -128,17 +138,24 @@ __global__ __launch_bounds__(256) void wide_gemv_n_finish(GVNArgs a) {
   if (a.n_regions > 2 && col >= a.reg[2].col0) R = a.reg[2];
   const int lc = col - R.col0;
   const bool on = !R.masked || a.mask[(int64_t)b * a.n_groups + lc / a.G] != 0;
-  float o = 0.f;
+  f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
   if (on) {
-    float s[NV];
+    f32x4 p[NV][KS];
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int q = 0; q < KS; ++q) p[v][q] = ld4f(a.part + (((int64_t)q * NV + v) * a.B + b) * ncols + col);
+    f32x4 s[NV];
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
-      s[v] = 0.f;
-      for (int q = 0; q < a.k_split; ++q) s[v] += a.part[(((int64_t)q * NV + v) * a.B + b) * ncols + col];
+      s[v] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int q = 0; q < KS; ++q) s[v] += p[v][q];
     }
-    o = SWIGLU ? silu(s[0]) * s[NV - 1] : s[0];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = SWIGLU ? silu(s[0][e]) * s[NV - 1][e] : s[0][e];
   }
-  R.out[(int64_t)b * R.ldo + lc] = f32_to_bf16(o);
+  st4bf(R.out + (int64_t)b * R.ldo + lc, o);
 }
 
 template <bool SWIGLU, int NTB, int NCB>
@@ -190,20 +207,21 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
   const int s_beg = (int)((int64_t)all_steps * kq / a.k_split);
   const int nsteps = (int)((int64_t)all_steps * (kq + 1) / a.k_split) - s_beg;
   const int my_steps = nsteps > w ? (nsteps - w + NW - 1) / NW : 0;
-  const uint16_t* wrow[NCB][NV];
+  // Every address is a workgroup-uniform base plus one per-lane offset
+  // (row ln of a block of 16, piece lq): weights and activations share it,
+  // both having row stride K.
+  // (raw buffer loads: 32-bit offsets, the uniform part in a scalar
+  // register; lanes of tokens past the batch read zeros through the range
+  // check)
+  const uint32_t loff = (uint32_t)(ln * K + lq * 8) * 2u;
+  const uint32_t slab = (uint32_t)(16 * NCB) * (uint32_t)K * 2u;
+  bufview_t wv[NV];
+  wv[0] = buf_view(R.w0 + (int64_t)n0 * K, slab);
+  if (SWIGLU) wv[NV - 1] = buf_view(R.w1 + (int64_t)n0 * K, slab);
+  const bufview_t xv = buf_view(a.x, (uint32_t)B * (uint32_t)K * 2u);
+  uint32_t xoff[NTB];
 #pragma unroll
-  for (int c = 0; c < NCB; ++c) {
-    wrow[c][0] = R.w0 + (int64_t)(n0 + c * 16 + ln) * K + lq * 8;
-    if (SWIGLU) wrow[c][NV - 1] = R.w1 + (int64_t)(n0 + c * 16 + ln) * K + lq * 8;
-  }
-  const uint16_t* xrow[NTB];
-  bool xon[NTB];
-#pragma unroll
-  for (int tb = 0; tb < NTB; ++tb) {
-    const int b = tb * 16 + ln;
-    xon[tb] = b < B;
-    xrow[tb] = a.x + (int64_t)(xon[tb] ? b : 0) * K + lq * 8;
-  }
+  for (int tb = 0; tb < NTB; ++tb) xoff[tb] = tb * 16 + ln < B ? (uint32_t)(tb * 16 * K) * 2u + loff : kOffNone;
 
   f32x4 acc[NCB][NV][NTB];
 #pragma unroll
@@ -222,13 +240,13 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
     for (int c = 0; c < NCB; ++c)
 #pragma unroll
       for (int v = 0; v < NV; ++v) {
-        r.w[c][v][0] = ldg16(wrow[c][v] + k);
-        r.w[c][v][1] = ldg16(wrow[c][v] + k + 32);
+        r.w[c][v][0] = buf_ld16s(wv[v], loff, (uint32_t)(c * 16 * K + k) * 2u);
+        r.w[c][v][1] = buf_ld16s(wv[v], loff, (uint32_t)(c * 16 * K + k + 32) * 2u);
       }
 #pragma unroll
     for (int tb = 0; tb < NTB; ++tb) {
-      r.x[tb][0] = xon[tb] ? ldg16(xrow[tb] + k) : u32x4{0, 0, 0, 0};
-      r.x[tb][1] = xon[tb] ? ldg16(xrow[tb] + k + 32) : u32x4{0, 0, 0, 0};
+      r.x[tb][0] = buf_ld16(xv, xoff[tb] == kOffNone ? kOffNone : xoff[tb] + (uint32_t)k * 2u);
+      r.x[tb][1] = buf_ld16(xv, xoff[tb] == kOffNone ? kOffNone : xoff[tb] + (uint32_t)(k + 32) * 2u);
     }
   };
   auto mma = [&](const Regs& r) {
@@ -275,13 +293,30 @@ __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
   const int kq = blockIdx.x % a.k_split;            // this workgroup's share of the union steps
   const int n0 = (blockIdx.x / a.k_split) * 16 * NCB;
   const int w = wave_id(), lane = lane_id();
-  for (int i = tid; i < ng; i += NT) s_act[i] = 0ull;
-  __syncthreads();
-  // (groups narrower than 64 arrive merged: a.merge mask columns per group
-  // of G; the inactive ones inside an active merged group hold exact zeros)
+  // Token sets per group: lane b of a wave reads token b's mask bytes of
+  // the wave's groups (every eighth), and one ballot per group collects
+  // them.  (Groups narrower than 64 arrive merged: a.merge mask columns per
+  // group of G; the inactive ones inside an active merged group hold exact
+  // zeros.)
   const int rng = ng * a.merge;
-  for (int i = tid; i < B * rng; i += NT)
-    if (a.mask[i] != 0) atomicOr(&s_act[(i % rng) / a.merge], 1ull << (i / rng));
+  {
+    constexpr int GB = 16;  // groups per wave whose loads are in flight together
+    for (int g0 = w; g0 < ng; g0 += NW * GB) {
+      uint32_t v[GB];
+#pragma unroll
+      for (int j = 0; j < GB; ++j) {
+        const int g = g0 + j * NW;
+        v[j] = 0;
+        if (lane < B && g < ng)
+          for (int m = 0; m < a.merge; ++m) v[j] |= a.mask[(int64_t)lane * rng + g * a.merge + m];
+      }
+#pragma unroll
+      for (int j = 0; j < GB; ++j) {
+        const uint64_t bal = __ballot(v[j] != 0);
+        if (lane == 0 && g0 + j * NW < ng) s_act[g0 + j * NW] = bal;
+      }
+    }
+  }
   if (tid == 0) n_union = 0;
   __syncthreads();
   // Union of the batch's active groups, compacted in ascending order.
@@ -319,16 +354,11 @@ __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
   for (int c = 0; c < NCB; ++c)
 #pragma unroll
     for (int i = 0; i < NTB; ++i) acc[c][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const uint16_t* wrow[NCB];
-#pragma unroll
-  for (int c = 0; c < NCB; ++c) wrow[c] = a.w + (int64_t)(n0 + c * 16 + ln) * K + lq * 8;
-  const uint16_t* xrow[NTB];
-  int tok[NTB];
-#pragma unroll
-  for (int tb = 0; tb < NTB; ++tb) {
-    tok[tb] = tb * 16 + ln;
-    xrow[tb] = a.a + (int64_t)(tok[tb] < B ? tok[tb] : 0) * K + lq * 8;
-  }
+  // workgroup-uniform bases plus one per-lane offset shared by weights and
+  // activations (both have row stride K)
+  const uint32_t loff = (uint32_t)(ln * K + lq * 8) * 2u;
+  const bufview_t wv = buf_view(a.w + (int64_t)n0 * K, (uint32_t)(16 * NCB) * (uint32_t)K * 2u);
+  const bufview_t xv = buf_view(a.a, (uint32_t)B * (uint32_t)K * 2u);
 
   struct Regs {
     u32x4 w[NCB][2];
@@ -341,14 +371,16 @@ __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
     const unsigned long long act = s_act[g];
 #pragma unroll
     for (int c = 0; c < NCB; ++c) {
-      r.w[c][0] = ldg16(wrow[c] + k);
-      r.w[c][1] = ldg16(wrow[c] + k + 32);
+      r.w[c][0] = buf_ld16s(wv, loff, (uint32_t)(c * 16 * K + k) * 2u);
+      r.w[c][1] = buf_ld16s(wv, loff, (uint32_t)(c * 16 * K + k + 32) * 2u);
     }
 #pragma unroll
     for (int tb = 0; tb < NTB; ++tb) {
-      const bool on = tok[tb] < B && ((act >> tok[tb]) & 1ull);  // inactive blocks are never read
-      r.x[tb][0] = on ? ldg16(xrow[tb] + k) : u32x4{0, 0, 0, 0};
-      r.x[tb][1] = on ? ldg16(xrow[tb] + k + 32) : u32x4{0, 0, 0, 0};
+      const int tok = tb * 16 + ln;
+      const bool on = tok < B && ((act >> tok) & 1ull);  // inactive blocks are never read
+      const uint32_t o = (uint32_t)(tb * 16 * K + k) * 2u + loff;
+      r.x[tb][0] = buf_ld16(xv, on ? o : kOffNone);
+      r.x[tb][1] = buf_ld16(xv, on ? o + 64u : kOffNone);
     }
   };
   auto mma = [&](const Regs& r) {
@@ -377,60 +409,64 @@ __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
   }
 }
 
-// y = bf16(sum over the k_split partial sums), in a fixed order.
-__global__ __launch_bounds__(256) void wide_gemv_k_finish(const float* __restrict__ part, int k_split,
-                                                          int64_t n, uint16_t* __restrict__ y) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// y = bf16(sum over the k_split partial sums), in a fixed order; four
+// adjacent outputs per thread (n is a multiple of 16).
+template <int KS>
+__global__ __launch_bounds__(256) void wide_gemv_k_finish(const float* __restrict__ part, int64_t n,
+                                                          uint16_t* __restrict__ y) {
+  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (i >= n) return;
-  float s = 0.f;
-  for (int q = 0; q < k_split; ++q) s += part[(int64_t)q * n + i];
-  y[i] = f32_to_bf16(s);
+  f32x4 p[KS];
+#pragma unroll
+  for (int q = 0; q < KS; ++q) p[q] = ld4f(part + (int64_t)q * n + i);
+  f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int q = 0; q < KS; ++q) s += p[q];
+  st4bf(y + i, s);
 }
 
 namespace {
 // Timing labels name the variant: "wide_gemv_n<true>/ntb2_ncb4" is
 // wide_gemv_n<true, 2, 4> (queries of "wide_gemv_n<true>" cover them all).
-#define WIDE_GV_LABEL(BASE, NTB, NCB) BASE "/ntb" #NTB "_ncb" #NCB
+constexpr int ncb_index(int ncb) { return ncb == 1 ? 0 : ncb == 2 ? 1 : ncb == 4 ? 2 : 3; }
+constexpr int ntb_index(int ntb) { return ntb == 1 ? 0 : ntb == 2 ? 1 : 2; }
+#define WIDE_GV_ROW(BASE, NTB) {BASE "/ntb" #NTB "_ncb1", BASE "/ntb" #NTB "_ncb2", BASE "/ntb" #NTB "_ncb4", BASE "/ntb" #NTB "_ncb8"}
+#define WIDE_GV_TABLE(BASE) {WIDE_GV_ROW(BASE, 1), WIDE_GV_ROW(BASE, 2), WIDE_GV_ROW(BASE, 4)}
+constexpr const char* kGemvNLabels[2][3][4] = {WIDE_GV_TABLE("wide_gemv_n<false>"), WIDE_GV_TABLE("wide_gemv_n<true>")};
+constexpr const char* kGemvKLabels[3][4] = WIDE_GV_TABLE("wide_gemv_k");
+#undef WIDE_GV_TABLE
+#undef WIDE_GV_ROW
 
 template <bool SW, int NTB, int NCB>
-constexpr const char* gemv_n_label() {
-  if constexpr (SW) {
-    if constexpr (NTB == 1) return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_n<true>", 1, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_n<true>", 1, 2) : WIDE_GV_LABEL("wide_gemv_n<true>", 1, 4);
-    if constexpr (NTB == 2) return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_n<true>", 2, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_n<true>", 2, 2) : WIDE_GV_LABEL("wide_gemv_n<true>", 2, 4);
-    return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_n<true>", 4, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_n<true>", 4, 2) : WIDE_GV_LABEL("wide_gemv_n<true>", 4, 4);
-  } else {
-    if constexpr (NTB == 1) return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_n<false>", 1, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_n<false>", 1, 2) : WIDE_GV_LABEL("wide_gemv_n<false>", 1, 4);
-    if constexpr (NTB == 2) return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_n<false>", 2, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_n<false>", 2, 2) : WIDE_GV_LABEL("wide_gemv_n<false>", 2, 4);
-    return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_n<false>", 4, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_n<false>", 4, 2) : WIDE_GV_LABEL("wide_gemv_n<false>", 4, 4);
-  }
-}
-
+constexpr const char* gemv_n_label() { return kGemvNLabels[SW ? 1 : 0][ntb_index(NTB)][ncb_index(NCB)]; }
 template <int NTB, int NCB>
-constexpr const char* gemv_k_label() {
-  if constexpr (NTB == 1) return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_k", 1, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_k", 1, 2) : WIDE_GV_LABEL("wide_gemv_k", 1, 4);
-  if constexpr (NTB == 2) return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_k", 2, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_k", 2, 2) : WIDE_GV_LABEL("wide_gemv_k", 2, 4);
-  return NCB == 1 ? WIDE_GV_LABEL("wide_gemv_k", 4, 1) : NCB == 2 ? WIDE_GV_LABEL("wide_gemv_k", 4, 2) : WIDE_GV_LABEL("wide_gemv_k", 4, 4);
-}
+constexpr const char* gemv_k_label() { return kGemvKLabels[ntb_index(NTB)][ncb_index(NCB)]; }
 
 template <bool SW, int NCB>
 hipError_t gemv_n_launch(const GVNArgs& a, int nb, hipStream_t s) {
   const int grid = nb / NCB * a.k_split;
-  if (a.B <= 16)
+  if constexpr (SW && NCB == 8)
+    return hipErrorInvalidValue;  // not instantiated: gemv_n_ncb never picks it
+  else if (a.B <= 16)
     WIDE_LAUNCH_NAMED((gemv_n_label<SW, 1, NCB>()), (wide_gemv_n<SW, 1, NCB>), dim3(grid), dim3(NT), 0, s, a);
   else if (a.B <= 32)
     WIDE_LAUNCH_NAMED((gemv_n_label<SW, 2, NCB>()), (wide_gemv_n<SW, 2, NCB>), dim3(grid), dim3(NT), 0, s, a);
-  else if constexpr (SW && NCB == 4)
+  else if constexpr ((SW && NCB == 4) || NCB == 8)
     return hipErrorInvalidValue;  // not instantiated: gemv_n_ncb never picks it
   else
     WIDE_LAUNCH_NAMED((gemv_n_label<SW, 4, NCB>()), (wide_gemv_n<SW, 4, NCB>), dim3(grid), dim3(NT), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.k_split == 1) return e;
-  const int64_t n = (int64_t)a.B * gv_total_cols(a);
+  const int64_t n = (int64_t)a.B * gv_total_cols(a) / 4;  // four columns per thread
   const dim3 fg((unsigned)((n + 255) / 256));
-  if (SW)
-    WIDE_LAUNCH_NAMED("wide_gemv_n_finish", (wide_gemv_n_finish<true>), fg, dim3(256), 0, s, a);
+  if (a.k_split == 2)
+    WIDE_LAUNCH_NAMED("wide_gemv_n_finish", (wide_gemv_n_finish<SW, 2>), fg, dim3(256), 0, s, a);
+  else if (a.k_split == 4)
+    WIDE_LAUNCH_NAMED("wide_gemv_n_finish", (wide_gemv_n_finish<SW, 4>), fg, dim3(256), 0, s, a);
+  else if (a.k_split == 8)
+    WIDE_LAUNCH_NAMED("wide_gemv_n_finish", (wide_gemv_n_finish<SW, 8>), fg, dim3(256), 0, s, a);
   else
-    WIDE_LAUNCH_NAMED("wide_gemv_n_finish", (wide_gemv_n_finish<false>), fg, dim3(256), 0, s, a);
+    return hipErrorInvalidValue;  // the split is a power of two up to 8
   return hipGetLastError();
 }
 
@@ -441,6 +477,8 @@ hipError_t gemv_k_launch(const GVKArgs& a, hipStream_t s) {
     WIDE_LAUNCH_NAMED((gemv_k_label<1, NCB>()), (wide_gemv_k<1, NCB>), dim3(grid), dim3(NT), 0, s, a);
   else if (a.B <= 32)
     WIDE_LAUNCH_NAMED((gemv_k_label<2, NCB>()), (wide_gemv_k<2, NCB>), dim3(grid), dim3(NT), 0, s, a);
+  else if constexpr (NCB == 8)
+    return hipErrorInvalidValue;  // not instantiated: gemv_k_ncb never picks it
   else
     WIDE_LAUNCH_NAMED((gemv_k_label<4, NCB>()), (wide_gemv_k<4, NCB>), dim3(grid), dim3(NT), 0, s, a);
   return hipGetLastError();
@@ -454,18 +492,23 @@ DecodeTuning& decode_tuning() {
 
 // Column blocks per workgroup: the most (4, 2 or 1) that divide every region
 // into runs inside one group and still leave at least 160 runs, so that the
-// chip is busy without a k split.  Measured on MI355X (B = 32, Llama-3-8B
-// projections): 64 columns per workgroup ran gate/up fastest even at 224
-// workgroups (activation re-reads fall with the run width), and Q/K/V at
-// 32 columns and no split beat 64 columns with a split plus its finishing
-// kernel.
+// chip is busy without a k split.  Measured on MI355X (Llama-3-8B and
+// Llama-7B projections, weights read from HBM): at 17..64 tokens 64 columns
+// per workgroup ran gate/up fastest even at 224 workgroups (activation
+// re-reads fall with the run width), and Q/K/V at 32 columns and no split
+// beat 64 columns with a split plus its finishing kernel; at 1..4 tokens,
+// where about half the groups are unused, gate/up at 16 columns ran 6..25%
+// faster, its active workgroups being spread over more CUs.
 int gemv_n_ncb(const GVNArgs& a) {
   const int forced = decode_tuning().n_ncb;
+  if (!forced && a.swiglu && a.B <= 4) return 1;
   int nb = 0;
   for (int i = 0; i < a.n_regions; ++i) nb += a.reg[i].n_blocks;
-  for (int ncb : {4, 2}) {
-    if (forced && ncb > forced) continue;
-    // gate/up at more than 32 tokens: four blocks would not fit the registers
+  for (int ncb : {8, 4, 2}) {
+    if (forced ? ncb > forced : ncb == 8) continue;
+    // eight blocks only for plain columns and up to 32 tokens; gate/up at
+    // more than 32 tokens: four blocks would not fit the registers
+    if (ncb == 8 && (a.swiglu || a.B > 32)) continue;
     if (ncb == 4 && a.swiglu && a.B > 32) continue;
     if ((a.G / 16) % ncb) continue;
     bool ok = true;
@@ -476,9 +519,9 @@ int gemv_n_ncb(const GVNArgs& a) {
 }
 
 // Split of the k steps over workgroups.  A split costs a finishing kernel
-// (~6 us on MI355X), which only pays when the column runs alone leave most
-// CUs idle: split (at most 8 ways, at least 4 k steps per share) until there
-// are 160 workgroups.
+// (about 4.5 us on MI355X inside a graph), which only pays when the column
+// runs alone leave most CUs idle: split (at most 8 ways, at least 4 k steps
+// per share) until there are 160 workgroups.
 int gemv_n_split(const GVNArgs& a) {
   int nb = 0;
   for (int i = 0; i < a.n_regions; ++i) nb += a.reg[i].n_blocks;
@@ -493,17 +536,28 @@ int gemv_n_split(const GVNArgs& a) {
   return ks;
 }
 
+namespace {
+// A long reduction (at least 128 k steps, as in a down projection) at more
+// than 16 tokens: 64 rows per workgroup and a 4-way split.  Each workgroup
+// then re-reads the activations once per 64 weight rows rather than per 16,
+// and at 17..64 tokens that saved more than the finishing kernel costs
+// (MI355X, Llama-3-8B and Llama-7B down at 32 and 64 tokens: 2..8%).  Short
+// reductions (the O projection) do not win it back.
+bool gemv_k_wide_rows(int N, int B, int K) {
+  return B > 16 && K / 64 >= 128 && N % 64 == 0 && N / 64 * 4 >= 192;
+}
+}  // namespace
+
 // Output rows per workgroup (16 * ncb): one block, unless that leaves fewer
-// than 192 workgroups.  Measured on MI355X (B = 32): 16 rows per workgroup
-// and no split read O and down fastest, ahead of wider blocks with a split
-// and its finishing kernel.
-int gemv_k_ncb(int N) {
+// than 192 workgroups (or the long-reduction rule above applies).
+int gemv_k_ncb(int N, int B, int K) {
   const int forced = decode_tuning().k_ncb;
   if (forced) {
-    for (int ncb : {4, 2})
-      if (ncb <= forced && N % (16 * ncb) == 0) return ncb;
+    for (int ncb : {8, 4, 2})  // (eight blocks: up to 32 tokens)
+      if (ncb <= forced && N % (16 * ncb) == 0 && (ncb < 8 || B <= 32)) return ncb;
     return 1;
   }
+  if (gemv_k_wide_rows(N, B, K)) return 4;
   if (N / 16 >= 192) return 1;
   for (int ncb : {4, 2})
     if (N % (16 * ncb) == 0) return ncb;
@@ -511,10 +565,11 @@ int gemv_k_ncb(int N) {
 }
 
 // Split the union steps until there are 192 workgroups (at most 8 ways).
-int gemv_k_split(int N) {
-  const int row_blocks = N / (16 * gemv_k_ncb(N));
+int gemv_k_split(int N, int B, int K) {
   const int forced = decode_tuning().k_split;
   if (forced) return forced;
+  if (!decode_tuning().k_ncb && gemv_k_wide_rows(N, B, K)) return 4;
+  const int row_blocks = N / (16 * gemv_k_ncb(N, B, K));
   int ks = 1;
   while (row_blocks * ks < 192 && ks < 8) ks *= 2;
   return ks;
@@ -533,20 +588,32 @@ hipError_t launch_gemv_n(const GVNArgs& a, bool swiglu, hipStream_t s) {
   if (swiglu)
     return ncb == 4 ? gemv_n_launch<true, 4>(a, nb, s)
                     : ncb == 2 ? gemv_n_launch<true, 2>(a, nb, s) : gemv_n_launch<true, 1>(a, nb, s);
-  return ncb == 4 ? gemv_n_launch<false, 4>(a, nb, s)
-                  : ncb == 2 ? gemv_n_launch<false, 2>(a, nb, s) : gemv_n_launch<false, 1>(a, nb, s);
+  return ncb == 8   ? gemv_n_launch<false, 8>(a, nb, s)
+         : ncb == 4 ? gemv_n_launch<false, 4>(a, nb, s)
+         : ncb == 2 ? gemv_n_launch<false, 2>(a, nb, s)
+                    : gemv_n_launch<false, 1>(a, nb, s);
 }
 
 hipError_t launch_gemv_k(const GVKArgs& a, hipStream_t s) {
   if (a.B == 0 || a.N == 0) return hipSuccess;
   // 16 * gemv_k_ncb output rows per workgroup, the union steps split over
   // k_split workgroups (chosen by the host, partials in a.part).
-  const int ncb = gemv_k_ncb(a.N);
-  hipError_t e = ncb == 4 ? gemv_k_launch<4>(a, s) : ncb == 2 ? gemv_k_launch<2>(a, s) : gemv_k_launch<1>(a, s);
+  const int ncb = gemv_k_ncb(a.N, a.B, a.K);
+  hipError_t e = ncb == 8   ? gemv_k_launch<8>(a, s)
+                 : ncb == 4 ? gemv_k_launch<4>(a, s)
+                 : ncb == 2 ? gemv_k_launch<2>(a, s)
+                            : gemv_k_launch<1>(a, s);
   if (e != hipSuccess || a.k_split == 1) return e;
   const int64_t n = (int64_t)a.B * a.N;
-  WIDE_LAUNCH(wide_gemv_k_finish, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a.part, a.k_split,
-              n, a.y);
+  const dim3 fg((unsigned)((n / 4 + 255) / 256));
+  if (a.k_split == 2)
+    WIDE_LAUNCH_NAMED("wide_gemv_k_finish", (wide_gemv_k_finish<2>), fg, dim3(256), 0, s, a.part, n, a.y);
+  else if (a.k_split == 4)
+    WIDE_LAUNCH_NAMED("wide_gemv_k_finish", (wide_gemv_k_finish<4>), fg, dim3(256), 0, s, a.part, n, a.y);
+  else if (a.k_split == 8)
+    WIDE_LAUNCH_NAMED("wide_gemv_k_finish", (wide_gemv_k_finish<8>), fg, dim3(256), 0, s, a.part, n, a.y);
+  else
+    return hipErrorInvalidValue;  // the split is a power of two up to 8
   return hipGetLastError();
 }
 

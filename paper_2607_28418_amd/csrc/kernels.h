@@ -172,8 +172,8 @@ struct GVKArgs {
 };
 // Decode K-axis: output rows per workgroup (16 * gemv_k_ncb) and the split of
 // the union steps over workgroups (see gemv.hip).
-int gemv_k_ncb(int N);
-int gemv_k_split(int N);
+int gemv_k_ncb(int N, int B, int K);
+int gemv_k_split(int N, int B, int K);
 
 // Decode tuning overrides, 0 = automatic (wide_set_option keys gemv_n_ncb,
 // gemv_n_split, gemv_k_ncb, gemv_k_split).

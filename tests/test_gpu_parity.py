@@ -34,6 +34,8 @@ def _options():
     W.wide_set_option("kd_pattern", 1)
     W.wide_set_option("mn_order", 3)
     W.wide_set_option("mn_tail", 1)
+    for key in ("gemv_n_ncb", "gemv_n_split", "gemv_k_ncb", "gemv_k_split"):
+        W.wide_set_option(key, 0)
 
 
 def ffn_dev(c):
@@ -144,6 +146,29 @@ def test_ffn_bf16_decode_small(orc, B):
     y = W.wide_ffn_masked(x, wg, wu, wd, m, 128, h_out=h)
     torch.cuda.synchronize()
     check_ffn(orc, c, y, h)
+
+
+# every decode variant the tuning options can select: column or row blocks
+# per workgroup (1..8) and the split of the k steps over workgroups (with
+# its finishing kernel)
+DECODE_FORCED = [(1, 1, 1, 1), (2, 2, 2, 2), (4, 4, 4, 4), (8, 1, 8, 8), (8, 4, 8, 4), (2, 8, 4, 2)]
+
+
+@pytest.mark.parametrize("B", [3, 24, 32, 64])
+@pytest.mark.parametrize("n_ncb,n_split,k_ncb,k_split", DECODE_FORCED)
+def test_decode_forced_variants(orc, B, n_ncb, n_split, k_ncb, k_split):
+    say("decode forced variants B", B, "n", n_ncb, n_split, "k", k_ncb, k_split)
+    W.wide_set_option("gemv_n_ncb", n_ncb)
+    W.wide_set_option("gemv_n_split", n_split)
+    W.wide_set_option("gemv_k_ncb", k_ncb)
+    W.wide_set_option("gemv_k_split", k_split)
+    c = synth.ffn_case(40 + B, B, 1024, 2048, 128, mask="beta")
+    x, wg, wu, wd, m = ffn_dev(c)
+    h = torch.empty((B, 2048), dtype=torch.bfloat16, device=dev())
+    y = W.wide_ffn_masked(x, wg, wu, wd, m, 128, h_out=h)
+    torch.cuda.synchronize()
+    check_ffn(orc, c, y, h, what="ffn")
+    check_qkvo(orc, synth.attn_case(50 + B, B, 1024, 8, 2, 128, 256, mask="topk"))
 
 
 def test_ffn_decode_equals_prefill_rows(orc):
