@@ -13,6 +13,20 @@ only valid for the kernels as they were when the counters were taken.
         --copy-bytes 1073741824 --command "..." --out profiles/x.json
     python -m paper_2607_28418_amd.profiling trace --trace run_kernel_trace.csv \\
         --skip 3 --command "..." --out profiles/x.md
+    python -m paper_2607_28418_amd.profiling mfma --pmc A.csv B.csv --command "..." \\
+        --out profiles/x.json
+
+The mfma summary turns SQ_/GRBM_ counter passes (each pass a separate
+rocprofv3 --pmc run of the same program) into per-kernel utilisation: the
+GRBM_GUI_ACTIVE counter is summed over the chip's 8 XCDs and the SQ_ busy
+counters over its 1024 SIMDs (256 CUs), so
+
+    clock_GHz      = GRBM_GUI_ACTIVE / 8 / duration
+    mfma_busy      = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE * 128)
+    wait_any       = SQ_WAIT_ANY / SQ_WAVE_CYCLES        (waves waiting on anything)
+    wait_lds       = SQ_WAIT_INST_LDS / SQ_WAVE_CYCLES
+    lds_fifo_full  = SQ_LDS_CMD_FIFO_FULL / (GRBM_GUI_ACTIVE * 32)   (per CU-cycle)
+    lds_conflict   = SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE
 """
 from __future__ import annotations
 
@@ -161,6 +175,81 @@ def trace_markdown(stats: dict, command: str, skip: int) -> str:
     return "\n".join(lines) + "\n"
 
 
+XCDS, SIMDS_PER_XCD, CUS_PER_XCD = 8, 128, 32
+
+
+def pmc_means(paths) -> dict:
+    """{kernel key: {counter: mean per dispatch, 'dispatches': n, 'avg_us': mean duration}}
+    over one or more counter dumps (one rocprofv3 --pmc run each)."""
+    acc = collections.defaultdict(lambda: collections.defaultdict(list))
+    dur = collections.defaultdict(dict)
+    for n, path in enumerate(paths):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                k = kernel_key(r["Kernel_Name"])
+                acc[k][r["Counter_Name"] + "@%d" % n].append(float(r["Counter_Value"]))
+                if r.get("Start_Timestamp") and r.get("End_Timestamp"):
+                    dur[k][(n, r.get("Dispatch_Id"))] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    out = {}
+    for k, cs in acc.items():
+        m = {}
+        for c, v in cs.items():
+            name, n = c.rsplit("@", 1)
+            m.setdefault(name, {})[n] = sum(v) / len(v)
+        # a counter in several passes (GRBM_GUI_ACTIVE) is kept per pass
+        out[k] = {"passes": m, "dispatches": max(len(v) for v in cs.values()),
+                  "avg_us": (sum(dur[k].values()) / len(dur[k])) if dur[k] else None}
+    return out
+
+
+def mfma_summary(paths, command: str, min_us: float = 5.0) -> dict:
+    raw = pmc_means(paths)
+    kernels = {}
+    for k, v in raw.items():
+        us = v["avg_us"]
+        if us is None or us < min_us:
+            continue
+        p = v["passes"]
+
+        def get(name):
+            d = p.get(name)
+            return None if not d else sum(d.values()) / len(d)
+
+        def same_pass(num, den):
+            """num / den with both counters taken in one pass where possible."""
+            dn, dd = p.get(num), p.get(den)
+            if not dn or not dd:
+                return None
+            common = set(dn) & set(dd)
+            if common:
+                n = sorted(common)[0]
+                return dn[n] / dd[n] if dd[n] else None
+            a, b = get(num), get(den)
+            return a / b if b else None
+
+        grbm = get("GRBM_GUI_ACTIVE")
+        row = {"dispatches": v["dispatches"], "avg_us": round(us, 2)}
+        if grbm:
+            row["clock_GHz"] = round(grbm / XCDS / (us * 1e3), 3)
+        busy = same_pass("SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE")
+        if busy is not None:
+            row["mfma_busy"] = round(busy / SIMDS_PER_XCD, 4)  # per SIMD-cycle
+        for name, num, den, scale in (("wait_any", "SQ_WAIT_ANY", "SQ_WAVE_CYCLES", 1.0),
+                                      ("wait_lds", "SQ_WAIT_INST_LDS", "SQ_WAVE_CYCLES", 1.0),
+                                      ("lds_fifo_full", "SQ_LDS_CMD_FIFO_FULL", "GRBM_GUI_ACTIVE", 1.0 / CUS_PER_XCD),
+                                      ("lds_data_fifo_full", "SQ_LDS_DATA_FIFO_FULL", "GRBM_GUI_ACTIVE",
+                                       1.0 / CUS_PER_XCD),
+                                      ("lds_conflict", "SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", 1.0)):
+            r = same_pass(num, den)
+            if r is not None:
+                row[name] = round(r * scale, 4)
+        row["counters"] = {c: round(get(c), 1) for c in sorted(p)}
+        kernels[k] = row
+    return dict(command=command, passes=len(paths), source_sha256=source_digest(),
+                normalisation="GRBM_GUI_ACTIVE summed over 8 XCDs; SQ busy counters over 1024 SIMDs",
+                kernels=dict(sorted(kernels.items(), key=lambda kv: -kv[1]["avg_us"] * kv[1]["dispatches"])))
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="what", required=True)
@@ -176,8 +265,19 @@ def main():
     t.add_argument("--command", required=True)
     t.add_argument("--header", default="")
     t.add_argument("--out", required=True)
+    mf = sub.add_parser("mfma")
+    mf.add_argument("--pmc", nargs="+", required=True)
+    mf.add_argument("--command", required=True)
+    mf.add_argument("--min-us", type=float, default=5.0)
+    mf.add_argument("--out", required=True)
     a = ap.parse_args()
-    if a.what == "counters":
+    if a.what == "mfma":
+        s = mfma_summary(a.pmc, a.command, a.min_us)
+        with open(a.out, "w") as f:
+            json.dump(s, f, indent=1)
+        print(json.dumps({k: {kk: vv for kk, vv in v.items() if kk != "counters"} for k, v in s["kernels"].items()},
+                         indent=1))
+    elif a.what == "counters":
         s = summarize(a.fetch, a.write, a.copy_bytes, a.command)
         with open(a.out, "w") as f:
             json.dump(s, f, indent=1)

@@ -70,3 +70,31 @@ def test_kernel_key_strips_namespaces_and_arguments():
         == "wide_attn_prep"
     assert label_matches("wide_attn_fwd<4>", "wide_attn_fwd")
     assert not label_matches("wide_attn_fwd<4>", "wide_attn_prep")
+
+
+def test_mfma_summary_normalisation(tmp_path):
+    """Utilisation from two counter passes: GRBM_GUI_ACTIVE counts cycles on
+    each of 8 XCDs, SQ_VALU_MFMA_BUSY_CYCLES on each of 1024 SIMDs."""
+    fields = ["Kernel_Name", "Dispatch_Id", "Counter_Name", "Counter_Value", "Start_Timestamp", "End_Timestamp"]
+    k = "void wide::wide_kd256<4, 64>(wide::KArgs)"
+    cycles = 2_000_000  # 1 ms at 2 GHz
+
+    def dump(path, counters):
+        with open(path, "w", newline="") as f:
+            w = csv.DictWriter(f, fieldnames=fields)
+            w.writeheader()
+            for d in (1, 2):
+                for c, v in counters.items():
+                    w.writerow({"Kernel_Name": k, "Dispatch_Id": d, "Counter_Name": c, "Counter_Value": v,
+                                "Start_Timestamp": 0, "End_Timestamp": 1_000_000})
+
+    dump(tmp_path / "a.csv", {"GRBM_GUI_ACTIVE": 8 * cycles, "SQ_VALU_MFMA_BUSY_CYCLES": 0.75 * 1024 * cycles,
+                              "SQ_WAVE_CYCLES": 1000.0, "SQ_WAIT_ANY": 250.0})
+    dump(tmp_path / "b.csv", {"GRBM_GUI_ACTIVE": 8 * cycles, "SQ_LDS_CMD_FIFO_FULL": 0.1 * 256 * cycles})
+    s = profiling.mfma_summary([str(tmp_path / "a.csv"), str(tmp_path / "b.csv")], "cmd")
+    r = s["kernels"]["wide_kd256<4, 64>"]
+    assert r["dispatches"] == 2 and r["avg_us"] == 1000.0
+    assert r["clock_GHz"] == 2.0
+    assert r["mfma_busy"] == 0.75
+    assert r["wait_any"] == 0.25
+    assert r["lds_fifo_full"] == 0.1
