@@ -51,7 +51,6 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=1024)
-    ap.add_argument("--ring-bk", type=int, default=0, help="k depth of a 256x256 stage (0: library default)")
     ap.add_argument("--k-path", type=int, default=0, help="K-axis schedule (0: library default)")
     ap.add_argument("--no-attention", action="store_true",
                     help="skip the masked-attention figures (prefill, outside the timed step)")
@@ -229,8 +228,6 @@ def main():
 
     assert torch.cuda.is_available(), "needs a GPU"
     W.lib()
-    if args.ring_bk:
-        W.wide_set_option("ring_bk", args.ring_bk)
     if args.k_path:
         W.wide_set_option("k_path", args.k_path)
     dev = torch.device("cuda", 0)

@@ -357,29 +357,27 @@ size_t wide_workspace_size(wide_op_t op, wide_dtype_t dt, int64_t M,
  *                   256-column slab come from one XCD.
  *   "big_tiles"     1 (default): prefill GEMMs use 256x256 tiles where the
  *                   shape allows; 0: always the 128x128 tiles.
- *   "ring_bk"       k depth of a 256x256 pipeline stage: 64 (two stages,
- *                   default) or 32 (five stages; four in the K-axis kernel).
  *   "gemv_n_ncb", "gemv_k_ncb"
  *                   decode: at most this many blocks of 16 output columns
- *                   (N-axis) or rows (K-axis) per workgroup: 1, 2 or 4; 0
- *                   (default) chooses by shape.
+ *                   (N-axis) or rows (K-axis) per workgroup: 1, 2, 4 or 8
+ *                   (8: up to 32 tokens, and for the N axis plain columns
+ *                   only); 0 (default) chooses by shape.
  *   "gemv_n_split", "gemv_k_split"
  *                   decode: workgroups sharing one block's reduction: 1, 2, 4
  *                   or 8; 0 (default) chooses by shape.  A split above one
  *                   adds a small kernel that sums the partial results.
  *                   Workspace sizes depend on these four options: query
  *                   wide_workspace_size after setting them.
- *   "attn_qb"       32-query blocks per wave in the prefill attention kernel:
- *                   1 (default) or 2 (each K/V fragment feeds two MFMAs, one
- *                   wave per SIMD; measured slower).
  *   "attn_split"    prefill attention key-range split: split when at most
  *                   this many query tiles are active (0..1024, default 1024;
- *                   0 never splits).  Only with attn_qb 1.  Changes the
+ *                   0 never splits).  Changes the
  *                   workspace size: query it again after setting this.
  *   "attn_split_rounds"  chunks per resident workgroup slot the split aims at
  *                   (1..8, default 1: the chunk length is the mean work per
  *                   slot, so only the longer key ranges split).
- * Not synchronised with calls running on other host threads.
+ * Process-wide settings, stored atomically; a call reads them at several
+ * points, so change them between calls, not while calls run on other host
+ * threads.
  */
 wide_status_t wide_set_option(const char* key, int64_t value);
 wide_status_t wide_get_option(const char* key, int64_t* value);

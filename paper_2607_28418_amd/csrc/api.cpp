@@ -7,6 +7,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -43,13 +44,16 @@ wide_status_t hip_fail(hipError_t e, const char* where) {
 }
 
 // ---- tunables (wide_set_option) ---------------------------------------------
-int64_t g_decode_max_m = 64;  // M <= this uses the decode (GEMV) kernels
-int g_k_path = 0;             // 0 auto, 1 dense-masked, 2 scatter
-int g_big_tiles = 1;          // 1: 256x256 tile kernels where the shape allows
-int g_mn_tail = 1;            // 1: 256-tile N-axis launches split each XCD's last partial round along k
-int g_mn_order = 3;           // bit 0: Q/K/V launch K and V before Q; bit 1: full tiles before partial ones
-int g_kd_pattern = 1;         // 1: dense-masked K axis reads rows in mask-pattern order (<= 8 groups)
-int g_ks_pack = 1;            // scatter K axis (256 tiles): K-groups per workgroup
+// Process-wide; atomics so that a setting made on one host thread is read
+// whole on another (a call still reads them at several points, so settings
+// are meant to change between calls, not during them).
+std::atomic<int64_t> g_decode_max_m{64};  // M <= this uses the decode (GEMV) kernels
+std::atomic<int> g_k_path{0};             // 0 auto, 1 dense-masked, 2 scatter
+std::atomic<int> g_big_tiles{1};          // 1: 256x256 tile kernels where the shape allows
+std::atomic<int> g_mn_tail{1};            // 1: 256-tile N-axis launches split each XCD's last partial round along k
+std::atomic<int> g_mn_order{3};           // bit 0: Q/K/V launch K and V before Q; bit 1: full tiles before partial ones
+std::atomic<int> g_kd_pattern{1};         // 1: dense-masked K axis reads rows in mask-pattern order (<= 8 groups)
+std::atomic<int> g_ks_pack{1};            // scatter K axis (256 tiles): K-groups per workgroup
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
@@ -75,7 +79,8 @@ bool use_decode(wide_dtype_t dt, int64_t M) {
 }
 
 int k_path_for(int G) {
-  if (g_k_path == 1 || g_k_path == 2) return g_k_path;
+  const int kp = g_k_path;
+  if (kp == 1 || kp == 2) return kp;
   // fp32 atomics ran at ~1 TB/s on MI355X, which makes the scatter schedule
   // slower than the dense-masked one unless G is very large.
   return G >= 2048 ? 2 : 1;
@@ -452,11 +457,6 @@ wide_status_t wide_set_option(const char* key, int64_t value) {
     g_k_path = (int)value;
     return ok();
   }
-  if (!strcmp(key, "ring_bk")) {
-    if (value != 32 && value != 64) return fail(WIDE_ERR_INVALID_ARG, "ring_bk must be 32 or 64");
-    wide::set_ring_bk((int)value);
-    return ok();
-  }
   if (!strcmp(key, "big_tiles")) {
     if (value < 0 || value > 1) return fail(WIDE_ERR_INVALID_ARG, "big_tiles must be 0 or 1");
     g_big_tiles = (int)value;
@@ -496,11 +496,6 @@ wide_status_t wide_set_option(const char* key, int64_t value) {
     g_kd_pattern = (int)value;
     return ok();
   }
-  if (!strcmp(key, "attn_qb")) {
-    if (value != 1 && value != 2) return fail(WIDE_ERR_INVALID_ARG, "attn_qb must be 1 or 2");
-    wide::g_attn_qb = (int)value;
-    return ok();
-  }
   if (!strcmp(key, "attn_split_rounds")) {
     if (value < 1 || value > 8) return fail(WIDE_ERR_INVALID_ARG, "attn_split_rounds must be 1..8");
     wide::g_attn_split_rounds = (int)value;
@@ -520,7 +515,6 @@ wide_status_t wide_get_option(const char* key, int64_t* value) {
   if (!strcmp(key, "decode_max_m")) *value = g_decode_max_m;
   else if (!strcmp(key, "k_path")) *value = g_k_path;
   else if (!strcmp(key, "big_tiles")) *value = g_big_tiles;
-  else if (!strcmp(key, "ring_bk")) *value = wide::get_ring_bk();
   else if (!strcmp(key, "gemv_n_ncb")) *value = wide::decode_tuning().n_ncb;
   else if (!strcmp(key, "gemv_n_split")) *value = wide::decode_tuning().n_split;
   else if (!strcmp(key, "gemv_k_ncb")) *value = wide::decode_tuning().k_ncb;
@@ -529,7 +523,6 @@ wide_status_t wide_get_option(const char* key, int64_t* value) {
   else if (!strcmp(key, "ks_pack")) *value = g_ks_pack;
   else if (!strcmp(key, "mn_order")) *value = g_mn_order;
   else if (!strcmp(key, "mn_tail")) *value = g_mn_tail;
-  else if (!strcmp(key, "attn_qb")) *value = wide::g_attn_qb;
   else if (!strcmp(key, "attn_split")) *value = wide::g_attn_split;
   else if (!strcmp(key, "attn_split_rounds")) *value = wide::g_attn_split_rounds;
   else return fail(WIDE_ERR_INVALID_ARG, "unknown option '%s'", key);

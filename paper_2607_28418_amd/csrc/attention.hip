@@ -42,9 +42,8 @@
 
 namespace wide {
 
-int g_attn_qb = 1;     // query blocks of 32 per wave in the prefill kernel (1 or 2)
-int g_attn_split_rounds = 1;
-int g_attn_split = 1024;  // key-range split when at most this many query tiles are active (0: never)
+std::atomic<int> g_attn_split_rounds{1};
+std::atomic<int> g_attn_split{1024};  // key-range split when at most this many query tiles are active (0: never)
 
 namespace {
 
@@ -76,8 +75,9 @@ __device__ __forceinline__ u32x4 lds16(const uint16_t* p) {
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // HB: query heads per workgroup (sharing one KV head); QB: 32-query blocks
-// per wave.  With QB = 2 every K / V^T fragment read from LDS feeds two
-// MFMAs (one per query block), halving the LDS reads per MFMA.
+// per wave.  The launcher instantiates QB = 1: with QB = 2 every K / V^T
+// fragment read from LDS feeds two MFMAs (one per query block), halving the
+// LDS reads per MFMA, but at one wave per SIMD it ran slower on MI355X.
 template <int HB, int QB>
 __global__ __launch_bounds__(kAT, QB == 1 ? 2 : 1) void wide_attn_fwd(AttnArgs a) {
   constexpr int RB = 4 / HB;         // row blocks (of 32*QB rows) per workgroup
@@ -735,17 +735,15 @@ __global__ __launch_bounds__(kAT) void wide_attn_prep(AttnArgs a, const uint16_t
 
 int attn_heads_per_block(int hpg, int qpk) { return attn_hb_of(hpg, qpk); }
 
-int attn_query_blocks() { return g_attn_qb; }
-
-int attn_slots(int T_q, int hb) { return (T_q + 32 * attn_query_blocks() * (4 / hb) - 1) / (32 * attn_query_blocks() * (4 / hb)); }
+int attn_slots(int T_q, int hb) { return (T_q + 32 * (4 / hb) - 1) / (32 * (4 / hb)); }
 
 int attn_split_tiles(int64_t n_seq, int T_q, int T_k, int n_q, int hpg, int qpk) {
   const int hb = attn_hb_of(hpg, qpk);
   const int nkt = (T_k + 63) / 64;
-  if (!g_attn_split || g_attn_qb != 1 || n_seq != 1 || nkt < 8 || nkt > kAttnMaxChunkTiles ||
+  if (!g_attn_split || n_seq != 1 || nkt < 8 || nkt > kAttnMaxChunkTiles ||
       n_q / hb > kAttnMaxSplitHB)
     return 0;
-  return (int)std::min<int64_t>(g_attn_split, (int64_t)(n_q / hb) * attn_slots(T_q, hb));
+  return (int)std::min<int64_t>(g_attn_split.load(), (int64_t)(n_q / hb) * attn_slots(T_q, hb));
 }
 
 hipError_t launch_attention(AttnArgs a, const uint16_t* v, int32_t* seq_off, hipStream_t s) {
@@ -768,15 +766,9 @@ hipError_t launch_attention(AttnArgs a, const uint16_t* v, int32_t* seq_off, hip
   const int64_t n_classic = (int64_t)(a.n_q / hb) * a.n_seq * a.n_slots;
   const int64_t max_units = std::min<int64_t>(kAttnMaxUnits, (int64_t)a.split_tiles * kAttnMaxChunks);
   const dim3 grid((unsigned)std::max<int64_t>(n_classic, a.sched ? max_units : 0));
-  if (g_attn_qb == 2) {
-    if (hb == 4) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<4, 2>), grid, dim3(kAT), 0, s, a);
-    else if (hb == 2) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<2, 2>), grid, dim3(kAT), 0, s, a);
-    else WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<1, 2>), grid, dim3(kAT), 0, s, a);
-  } else {
-    if (hb == 4) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<4, 1>), grid, dim3(kAT), 0, s, a);
-    else if (hb == 2) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<2, 1>), grid, dim3(kAT), 0, s, a);
-    else WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<1, 1>), grid, dim3(kAT), 0, s, a);
-  }
+  if (hb == 4) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<4, 1>), grid, dim3(kAT), 0, s, a);
+  else if (hb == 2) WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<2, 1>), grid, dim3(kAT), 0, s, a);
+  else WIDE_LAUNCH_NAMED("wide_attn_fwd", (wide_attn_fwd<1, 1>), grid, dim3(kAT), 0, s, a);
   if (a.sched) {
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const dim3 mg((unsigned)a.split_tiles);

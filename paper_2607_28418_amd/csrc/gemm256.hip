@@ -684,8 +684,6 @@ __global__ __launch_bounds__(NT, 1) void wide_ks256(KArgs a) {
 
 // ------------------------------------------------------------------ launchers
 namespace {
-int g_ring_bk = 64;
-
 template <class F>
 hipError_t allow_big_lds(F* f, int bytes) {
   return hipFuncSetAttribute(reinterpret_cast<const void*>(f),
@@ -700,17 +698,14 @@ hipError_t prepare() {
 }
 }  // namespace
 
-void set_ring_bk(int bk) { g_ring_bk = bk; }
-int get_ring_bk() { return g_ring_bk; }
-
+// Stages of k depth 64 (two in the ring).  The kernels are written for any
+// stage depth; 32-deep stages (five in the ring) ran slower on MI355X and
+// are not instantiated.
 #define WIDE_RING_LAUNCH(NAME, KT, RG, GRID, STREAM, ARGS)                                        \
   do {                                                                                            \
-    hipError_t e_ = g_ring_bk == 32 ? prepare<KT(32), RG<32>::LDS>() : prepare<KT(64), RG<64>::LDS>(); \
+    hipError_t e_ = prepare<KT(64), RG<64>::LDS>();                                               \
     if (e_ != hipSuccess) return e_;                                                              \
-    if (g_ring_bk == 32)                                                                          \
-      WIDE_LAUNCH_NAMED(NAME "/bk32", (KT(32)), dim3(GRID), dim3(NT), RG<32>::LDS, STREAM, ARGS); \
-    else                                                                                          \
-      WIDE_LAUNCH_NAMED(NAME "/bk64", (KT(64)), dim3(GRID), dim3(NT), RG<64>::LDS, STREAM, ARGS); \
+    WIDE_LAUNCH_NAMED(NAME "/bk64", (KT(64)), dim3(GRID), dim3(NT), RG<64>::LDS, STREAM, ARGS);   \
   } while (0)
 
 #define MN_SW(bk) wide_mn256<true, bk>

@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace wide {
 
 // ---- mask reorder ---------------------------------------------------------
@@ -130,8 +132,6 @@ hipError_t launch_mn256(const MN256Args& a, bool swiglu, hipStream_t s);
 hipError_t launch_kd256(const KArgs& a, hipStream_t s);
 hipError_t launch_ks256(const KArgs& a, hipStream_t s);
 constexpr int kKd256MaxGroups = 512;
-void set_ring_bk(int bk);   // 64 (two stages) or 32 (four stages)
-int get_ring_bk();
 hipError_t launch_zero_f32(float* p, int64_t n, hipStream_t s);
 hipError_t launch_f32_to_bf16(const float* src, uint16_t* dst, int64_t n, hipStream_t s);
 
@@ -178,7 +178,7 @@ int gemv_k_split(int N, int B, int K);
 // Decode tuning overrides, 0 = automatic (wide_set_option keys gemv_n_ncb,
 // gemv_n_split, gemv_k_ncb, gemv_k_split).
 struct DecodeTuning {
-  int n_ncb, n_split, k_ncb, k_split;
+  std::atomic<int> n_ncb, n_split, k_ncb, k_split;
 };
 DecodeTuning& decode_tuning();
 
@@ -245,9 +245,8 @@ int attn_split_tiles(int64_t n_seq, int T_q, int T_k, int n_q, int hpg, int qpk)
 hipError_t launch_attention(AttnArgs a, const uint16_t* v, int32_t* seq_off, hipStream_t s);
 int attn_heads_per_block(int hpg, int qpk);
 int attn_slots(int T_q, int hb);
-extern int g_attn_split_rounds;  // units per resident workgroup slot the split aims at (1..8)
-extern int g_attn_split;  // split the causal key ranges when at most this many query tiles exist (0: never)
-extern int g_attn_qb;  // 32-query blocks per wave in the prefill attention kernel (1 or 2)
+extern std::atomic<int> g_attn_split_rounds;  // units per resident workgroup slot the split aims at (1..8)
+extern std::atomic<int> g_attn_split;  // split the causal key ranges when at most this many query tiles exist (0: never)
 
 // ---- masked attention, decode (attention_decode.hip)
 struct AttnDecArgs {

@@ -114,12 +114,14 @@ def test_options():
     W.wide_set_option("decode_max_m", 64)
     with pytest.raises(W.WideError):
         W.wide_set_option("k_path", 9)
-    with pytest.raises(W.WideError):
-        W.wide_set_option("nope", 1)
-    for key, default, bad in (("mn_order", 3, 4), ("kd_pattern", 1, 2), ("attn_qb", 1, 3), ("mn_tail", 1, 2),
-                               ("attn_split", 1024, 1025), ("attn_split_rounds", 1, 9), ("ks_pack", 1, 0)):
+    for gone in ("nope", "ring_bk", "attn_qb"):  # (the measured-slower variants are not built)
+        with pytest.raises(W.WideError):
+            W.wide_set_option(gone, 1)
+    for key, default, bad in (("mn_order", 3, 4), ("kd_pattern", 1, 2), ("mn_tail", 1, 2),
+                               ("attn_split", 1024, 1025), ("attn_split_rounds", 1, 9), ("ks_pack", 1, 0),
+                               ("gemv_n_ncb", 0, 3), ("gemv_k_split", 0, 16)):
         assert W.wide_get_option(key) == default
-        W.wide_set_option(key, {"attn_qb": 2, "attn_split_rounds": 3, "ks_pack": 4}.get(key, 0))
+        W.wide_set_option(key, {"attn_split_rounds": 3, "ks_pack": 4, "gemv_n_ncb": 8, "gemv_k_split": 8}.get(key, 0))
         with pytest.raises(W.WideError):
             W.wide_set_option(key, bad)
         W.wide_set_option(key, default)

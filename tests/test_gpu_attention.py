@@ -344,18 +344,6 @@ def test_attention_decode_timing_labels_are_distinct():
     assert n_dec == 1 and n_merge == 1
 
 
-@pytest.mark.parametrize("n_seq,T_q,T_k,n_q,n_kv,G,causal", [
-    (1, 300, 300, 8, 2, 512, True), (2, 150, 150, 4, 4, 128, True), (3, 70, 130, 8, 2, 256, True),
-    (2, 100, 37, 4, 1, 256, False), (1, 257, 257, 32, 8, 512, True)])
-def test_attention_two_query_blocks_per_wave(orc, n_seq, T_q, T_k, n_q, n_kv, G, causal):
-    say("attention two query blocks", n_seq, T_q, T_k, n_q, n_kv, G, causal)
-    W.wide_set_option("attn_qb", 2)
-    try:
-        run_case(orc, n_seq, T_q, T_k, n_q, n_kv, G, causal, seed=T_q + 5)
-    finally:
-        W.wide_set_option("attn_qb", 1)
-
-
 def test_attention_calls_replay_in_hip_graph():
     """Prefill and decode attention captured in one HIP graph: every replay
     (with eager work and syncs in between) equals the eager result bitwise."""

@@ -30,7 +30,6 @@ def _options():
     W.wide_set_option("decode_max_m", 64)
     W.wide_set_option("k_path", 0)
     W.wide_set_option("big_tiles", 1)
-    W.wide_set_option("ring_bk", 64)
     W.wide_set_option("kd_pattern", 1)
     W.wide_set_option("mn_order", 3)
     W.wide_set_option("mn_tail", 1)
@@ -93,48 +92,6 @@ def test_ffn_bf16_prefill_small(orc, M, D, Dff, G, kind, kpath, big):
     y = W.wide_ffn_masked(x, wg, wu, wd, m, G, h_out=h)
     torch.cuda.synchronize()
     check_ffn(orc, c, y, h)
-
-
-@pytest.mark.parametrize("M,D,Dff,G,kpath", [
-    (300, 256, 512, 128, 1), (700, 512, 768, 128, 2), (513, 256, 1024, 512, 1), (1000, 512, 2048, 256, 1)])
-def test_ffn_bf16_prefill_ring32(orc, M, D, Dff, G, kpath):
-    say("ffn prefill ring32", M, D, Dff, G, kpath)
-    W.wide_set_option("ring_bk", 32)
-    W.wide_set_option("k_path", kpath)
-    c = synth.ffn_case(M + 3 * G, M, D, Dff, G, mask="topk")
-    x, wg, wu, wd, m = ffn_dev(c)
-    h = torch.empty((M, Dff), dtype=torch.bfloat16, device=dev())
-    y = W.wide_ffn_masked(x, wg, wu, wd, m, G, h_out=h)
-    torch.cuda.synchronize()
-    check_ffn(orc, c, y, h)
-
-
-@pytest.mark.parametrize("M,D,Dff,G", [(513, 256, 1024, 512), (700, 512, 768, 128), (300, 4096, 1024, 128)])
-def test_ring_depths_agree_bitwise(M, D, Dff, G):
-    """Both pipeline depths add the same MFMA products in the same k order, and
-    the dense-masked K path has no atomics: outputs must match bit for bit."""
-    say("ring32 vs ring64", M, D, Dff, G)
-    W.wide_set_option("k_path", 1)
-    c = synth.ffn_case(M + 3 * G, M, D, Dff, G, mask="topk")
-    x, wg, wu, wd, m = ffn_dev(c)
-    out = {}
-    for bk in (64, 32):
-        W.wide_set_option("ring_bk", bk)
-        h = torch.empty((M, Dff), dtype=torch.bfloat16, device=dev())
-        y = W.wide_ffn_masked(x, wg, wu, wd, m, G, h_out=h)
-        torch.cuda.synchronize()
-        out[bk] = (h.cpu(), y.cpu())
-    dh = (out[64][0].float() != out[32][0].float()).sum().item()
-    dy = (out[64][1].float() != out[32][1].float()).sum().item()
-    assert dh == 0 and dy == 0, f"h differs in {dh}, y in {dy} elements"
-
-
-@pytest.mark.parametrize("M,n_q,n_kv,G", [(300, 8, 2, 512), (600, 16, 4, 256)])
-def test_qkvo_bf16_ring32(orc, M, n_q, n_kv, G):
-    say("qkvo ring32", M, n_q, n_kv, G)
-    W.wide_set_option("ring_bk", 32)
-    c = synth.attn_case(M + G, M, 512, n_q, n_kv, 128, G, mask="topk")
-    check_qkvo(orc, c)
 
 
 @pytest.mark.parametrize("B", [1, 4, 16, 33, 48, 64])
