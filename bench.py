@@ -52,6 +52,7 @@ def parse():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=1024)
     ap.add_argument("--k-path", type=int, default=0, help="K-axis schedule (0: library default)")
+    ap.add_argument("--ks-pack", type=int, default=0, help="scatter K axis: K-groups per workgroup (0: library default)")
     ap.add_argument("--no-attention", action="store_true",
                     help="skip the masked-attention figures (prefill, outside the timed step)")
     ap.add_argument("--no-sweeps", action="store_true",
@@ -230,6 +231,8 @@ def main():
     W.lib()
     if args.k_path:
         W.wide_set_option("k_path", args.k_path)
+    if args.ks_pack:
+        W.wide_set_option("ks_pack", args.ks_pack)
     dev = torch.device("cuda", 0)
     t0 = time.time()
     L = Layer(5, args.prefill_tokens, args.decode_batch, args.keep)
