@@ -246,7 +246,12 @@ def mfma_summary(paths, command: str, min_us: float = 5.0) -> dict:
         row["counters"] = {c: round(get(c), 1) for c in sorted(p)}
         kernels[k] = row
     return dict(command=command, passes=len(paths), source_sha256=source_digest(),
-                normalisation="GRBM_GUI_ACTIVE summed over 8 XCDs; SQ busy counters over 1024 SIMDs",
+                normalisation="GRBM_GUI_ACTIVE summed over 8 XCDs; SQ busy counters over 1024 SIMDs; "
+                              "kernels launched for less than min_us are left out: GRBM_GUI_ACTIVE also "
+                              "counts cycles around a launch, which only long launches make negligible; "
+                              "launches of one kernel name (e.g. a library GEMM used at several shapes) "
+                              "are averaged together",
+                min_us=min_us,
                 kernels=dict(sorted(kernels.items(), key=lambda kv: -kv[1]["avg_us"] * kv[1]["dispatches"])))
 
 
