@@ -25,8 +25,10 @@ using namespace t256;
 namespace {
 __device__ __attribute__((aligned(16))) uint16_t g_zero_blk[64];  // stays zero: never written
 
-// Rings: two stages of BK = 64 or five of BK = 32 (all of LDS); the
-// K-axis dense-masked kernel keeps 17 KB for the tile's mask bits, so four.
+// Rings: two stages of BK = 64 (128 KB).  The kernels are written for any
+// stage depth; with BK = 32 the ring would take five stages (all of LDS), or
+// four in the K-axis dense-masked kernel, which keeps 17 KB for the tile's
+// mask bits.  Only BK = 64 is launched (32-deep stages measured slower).
 template <int BK>
 using RingMN = Ring<BK, BK == 64 ? 2 : 5>;
 template <int BK>

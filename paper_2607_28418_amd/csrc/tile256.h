@@ -5,11 +5,11 @@
 // accumulators per lane).  Operands stream from global memory straight into
 // LDS with global_load_lds_dwordx4 (no VGPR staging): one wave instruction
 // moves 1 KB, lane i landing at byte 16*i of the destination.  A stage holds
-// A [256 rows][BK] and B [256 rows][BK] in bf16; NS stages of 128 KB in total
-// form a ring, so the loads of step k+NS-1 are in flight while step k is
-// multiplied.  Two shapes of the ring are compiled: BK = 64 x 2 stages
-// (128 KB) and BK = 32 x 4 or 5 stages (128 or 160 KB: a prefetch distance
-// of 96 or 128 k instead of 64, at twice the barriers).
+// A [256 rows][BK] and B [256 rows][BK] in bf16; NS stages form a ring, so
+// the loads of step k+NS-1 are in flight while step k is multiplied.  The
+// library launches BK = 64 x 2 stages (128 KB); the ring also takes BK = 32
+// with 4 or 5 stages (a prefetch distance of 96 or 128 k at twice the
+// barriers), which measured slower on MI355X.
 //
 // LDS layout: a row of BK bf16 is BK/8 chunks of 16 bytes.  Logical chunk c
 // of row r sits at physical chunk c ^ f(r).  A 128-bit LDS read is served 16

@@ -6,8 +6,9 @@ do not read exactly the bytes moved, so each one is scaled by what it reads
 for a plain device copy of known size, recorded in the same run (the
 benchmark's --calibration-copy option issues two 1 GiB copies).
 
-The summary also records a digest of the library sources: a traffic figure is
-only valid for the kernels as they were when the counters were taken.
+The summary also records a digest of the library sources (their code, without
+comments): a traffic figure is only valid for the kernels as they were when
+the counters were taken.
 
     python -m paper_2607_28418_amd.profiling counters --fetch F.csv --write W.csv \\
         --copy-bytes 1073741824 --command "..." --out profiles/x.json
@@ -44,8 +45,36 @@ COPY_KERNEL = "__amd_rocclr_copyBuffer"
 CALIBRATION_COPIES = 2  # bench.py --calibration-copy ends with two copies of copy_bytes
 
 
+def code_text(src: str) -> str:
+    """C/C++/HIP source with comments removed and whitespace runs collapsed:
+    what the compiler sees, so that editing a comment does not invalidate a
+    profile taken on the same kernels."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if c == "/" and i + 1 < n and src[i + 1] == "/":
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+            out.append(" ")
+        elif c == "/" and i + 1 < n and src[i + 1] == "*":
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        elif c in "\"'":
+            j = i + 1
+            while j < n and src[j] != c:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def source_digest() -> str:
-    """sha256 over the library's kernel and ABI sources, in name order."""
+    """sha256 over the library's kernel and ABI sources (comments and
+    whitespace left out), in name order."""
     h = hashlib.sha256()
     csrc = os.path.join(HERE, "csrc")
     paths = sorted(os.path.join(csrc, f) for f in os.listdir(csrc)
@@ -53,8 +82,8 @@ def source_digest() -> str:
     paths.append(os.path.join(ROOT, "include", "wide.h"))
     for p in paths:
         h.update(os.path.basename(p).encode())
-        with open(p, "rb") as f:
-            h.update(f.read())
+        with open(p, encoding="utf-8") as f:
+            h.update(code_text(f.read()).encode())
     return h.hexdigest()
 
 

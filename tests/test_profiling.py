@@ -98,3 +98,14 @@ def test_mfma_summary_normalisation(tmp_path):
     assert r["mfma_busy"] == 0.75
     assert r["wait_any"] == 0.25
     assert r["lds_fifo_full"] == 0.1
+
+
+def test_source_digest_ignores_comments_not_code():
+    a = 'int f() { return 1; } // one\n/* block\n comment */ const char* s = "// not a comment";\n'
+    b = 'int f() {   return 1; }\n\n// a different comment\nconst char* s = "// not a comment";'
+    c = 'int f() { return 2; } // one\nconst char* s = "// not a comment";\n'
+    d = 'int f() { return 1; }\nconst char* s = "// changed";\n'
+    assert profiling.code_text(a) == profiling.code_text(b)
+    assert profiling.code_text(a) != profiling.code_text(c)
+    assert profiling.code_text(a) != profiling.code_text(d)
+    assert profiling.code_text("char q = '\\\"'; x(); // c") == "char q = '\\\"'; x();"
