@@ -103,8 +103,13 @@ wide_status_t wide_mask_reorder(const uint8_t* mask, int64_t M, int32_t n_groups
  *   d_model, d_ff, group_size (G): G must be a power of two >= 16 dividing
  *               d_ff (Section 3.1: the tile-size set {2^k, k >= 4}), or d_ff
  *               itself: one group, so each token runs the whole FFN or none
- *               of it (the M-axis case of Appendix A; bf16 needs d_ff % 128
- *               == 0 there).
+ *               of it (the M-axis case of Appendix A).  d_model and d_ff are
+ *               multiples of 8 and there are at most 4096 groups
+ *               (WIDE_ERR_INVALID_ARG / WIDE_ERR_UNSUPPORTED otherwise).
+ *               Limits of the kernels (WIDE_ERR_UNSUPPORTED): bf16 needs
+ *               d_model % 256 == 0; with G = 16 or 32 also d_ff % 128 == 0
+ *               and d_ff <= 32768; with G = d_ff not a power of two, d_ff %
+ *               128 == 0.  fp32 needs d_model and d_ff multiples of 16.
  *   mask        [M][d_ff/G] uint8.
  *   idx, counts optional reorder of `mask` from wide_mask_reorder (reusable by
  *               every operator under the same routing decision, Appendix B);
@@ -172,7 +177,11 @@ size_t wide_static_scratch_bytes(void);
  *   in = attention output [M][n_q*hd]; w_o [d_model][n_q*hd]; y [M][d_model].
  *   Inactive blocks of `in` are never read.  w_q/w_k/w_v/q/k/v are ignored.
  * Shapes: n_q a multiple of n_kv; G a multiple of head_dim dividing n_q*hd
- * (the paper's default is (n_q/n_kv)*head_dim, one KV head per group).
+ * (the paper's default is (n_q/n_kv)*head_dim, one KV head per group); at
+ * most 4096 groups.  Limits of the kernels (WIDE_ERR_UNSUPPORTED): bf16
+ * needs d_model % 256 == 0, n_kv*hd % 128 == 0 and G = 64 (then n_q*hd and
+ * n_kv*hd % 256 == 0) or a multiple of 128; fp32 needs d_model, n_kv*hd and
+ * G multiples of 16.
  * mask [M][n_q*hd/G]; idx/counts as for wide_ffn_masked (same routing
  * decision for both phases, Appendix B).
  * ws >= wide_workspace_size(phase == QKV ? WIDE_OP_QKV : WIDE_OP_O, dt, M,
