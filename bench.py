@@ -978,11 +978,22 @@ def main():
         dt = time.time() - t1
         fl = L.active_flops("prefill", rows)["total"]
         one = cpu_one_core(L, 64)
+        # the reorder on its own (single-threaded loops): the FFN mask of the
+        # whole prefill batch, repeated to about a second
+        mf = b["mask_ffn"]
+        n_re, t2 = 0, time.time()
+        while n_re < 3 or (time.time() - t2 < 1.0 and n_re < 1000):
+            oracle.mask_reorder(mf)
+            n_re += 1
+        re_s = (time.time() - t2) / n_re
         cpu = dict(value=round(fl / dt / 1e12, 6), unit="TFLOP/s", cores=oracle.num_threads(),
                    kind="oracle", seconds=round(dt, 2),
                    sample=f"the full layer's projections (Q, K, V, O, gate/up, down) for the first "
                           f"{len(rows)} of the {args.prefill_tokens} prefill tokens, fp64, same inputs",
-                   host=host_info(), one_core=one)
+                   host=host_info(), one_core=one,
+                   reorder=dict(ms=round(1000 * re_s, 3), mask=list(mf.shape), calls=n_re,
+                                gpu_kernel_us=round(kernels["wide_reorder_fused"]["avg_us"], 2)
+                                if "wide_reorder_fused" in kernels else None))
 
     out = {
         "metric": "speedup vs dense at 50% sparsity; prefill TFLOP/s, decode HBM GB/s",
