@@ -464,6 +464,36 @@ __global__ __launch_bounds__(NT) void wide_mn256_tail(MN256Args a) {
 // NWR: mask words (32 groups each) of the lane's slot rows held in registers
 // for the whole k loop (1: up to 32 groups, 4: up to 128); 0 reads them from
 // LDS at every step.
+// Tile order of the dense-masked K axis.  One workgroup fits a CU, so the
+// chip runs the tiles in rounds of 256.  When the column tiles divide a
+// round (n_tiles even, 256 / n_tiles a multiple of 4), round r covers the
+// m-tiles [r*mr, (r+1)*mr) (mr = 256 / n_tiles) times every column tile, and
+// XCD x takes a block of mr/4 m-tiles x n_tiles/2 column tiles of it: a
+// round's operands (mr row panels and all of W) then fit the last-level
+// cache, and the tiles of one XCD share 12 k slices per step in its L2
+// (Llama-3-8B down, 8192 x 4096 x 14336: 4-6% faster than walking the m-tiles
+// of each XCD's contiguous range in turn, which needs 18 and, chip-wide,
+// every row panel in each round).  Tiles past the last full round, and
+// shapes the blocks do not fit, keep that m-major walk.
+__device__ __forceinline__ void kd256_coords(int n_tiles, int m_tiles, int& m_tile, int& n_tile) {
+  const int total = m_tiles * n_tiles;
+  const bool blocks = n_tiles % 2 == 0 && n_tiles <= 256 && 256 % n_tiles == 0 && (256 / n_tiles) % 4 == 0;
+  const int rounds = blocks ? total / 256 : 0;
+  const int id = blockIdx.x;
+  if (id < rounds * 256) {
+    const int xcd = id % 8, local = id / 8;  // workgroups are dealt round-robin to the 8 XCDs
+    const int r = local / 32, q = local % 32;
+    const int mr = 256 / n_tiles, bm = mr / 4, bn = n_tiles / 2;
+    m_tile = r * mr + (xcd % 4) * bm + q % bm;
+    n_tile = (xcd / 4) * bn + q / bm;
+    return;
+  }
+  const int base = rounds * 256;
+  const int tile = base + xcd_remap(id - base, total - base);  // m-major: n-tiles share the A panel
+  m_tile = tile / n_tiles;
+  n_tile = tile % n_tiles;
+}
+
 template <int NWR, int BK>
 __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
@@ -475,8 +505,8 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
   constexpr int S = Rg::SLOTS;
   const uint16_t* zero = g_zero_blk;
   const int n_tiles = a.N / BN;
-  const int tile = xcd_remap(blockIdx.x, gridDim.x);
-  const int m_tile = tile / n_tiles, n_tile = tile % n_tiles;  // m-major: n-tiles share the A panel
+  int m_tile, n_tile;
+  kd256_coords(n_tiles, (int)((a.M + BM - 1) / BM), m_tile, n_tile);
   const int64_t m0 = (int64_t)m_tile * BM;
   const int n0 = n_tile * BN;
   const int ng = a.K / a.G;
