@@ -111,6 +111,65 @@ __device__ __host__ __forceinline__ int gv_total_cols(const GVNArgs& a) {
   return n;
 }
 
+// Activations go through LDS.  Loaded straight into MFMA operand registers,
+// a 16-token block of one 64-wide k step is 16 rows x 64 bytes per load
+// instruction, and such half-line loads cost the vector memory path as much
+// as the weight stream itself (measured on MI355X: the down projection at
+// B = 32 took 40 us with them, 25 us without).  Instead each wave moves a
+// step's activations with whole-line direct-to-LDS loads (8 token rows x 128
+// bytes per instruction, lane L landing at byte 16*L: row L/8, physical chunk
+// L%8) into a ring of D slots of its own, and reads the fragments back from
+// LDS.  Logical chunk c of row r sits at physical chunk c ^ xf(r), so the 16
+// rows an MFMA fragment reads at one chunk fall in 16 distinct bank groups.
+typedef const void __attribute__((address_space(1)))* gv_gptr;
+typedef void __attribute__((address_space(3)))* gv_lptr;
+__device__ __attribute__((aligned(16))) uint16_t g_gv_zero[8];  // 16 bytes, stays zero: never written
+
+__device__ __forceinline__ int xf(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+// Pipeline depth for weight registers of `reg_dwords` per step and NTB token
+// blocks of activations in LDS (8 waves x D slots x 2*NTB KB, at most about
+// 130 KB), from 2 to 4.
+template <int REG_DWORDS, int NTB>
+constexpr int gv_depth() {
+  constexpr int by_regs = 160 / REG_DWORDS >= 4 ? 4 : 160 / REG_DWORDS >= 3 ? 3 : 2;
+  constexpr int by_lds = 130 / (NW * 2 * NTB);
+  return by_regs < by_lds ? by_regs : (by_lds < 2 ? 2 : by_lds);
+}
+
+// Issue one step's activation loads into ring slot `slot` (2*NTB KB):
+// token row r of the slot reads x[r][k0 .. k0+64) when rowok(r), else zeros.
+template <int NTB, class RowOk>
+__device__ __forceinline__ void x_to_lds(u32x4* slot, const uint16_t* x, int K, int k0, RowOk rowok) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int i = 0; i < 2 * NTB; ++i) {
+    const int r = i * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ xf(r);
+    const uint16_t* src = rowok(r) ? x + (int64_t)r * K + k0 + c * 8 : g_gv_zero;
+    __builtin_amdgcn_global_load_lds((gv_gptr)src, (gv_lptr)(slot + i * 64), 16, 0, 0);
+  }
+}
+
+// Token block tb's operand for half h (k 32h .. 32h+32 of the step): lane
+// (ln, lq) holds row tb*16 + ln, logical chunk 4h + lq.
+__device__ __forceinline__ u32x4 x_frag(const u32x4* slot, int tb, int h) {
+  const int lane = lane_id(), r = tb * 16 + (lane & 15), c = h * 4 + (lane >> 4);
+  return slot[(r >> 3) * 64 + ((r & 7) << 3) + (c ^ xf(r))];
+}
+
+// Wait until step q's loads (P per step) have landed, given that the steps
+// after it up to q + D - 1 (or the last step n - 1) were issued after it.
+template <int P, int D>
+__device__ __forceinline__ void wait_step_loads(int q, int n) {
+  static_assert((D - 1) * P <= 63, "vmcnt range");
+  const int younger = min(D - 1, n - 1 - q);
+  if (younger >= 3) __builtin_amdgcn_s_waitcnt(((3 * P) & 15) | (((3 * P) >> 4) << 14) | (7 << 4) | (15 << 8));
+  else if (younger == 2) __builtin_amdgcn_s_waitcnt(((2 * P) & 15) | (((2 * P) >> 4) << 14) | (7 << 4) | (15 << 8));
+  else if (younger == 1) __builtin_amdgcn_s_waitcnt((P & 15) | ((P >> 4) << 14) | (7 << 4) | (15 << 8));
+  else __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));
+}
+
 }  // namespace
 
 // Sum the k_split partials of every (token, column) in a fixed order, apply
@@ -161,7 +220,14 @@ __global__ __launch_bounds__(256) void wide_gemv_n_finish(GVNArgs a) {
 template <bool SWIGLU, int NTB, int NCB>
 __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
   constexpr int NV = SWIGLU ? 2 : 1;
-  __shared__ float red[NW / 2 * NV][kDecodeMaxB][16];
+  constexpr int REG = NCB * NV * 2 * 4;        // weight dwords per step per lane
+  constexpr int D = gv_depth<REG, NTB>();
+  constexpr int P = NCB * NV * 2 + 2 * NTB;    // vector-memory instructions per step
+  constexpr int RING = NW * D * 2 * NTB * 64;  // u32x4 of the activation rings
+  constexpr int RED = NW / 2 * NV * kDecodeMaxB * 16;  // floats of the wave reduction
+  // the reduction reuses the rings' bytes once the k loop is done
+  __shared__ __attribute__((aligned(16))) u32x4 lds[RING > RED / 4 ? RING : RED / 4];
+  float (*red)[kDecodeMaxB][16] = reinterpret_cast<float (*)[kDecodeMaxB][16]>(lds);
   __shared__ int any_active;
   __shared__ uint8_t s_on[kDecodeMaxB];  // token b runs group g (read once, used by the epilogue)
 
@@ -207,21 +273,15 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
   const int s_beg = (int)((int64_t)all_steps * kq / a.k_split);
   const int nsteps = (int)((int64_t)all_steps * (kq + 1) / a.k_split) - s_beg;
   const int my_steps = nsteps > w ? (nsteps - w + NW - 1) / NW : 0;
-  // Every address is a workgroup-uniform base plus one per-lane offset
-  // (row ln of a block of 16, piece lq): weights and activations share it,
-  // both having row stride K.
-  // (raw buffer loads: 32-bit offsets, the uniform part in a scalar
-  // register; lanes of tokens past the batch read zeros through the range
-  // check)
+  // Weights: a workgroup-uniform part plus one per-lane offset (row ln of a
+  // block of 16, piece lq), raw buffer loads with the uniform part in a
+  // scalar register.
   const uint32_t loff = (uint32_t)(ln * K + lq * 8) * 2u;
   const uint32_t slab = (uint32_t)(16 * NCB) * (uint32_t)K * 2u;
   bufview_t wv[NV];
   wv[0] = buf_view(R.w0 + (int64_t)n0 * K, slab);
   if (SWIGLU) wv[NV - 1] = buf_view(R.w1 + (int64_t)n0 * K, slab);
-  const bufview_t xv = buf_view(a.x, (uint32_t)B * (uint32_t)K * 2u);
-  uint32_t xoff[NTB];
-#pragma unroll
-  for (int tb = 0; tb < NTB; ++tb) xoff[tb] = tb * 16 + ln < B ? (uint32_t)(tb * 16 * K) * 2u + loff : kOffNone;
+  u32x4* ring = lds + w * (D * 2 * NTB * 64);
 
   f32x4 acc[NCB][NV][NTB];
 #pragma unroll
@@ -233,9 +293,9 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
 
   struct Regs {
     u32x4 w[NCB][NV][2];
-    u32x4 x[NTB][2];
   };
-  auto load = [&](int k, Regs& r) {
+  auto load = [&](int q, int slot, Regs& r) {
+    const int k = (s_beg + w + q * NW) * 64;
 #pragma unroll
     for (int c = 0; c < NCB; ++c)
 #pragma unroll
@@ -243,24 +303,42 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
         r.w[c][v][0] = buf_ld16s(wv[v], loff, (uint32_t)(c * 16 * K + k) * 2u);
         r.w[c][v][1] = buf_ld16s(wv[v], loff, (uint32_t)(c * 16 * K + k + 32) * 2u);
       }
+    x_to_lds<NTB>(ring + slot * (2 * NTB * 64), a.x, K, k, [&](int row) { return row < B; });
+  };
+  auto mma = [&](int q, int slot, const Regs& r) {
+    wait_step_loads<P, D>(q, my_steps);
+    const u32x4* sl = ring + slot * (2 * NTB * 64);
+    u32x4 xr[NTB][2];
 #pragma unroll
     for (int tb = 0; tb < NTB; ++tb) {
-      r.x[tb][0] = buf_ld16(xv, xoff[tb] == kOffNone ? kOffNone : xoff[tb] + (uint32_t)k * 2u);
-      r.x[tb][1] = buf_ld16(xv, xoff[tb] == kOffNone ? kOffNone : xoff[tb] + (uint32_t)(k + 32) * 2u);
+      xr[tb][0] = x_frag(sl, tb, 0);
+      xr[tb][1] = x_frag(sl, tb, 1);
     }
-  };
-  auto mma = [&](const Regs& r) {
 #pragma unroll
     for (int tb = 0; tb < NTB; ++tb)
 #pragma unroll
       for (int c = 0; c < NCB; ++c)
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
-          acc[c][v][tb] = mfma16(r.x[tb][0], r.w[c][v][0], acc[c][v][tb]);
-          acc[c][v][tb] = mfma16(r.x[tb][1], r.w[c][v][1], acc[c][v][tb]);
+          acc[c][v][tb] = mfma16(xr[tb][0], r.w[c][v][0], acc[c][v][tb]);
+          acc[c][v][tb] = mfma16(xr[tb][1], r.w[c][v][1], acc[c][v][tb]);
         }
+    asm volatile("" ::: "memory");  // the slot's reads stay ahead of its next loads
   };
-  stream_steps<Regs>(my_steps, [&](int q, Regs& r) { load((s_beg + w + q * NW) * 64, r); }, mma);
+  Regs rr[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j)
+    if (j < my_steps) load(j, j, rr[j]);
+  for (int q = 0; q < my_steps; q += D) {
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+      if (q + j < my_steps) {
+        mma(q + j, j, rr[j]);
+        if (q + j + D < my_steps) load(q + j + D, j, rr[j]);
+      }
+    }
+  }
+  __syncthreads();  // the reduction below reuses the rings' LDS
   // C[row = token (lane/16)*4 + i][col = lane%16], one column block at a time
 #pragma unroll
   for (int c = 0; c < NCB; ++c) {
