@@ -81,29 +81,10 @@ __device__ __forceinline__ void reduce_out(float (*red)[kDecodeMaxB][16], const 
   }
 }
 
-// A wave's k steps as a software pipeline over D register sets: the loads
-// of step q+D go out right after step q's MFMAs, so D steps of weights stay
-// in flight per lane for the whole loop (loading a few steps and then
-// multiplying them drains the memory pipeline at every iteration).  D is
-// as large as about 160 registers of staging allow, from 2 to 4.
-template <class Regs, class Load, class Mma>
-__device__ __forceinline__ void stream_steps(int n, Load load, Mma mma) {
-  constexpr int per = (int)(sizeof(Regs) / 4);
-  constexpr int D = 160 / per >= 4 ? 4 : 160 / per >= 3 ? 3 : 2;
-  Regs r[D];
-#pragma unroll
-  for (int j = 0; j < D; ++j)
-    if (j < n) load(j, r[j]);
-  for (int q = 0; q < n; q += D) {
-#pragma unroll
-    for (int j = 0; j < D; ++j) {
-      if (q + j < n) {
-        mma(r[j]);
-        if (q + j + D < n) load(q + j + D, r[j]);
-      }
-    }
-  }
-}
+// The k loop of a wave is a software pipeline over D register sets and LDS
+// slots: the loads of step q+D go out right after step q's MFMAs, so D steps
+// stay in flight per lane for the whole loop (loading a few steps and then
+// multiplying them drains the memory pipeline at every iteration).
 
 __device__ __host__ __forceinline__ int gv_total_cols(const GVNArgs& a) {
   int n = 0;
@@ -128,12 +109,12 @@ __device__ __attribute__((aligned(16))) uint16_t g_gv_zero[8];  // 16 bytes, sta
 __device__ __forceinline__ int xf(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 // Pipeline depth for weight registers of `reg_dwords` per step and NTB token
-// blocks of activations in LDS (8 waves x D slots x 2*NTB KB, at most about
-// 130 KB), from 2 to 4.
-template <int REG_DWORDS, int NTB>
+// blocks of activations in LDS (8 waves x D slots x 2*NTB KB, at most
+// LDS_KB), from 2 to 4.
+template <int REG_DWORDS, int NTB, int LDS_KB = 130>
 constexpr int gv_depth() {
   constexpr int by_regs = 160 / REG_DWORDS >= 4 ? 4 : 160 / REG_DWORDS >= 3 ? 3 : 2;
-  constexpr int by_lds = 130 / (NW * 2 * NTB);
+  constexpr int by_lds = LDS_KB / (NW * 2 * NTB);
   return by_regs < by_lds ? by_regs : (by_lds < 2 ? 2 : by_lds);
 }
 
@@ -360,6 +341,14 @@ __global__ __launch_bounds__(NT) void wide_gemv_n(GVNArgs a) {
 
 template <int NTB, int NCB>
 __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
+  // Up to 32 tokens the activations go through per-wave LDS rings (see
+  // x_to_lds); at 33..64 tokens the rings would not fit beside the group
+  // tables, and the activations load straight into registers.
+  constexpr bool XLDS = NTB <= 2;
+  constexpr int REG = XLDS ? NCB * 2 * 4 : (NCB * 2 + NTB * 2) * 4;  // staged dwords per step
+  constexpr int D = XLDS ? gv_depth<REG, NTB, 96>() : (160 / REG >= 4 ? 4 : 160 / REG >= 3 ? 3 : 2);
+  constexpr int P = NCB * 2 + 2 * NTB;  // vector-memory instructions per step
+  __shared__ __attribute__((aligned(16))) u32x4 xring[XLDS ? NW * D * 2 * NTB * 64 : 1];
   __shared__ float red[NW / 2][kDecodeMaxB][16];
   __shared__ unsigned long long s_act[4096];  // bit b: token b active in group g
   __shared__ uint16_t ulist[4096];
@@ -433,16 +422,17 @@ __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
 #pragma unroll
     for (int i = 0; i < NTB; ++i) acc[c][i] = f32x4{0.f, 0.f, 0.f, 0.f};
   // workgroup-uniform bases plus one per-lane offset shared by weights and
-  // activations (both have row stride K)
+  // (in registers) activations, both of row stride K
   const uint32_t loff = (uint32_t)(ln * K + lq * 8) * 2u;
   const bufview_t wv = buf_view(a.w + (int64_t)n0 * K, (uint32_t)(16 * NCB) * (uint32_t)K * 2u);
   const bufview_t xv = buf_view(a.a, (uint32_t)B * (uint32_t)K * 2u);
+  u32x4* ring = xring + (XLDS ? w * (D * 2 * NTB * 64) : 0);
 
   struct Regs {
     u32x4 w[NCB][2];
-    u32x4 x[NTB][2];
+    u32x4 x[XLDS ? 1 : NTB][2];
   };
-  auto load = [&](int q, Regs& r) {
+  auto load = [&](int q, int slot, Regs& r) {
     const int s = s_beg + w + q * NW;
     const int g = ulist[s / spg];
     const int k = g * G + (s % spg) * 64;
@@ -452,25 +442,60 @@ __global__ __launch_bounds__(NT) void wide_gemv_k(GVKArgs a) {
       r.w[c][0] = buf_ld16s(wv, loff, (uint32_t)(c * 16 * K + k) * 2u);
       r.w[c][1] = buf_ld16s(wv, loff, (uint32_t)(c * 16 * K + k + 32) * 2u);
     }
+    // inactive (token, group) blocks are never read: they load zeros
+    if constexpr (XLDS) {
+      x_to_lds<NTB>(ring + slot * (2 * NTB * 64), a.a, K, k,
+                    [&](int row) { return row < B && ((act >> row) & 1ull); });
+    } else {
 #pragma unroll
-    for (int tb = 0; tb < NTB; ++tb) {
-      const int tok = tb * 16 + ln;
-      const bool on = tok < B && ((act >> tok) & 1ull);  // inactive blocks are never read
-      const uint32_t o = (uint32_t)(tb * 16 * K + k) * 2u + loff;
-      r.x[tb][0] = buf_ld16(xv, on ? o : kOffNone);
-      r.x[tb][1] = buf_ld16(xv, on ? o + 64u : kOffNone);
+      for (int tb = 0; tb < NTB; ++tb) {
+        const int tok = tb * 16 + ln;
+        const bool on = tok < B && ((act >> tok) & 1ull);
+        const uint32_t o = (uint32_t)(tb * 16 * K + k) * 2u + loff;
+        r.x[tb][0] = buf_ld16(xv, on ? o : kOffNone);
+        r.x[tb][1] = buf_ld16(xv, on ? o + 64u : kOffNone);
+      }
     }
   };
-  auto mma = [&](const Regs& r) {
+  auto mma = [&](int q, int slot, const Regs& r) {
+    u32x4 xr[NTB][2];
+    if constexpr (XLDS) {
+      wait_step_loads<P, D>(q, my_steps);
+      const u32x4* sl = ring + slot * (2 * NTB * 64);
+#pragma unroll
+      for (int tb = 0; tb < NTB; ++tb) {
+        xr[tb][0] = x_frag(sl, tb, 0);
+        xr[tb][1] = x_frag(sl, tb, 1);
+      }
+    } else {
+#pragma unroll
+      for (int tb = 0; tb < NTB; ++tb) {
+        xr[tb][0] = r.x[XLDS ? 0 : tb][0];
+        xr[tb][1] = r.x[XLDS ? 0 : tb][1];
+      }
+    }
 #pragma unroll
     for (int tb = 0; tb < NTB; ++tb)
 #pragma unroll
       for (int c = 0; c < NCB; ++c) {
-        acc[c][tb] = mfma16(r.x[tb][0], r.w[c][0], acc[c][tb]);
-        acc[c][tb] = mfma16(r.x[tb][1], r.w[c][1], acc[c][tb]);
+        acc[c][tb] = mfma16(xr[tb][0], r.w[c][0], acc[c][tb]);
+        acc[c][tb] = mfma16(xr[tb][1], r.w[c][1], acc[c][tb]);
       }
+    asm volatile("" ::: "memory");  // the slot's reads stay ahead of its next loads
   };
-  stream_steps<Regs>(my_steps, load, mma);
+  Regs rr[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j)
+    if (j < my_steps) load(j, j, rr[j]);
+  for (int q = 0; q < my_steps; q += D) {
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+      if (q + j < my_steps) {
+        mma(q + j, j, rr[j]);
+        if (q + j + D < my_steps) load(q + j + D, j, rr[j]);
+      }
+    }
+  }
 #pragma unroll
   for (int c = 0; c < NCB; ++c) {
     f32x4 one[1][NTB];
