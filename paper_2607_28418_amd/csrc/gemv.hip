@@ -599,12 +599,14 @@ DecodeTuning& decode_tuning() {
 // Llama-7B projections, weights read from HBM): at 17..64 tokens 64 columns
 // per workgroup ran gate/up fastest even at 224 workgroups (activation
 // re-reads fall with the run width), and Q/K/V at 32 columns and no split
-// beat 64 columns with a split plus its finishing kernel; at 1..4 tokens,
-// where about half the groups are unused, gate/up at 16 columns ran 6..25%
-// faster, its active workgroups being spread over more CUs.
+// beat 64 columns with a split plus its finishing kernel.  With fewer tokens
+// 16 columns per workgroup ran fastest -- gate/up up to 8 tokens (0-25%
+// faster; at 16 tokens 3% slower on the Llama-3-8B shape), Q/K/V up to 16
+// tokens (2-7%): the activations of one token block cost little, and narrow
+// workgroups spread the active ones over more CUs.
 int gemv_n_ncb(const GVNArgs& a) {
   const int forced = decode_tuning().n_ncb;
-  if (!forced && a.swiglu && a.B <= 4) return 1;
+  if (!forced && a.B <= (a.swiglu ? 8 : 16)) return 1;
   int nb = 0;
   for (int i = 0; i < a.n_regions; ++i) nb += a.reg[i].n_blocks;
   for (int ncb : {8, 4, 2}) {
