@@ -343,12 +343,16 @@ size_t wide_workspace_size(wide_op_t op, wide_dtype_t dt, int64_t M,
  *   "k_path"        schedule of the prefill K-axis product (down, O):
  *                   0 automatic (default), 1 dense-masked (no atomics),
  *                   2 scatter (the paper's GEMM-K with fp32 atomics).
- *   "mn_order"      tile order of the 256x256 N-axis kernels, two bits
- *                   (default 3).  Bit 1: each XCD runs the full tiles of its
- *                   groups first, then their partial last m-tiles, then the
- *                   empty ones.  Bit 0: the Q/K/V call puts the dense K and
- *                   V tiles before the masked Q tiles, so the partial Q tiles
- *                   come last.  Outputs are identical for all values.
+ *   "mn_order"      tile order of the 256x256 N-axis kernels, three bits
+ *                   (default 7).  Bit 2: in the FFN call, each XCD runs the
+ *                   gate/up tiles of its groups m-tile by m-tile (m-tile 0
+ *                   of every group, then m-tile 1, ...); it takes precedence
+ *                   over bit 1 there.  Bit 1: each XCD runs the full tiles
+ *                   of its groups first, then their partial last m-tiles,
+ *                   then the empty ones.  Bit 0: the Q/K/V call puts the
+ *                   dense K and V tiles before the masked Q tiles, so the
+ *                   partial Q tiles come last.  Outputs are identical for
+ *                   all values.
  *   "mn_tail"       1 (default): in the Q/K/V call, each XCD's last partial
  *                   round of 256x256 tiles is cut along k into chunks run by
  *                   extra workgroups (fp32 partial tiles in the workspace,

@@ -51,7 +51,8 @@ std::atomic<int64_t> g_decode_max_m{64};  // M <= this uses the decode (GEMV) ke
 std::atomic<int> g_k_path{0};             // 0 auto, 1 dense-masked, 2 scatter
 std::atomic<int> g_big_tiles{1};          // 1: 256x256 tile kernels where the shape allows
 std::atomic<int> g_mn_tail{1};            // 1: 256-tile N-axis launches split each XCD's last partial round along k
-std::atomic<int> g_mn_order{3};           // bit 0: Q/K/V launch K and V before Q; bit 1: full tiles before partial ones
+std::atomic<int> g_mn_order{7};           // bit 0: Q/K/V launch K and V before Q; bit 1: full tiles before partial ones;
+                                          // bit 2: gate/up tiles m-tile by m-tile over each XCD's groups
 std::atomic<int> g_kd_pattern{1};         // 1: dense-masked K axis reads rows in mask-pattern order (<= 8 groups)
 std::atomic<int> g_ks_pack{1};            // scatter K axis (256 tiles): K-groups per workgroup
 
@@ -482,7 +483,7 @@ wide_status_t wide_set_option(const char* key, int64_t value) {
     return ok();
   }
   if (!strcmp(key, "mn_order")) {
-    if (value < 0 || value > 3) return fail(WIDE_ERR_INVALID_ARG, "mn_order must be 0..3");
+    if (value < 0 || value > 7) return fail(WIDE_ERR_INVALID_ARG, "mn_order must be 0..7");
     g_mn_order = (int)value;
     return ok();
   }
@@ -722,6 +723,7 @@ wide_status_t wide_ffn_masked(wide_dtype_t dt, int64_t M, int32_t d_model, int32
   if (g_big_tiles && G % 128 == 0) {
     wide::MN256Args ma{};
     ma.order = (g_mn_order >> 1) & 1;
+    ma.mblock = (g_mn_order >> 2) & 1;
     ma.x = static_cast<const uint16_t*>(x);
     ma.M = M;
     ma.K = D;

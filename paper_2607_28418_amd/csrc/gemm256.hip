@@ -90,8 +90,8 @@ __device__ __forceinline__ void run_tile(uint16_t* smem, int nsteps, Src src, in
 
 // Tile order inside an XCD's share of a region: group, then sorted m-tile,
 // then column tile inside the group, so the tiles an XCD runs together share
-// the group's weight panel in L2 (measured faster than blocking m-tiles
-// across groups).  A group wider than four column tiles (one group over a
+// the group's weight panel in L2 (gate/up runs m-blocked instead, see
+// mn256_mblocked).  A group wider than four column tiles (one group over a
 // whole projection, the M-axis case) goes column tile first: each XCD then
 // covers a slice of the weight once and re-reads the gathered rows, which
 // fit the last-level cache, instead of streaming the whole weight once per
@@ -107,6 +107,22 @@ __device__ __forceinline__ bool mn256_ordered(const MN256Args& a, const MN256Reg
          share % per_group == 0;
 }
 
+// "m-blocked" (gate/up): when an XCD's share is a whole number of groups, it
+// runs m-tile 0 of each of its groups, then m-tile 1, and so on.  The tiles
+// that run together then gather rows from one stretch of tokens (a sorted
+// m-tile of any group covers about the same token range) instead of one
+// group's whole token list, so the gathered rows are mostly shared in L2
+// while each group's weight panel is re-read once per m-tile.  Measured on
+// the Llama-3-8B gate/up at T = 8192 (topk, keep 0.5): traffic from beyond
+// L2 down 37%, time down 2%; blocks of 4 or 8 m-tiles per group cut the
+// traffic as much but ran 7-9% slower than group by group.
+template <int BNO>
+__device__ __forceinline__ bool mn256_mblocked(const MN256Args& a, const MN256Region& R) {
+  const int share = mn256_share(R.tiles), per_group = R.gw / BNO * a.m_tiles;
+  return a.mblock && R.masked == kMN256Sorted && R.gw / BNO <= 4 && 8 * share == R.tiles &&
+         share % per_group == 0;
+}
+
 template <int BNO>
 __device__ __forceinline__ void mn256_coords(const MN256Args& a, const MN256Region& R, int xcd, int local,
                                              int& g, int& m_tile, int& nt_in) {
@@ -114,6 +130,13 @@ __device__ __forceinline__ void mn256_coords(const MN256Args& a, const MN256Regi
   const int tile = xcd * share + local;
   const int ntpg = R.gw / BNO;  // tiles per group
   const int per_group = ntpg * a.m_tiles;
+  if (mn256_mblocked<BNO>(a, R)) {
+    const int gps = share / per_group, r = local % (gps * ntpg);
+    m_tile = local / (gps * ntpg);
+    g = xcd * gps + r / ntpg;
+    nt_in = r % ntpg;
+    return;
+  }
   if (mn256_ordered<BNO>(a, R)) {
     const int gps = share / per_group, gb = xcd * gps, gl = gb + gps - 1;
     int n_full = 0, n_part = 0;
@@ -771,7 +794,8 @@ bool mn256_tail_ok(const MN256Args& a, int bno) {
     const MN256Region& R = a.reg[i];
     if (R.masked != kMN256Sorted) continue;  // dense and token-order regions: every tile is real
     const int share = mn256_share(R.tiles), per_group = R.gw / bno * a.m_tiles;
-    if (!(a.order && R.gw / bno <= 4 && 8 * share == R.tiles && share % per_group == 0)) return false;
+    if (!(a.order && !a.mblock && R.gw / bno <= 4 && 8 * share == R.tiles && share % per_group == 0))
+      return false;
   }
   return true;
 }

@@ -114,6 +114,7 @@ struct MN256Args {
   int m_tiles;
   int n_regions;
   int order;  // 1: each XCD runs its groups' full tiles, then the partial, then the empty ones
+  int mblock; // 1: each XCD runs m-tile 0 of all its groups, then m-tile 1, ... (gate/up)
   int tail;   // 1: split each XCD's last partial round of tiles along k (regions dense or ordered)
   float* tail_ws;  // kMN256TailFloats floats when tail
   const uint8_t* mask;  // [M][mask_ng]: the routing mask (token-order regions only)

@@ -117,7 +117,7 @@ def test_options():
     for gone in ("nope", "ring_bk", "attn_qb"):  # (the measured-slower variants are not built)
         with pytest.raises(W.WideError):
             W.wide_set_option(gone, 1)
-    for key, default, bad in (("mn_order", 3, 4), ("kd_pattern", 1, 2), ("mn_tail", 1, 2),
+    for key, default, bad in (("mn_order", 7, 8), ("kd_pattern", 1, 2), ("mn_tail", 1, 2),
                                ("attn_split", 1024, 1025), ("attn_split_rounds", 1, 9), ("ks_pack", 1, 0),
                                ("gemv_n_ncb", 0, 3), ("gemv_k_split", 0, 16)):
         assert W.wide_get_option(key) == default

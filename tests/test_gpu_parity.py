@@ -31,7 +31,7 @@ def _options():
     W.wide_set_option("k_path", 0)
     W.wide_set_option("big_tiles", 1)
     W.wide_set_option("kd_pattern", 1)
-    W.wide_set_option("mn_order", 3)
+    W.wide_set_option("mn_order", 7)
     W.wide_set_option("mn_tail", 1)
     for key in ("gemv_n_ncb", "gemv_n_split", "gemv_k_ncb", "gemv_k_split"):
         W.wide_set_option(key, 0)
@@ -545,11 +545,12 @@ def _edge_count_mask(g, M, ng):
     return mask
 
 
-@pytest.mark.parametrize("order", [2, 0])
-@pytest.mark.parametrize("M,ng", [(1000, 16), (1300, 8), (256, 8)])
+@pytest.mark.parametrize("order", [6, 2, 0])
+@pytest.mark.parametrize("M,ng", [(1000, 16), (700, 24), (1300, 8), (256, 8)])
 def test_ffn_tile_order_edge_counts(orc, M, ng, order):
-    """Each XCD's share of gate/up tiles runs its full tiles, then partial,
-    then empty ones; every (group, m-tile) must still be written once."""
+    """Each XCD's share of gate/up tiles runs m-tile by m-tile over its
+    groups (6), or its full tiles, then partial, then empty ones (2), or
+    group by group (0); every (group, m-tile) must still be written once."""
     say("ffn tile order", M, ng, order)
     W.wide_set_option("decode_max_m", 0)
     W.wide_set_option("mn_order", order)
