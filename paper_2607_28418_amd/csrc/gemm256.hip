@@ -80,11 +80,26 @@ __host__ __device__ __forceinline__ int mn256_share(int tiles) { return (tiles +
 template <class Rg, class Src>
 __device__ __forceinline__ void run_tile(uint16_t* smem, int nsteps, Src src, int brow0, int brow1,
                                          int live, f32x16 (&acc)[4][2]) {
-  live = __builtin_amdgcn_readfirstlane(live);
-  if (live == 0xF)
-    mainloop<Rg, true>(smem, nsteps, src, brow0, brow1, live, acc);
-  else
-    mainloop<Rg, false>(smem, nsteps, src, brow0, brow1, live, acc);
+  // `live` marks the wave's fragments with active rows: always a prefix
+  // (rows past the active count, or past M, come last in a tile).
+  const int nlive = __builtin_popcount(__builtin_amdgcn_readfirstlane(live));
+  const bool aon = Rg::NS != 2 || (wave_id() & 3) < nlive;  // this wave's A load rows are multiplied
+  switch (nlive) {
+    case 4: mainloop<Rg, 4, true>(smem, nsteps, src, brow0, brow1, acc); break;
+    case 3:
+      if (aon) mainloop<Rg, 3, true>(smem, nsteps, src, brow0, brow1, acc);
+      else mainloop<Rg, 3, false>(smem, nsteps, src, brow0, brow1, acc);
+      break;
+    case 2:
+      if (aon) mainloop<Rg, 2, true>(smem, nsteps, src, brow0, brow1, acc);
+      else mainloop<Rg, 2, false>(smem, nsteps, src, brow0, brow1, acc);
+      break;
+    case 1:
+      if (aon) mainloop<Rg, 1, true>(smem, nsteps, src, brow0, brow1, acc);
+      else mainloop<Rg, 1, false>(smem, nsteps, src, brow0, brow1, acc);
+      break;
+    default: mainloop<Rg, 0, Rg::NS != 2>(smem, nsteps, src, brow0, brow1, acc); break;
+  }
 }
 }  // namespace
 

@@ -117,9 +117,13 @@ struct Frags {
   u32x4 b0, b1;
 };
 
-template <class Rg>
+// Fragments of a partial tile: the tile rows this wave multiplies that are
+// active form a prefix, so NLIVE (0..4) of its A fragments are live and the
+// rest are skipped at compile time (no reads, no MFMAs).
+template <class Rg, int NLIVE = 4>
 __device__ __forceinline__ void read_frags(const uint16_t* stage, int kk, int brow0, int brow1,
                                            Frags& f) {
+  if (NLIVE == 0) return;
   const int lane = lane_id();
   const int wm = wave_id() >> 2;
   const int l32 = lane & 31, lhi = lane >> 5;
@@ -129,20 +133,28 @@ __device__ __forceinline__ void read_frags(const uint16_t* stage, int kk, int br
   f.b0 = *reinterpret_cast<const u32x4*>(&Bs[Rg::swz(brow0, ch)]);
   f.b1 = *reinterpret_cast<const u32x4*>(&Bs[Rg::swz(brow1, ch)]);
 #pragma unroll
-  for (int fm = 0; fm < 4; ++fm)
+  for (int fm = 0; fm < NLIVE; ++fm)
     f.a[fm] = *reinterpret_cast<const u32x4*>(&As[Rg::swz(wm * 128 + fm * 32 + l32, ch)]);
 }
 
-// A fragment is skipped unless bit fm of `live` is set (FULL: all four live,
-// no test).
-template <bool FULL, int F0 = 0, int F1 = 4>
-__device__ __forceinline__ void mma_frags(const Frags& f, int live, f32x16 (&acc)[4][2]) {
+template <int NLIVE, int F0 = 0, int F1 = 4>
+__device__ __forceinline__ void mma_frags(const Frags& f, f32x16 (&acc)[4][2]) {
 #pragma unroll
-  for (int fm = F0; fm < F1; ++fm) {
-    if (FULL || (live & (1 << fm))) {
-      acc[fm][0] = mfma32(f.a[fm], f.b0, acc[fm][0]);
-      acc[fm][1] = mfma32(f.a[fm], f.b1, acc[fm][1]);
-    }
+  for (int fm = F0; fm < (F1 < NLIVE ? F1 : NLIVE); ++fm) {
+    acc[fm][0] = mfma32(f.a[fm], f.b0, acc[fm][0]);
+    acc[fm][1] = mfma32(f.a[fm], f.b1, acc[fm][1]);
+  }
+}
+
+// Interleave hints for a partial tile's sub-step: each MFMA followed by one
+// fragment read and up to VM_PER loads while they last.
+template <int MF, int RD, int VM, int VM_PER>
+__device__ __forceinline__ void sched_partial() {
+#pragma unroll
+  for (int i = 0; i < (MF > 0 ? MF : 1); ++i) {
+    if (i < MF) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (i < RD) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    if (VM_PER > 0 && i * VM_PER < VM) __builtin_amdgcn_sched_group_barrier(0x020, VM_PER, 0);
   }
 }
 
@@ -164,10 +176,21 @@ __device__ __forceinline__ void mma_frags(const Frags& f, int live, f32x16 (&acc
 //     the barrier (which also retires every read of step kt's stage) and
 //     reads step kt+1's first fragments between its first two and its last
 //     six MFMAs: the barrier wait overlaps the MFMAs already in the pipe.
-template <class Rg, bool FULL, class Src>
+//
+// NLIVE < 4 (a partial tile) skips the dead fragments' reads and MFMAs at
+// compile time (a branch around each fragment's MFMAs made the compiler wait
+// for every LDS read before them).  A wave's A load slots cover the 32 tile
+// rows of fragment (w >> 2, w & 3); AON = false (that fragment is dead; the
+// two-stage ring only, where every wait is for all of the wave's loads) also
+// skips those loads.
+template <class Rg, int NLIVE, bool AON, class Src>
 __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Src src, int brow0, int brow1,
-                                         int live, f32x16 (&acc)[4][2]) {
+                                         f32x16 (&acc)[4][2]) {
+  constexpr bool FULL = NLIVE == 4;
+  static_assert(AON || Rg::NS == 2, "skipped loads would upset the vmcnt bounds of deeper rings");
   constexpr int NS = Rg::NS, L = Rg::LOADS_PER_STEP, S = Rg::SLOTS, KK = Rg::BK / 16;
+  constexpr int MF = 2 * NLIVE, RD = NLIVE > 0 ? NLIVE + 2 : 0;  // MFMAs and reads per sub-step
+  constexpr int VM = (AON ? 2 : 1) * S, VM_PER = MF > 0 ? (VM + MF - 1) / MF : 0;  // loads per step
   auto issue_all = [&](int s) {
     const uint16_t* ap[S];
     const uint16_t* bp[S];
@@ -189,7 +212,7 @@ __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Src src, in
     const uint16_t* bp[S];
     src(0, ap, bp);
     Rg::issue_b(smem, bp);
-    Rg::issue_a(smem, ap);
+    if (AON) Rg::issue_a(smem, ap);
   } else {
     for (int s = 0; s < pro; ++s) issue_all(s);
   }
@@ -199,7 +222,7 @@ __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Src src, in
   // so the parity carries over from one step to the next without copies.
   static_assert(KK % 2 == 0, "even number of sub-steps");
   Frags fr[2];
-  read_frags<Rg>(smem, 0, brow0, brow1, fr[0]);
+  read_frags<Rg, NLIVE>(smem, 0, brow0, brow1, fr[0]);
   for (int kt = 0; kt < nsteps; ++kt) {
     const int nxt = kt + NS - 1;
     const bool more = nxt < nsteps;
@@ -224,22 +247,26 @@ __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Src src, in
         // MFMA) and the six fragment reads of sub-step 1 interleave with the
         // MFMAs.
         __builtin_amdgcn_sched_barrier(0);
-        mma_frags<FULL, 0, 4>(fr[0], live, acc);
-        Rg::issue_a(nstage, ap);
+        mma_frags<NLIVE, 0, 4>(fr[0], acc);
+        if (AON) Rg::issue_a(nstage, ap);
         Rg::issue_b(nstage, bp);
-        read_frags<Rg>(cstage, 1, brow0, brow1, fr[1]);
+        read_frags<Rg, NLIVE>(cstage, 1, brow0, brow1, fr[1]);
+        if (FULL) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
-        }
+          for (int i = 0; i < 4; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
+          }
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          for (int i = 0; i < 2; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        } else {
+          sched_partial<MF, RD, VM, VM_PER>();
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
         __builtin_amdgcn_sched_barrier(0);
         continue;
       }
@@ -249,29 +276,33 @@ __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Src src, in
         // sees one read per MFMA instead of a burst (measured 1-2% faster
         // than two MFMAs, six reads, six MFMAs).
         __builtin_amdgcn_sched_barrier(0);
-        mma_frags<FULL, 0, 4>(fr[kk & 1], live, acc);
-        read_frags<Rg>(cstage, kk + 1, brow0, brow1, fr[(kk + 1) & 1]);
+        mma_frags<NLIVE, 0, 4>(fr[kk & 1], acc);
+        read_frags<Rg, NLIVE>(cstage, kk + 1, brow0, brow1, fr[(kk + 1) & 1]);
+        if (FULL) {
 #pragma unroll
-        for (int i = 0; i < 6; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          for (int i = 0; i < 6; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        } else {
+          sched_partial<MF, RD, 0, 0>();
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
         __builtin_amdgcn_sched_barrier(0);
         continue;
       }
       // Last sub-step: the first two MFMAs go out before the barrier and the
       // next stage's first fragment reads, so the matrix core is busy while
       // they wait.
-      mma_frags<FULL, 0, 1>(fr[kk & 1], live, acc);
+      mma_frags<NLIVE, 0, 1>(fr[kk & 1], acc);
       __builtin_amdgcn_sched_barrier(0);
       if (kt + 1 < nsteps) {
         wait_step(kt + 1, min(nxt, nsteps - 1));
         stage_barrier();
-        read_frags<Rg>(smem + ((kt + 1) % NS) * Rg::STAGE, 0, brow0, brow1, fr[0]);
+        read_frags<Rg, NLIVE>(smem + ((kt + 1) % NS) * Rg::STAGE, 0, brow0, brow1, fr[0]);
       }
       __builtin_amdgcn_sched_barrier(0);
-      mma_frags<FULL, 1, 4>(fr[kk & 1], live, acc);
+      mma_frags<NLIVE, 1, 4>(fr[kk & 1], acc);
     }
   }
   if (NS == 2) wait_vm<0>();  // the last step's repeated loads
