@@ -596,9 +596,9 @@ def test_ffn_kd256_group_counts(orc, Dff):
 
 @pytest.mark.parametrize("M,D,Dff", [(1000, 256, 2048), (3000, 512, 4096), (300, 256, 1024)])
 def test_ffn_tail_split_matches(orc, M, D, Dff):
-    """Each XCD's last partial round of gate/up tiles is cut along k into
-    chunks (fp32 partial tiles, added in order by a second kernel); with and
-    without the split the outputs match the oracle."""
+    """The tail split (each XCD's last partial round cut along k) serves
+    Q/K/V only; gate/up runs its last round whole, so the FFN matches the
+    oracle with the option on or off."""
     say("ffn tail split", M, D, Dff)
     W.wide_set_option("decode_max_m", 0)
     G = 128
