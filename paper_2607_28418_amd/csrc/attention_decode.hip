@@ -54,6 +54,7 @@ struct Unit {
 // HMAX: the most query heads per KV head this instance serves (qpk <= HMAX).
 template <int HMAX>
 __global__ __launch_bounds__(kDT) void wide_attn_decode(AttnDecArgs a) {
+  constexpr int HB = HMAX < 4 ? HMAX : 4;  // head columns per LDS read group
   __shared__ __attribute__((aligned(16))) float s_p[4][kU][16];  // per wave: p[key][head]
   __shared__ __attribute__((aligned(16))) float s_al[4][16];     // per wave: rescale per head
   const int w = wave_id(), lane = lane_id();
@@ -132,14 +133,19 @@ __global__ __launch_bounds__(kDT) void wide_attn_decode(AttnDecArgs a) {
     for (int r = 0; r < 4; ++r) s_p[w][4 * g4 + r][l16] = pr[r];
     if (g4 == 0) s_al[w][l16] = alpha;
     wave_lds_sync();  // this unit's values are visible to every lane of the wave
+    // Up to four head columns, every column up to HMAX is carried, active or
+    // not (an inactive or padding column has a zero query: finite scores,
+    // discarded at the end), so the unit's arithmetic is straight-line code
+    // (3-5% faster at Llama-3-8B's four heads per KV head); wider instances
+    // test each head (the registers would not hold more).
 #pragma unroll
-    for (int h4 = 0; h4 < HMAX; h4 += 4) {
-      float al[4];  // (element reads through float: the writes above are float)
+    for (int h4 = 0; h4 < HMAX; h4 += HB) {
+      float al[HB];  // (element reads through float: the writes above are float)
 #pragma unroll
-      for (int t = 0; t < 4; ++t) al[t] = s_al[w][h4 + t];
+      for (int t = 0; t < HB; ++t) al[t] = s_al[w][h4 + t];
 #pragma unroll
-      for (int h = h4; h < h4 + 4; ++h)
-        if ((act >> h) & 1u)
+      for (int h = h4; h < h4 + HB; ++h)
+        if (HMAX <= 4 || ((act >> h) & 1u))
 #pragma unroll
           for (int e = 0; e < 8; ++e) acc[h][e] *= al[h - h4];
     }
@@ -152,13 +158,13 @@ __global__ __launch_bounds__(kDT) void wide_attn_decode(AttnDecArgs a) {
         vf[2 * e + 1] = __uint_as_float(U.v[i][e] & 0xffff0000u);
       }
 #pragma unroll
-      for (int h4 = 0; h4 < HMAX; h4 += 4) {
-        float p4[4];
+      for (int h4 = 0; h4 < HMAX; h4 += HB) {
+        float p4[HB];
 #pragma unroll
-        for (int t = 0; t < 4; ++t) p4[t] = s_p[w][4 * i + g4][h4 + t];
+        for (int t = 0; t < HB; ++t) p4[t] = s_p[w][4 * i + g4][h4 + t];
 #pragma unroll
-        for (int h = h4; h < h4 + 4; ++h)
-          if ((act >> h) & 1u)
+        for (int h = h4; h < h4 + HB; ++h)
+          if (HMAX <= 4 || ((act >> h) & 1u))
 #pragma unroll
             for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(p4[h - h4], vf[e], acc[h][e]);
       }
@@ -267,7 +273,9 @@ hipError_t launch_attention_decode(AttnDecArgs a, hipStream_t s) {
   if (a.B == 0) return hipSuccess;
   const int64_t items = (int64_t)a.B * a.n_kv * a.n_chunks;
   const dim3 grid((unsigned)((items + 3) / 4));
-  if (a.qpk <= 4) WIDE_LAUNCH_NAMED("wide_attn_decode", (wide_attn_decode<4>), grid, dim3(kDT), 0, s, a);
+  if (a.qpk == 1) WIDE_LAUNCH_NAMED("wide_attn_decode", (wide_attn_decode<1>), grid, dim3(kDT), 0, s, a);
+  else if (a.qpk == 2) WIDE_LAUNCH_NAMED("wide_attn_decode", (wide_attn_decode<2>), grid, dim3(kDT), 0, s, a);
+  else if (a.qpk <= 4) WIDE_LAUNCH_NAMED("wide_attn_decode", (wide_attn_decode<4>), grid, dim3(kDT), 0, s, a);
   else if (a.qpk <= 8) WIDE_LAUNCH_NAMED("wide_attn_decode", (wide_attn_decode<8>), grid, dim3(kDT), 0, s, a);
   else WIDE_LAUNCH_NAMED("wide_attn_decode", (wide_attn_decode<16>), grid, dim3(kDT), 0, s, a);
   hipError_t e = hipGetLastError();

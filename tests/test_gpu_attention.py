@@ -300,6 +300,7 @@ def run_decode(orc, B, L, n_q, n_kv, G, mask="bernoulli", keep=0.5, qk_std=1.0, 
     (5, 300, 8, 2, 256, False),      # ragged last 64-key step, two heads per group
     (3, 3000, 8, 2, 512, True),      # many chunks, per-sequence lengths
     (4, 200, 4, 4, 128, False),      # one head per KV head
+    (6, 500, 8, 4, 256, True),       # two query heads per KV head
     (2, 777, 16, 2, 512, True),      # eight query heads per KV head
     (2, 130, 16, 1, 1024, False),    # 16 query heads on one KV head
     (32, 2048, 32, 8, 512, False),   # Llama-3-8B heads, 32 sequences
