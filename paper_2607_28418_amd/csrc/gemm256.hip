@@ -1,4 +1,4 @@
-// Large-tile prefill kernels (256 x 256 tiles, 8 waves, direct-to-LDS loads).
+// Large-tile prefill kernels (256 x 256 tiles, 4 waves, direct-to-LDS loads).
 //
 //   wide_mn256<SWIGLU,BK>  N-axis masked projection (GEMM-MN): gate/up + SwiGLU
 //                          (one tile = 256 sorted tokens x one 128-column slice
@@ -12,7 +12,7 @@
 // (1)-(3); Section 3.3; Appendix B, Algorithms 2 and 3); only the tile engine
 // differs (tile256.h).  Tiles whose 256 rows are all active take the
 // all-active path (no per-fragment tests), as the paper does for full tiles
-// of a sorted column.
+// of a sorted column.  BK is the ring's k depth, 64.
 #include "common.h"
 #include "kernels.h"
 #include "launch.h"
@@ -25,14 +25,12 @@ using namespace t256;
 namespace {
 __device__ __attribute__((aligned(16))) uint16_t g_zero_blk[64];  // stays zero: never written
 
-// Rings: two stages of BK = 64 (128 KB).  The kernels are written for any
-// stage depth; with BK = 32 the ring would take five stages (all of LDS), or
-// four in the K-axis dense-masked kernel, which keeps 17 KB for the tile's
-// mask bits.  Only BK = 64 is launched (32-deep stages measured slower).
-template <int BK>
-using RingMN = Ring<BK, BK == 64 ? 2 : 5>;
-template <int BK>
-using RingKD = Ring<BK, BK == 64 ? 2 : 4>;
+// Rings: three stages of A and two of B (160 KB, all of LDS), except the
+// dense-masked K-axis kernel over more than 128 groups, which keeps 17 KB for
+// its tile's mask bits and so runs two A stages.
+using RingMN = Ring<3>;
+template <int NWR>
+using RingKD = Ring<NWR == 0 ? 2 : 3>;
 
 // Epilogue row map.  Output rows go back to token order through a per-row
 // index (the reorder, or the pattern order); fetching it per output element
@@ -77,28 +75,30 @@ __device__ __forceinline__ uint32_t mask_bits32(const uint8_t* mr, int n, int ng
 // Tiles of one region that each XCD runs (the region padded to a multiple of 8).
 __host__ __device__ __forceinline__ int mn256_share(int tiles) { return (tiles + 7) / 8; }
 
-template <class Rg, class Src>
-__device__ __forceinline__ void run_tile(uint16_t* smem, int nsteps, Src src, int brow0, int brow1,
-                                         int live, f32x16 (&acc)[4][2]) {
-  // `live` marks the wave's fragments with active rows: always a prefix
-  // (rows past the active count, or past M, come last in a tile).
-  const int nlive = __builtin_popcount(__builtin_amdgcn_readfirstlane(live));
-  const bool aon = Rg::NS != 2 || (wave_id() & 3) < nlive;  // this wave's A load rows are multiplied
-  switch (nlive) {
-    case 4: mainloop<Rg, 4, true>(smem, nsteps, src, brow0, brow1, acc); break;
-    case 3:
-      if (aon) mainloop<Rg, 3, true>(smem, nsteps, src, brow0, brow1, acc);
-      else mainloop<Rg, 3, false>(smem, nsteps, src, brow0, brow1, acc);
-      break;
+// The k loop of one tile with the wave's live A fragments and A loads:
+// `act` tile rows are active, always a prefix (rows past the active count, or
+// past M, come last in a tile).
+template <class Rg, class Koff, class At>
+__device__ __forceinline__ void run_tile(uint16_t* smem, int nsteps, Koff koff, At at, const int (&bb)[4],
+                                         int64_t act, f32x16 (&acc)[4][4]) {
+  const int p = (int)(act < 0 ? 0 : act > BM ? BM : act);
+  const int w = wave_id(), wm = w >> 1;
+  const int nl = min(4, max(0, (p - wm * 128 + 31) / 32));  // live A fragments of the wave
+  const bool aon = 64 * w < p;                              // the wave's A load rows [64 w, 64 w + 64)
+  // (nl, aon): (4|3, true) full or nearly; (2|1, true|false); (0, false) -- the
+  // waves of the lower half of a tile with at most 128 active rows
+  switch (nl) {
+    case 4: mainloop<Rg, 4, true>(smem, nsteps, koff, at, bb, acc); break;
+    case 3: mainloop<Rg, 3, true>(smem, nsteps, koff, at, bb, acc); break;
     case 2:
-      if (aon) mainloop<Rg, 2, true>(smem, nsteps, src, brow0, brow1, acc);
-      else mainloop<Rg, 2, false>(smem, nsteps, src, brow0, brow1, acc);
+      if (aon) mainloop<Rg, 2, true>(smem, nsteps, koff, at, bb, acc);
+      else mainloop<Rg, 2, false>(smem, nsteps, koff, at, bb, acc);
       break;
     case 1:
-      if (aon) mainloop<Rg, 1, true>(smem, nsteps, src, brow0, brow1, acc);
-      else mainloop<Rg, 1, false>(smem, nsteps, src, brow0, brow1, acc);
+      if (aon) mainloop<Rg, 1, true>(smem, nsteps, koff, at, bb, acc);
+      else mainloop<Rg, 1, false>(smem, nsteps, koff, at, bb, acc);
       break;
-    default: mainloop<Rg, 0, Rg::NS != 2>(smem, nsteps, src, brow0, brow1, acc); break;
+    default: mainloop<Rg, 0, false>(smem, nsteps, koff, at, bb, acc); break;
   }
 }
 }  // namespace
@@ -271,7 +271,8 @@ __device__ __forceinline__ void mn256_chunk_steps(int K, int c, int n, int& s0, 
 template <bool SWIGLU, int BK>
 __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
-  using Rg = RingMN<BK>;
+  static_assert(BK == t256::BK, "64-deep ring");
+  using Rg = RingMN;
   constexpr int S = Rg::SLOTS;
   constexpr int BNO = SWIGLU ? 128 : 256;  // output columns per tile
   const uint16_t* zero = g_zero_blk;
@@ -377,31 +378,29 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
     else
       bbase[j] = R.w0 + (int64_t)(n0 + rr) * K + c8;
   }
-  const int lane = lane_id(), w = wave_id();
-  const int wm = w >> 2, wn = w & 3;
-  const int l32 = lane & 31;
-  const int brow0 = SWIGLU ? wn * 32 + l32 : wn * 64 + l32;
-  const int brow1 = SWIGLU ? 128 + wn * 32 + l32 : wn * 64 + 32 + l32;
-  int live = 0;  // l = 2: fragments wholly past the active prefix issue no MFMA
+  // B fragments of the wave: SwiGLU pairs gate column c (B rows 0..127) with
+  // up column c (B rows 128..255), so a wave takes 64 gate rows (fragments 0
+  // and 1) and the same 64 up rows (fragments 2 and 3)
+  const int wn = wave_id() & 1;
+  int bb[4];
 #pragma unroll
-  for (int fm = 0; fm < 4; ++fm)
-    if (m0 + wm * 128 + fm * 32 < cnt) live |= 1 << fm;
+  for (int fn = 0; fn < 4; ++fn)
+    bb[fn] = SWIGLU ? (fn >> 1) * 128 + wn * 64 + (fn & 1) * 32 : wn * 128 + fn * 32;
 
-  f32x16 acc[4][2];
+  f32x16 acc[4][4];
   zero_acc(acc);
   int s0 = 0, ns = K / BK;  // a tail chunk runs its share of the k steps
   if (job >= 0) mn256_chunk_steps<BK>(K, chunk, nchunks, s0, ns);
-  auto src = [&](int s, const uint16_t* (&ap)[S], const uint16_t* (&bp)[S]) {
-    const int k0 = (s0 + s) * BK;
-#pragma unroll
-    for (int j = 0; j < S; ++j) {
-      ap[j] = abase[j] ? abase[j] + k0 : zero;
-      bp[j] = bbase[j] + k0;
-    }
+  auto koff = [&](int s) { return (s0 + s) * BK; };
+  auto at = [&](int k0, int j, int op) -> const uint16_t* {
+    if (op) return bbase[j] + k0;
+    return abase[j] ? abase[j] + k0 : zero;
   };
   int my_row = -1;
   if (job < 0 && tid < BM && m0 + tid < M) my_row = rows ? rows[m0 + tid] : (int)(m0 + tid);
-  run_tile<Rg>(smem, ns, src, brow0, brow1, live, acc);
+  // l = 2: fragments wholly past the active prefix issue no MFMA
+  run_tile<Rg>(smem, ns, koff, at, bb, cnt - m0, acc);
+  const int col = acc_col();
 
   if (job >= 0) {  // tail chunk: fp32 partial tile [256 rows][256 B-tile rows]
     float* P = a.tail_ws + ((int64_t)xcd * kMN256TailJobs + job) * (BM * BN);
@@ -410,8 +409,8 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int r = acc_row(fm, i);
-        P[r * BN + brow0] = acc[fm][0][i];
-        P[r * BN + brow1] = acc[fm][1][i];
+#pragma unroll
+        for (int fn = 0; fn < 4; ++fn) P[r * BN + bb[fn] + col] = acc[fm][fn][i];
       }
     return;
   }
@@ -419,10 +418,8 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
   // Epilogue: rows back to token order; rows past cnt hold +0 accumulators.
   // A token-order region stores +0 where the row's group is inactive.
   const int* map = stage_row_map(smem, my_row, (int)rbits);
-  const int col = acc_col();
   const int gsh = tok_order ? __builtin_ctz(a.mask_G) : 0;
-  const int c0 = SWIGLU ? wn * 32 + col : wn * 64 + col;  // tile columns of the two fragments
-  const int c1 = SWIGLU ? c0 : c0 + 32;
+  constexpr int NO = SWIGLU ? 2 : 4;  // output fragments of the wave
 #pragma unroll
   for (int fm = 0; fm < 4; ++fm) {
 #pragma unroll
@@ -431,14 +428,13 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
       const int t = map[r];
       if (t < 0) continue;
       const int rb = tok_order ? map[BM + r] : 0;
-      const bool on0 = !tok_order || ((rb >> (c0 >> gsh)) & 1);
-      const bool on1 = !tok_order || ((rb >> (c1 >> gsh)) & 1);
       uint16_t* o = R.out + (int64_t)t * R.ldo + n0;
-      if (SWIGLU) {
-        o[c0] = f32_to_bf16_hw(on0 ? silu(acc[fm][0][i]) * acc[fm][1][i] : 0.f);
-      } else {
-        o[c0] = f32_to_bf16_hw(on0 ? acc[fm][0][i] : 0.f);
-        o[c1] = f32_to_bf16_hw(on1 ? acc[fm][1][i] : 0.f);
+#pragma unroll
+      for (int fn = 0; fn < NO; ++fn) {
+        const int c = bb[fn] + col;  // output column in the tile
+        const bool on = !tok_order || ((rb >> (c >> gsh)) & 1);
+        const float v = SWIGLU ? silu(acc[fm][fn][i]) * acc[fm][fn + 2][i] : acc[fm][fn][i];
+        o[c] = f32_to_bf16_hw(on ? v : 0.f);
       }
     }
   }
@@ -532,15 +528,29 @@ __device__ __forceinline__ void kd256_coords(int n_tiles, int m_tiles, int& m_ti
   n_tile = tile % n_tiles;
 }
 
+// Mask tables of a dense-masked tile: the rows' mask bits, the groups some
+// row uses (ascending), their union and count.  With NWR > 0 they live in the
+// ring's LDS before its first load and move to registers (the ring then takes
+// all of LDS); with NWR = 0 they sit past a ring of two A stages.
+struct KdTables {
+  uint32_t mbits[BM][kKd256MaxGroups / 32];
+  uint16_t groups[kKd256MaxGroups];
+  uint32_t uni[kKd256MaxGroups / 32];
+  int n_live;
+};
+template <int NWR>
+constexpr int kd256_lds() {
+  return NWR == 0 ? RingKD<0>::LDS + (int)sizeof(KdTables) : RingKD<NWR>::LDS;
+}
+static_assert(kd256_lds<0>() <= LDS_MAX && (int)sizeof(KdTables) <= RingKD<4>::LDS, "tables fit");
+
 template <int NWR, int BK>
 __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
+  static_assert(BK == t256::BK, "64-deep ring");
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
-  __shared__ uint32_t s_mbits[BM][kKd256MaxGroups / 32];  // mask bits of the tile's rows
-  __shared__ uint16_t s_groups[kKd256MaxGroups];          // groups with an active row, ascending
-  __shared__ uint32_t s_union[kKd256MaxGroups / 32];       // union of the tile's mask rows
-  __shared__ int s_ng_live;
-  using Rg = RingKD<BK>;
+  using Rg = RingKD<NWR>;
   constexpr int S = Rg::SLOTS;
+  KdTables& tb = *reinterpret_cast<KdTables*>(reinterpret_cast<char*>(smem) + (NWR == 0 ? Rg::LDS : 0));
   const uint16_t* zero = g_zero_blk;
   const int n_tiles = a.N / BN;
   int m_tile, n_tile;
@@ -551,7 +561,7 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
   const int nw = (ng + 31) / 32;
   const int tid = threadIdx.x;
 
-  if (tid < nw) s_union[tid] = 0u;
+  if (tid < nw) tb.uni[tid] = 0u;
   __syncthreads();
   // Tile row r is token m0 + r, or perm[m0 + r] when the rows are ordered by
   // mask pattern (rows that share groups then share the tile).
@@ -562,26 +572,26 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
     const int64_t t = p < a.M ? token(p) : a.M;
     uint32_t bits = 0;
     if (t < a.M) bits = mask_bits32(a.mask + t * ng + wd * 32, min(32, ng - wd * 32), ng);
-    s_mbits[r][wd] = bits;
-    if (bits) atomicOr(&s_union[wd], bits);
+    tb.mbits[r][wd] = bits;
+    if (bits) atomicOr(&tb.uni[wd], bits);
   }
   __syncthreads();
   // groups some row of the tile uses, ascending: thread g places group g at
   // the count of union bits below it (no serial pass over the union)
-  if (tid < nw * 32) {
-    const int wd = tid >> 5, b = tid & 31;
-    int pos = __builtin_popcount(s_union[wd] & ((1u << b) - 1u));
-    for (int i = 0; i < wd; ++i) pos += __builtin_popcount(s_union[i]);
-    if ((s_union[wd] >> b) & 1u) s_groups[pos] = (uint16_t)tid;
-    if (tid == 0) {
+  for (int gi = tid; gi < nw * 32; gi += NT) {
+    const int wd = gi >> 5, b = gi & 31;
+    int pos = __builtin_popcount(tb.uni[wd] & ((1u << b) - 1u));
+    for (int i = 0; i < wd; ++i) pos += __builtin_popcount(tb.uni[i]);
+    if ((tb.uni[wd] >> b) & 1u) tb.groups[pos] = (uint16_t)gi;
+    if (gi == 0) {
       int n = 0;
-      for (int i = 0; i < nw; ++i) n += __builtin_popcount(s_union[i]);
-      s_ng_live = n;
+      for (int i = 0; i < nw; ++i) n += __builtin_popcount(tb.uni[i]);
+      tb.n_live = n;
     }
   }
   __syncthreads();
   const int spg = a.G / BK;  // k steps per group
-  const int nsteps = s_ng_live * spg;
+  const int nsteps = __builtin_amdgcn_readfirstlane(tb.n_live) * spg;
 
   int srow[S];
   const uint16_t* abase[S];
@@ -595,60 +605,61 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
     abase[j] = p < a.M ? a.a + token(p) * a.K + c8 : nullptr;
     bbase[j] = a.w + (int64_t)(n0 + rr) * a.K + c8;
   }
-  const int lane = lane_id(), w = wave_id();
-  const int wm = w >> 2, wn = w & 3;
-  const int l32 = lane & 31;
-  const int brow0 = wn * 64 + l32, brow1 = wn * 64 + 32 + l32;
-  int live = 0;
+  const int lane = lane_id(), wn = wave_id() & 1;
+  int bb[4];
 #pragma unroll
-  for (int fm = 0; fm < 4; ++fm)
-    if (m0 + wm * 128 + fm * 32 < a.M) live |= 1 << fm;
+  for (int fn = 0; fn < 4; ++fn) bb[fn] = wn * 128 + fn * 32;
 
-  f32x16 acc[4][2];
+  f32x16 acc[4][4];
   zero_acc(acc);
   // Every step needs, per slot row, one bit of its mask row.  Reading them
   // from LDS at each step put several dependent LDS round trips in front of
   // the step's loads; with NWR > 0 the rows' mask words sit in registers
-  // (rows past M hold zero words, so their blocks read as zeros).
+  // (rows past M hold zero words, so their blocks read as zeros), and so
+  // does the union's group list: lane l holds groups l and 64 + l, and a
+  // step takes its group with a readlane.
   // (words past the row's last group are never selected: any value will do)
   uint64_t mlo[S], mhi[S];
 #pragma unroll
   for (int j = 0; j < S; ++j) {
     mlo[j] = mhi[j] = 0;
-    if (NWR >= 1) mlo[j] = s_mbits[srow[j]][0];
+    if (NWR >= 1) mlo[j] = tb.mbits[srow[j]][0];
     if (NWR >= 4) {
-      mlo[j] |= (uint64_t)s_mbits[srow[j]][1] << 32;
-      mhi[j] = s_mbits[srow[j]][2] | (uint64_t)s_mbits[srow[j]][3] << 32;
+      mlo[j] |= (uint64_t)tb.mbits[srow[j]][1] << 32;
+      mhi[j] = tb.mbits[srow[j]][2] | (uint64_t)tb.mbits[srow[j]][3] << 32;
     }
   }
-  const uint32_t u0 = s_union[0];
-  auto src = [&](int s, const uint16_t* (&ap)[S], const uint16_t* (&bp)[S]) {
-    const int gi = s / spg;
-    int gg;
-    if (NWR == 1) {  // gi-th group of the tile's union (one word, kept in scalars)
-      uint32_t u = u0;
-      for (int i = 0; i < gi; ++i) u &= u - 1;
-      gg = __builtin_ctz(u);
-    } else {
-      gg = s_groups[gi];
+  const int glo = NWR >= 1 ? tb.groups[lane] : 0;
+  const int ghi = NWR >= 4 ? tb.groups[64 + lane] : 0;
+  if (NWR > 0) __syncthreads();  // the ring's first loads overwrite the tables
+  auto group = [&](int gi) -> int {  // gi-th group of the tile's union
+    if (NWR == 1) return __builtin_amdgcn_readlane(glo, gi);
+    if (NWR == 4) {  // both reads and a scalar select: no branch in the k loop
+      const int lo = __builtin_amdgcn_readlane(glo, gi & 63), hi = __builtin_amdgcn_readlane(ghi, gi & 63);
+      return gi < 64 ? lo : hi;
     }
-    const int k0 = gg * a.G + (s - gi * spg) * BK;
-#pragma unroll
-    for (int j = 0; j < S; ++j) {
-      bool on;
-      if (NWR == 0)
-        on = (s_mbits[srow[j]][gg >> 5] >> (gg & 31)) & 1u;
-      else if (NWR == 1)
-        on = (mlo[j] >> gg) & 1u;
-      else
-        on = ((gg < 64 ? mlo[j] : mhi[j]) >> (gg & 63)) & 1u;
-      ap[j] = on ? abase[j] + k0 : zero;  // inactive (t, g) blocks are never read
-      bp[j] = bbase[j] + k0;
-    }
+    return tb.groups[gi];
+  };
+  const int lg = __builtin_ctz(a.G), lsp = lg - 6;  // G is a power of two, at least BK
+  auto koff = [&](int s) {
+    const int gi = s >> lsp;
+    return group(gi) * a.G + (s & (spg - 1)) * BK;
+  };
+  auto at = [&](int k0, int j, int op) -> const uint16_t* {
+    if (op) return bbase[j] + k0;
+    const int gg = k0 >> lg;
+    bool on;
+    if (NWR == 0)
+      on = (tb.mbits[srow[j]][gg >> 5] >> (gg & 31)) & 1u;
+    else if (NWR == 1)
+      on = (mlo[j] >> gg) & 1u;
+    else
+      on = ((gg < 64 ? mlo[j] : mhi[j]) >> (gg & 63)) & 1u;
+    return on ? abase[j] + k0 : zero;  // inactive (t, g) blocks are never read
   };
   int my_row = -1;
   if (tid < BM && m0 + tid < a.M) my_row = (int)token(m0 + tid);
-  run_tile<Rg>(smem, nsteps, src, brow0, brow1, live, acc);
+  run_tile<Rg>(smem, nsteps, koff, at, bb, a.M - m0, acc);
 
   const int* map = stage_row_map(smem, my_row);
   const int col = acc_col();
@@ -658,9 +669,9 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
     for (int i = 0; i < 16; ++i) {
       const int t = map[acc_row(fm, i)];
       if (t < 0) continue;
-      uint16_t* o = a.y + (int64_t)t * a.N + n0 + wn * 64;
-      o[col] = f32_to_bf16_hw(acc[fm][0][i]);
-      o[32 + col] = f32_to_bf16_hw(acc[fm][1][i]);
+      uint16_t* o = a.y + (int64_t)t * a.N + n0 + col;
+#pragma unroll
+      for (int fn = 0; fn < 4; ++fn) o[bb[fn]] = f32_to_bf16_hw(acc[fm][fn][i]);
     }
 }
 
@@ -673,8 +684,9 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
 // slab runs on the same XCD.
 template <int BK>
 __global__ __launch_bounds__(NT, 1) void wide_ks256(KArgs a) {
+  static_assert(BK == t256::BK, "64-deep ring");
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
-  using Rg = RingMN<BK>;
+  using Rg = RingMN;
   constexpr int S = Rg::SLOTS;
   const uint16_t* zero = g_zero_blk;
   const int n_tiles = a.N / BN;
@@ -697,10 +709,10 @@ __global__ __launch_bounds__(NT, 1) void wide_ks256(KArgs a) {
   const int g_end = min(ng, (split + 1) * a.pack);
   const int64_t m0 = (int64_t)m_tile * BM;
   const int n0 = n_tile * BN;
-  const int lane = lane_id(), w = wave_id();
-  const int wm = w >> 2, wn = w & 3;
-  const int l32 = lane & 31;
-  const int brow0 = wn * 64 + l32, brow1 = wn * 64 + 32 + l32;
+  const int wn = wave_id() & 1;
+  int bb[4];
+#pragma unroll
+  for (int fn = 0; fn < 4; ++fn) bb[fn] = wn * 128 + fn * 32;
   const int col = acc_col();
   const int* map = reinterpret_cast<const int*>(smem);
   for (int g = split * a.pack; g < g_end; ++g) {
@@ -717,36 +729,28 @@ __global__ __launch_bounds__(NT, 1) void wide_ks256(KArgs a) {
       abase[j] = p < cnt ? a.a + (int64_t)rows[p] * a.K + c8 : nullptr;  // l = 1
       bbase[j] = a.w + (int64_t)(n0 + rr) * a.K + c8;
     }
-    int live = 0;  // l = 2
-#pragma unroll
-    for (int fm = 0; fm < 4; ++fm)
-      if (m0 + wm * 128 + fm * 32 < cnt) live |= 1 << fm;
-    f32x16 acc[4][2];
+    f32x16 acc[4][4];
     zero_acc(acc);
     const int kbeg = g * a.G;
-    auto src = [&](int s, const uint16_t* (&ap)[S], const uint16_t* (&bp)[S]) {
-      const int k0 = kbeg + s * BK;
-#pragma unroll
-      for (int j = 0; j < S; ++j) {
-        ap[j] = abase[j] ? abase[j] + k0 : zero;
-        bp[j] = bbase[j] + k0;
-      }
+    auto koff = [&](int s) { return kbeg + s * BK; };
+    auto at = [&](int k0, int j, int op) -> const uint16_t* {
+      if (op) return bbase[j] + k0;
+      return abase[j] ? abase[j] + k0 : zero;
     };
     int my_row = -1;
     if ((int)threadIdx.x < BM && m0 + (int)threadIdx.x < cnt) my_row = rows[m0 + threadIdx.x];
     __syncthreads();  // the previous group's epilogue is done with the row map in the ring
-    run_tile<Rg>(smem, a.G / BK, src, brow0, brow1, live, acc);
+    run_tile<Rg>(smem, a.G / BK, koff, at, bb, cnt - m0, acc);  // l = 2: dead fragments skipped
     stage_row_map(smem, my_row);
 #pragma unroll
     for (int fm = 0; fm < 4; ++fm) {
-      if (!(live & (1 << fm))) continue;
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int t = map[acc_row(fm, i)];
         if (t < 0) continue;
-        float* o = a.acc32 + (int64_t)t * a.N + n0 + wn * 64;
-        unsafeAtomicAdd(o + col, acc[fm][0][i]);
-        unsafeAtomicAdd(o + 32 + col, acc[fm][1][i]);
+        float* o = a.acc32 + (int64_t)t * a.N + n0 + col;
+#pragma unroll
+        for (int fn = 0; fn < 4; ++fn) unsafeAtomicAdd(o + bb[fn], acc[fm][fn][i]);
       }
     }
   }
@@ -768,22 +772,12 @@ hipError_t prepare() {
 }
 }  // namespace
 
-// Stages of k depth 64 (two in the ring).  The kernels are written for any
-// stage depth; 32-deep stages (five in the ring) ran slower on MI355X and
-// are not instantiated.
-#define WIDE_RING_LAUNCH(NAME, KT, RG, GRID, STREAM, ARGS)                                        \
+#define WIDE_RING_LAUNCH(NAME, KERN, LDSB, GRID, STREAM, ARGS)                                    \
   do {                                                                                            \
-    hipError_t e_ = prepare<KT(64), RG<64>::LDS>();                                               \
+    hipError_t e_ = prepare<KERN, LDSB>();                                                        \
     if (e_ != hipSuccess) return e_;                                                              \
-    WIDE_LAUNCH_NAMED(NAME "/bk64", (KT(64)), dim3(GRID), dim3(NT), RG<64>::LDS, STREAM, ARGS);   \
+    WIDE_LAUNCH_NAMED(NAME "/bk64", (KERN), dim3(GRID), dim3(NT), LDSB, STREAM, ARGS);            \
   } while (0)
-
-#define MN_SW(bk) wide_mn256<true, bk>
-#define MN_PL(bk) wide_mn256<false, bk>
-#define KD(bk) wide_kd256<0, bk>
-#define KD1(bk) wide_kd256<1, bk>
-#define KD4(bk) wide_kd256<4, bk>
-#define KS(bk) wide_ks256<bk>
 
 hipError_t launch_mn256(const MN256Args& a, bool swiglu, hipStream_t s) {
   int64_t total = 0;
@@ -791,9 +785,9 @@ hipError_t launch_mn256(const MN256Args& a, bool swiglu, hipStream_t s) {
   if (total == 0) return hipSuccess;
   if (a.tail) total += 8 * kMN256TailJobs;  // the tail blocks of every XCD, dispatched last
   if (swiglu)
-    WIDE_RING_LAUNCH("wide_mn256<true>", MN_SW, RingMN, (unsigned)total, s, a);
+    WIDE_RING_LAUNCH("wide_mn256<true>", (wide_mn256<true, 64>), RingMN::LDS, (unsigned)total, s, a);
   else
-    WIDE_RING_LAUNCH("wide_mn256<false>", MN_PL, RingMN, (unsigned)total, s, a);
+    WIDE_RING_LAUNCH("wide_mn256<false>", (wide_mn256<false, 64>), RingMN::LDS, (unsigned)total, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !a.tail) return e;
   const dim3 tg(8 * kMN256TailJobs * (BM / kTailRows));
@@ -822,11 +816,11 @@ hipError_t launch_kd256(const KArgs& a, hipStream_t s) {
   if (a.K / a.G > kKd256MaxGroups) return hipErrorInvalidValue;
   const int ng = a.K / a.G;
   if (ng <= 32)
-    WIDE_RING_LAUNCH("wide_kd256<1>", KD1, RingKD, (unsigned)total, s, a);
+    WIDE_RING_LAUNCH("wide_kd256<1>", (wide_kd256<1, 64>), kd256_lds<1>(), (unsigned)total, s, a);
   else if (ng <= 128)
-    WIDE_RING_LAUNCH("wide_kd256<4>", KD4, RingKD, (unsigned)total, s, a);
+    WIDE_RING_LAUNCH("wide_kd256<4>", (wide_kd256<4, 64>), kd256_lds<4>(), (unsigned)total, s, a);
   else
-    WIDE_RING_LAUNCH("wide_kd256<0>", KD, RingKD, (unsigned)total, s, a);
+    WIDE_RING_LAUNCH("wide_kd256<0>", (wide_kd256<0, 64>), kd256_lds<0>(), (unsigned)total, s, a);
   return hipGetLastError();
 }
 
@@ -836,7 +830,7 @@ hipError_t launch_ks256(const KArgs& a, hipStream_t s) {
   const int64_t splits = (a.K / a.G + pack - 1) / pack;
   const int64_t total = splits * m_tiles * (a.N / BN);
   if (total == 0) return hipSuccess;
-  WIDE_RING_LAUNCH("wide_ks256", KS, RingMN, (unsigned)total, s, a);
+  WIDE_RING_LAUNCH("wide_ks256", (wide_ks256<64>), RingMN::LDS, (unsigned)total, s, a);
   return hipGetLastError();
 }
 
