@@ -79,6 +79,17 @@ __device__ __forceinline__ void stg16(void* p, u32x4 v) {
 typedef __amdgpu_buffer_rsrc_t bufview_t;
 constexpr uint32_t kOffNone = 0xFFFFFFF0u;
 
+// A pointer the whole wave shares, moved to scalar registers: a buffer view
+// built from a value the compiler cannot prove uniform is loaded through a
+// per-lane loop over the distinct values.
+template <class T>
+__device__ __forceinline__ T* uniform_ptr(T* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return reinterpret_cast<T*>(((uint64_t)hi << 32) | lo);
+}
+
 __device__ __forceinline__ bufview_t buf_view(const void* base, uint32_t bytes) {
   // third descriptor word of the gfx9 family: 32-bit data format, no swizzle
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
@@ -88,8 +99,9 @@ __device__ __forceinline__ u32x4 buf_ld16(bufview_t v, uint32_t byte_off) {
   return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(v, (int)byte_off, 0, 0));
 }
 
-// The same with a workgroup-uniform part of the offset in a scalar register
-// (no range check applies to it: the sum must lie inside the view).
+// The same with a workgroup-uniform part of the offset in a scalar register.
+// The range check applies to the sum (dword by dword): a lane reads zeros
+// where byte_off + uniform_off lies past the view's end.
 __device__ __forceinline__ u32x4 buf_ld16s(bufview_t v, uint32_t byte_off, uint32_t uniform_off) {
   return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(v, (int)byte_off, (int)uniform_off, 0));
 }

@@ -78,8 +78,8 @@ __host__ __device__ __forceinline__ int mn256_share(int tiles) { return (tiles +
 // The k loop of one tile with the wave's live A fragments and A loads:
 // `act` tile rows are active, always a prefix (rows past the active count, or
 // past M, come last in a tile).
-template <class Rg, class Koff, class At>
-__device__ __forceinline__ void run_tile(uint16_t* smem, int nsteps, Koff koff, At at, const int (&bb)[4],
+template <class Rg, class Koff, class LdA, class LdB>
+__device__ __forceinline__ void run_tile(uint16_t* smem, int nsteps, Koff koff, LdA lda, LdB ldb, const int (&bb)[4],
                                          int64_t act, f32x16 (&acc)[4][4]) {
   const int p = (int)(act < 0 ? 0 : act > BM ? BM : act);
   const int w = wave_id(), wm = w >> 1;
@@ -88,17 +88,17 @@ __device__ __forceinline__ void run_tile(uint16_t* smem, int nsteps, Koff koff, 
   // (nl, aon): (4|3, true) full or nearly; (2|1, true|false); (0, false) -- the
   // waves of the lower half of a tile with at most 128 active rows
   switch (nl) {
-    case 4: mainloop<Rg, 4, true>(smem, nsteps, koff, at, bb, acc); break;
-    case 3: mainloop<Rg, 3, true>(smem, nsteps, koff, at, bb, acc); break;
+    case 4: mainloop<Rg, 4, true>(smem, nsteps, koff, lda, ldb, bb, acc); break;
+    case 3: mainloop<Rg, 3, true>(smem, nsteps, koff, lda, ldb, bb, acc); break;
     case 2:
-      if (aon) mainloop<Rg, 2, true>(smem, nsteps, koff, at, bb, acc);
-      else mainloop<Rg, 2, false>(smem, nsteps, koff, at, bb, acc);
+      if (aon) mainloop<Rg, 2, true>(smem, nsteps, koff, lda, ldb, bb, acc);
+      else mainloop<Rg, 2, false>(smem, nsteps, koff, lda, ldb, bb, acc);
       break;
     case 1:
-      if (aon) mainloop<Rg, 1, true>(smem, nsteps, koff, at, bb, acc);
-      else mainloop<Rg, 1, false>(smem, nsteps, koff, at, bb, acc);
+      if (aon) mainloop<Rg, 1, true>(smem, nsteps, koff, lda, ldb, bb, acc);
+      else mainloop<Rg, 1, false>(smem, nsteps, koff, lda, ldb, bb, acc);
       break;
-    default: mainloop<Rg, 0, false>(smem, nsteps, koff, at, bb, acc); break;
+    default: mainloop<Rg, 0, false>(smem, nsteps, koff, lda, ldb, bb, acc); break;
   }
 }
 }  // namespace
@@ -268,7 +268,7 @@ __device__ __forceinline__ void mn256_chunk_steps(int K, int c, int n, int& s0, 
 }
 
 // --------------------------------------------------------------------- GEMM-MN
-template <bool SWIGLU, int BK>
+template <bool SWIGLU, int BK, bool BUF>
 __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   static_assert(BK == t256::BK, "64-deep ring");
@@ -364,6 +364,12 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
     return;
   }
 
+  // Sources of the lane's load slots.  l = 1: rows past the active prefix
+  // read zeros.  Under SwiGLU waves 0 and 1 load gate rows, 2 and 3 up rows.
+  const uint16_t* wpanel = uniform_ptr((SWIGLU && wave_id() >= 2 ? R.w1 : R.w0) + (int64_t)n0 * K);
+  const bufview_t va = buf_view(uniform_ptr(a.x), BUF ? (uint32_t)(M * K * 2) : 0u);
+  const bufview_t vb = buf_view(wpanel, BUF ? (uint32_t)((SWIGLU ? 128 : 256) * K * 2) : 0u);
+  uint32_t aoff[S], boff[S];
   const uint16_t* abase[S];
   const uint16_t* bbase[S];
 #pragma unroll
@@ -371,12 +377,15 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
     const int rr = Rg::slot_row(j);
     const int c8 = Rg::slot_chunk(j) * 8;
     const int64_t p = m0 + rr;
-    // l = 1: rows past the active prefix read the zero block
-    abase[j] = p < cnt ? a.x + (rows ? (int64_t)rows[p] : p) * K + c8 : nullptr;
-    if (SWIGLU)
-      bbase[j] = rr < 128 ? R.w0 + (int64_t)(n0 + rr) * K + c8 : R.w1 + (int64_t)(n0 + rr - 128) * K + c8;
-    else
-      bbase[j] = R.w0 + (int64_t)(n0 + rr) * K + c8;
+    const int64_t arow = p < cnt ? (rows ? (int64_t)rows[p] : p) : -1;
+    const int64_t brow = SWIGLU ? (rr & 127) : rr;
+    if (BUF) {
+      aoff[j] = arow >= 0 ? (uint32_t)((arow * K + c8) * 2) : kOffDead;
+      boff[j] = (uint32_t)((brow * K + c8) * 2);
+    } else {
+      abase[j] = arow >= 0 ? a.x + arow * K + c8 : nullptr;
+      bbase[j] = wpanel + brow * K + c8;
+    }
   }
   // B fragments of the wave: SwiGLU pairs gate column c (B rows 0..127) with
   // up column c (B rows 128..255), so a wave takes 64 gate rows (fragments 0
@@ -392,14 +401,18 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
   int s0 = 0, ns = K / BK;  // a tail chunk runs its share of the k steps
   if (job >= 0) mn256_chunk_steps<BK>(K, chunk, nchunks, s0, ns);
   auto koff = [&](int s) { return (s0 + s) * BK; };
-  auto at = [&](int k0, int j, int op) -> const uint16_t* {
-    if (op) return bbase[j] + k0;
-    return abase[j] ? abase[j] + k0 : zero;
+  auto lda = [&](uint16_t* st, int k0, int j) {
+    if (BUF) Rg::issue_buf(st, va, aoff[j], 2u * k0, j);
+    else Rg::issue_ptr(st, abase[j] ? abase[j] + k0 : zero, j);
+  };
+  auto ldb = [&](uint16_t* st, int k0, int j) {
+    if (BUF) Rg::issue_buf(st, vb, boff[j], 2u * k0, j);
+    else Rg::issue_ptr(st, bbase[j] + k0, j);
   };
   int my_row = -1;
   if (job < 0 && tid < BM && m0 + tid < M) my_row = rows ? rows[m0 + tid] : (int)(m0 + tid);
   // l = 2: fragments wholly past the active prefix issue no MFMA
-  run_tile<Rg>(smem, ns, koff, at, bb, cnt - m0, acc);
+  run_tile<Rg>(smem, ns, koff, lda, ldb, bb, cnt - m0, acc);
   const int col = acc_col();
 
   if (job >= 0) {  // tail chunk: fp32 partial tile [256 rows][256 B-tile rows]
@@ -544,7 +557,7 @@ constexpr int kd256_lds() {
 }
 static_assert(kd256_lds<0>() <= LDS_MAX && (int)sizeof(KdTables) <= RingKD<4>::LDS, "tables fit");
 
-template <int NWR, int BK>
+template <int NWR, int BK, bool BUF>
 __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
   static_assert(BK == t256::BK, "64-deep ring");
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
@@ -594,6 +607,10 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
   const int nsteps = __builtin_amdgcn_readfirstlane(tb.n_live) * spg;
 
   int srow[S];
+  const uint16_t* wpanel = uniform_ptr(a.w + (int64_t)n0 * a.K);
+  const bufview_t va = buf_view(uniform_ptr(a.a), BUF ? (uint32_t)(a.M * a.K * 2) : 0u);
+  const bufview_t vb = buf_view(wpanel, BUF ? (uint32_t)(BN * a.K * 2) : 0u);
+  uint32_t aoff[S], boff[S];
   const uint16_t* abase[S];
   const uint16_t* bbase[S];
 #pragma unroll
@@ -601,9 +618,15 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
     const int rr = Rg::slot_row(j);
     const int c8 = Rg::slot_chunk(j) * 8;
     const int64_t p = m0 + rr;
+    const int64_t arow = p < a.M ? token(p) : -1;
     srow[j] = rr;
-    abase[j] = p < a.M ? a.a + token(p) * a.K + c8 : nullptr;
-    bbase[j] = a.w + (int64_t)(n0 + rr) * a.K + c8;
+    if (BUF) {
+      aoff[j] = arow >= 0 ? (uint32_t)((arow * a.K + c8) * 2) : kOffDead;
+      boff[j] = (uint32_t)(((int64_t)rr * a.K + c8) * 2);
+    } else {
+      abase[j] = arow >= 0 ? a.a + arow * a.K + c8 : nullptr;
+      bbase[j] = wpanel + (int64_t)rr * a.K + c8;
+    }
   }
   const int lane = lane_id(), wn = wave_id() & 1;
   int bb[4];
@@ -638,15 +661,14 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
       const int lo = __builtin_amdgcn_readlane(glo, gi & 63), hi = __builtin_amdgcn_readlane(ghi, gi & 63);
       return gi < 64 ? lo : hi;
     }
-    return tb.groups[gi];
+    return __builtin_amdgcn_readfirstlane(tb.groups[gi]);  // one LDS word, the same for every lane
   };
   const int lg = __builtin_ctz(a.G), lsp = lg - 6;  // G is a power of two, at least BK
   auto koff = [&](int s) {
     const int gi = s >> lsp;
     return group(gi) * a.G + (s & (spg - 1)) * BK;
   };
-  auto at = [&](int k0, int j, int op) -> const uint16_t* {
-    if (op) return bbase[j] + k0;
+  auto lda = [&](uint16_t* st, int k0, int j) {
     const int gg = k0 >> lg;
     bool on;
     if (NWR == 0)
@@ -655,11 +677,17 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
       on = (mlo[j] >> gg) & 1u;
     else
       on = ((gg < 64 ? mlo[j] : mhi[j]) >> (gg & 63)) & 1u;
-    return on ? abase[j] + k0 : zero;  // inactive (t, g) blocks are never read
+    // inactive (t, g) blocks are never read
+    if (BUF) Rg::issue_buf(st, va, on ? aoff[j] : kOffDead, 2u * k0, j);
+    else Rg::issue_ptr(st, on ? abase[j] + k0 : zero, j);
+  };
+  auto ldb = [&](uint16_t* st, int k0, int j) {
+    if (BUF) Rg::issue_buf(st, vb, boff[j], 2u * k0, j);
+    else Rg::issue_ptr(st, bbase[j] + k0, j);
   };
   int my_row = -1;
   if (tid < BM && m0 + tid < a.M) my_row = (int)token(m0 + tid);
-  run_tile<Rg>(smem, nsteps, koff, at, bb, a.M - m0, acc);
+  run_tile<Rg>(smem, nsteps, koff, lda, ldb, bb, a.M - m0, acc);
 
   const int* map = stage_row_map(smem, my_row);
   const int col = acc_col();
@@ -682,7 +710,7 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
 // packs K-groups into one CTA).  When the column tiles divide among the 8
 // XCDs, workgroup ids are dealt so that every workgroup adding into a column
 // slab runs on the same XCD.
-template <int BK>
+template <int BK, bool BUF>
 __global__ __launch_bounds__(NT, 1) void wide_ks256(KArgs a) {
   static_assert(BK == t256::BK, "64-deep ring");
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
@@ -715,10 +743,14 @@ __global__ __launch_bounds__(NT, 1) void wide_ks256(KArgs a) {
   for (int fn = 0; fn < 4; ++fn) bb[fn] = wn * 128 + fn * 32;
   const int col = acc_col();
   const int* map = reinterpret_cast<const int*>(smem);
+  const uint16_t* wpanel = uniform_ptr(a.w + (int64_t)n0 * a.K);
+  const bufview_t va = buf_view(uniform_ptr(a.a), BUF ? (uint32_t)(a.M * a.K * 2) : 0u);
+  const bufview_t vb = buf_view(wpanel, BUF ? (uint32_t)(BN * a.K * 2) : 0u);
   for (int g = split * a.pack; g < g_end; ++g) {
     const int64_t cnt = a.cnt[g];
     if (m0 >= cnt) continue;  // l = 0 for this group
     const int32_t* rows = a.idx + (int64_t)g * a.M;
+    uint32_t aoff[S], boff[S];
     const uint16_t* abase[S];
     const uint16_t* bbase[S];
 #pragma unroll
@@ -726,21 +758,31 @@ __global__ __launch_bounds__(NT, 1) void wide_ks256(KArgs a) {
       const int rr = Rg::slot_row(j);
       const int c8 = Rg::slot_chunk(j) * 8;
       const int64_t p = m0 + rr;
-      abase[j] = p < cnt ? a.a + (int64_t)rows[p] * a.K + c8 : nullptr;  // l = 1
-      bbase[j] = a.w + (int64_t)(n0 + rr) * a.K + c8;
+      const int64_t arow = p < cnt ? (int64_t)rows[p] : -1;  // l = 1
+      if (BUF) {
+        aoff[j] = arow >= 0 ? (uint32_t)((arow * a.K + c8) * 2) : kOffDead;
+        boff[j] = (uint32_t)(((int64_t)rr * a.K + c8) * 2);
+      } else {
+        abase[j] = arow >= 0 ? a.a + arow * a.K + c8 : nullptr;
+        bbase[j] = wpanel + (int64_t)rr * a.K + c8;
+      }
     }
     f32x16 acc[4][4];
     zero_acc(acc);
     const int kbeg = g * a.G;
     auto koff = [&](int s) { return kbeg + s * BK; };
-    auto at = [&](int k0, int j, int op) -> const uint16_t* {
-      if (op) return bbase[j] + k0;
-      return abase[j] ? abase[j] + k0 : zero;
+    auto lda = [&](uint16_t* st, int k0, int j) {
+      if (BUF) Rg::issue_buf(st, va, aoff[j], 2u * k0, j);
+      else Rg::issue_ptr(st, abase[j] ? abase[j] + k0 : zero, j);
+    };
+    auto ldb = [&](uint16_t* st, int k0, int j) {
+      if (BUF) Rg::issue_buf(st, vb, boff[j], 2u * k0, j);
+      else Rg::issue_ptr(st, bbase[j] + k0, j);
     };
     int my_row = -1;
     if ((int)threadIdx.x < BM && m0 + (int)threadIdx.x < cnt) my_row = rows[m0 + threadIdx.x];
     __syncthreads();  // the previous group's epilogue is done with the row map in the ring
-    run_tile<Rg>(smem, a.G / BK, koff, at, bb, cnt - m0, acc);  // l = 2: dead fragments skipped
+    run_tile<Rg>(smem, a.G / BK, koff, lda, ldb, bb, cnt - m0, acc);  // l = 2: dead fragments skipped
     stage_row_map(smem, my_row);
 #pragma unroll
     for (int fm = 0; fm < 4; ++fm) {
@@ -779,15 +821,24 @@ hipError_t prepare() {
     WIDE_LAUNCH_NAMED(NAME "/bk64", (KERN), dim3(GRID), dim3(NT), LDSB, STREAM, ARGS);            \
   } while (0)
 
+// Buffer-view sources when the token-row operand fits a view (2 GB); the
+// same kernels on 64-bit addresses beyond.
+bool views_fit(int64_t rows, int K) { return rows * (int64_t)K * 2 <= kBufViewMax; }
+
 hipError_t launch_mn256(const MN256Args& a, bool swiglu, hipStream_t s) {
   int64_t total = 0;
   for (int i = 0; i < a.n_regions; ++i) total += 8 * (int64_t)mn256_share(a.reg[i].tiles);
   if (total == 0) return hipSuccess;
   if (a.tail) total += 8 * kMN256TailJobs;  // the tail blocks of every XCD, dispatched last
-  if (swiglu)
-    WIDE_RING_LAUNCH("wide_mn256<true>", (wide_mn256<true, 64>), RingMN::LDS, (unsigned)total, s, a);
+  const bool buf = views_fit(a.M, a.K);
+  if (swiglu && buf)
+    WIDE_RING_LAUNCH("wide_mn256<true>", (wide_mn256<true, 64, true>), RingMN::LDS, (unsigned)total, s, a);
+  else if (swiglu)
+    WIDE_RING_LAUNCH("wide_mn256<true>", (wide_mn256<true, 64, false>), RingMN::LDS, (unsigned)total, s, a);
+  else if (buf)
+    WIDE_RING_LAUNCH("wide_mn256<false>", (wide_mn256<false, 64, true>), RingMN::LDS, (unsigned)total, s, a);
   else
-    WIDE_RING_LAUNCH("wide_mn256<false>", (wide_mn256<false, 64>), RingMN::LDS, (unsigned)total, s, a);
+    WIDE_RING_LAUNCH("wide_mn256<false>", (wide_mn256<false, 64, false>), RingMN::LDS, (unsigned)total, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !a.tail) return e;
   const dim3 tg(8 * kMN256TailJobs * (BM / kTailRows));
@@ -815,12 +866,19 @@ hipError_t launch_kd256(const KArgs& a, hipStream_t s) {
   if (total == 0) return hipSuccess;
   if (a.K / a.G > kKd256MaxGroups) return hipErrorInvalidValue;
   const int ng = a.K / a.G;
-  if (ng <= 32)
-    WIDE_RING_LAUNCH("wide_kd256<1>", (wide_kd256<1, 64>), kd256_lds<1>(), (unsigned)total, s, a);
+  const bool buf = views_fit(a.M, a.K);
+  if (ng <= 32 && buf)
+    WIDE_RING_LAUNCH("wide_kd256<1>", (wide_kd256<1, 64, true>), kd256_lds<1>(), (unsigned)total, s, a);
+  else if (ng <= 32)
+    WIDE_RING_LAUNCH("wide_kd256<1>", (wide_kd256<1, 64, false>), kd256_lds<1>(), (unsigned)total, s, a);
+  else if (ng <= 128 && buf)
+    WIDE_RING_LAUNCH("wide_kd256<4>", (wide_kd256<4, 64, true>), kd256_lds<4>(), (unsigned)total, s, a);
   else if (ng <= 128)
-    WIDE_RING_LAUNCH("wide_kd256<4>", (wide_kd256<4, 64>), kd256_lds<4>(), (unsigned)total, s, a);
+    WIDE_RING_LAUNCH("wide_kd256<4>", (wide_kd256<4, 64, false>), kd256_lds<4>(), (unsigned)total, s, a);
+  else if (buf)
+    WIDE_RING_LAUNCH("wide_kd256<0>", (wide_kd256<0, 64, true>), kd256_lds<0>(), (unsigned)total, s, a);
   else
-    WIDE_RING_LAUNCH("wide_kd256<0>", (wide_kd256<0, 64>), kd256_lds<0>(), (unsigned)total, s, a);
+    WIDE_RING_LAUNCH("wide_kd256<0>", (wide_kd256<0, 64, false>), kd256_lds<0>(), (unsigned)total, s, a);
   return hipGetLastError();
 }
 
@@ -830,7 +888,10 @@ hipError_t launch_ks256(const KArgs& a, hipStream_t s) {
   const int64_t splits = (a.K / a.G + pack - 1) / pack;
   const int64_t total = splits * m_tiles * (a.N / BN);
   if (total == 0) return hipSuccess;
-  WIDE_RING_LAUNCH("wide_ks256", (wide_ks256<64>), RingMN::LDS, (unsigned)total, s, a);
+  if (views_fit(a.M, a.K))
+    WIDE_RING_LAUNCH("wide_ks256", (wide_ks256<64, true>), RingMN::LDS, (unsigned)total, s, a);
+  else
+    WIDE_RING_LAUNCH("wide_ks256", (wide_ks256<64, false>), RingMN::LDS, (unsigned)total, s, a);
   return hipGetLastError();
 }
 

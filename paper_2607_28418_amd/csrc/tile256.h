@@ -72,10 +72,26 @@ struct Ring {
     return (lane_id() % CPR) ^ f(slot_row(j));
   }
   // Load slot j of one operand stage; p points at the lane's 16 bytes.
-  __device__ static __forceinline__ void issue(uint16_t* stage, const uint16_t* p, int j) {
+  __device__ static __forceinline__ void issue_ptr(uint16_t* stage, const uint16_t* p, int j) {
     __builtin_amdgcn_global_load_lds((gptr_t)p, (lptr_t)(stage + (wave_id() * SLOTS + j) * RPI * BK), 16, 0, 0);
   }
+  // The same through a buffer view: the lane's 16 bytes at byte voff + soff
+  // (soff wave-uniform).  Lanes past the view's end land zeros.
+  __device__ static __forceinline__ void issue_buf(uint16_t* stage, bufview_t v, uint32_t voff, uint32_t soff, int j) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(v, (lptr_t)(stage + (wave_id() * SLOTS + j) * RPI * BK), 16, (int)voff,
+                                             (int)soff, 0, 0);
+  }
 };
+
+// Operand sources.  With a buffer view (views under 2^31 bytes) each lane
+// keeps one 32-bit byte offset per load slot for the whole tile and a step
+// adds its k offset as a scalar; a 128-bit global address per slot and step
+// cost the same loads 3-4% (measured on dense 256x256 tiles) besides the
+// VALU work.  The range check covers the scalar part too, so a dead row
+// (zeros) takes kOffDead: past every view, and still past it (no 32-bit
+// wrap) with any scalar offset below 2^31.
+constexpr uint32_t kOffDead = 0x80000000u;
+constexpr int64_t kBufViewMax = (int64_t(1) << 31) - 256;  // bytes of a view the tile kernels use
 
 // Wait until at most n of this wave's vector-memory operations are in
 // flight (expcnt and lgkmcnt untouched).  n <= 63.
@@ -186,10 +202,10 @@ __device__ __forceinline__ void substep(const Frags& f, f32x16 (&acc)[4][4], Rd 
 
 // The pipelined k loop over `nsteps` 64-deep steps.  koff(s) gives step s's
 // k offset into the operand rows (scalar work, once per step and operand);
-// at(k, j, op) the lane's source of load slot j at k offset k, op 0 for A and
-// 1 for B.  at is called beside each load, so its arithmetic sits between
-// MFMAs (with one wave per SIMD, a step's address work done in one burst
-// stalls the matrix core).  acc must be zeroed by the caller.
+// lda(stage, k, j) / ldb(stage, k, j) issue load slot j of A / B at k offset
+// k into the stage.  They are called beside each load, so their arithmetic
+// sits between MFMAs (with one wave per SIMD, a step's address work done in
+// one burst stalls the matrix core).  acc must be zeroed by the caller.
 //
 // Schedule of step kt (four 16-deep sub-steps, fragment sets alternating):
 //   - sub-step kk interleaves the LDS reads of sub-step kk+1 with its own
@@ -210,8 +226,8 @@ __device__ __forceinline__ void substep(const Frags& f, f32x16 (&acc)[4][4], Rd 
 // NL < 4 (a partial tile) skips the dead A fragments' reads and MFMAs at
 // compile time.  A wave's A load slots cover tile rows [64 w, 64 w + 64);
 // AON = false (all of them past the active rows) skips its A loads.
-template <class Rg, int NL, bool AON, class Koff, class At>
-__device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Koff koff, At at, const int (&bb)[4],
+template <class Rg, int NL, bool AON, class Koff, class LdA, class LdB>
+__device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Koff koff, LdA lda, LdB ldb, const int (&bb)[4],
                                          f32x16 (&acc)[4][4]) {
   constexpr int S = Rg::SLOTS, LEAD = Rg::LEAD;
   constexpr int RDN = NL > 0 ? NL + 4 : 0;  // fragment reads per sub-step
@@ -220,15 +236,15 @@ __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Koff koff, 
   if (nsteps > 0) {
     const int k0 = koff(0);
 #pragma unroll
-    for (int j = 0; j < S; ++j) Rg::issue(Rg::b_stage(smem, 0), at(k0, j, 1), j);
+    for (int j = 0; j < S; ++j) ldb(Rg::b_stage(smem, 0), k0, j);
     if (AON) {
 #pragma unroll
-      for (int j = 0; j < S; ++j) Rg::issue(Rg::a_stage(smem, 0), at(k0, j, 0), j);
+      for (int j = 0; j < S; ++j) lda(Rg::a_stage(smem, 0), k0, j);
     }
     if (AON && LEAD == 2 && nsteps > 1) {
       const int k1 = koff(1);
 #pragma unroll
-      for (int j = 0; j < S; ++j) Rg::issue(Rg::a_stage(smem, 1), at(k1, j, 0), j);
+      for (int j = 0; j < S; ++j) lda(Rg::a_stage(smem, 1), k1, j);
       wait_vm<S>();
     } else {
       wait_vm<0>();
@@ -254,9 +270,9 @@ __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Koff koff, 
       auto rd = [&](int kk, Frags& f) { return [&, kk](int r) { read_frag<Rg>(as, bs, kk, bb, f, r); }; };
       auto none = [](int) {};
       sched_fence();
-      substep<NL, 0, 16, RDN, LS ? S : 0>(f0, acc, rd(1, f1), [&](int j) { Rg::issue(lb, at(kb, j, 1), j); });
+      substep<NL, 0, 16, RDN, LS ? S : 0>(f0, acc, rd(1, f1), [&](int j) { ldb(lb, kb, j); });
       substep<NL, 0, 16, RDN, 0>(f1, acc, rd(2, f0), none);
-      substep<NL, 0, 16, RDN, LA ? S : 0>(f0, acc, rd(3, f1), [&](int j) { Rg::issue(la, at(ka, j, 0), j); });
+      substep<NL, 0, 16, RDN, LA ? S : 0>(f0, acc, rd(3, f1), [&](int j) { lda(la, ka, j); });
       substep<NL, 0, PRE, 0, 0>(f1, acc, none, none);
       if (NEXT) {
         wait_vm<WN>();

@@ -14,6 +14,10 @@ kernel variants ran.
 Part 2 covers group sizes 16 and 32 (Section 3.1: channel groups of 2^k,
 k >= 4; Table 1 uses 32) and attention groups of one 64-wide head: prefill,
 decode, degenerate masks, and weights of unused groups poisoned with NaN.
+
+Part 3 runs prefill with token-row operands larger than 2 GiB, past what
+the tile kernels' 32-bit buffer offsets reach, so the same kernels load
+through 64-bit addresses: sampled rows on both sides of the 2 GiB line.
 """
 import dataclasses
 import sys
@@ -313,3 +317,68 @@ def test_misaligned_mask_is_copied_by_the_binding(orc):
     y = W.wide_qkvo_masked(W.PHASE_O, d["a"][1:].contiguous(), m1, 128, 8, 2, 128, w_o=d["w_o"])
     torch.cuda.synchronize()
     check_kproj(orc, c.a[1:], c.w_o, c.mask[1:], 128, y, what="o")
+
+
+# ------------------------------------------------------------------ part 3
+
+class _Periodic:
+    """Rows of an [M][D] matrix that repeats a block of P rows.  P is odd,
+    so a row address off by any power of two lands on a different row."""
+
+    def __init__(self, block):
+        self.block = block
+
+    def __getitem__(self, rows):
+        return self.block[np.asarray(rows) % len(self.block)]
+
+
+def _periodic_dev(block, M):
+    b = to_dev(block)
+    return b.repeat(-(-M // len(block)), 1)[:M].contiguous()
+
+
+def _rows_across(M, edge, seed):
+    return np.unique(np.concatenate([[0, edge - 1, edge, edge + 1, M - 1],
+                                     synth.rng(seed).integers(0, M, 8)]))
+
+
+def test_ffn_token_operands_past_2gib(orc):
+    D, Dff, G, P = 4096, 4096, 128, 4099
+    edge = (1 << 31) // (2 * D)  # first token row past 2 GiB of x (and of H: Dff = D)
+    M = edge + 1500
+    say("ffn prefill, x and H past 2 GiB: M", M)
+    g = synth.rng(41)
+    block = synth.normal(g, (P, D), 1.0, "bf16")
+    wg = synth.normal(g, (Dff, D), 0.02, "bf16")
+    wu = synth.normal(g, (Dff, D), 0.02, "bf16")
+    wd = synth.normal(g, (D, Dff), 0.02, "bf16")
+    mask = synth.make_mask(g, "bernoulli", M, Dff // G, 0.5)
+    x = _periodic_dev(block, M)
+    y = W.wide_ffn_masked(x, to_dev(wg), to_dev(wu), to_dev(wd), to_dev(mask), G)
+    torch.cuda.synchronize()
+    del x
+    c = synth.FFNCase(_Periodic(block), wg, wu, wd, mask, G, "bf16")
+    check_ffn(orc, c, y, rows=_rows_across(M, edge, 3), what="past 2 GiB")
+
+
+def test_qkv_token_operand_past_2gib(orc):
+    D, n_q, n_kv, hd, G, P = 4096, 4, 2, 128, 256, 4099
+    edge = (1 << 31) // (2 * D)
+    M = edge + 700
+    say("q/k/v prefill, x past 2 GiB: M", M)
+    g = synth.rng(43)
+    block = synth.normal(g, (P, D), 1.0, "bf16")
+    wq = synth.normal(g, (n_q * hd, D), 0.02, "bf16")
+    wk = synth.normal(g, (n_kv * hd, D), 0.02, "bf16")
+    wv = synth.normal(g, (n_kv * hd, D), 0.02, "bf16")
+    mask = synth.make_mask(g, "bernoulli", M, n_q * hd // G, 0.5)
+    x = _periodic_dev(block, M)
+    q, k, v = W.wide_qkvo_masked(W.PHASE_QKV, x, to_dev(mask), G, n_q, n_kv, hd,
+                                 w_q=to_dev(wq), w_k=to_dev(wk), w_v=to_dev(wv))
+    torch.cuda.synchronize()
+    del x
+    rows = _rows_across(M, edge, 5)
+    xs = _Periodic(block)
+    check_nproj(orc, xs, wq, mask, G, q, rows=rows, what="q past 2 GiB")
+    check_nproj(orc, xs, wk, None, 0, k, rows=rows, what="k past 2 GiB")
+    check_nproj(orc, xs, wv, None, 0, v, rows=rows, what="v past 2 GiB")
