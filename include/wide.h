@@ -411,6 +411,15 @@ const char* wide_last_error(void);
  * capturing a graph.
  */
 wide_status_t wide_timing_enable(int enable);
+/*
+ * Restrict timing to launches whose label matches `name` (the same rule as
+ * wide_timing_query); NULL or "" times every launch again.  Each timed
+ * launch adds two event records to its stream, and between short kernels
+ * they lengthen the stream by several microseconds each; a measurement of a
+ * whole pass can time just the kernel it needs.  Takes effect for launches
+ * issued after the call; the recorded events are kept.
+ */
+wide_status_t wide_timing_filter(const char* name);
 wide_status_t wide_timing_reset(void);
 wide_status_t wide_timing_query(const char* name, double* total_ms,
                                 int64_t* launches);

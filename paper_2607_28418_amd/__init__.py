@@ -16,7 +16,7 @@ __all__ = [
     "WideError", "lib", "wide_mask_reorder", "wide_ffn_masked", "wide_qkvo_masked", "wide_router",
     "wide_attention_masked", "wide_attention_workspace_size", "wide_attention_decode",
     "wide_attention_decode_workspace_size", "wide_workspace_size", "wide_set_option", "wide_get_option", "wide_timing_enable",
-    "wide_timing_reset", "wide_timing_query", "wide_ffn_masked_noalloc", "wide_static_scratch_bytes", "LIB_PATH",
+    "wide_timing_reset", "wide_timing_query", "wide_timing_filter", "wide_ffn_masked_noalloc", "wide_static_scratch_bytes", "LIB_PATH",
     "OP_REORDER", "OP_FFN", "OP_QKV", "OP_O", "OP_ROUTER", "PHASE_QKV", "PHASE_O", "F32", "BF16",
 ]
 
@@ -82,6 +82,8 @@ def lib() -> ctypes.CDLL:
         L.wide_timing_enable.argtypes = [ci]
         L.wide_timing_reset.restype = ci
         L.wide_timing_reset.argtypes = []
+        L.wide_timing_filter.restype = ci
+        L.wide_timing_filter.argtypes = [ctypes.c_char_p]
         L.wide_timing_query.restype = ci
         L.wide_timing_query.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(i64)]
@@ -168,6 +170,11 @@ def wide_timing_enable(on: bool = True) -> None:
 
 def wide_timing_reset() -> None:
     _check("wide_timing_reset", lib().wide_timing_reset())
+
+
+def wide_timing_filter(name=None) -> None:
+    """Time only launches labelled `name` (query's matching rule); None: all."""
+    _check("wide_timing_filter", lib().wide_timing_filter(name.encode() if name else None))
 
 
 def wide_timing_query(name: str):

@@ -413,6 +413,14 @@ bool g_timing = false;
 std::vector<TimingRec> g_pool;
 size_t g_used = 0;
 std::vector<std::string> g_names;
+std::string g_timing_filter;  // only launches whose label it matches are timed ("": every launch)
+
+// `label` is `want` exactly, or `want` followed by a template argument list or
+// a "/variant" suffix.
+bool label_matches(const std::string& label, const std::string& want) {
+  return label.compare(0, want.size(), want) == 0 &&
+         (label.size() == want.size() || label[want.size()] == '<' || label[want.size()] == '/');
+}
 
 int name_id(const char* n) {
   for (size_t i = 0; i < g_names.size(); ++i)
@@ -429,6 +437,7 @@ int timing_begin(const char* name, hipStream_t s) {
   if (!g_timing) return -1;
   std::lock_guard<std::mutex> lk(g_tmu);
   if (!g_timing || g_used >= g_pool.size()) return -1;
+  if (!g_timing_filter.empty() && !label_matches(name, g_timing_filter)) return -1;
   const int slot = (int)g_used++;
   g_pool[slot].name = name_id(name);
   (void)hipEventRecord(g_pool[slot].start, s);
@@ -982,6 +991,12 @@ wide_status_t wide_timing_enable(int enable) {
   return ok();
 }
 
+wide_status_t wide_timing_filter(const char* name) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  g_timing_filter = name ? name : "";
+  return ok();
+}
+
 wide_status_t wide_timing_reset(void) {
   std::lock_guard<std::mutex> lk(g_tmu);
   g_used = 0;
@@ -995,10 +1010,7 @@ wide_status_t wide_timing_query(const char* name, double* total_ms, int64_t* lau
   double tot = 0.0;
   int64_t n = 0;
   for (size_t i = 0; i < g_used; ++i) {
-    const std::string& label = g_names[g_pool[i].name];
-    const bool hit = label.compare(0, want.size(), want) == 0 &&
-                     (label.size() == want.size() || label[want.size()] == '<' || label[want.size()] == '/');
-    if (!hit) continue;
+    if (!label_matches(g_names[g_pool[i].name], want)) continue;
     hipError_t e = hipEventSynchronize(g_pool[i].stop);
     if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
     float ms = 0.f;

@@ -404,6 +404,25 @@ def test_timing_records_kernels():
     assert n == 1 and ms > 0
 
 
+def test_timing_filter_times_only_matching_launches():
+    say("timing filter")
+    c = synth.ffn_case(1, 256, 256, 512, 128, mask="bernoulli")
+    x, wg, wu, wd, m = ffn_dev(c)
+    W.wide_timing_enable(True)
+    W.wide_timing_reset()
+    try:
+        W.wide_timing_filter("wide_mn256<true>")
+        W.wide_ffn_masked(x, wg, wu, wd, m, 128)
+        W.wide_timing_filter(None)
+        W.wide_ffn_masked(x, wg, wu, wd, m, 128)
+        n_up = W.wide_timing_query("wide_mn256<true>")[1]
+        n_down = W.wide_timing_query("wide_kd256")[1]
+    finally:
+        W.wide_timing_filter(None)
+        W.wide_timing_enable(False)
+    assert n_up == 2 and n_down == 1
+
+
 # ------------------------------------------------------------------ router
 
 def _router_case(M, D, r, ng, seed):
