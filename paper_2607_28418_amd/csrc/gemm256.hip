@@ -429,27 +429,41 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
   }
 
   // Epilogue: rows back to token order; rows past cnt hold +0 accumulators.
-  // A token-order region stores +0 where the row's group is inactive.
+  // A token-order region stores +0 where the row's group is inactive.  The
+  // bf16 tile goes through the idle ring LDS (after the row map), rows
+  // padded by 16 bytes, so that each lane then stores whole 16-byte pieces of
+  // an output row: 8 times fewer store instructions than a 2-byte store per
+  // accumulator, which is how the MFMA layout holds them (those stores cost
+  // gate/up 3%; staged, gate/up is 1.5% faster).
   const int* map = stage_row_map(smem, my_row, (int)rbits);
   const int gsh = tok_order ? __builtin_ctz(a.mask_G) : 0;
   constexpr int NO = SWIGLU ? 2 : 4;  // output fragments of the wave
+  constexpr int PITCH = BNO + 8;      // bf16 per staged row
+  static_assert(2 * BM * (int)sizeof(int) + BM * PITCH * 2 <= Rg::LDS, "row map and staged tile fit the ring");
+  uint16_t* ot = smem + 2 * BM * (int)(sizeof(int) / sizeof(uint16_t));
 #pragma unroll
   for (int fm = 0; fm < 4; ++fm) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int r = acc_row(fm, i);
-      const int t = map[r];
-      if (t < 0) continue;
       const int rb = tok_order ? map[BM + r] : 0;
-      uint16_t* o = R.out + (int64_t)t * R.ldo + n0;
 #pragma unroll
       for (int fn = 0; fn < NO; ++fn) {
         const int c = bb[fn] + col;  // output column in the tile
         const bool on = !tok_order || ((rb >> (c >> gsh)) & 1);
         const float v = SWIGLU ? silu(acc[fm][fn][i]) * acc[fm][fn + 2][i] : acc[fm][fn][i];
-        o[c] = f32_to_bf16_hw(on ? v : 0.f);
+        ot[r * PITCH + c] = f32_to_bf16_hw(on ? v : 0.f);
       }
     }
+  }
+  __syncthreads();
+  constexpr int CPR = BNO / 8;  // 16-byte pieces per output row
+#pragma unroll 4
+  for (int q = tid; q < BM * CPR; q += NT) {
+    const int r = q / CPR, c8 = q % CPR;
+    const int t = map[r];
+    if (t >= 0)
+      stg16(R.out + (int64_t)t * R.ldo + n0 + c8 * 8, *reinterpret_cast<const u32x4*>(ot + r * PITCH + c8 * 8));
   }
 }
 
