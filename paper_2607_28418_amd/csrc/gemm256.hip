@@ -123,14 +123,18 @@ __device__ __forceinline__ bool mn256_ordered(const MN256Args& a, const MN256Reg
 }
 
 // "m-blocked" (gate/up): when an XCD's share is a whole number of groups, it
-// runs m-tile 0 of each of its groups, then m-tile 1, and so on.  The tiles
-// that run together then gather rows from one stretch of tokens (a sorted
-// m-tile of any group covers about the same token range) instead of one
-// group's whole token list, so the gathered rows are mostly shared in L2
-// while each group's weight panel is re-read once per m-tile.  Measured on
-// the Llama-3-8B gate/up at T = 8192 (topk, keep 0.5): traffic from beyond
-// L2 down 37%, time down 2%; blocks of 4 or 8 m-tiles per group cut the
-// traffic as much but ran 7-9% slower than group by group.
+// runs m-tile 0 of each of its groups, then m-tile 1, and so on, over one
+// half of its groups and then the other.  The tiles that run together then
+// gather rows from one stretch of tokens (a sorted m-tile of any group
+// covers about the same token range) instead of one group's whole token
+// list, so the gathered rows are mostly shared in L2 while each group's
+// weight panel is re-read once per m-tile.  Measured on the Llama-3-8B
+// gate/up at T = 8192 (topk, keep 0.5): traffic from beyond L2 down 37%,
+// time down 2% against group by group; blocks of 4 or 8 m-tiles per group
+// cut the traffic as much but ran 7-9% slower.  Halves (7 of the XCD's 14
+// groups at a time, so fewer weight panels per k step, and the first
+// half's partial m-tiles run beside the second half's full ones) took
+// another 2.5% off; pairs of groups did the same.
 template <int BNO>
 __device__ __forceinline__ bool mn256_mblocked(const MN256Args& a, const MN256Region& R) {
   const int share = mn256_share(R.tiles), per_group = R.gw / BNO * a.m_tiles;
@@ -146,9 +150,12 @@ __device__ __forceinline__ void mn256_coords(const MN256Args& a, const MN256Regi
   const int ntpg = R.gw / BNO;  // tiles per group
   const int per_group = ntpg * a.m_tiles;
   if (mn256_mblocked<BNO>(a, R)) {
-    const int gps = share / per_group, r = local % (gps * ntpg);
-    m_tile = local / (gps * ntpg);
-    g = xcd * gps + r / ntpg;
+    // the XCD's groups in two halves, each walked m-tile by m-tile
+    const int gps = share / per_group, parts = gps % 2 == 0 && gps >= 4 ? 2 : 1, gpp = gps / parts;
+    const int per_part = gpp * ntpg * a.m_tiles, part = local / per_part, l = local % per_part;
+    const int r = l % (gpp * ntpg);
+    m_tile = l / (gpp * ntpg);
+    g = xcd * gps + part * gpp + r / ntpg;
     nt_in = r % ntpg;
     return;
   }
