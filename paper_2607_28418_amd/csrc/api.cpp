@@ -409,7 +409,7 @@ struct TimingRec {
 };
 
 std::mutex g_tmu;
-bool g_timing = false;
+std::atomic<bool> g_timing{false};  // read unlocked by every launch
 std::vector<TimingRec> g_pool;
 size_t g_used = 0;
 std::vector<std::string> g_names;
