@@ -658,19 +658,19 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
   zero_acc(acc);
   // Every step needs, per slot row, one bit of its mask row.  Reading them
   // from LDS at each step put several dependent LDS round trips in front of
-  // the step's loads; with NWR > 0 the rows' mask words sit in registers
-  // (rows past M hold zero words, so their blocks read as zeros), and so
-  // does the union's group list: lane l holds groups l and 64 + l, and a
-  // step takes its group with a readlane.
+  // the step's loads; with NWR > 0 the rows' mask words sit in registers,
+  // inverted (rows past M hold zero words, all ones inverted, so their
+  // blocks read as zeros), and so does the union's group list: lane l holds
+  // groups l and 64 + l, and a step takes its group with a readlane.
   // (words past the row's last group are never selected: any value will do)
-  uint64_t mlo[S], mhi[S];
+  uint64_t nlo[S], nhi[S];
 #pragma unroll
   for (int j = 0; j < S; ++j) {
-    mlo[j] = mhi[j] = 0;
-    if (NWR >= 1) mlo[j] = tb.mbits[srow[j]][0];
+    nlo[j] = nhi[j] = ~0ull;
+    if (NWR >= 1) nlo[j] = ~(uint64_t)tb.mbits[srow[j]][0];
     if (NWR >= 4) {
-      mlo[j] |= (uint64_t)tb.mbits[srow[j]][1] << 32;
-      mhi[j] = tb.mbits[srow[j]][2] | (uint64_t)tb.mbits[srow[j]][3] << 32;
+      nlo[j] = ~((uint64_t)tb.mbits[srow[j]][0] | (uint64_t)tb.mbits[srow[j]][1] << 32);
+      nhi[j] = ~((uint64_t)tb.mbits[srow[j]][2] | (uint64_t)tb.mbits[srow[j]][3] << 32);
     }
   }
   const int glo = NWR >= 1 ? tb.groups[lane] : 0;
@@ -689,18 +689,24 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
     const int gi = s >> lsp;
     return group(gi) * a.G + (s & (spg - 1)) * BK;
   };
+  // Inactive (t, g) blocks are never read.  Bit 31 of `dead` is set for
+  // them: the inverted mask bit shifted up to bit 31 (one 64-bit shift by a
+  // uniform amount) and merged into the row's view offset.  A row's offset
+  // plus any step's k offset is a byte inside the view, below 2^31, so with
+  // bit 31 added the sum is past the view and below 2^32 (no wrap).  Four
+  // vector instructions per load where a compare and a select took six.
   auto lda = [&](uint16_t* st, int k0, int j) {
     const int gg = k0 >> lg;
-    bool on;
+    uint32_t dead;
     if (NWR == 0)
-      on = (tb.mbits[srow[j]][gg >> 5] >> (gg & 31)) & 1u;
+      dead = (tb.mbits[srow[j]][gg >> 5] >> (gg & 31)) & 1u ? 0u : kOffDead;
     else if (NWR == 1)
-      on = (mlo[j] >> gg) & 1u;
+      dead = (uint32_t)nlo[j] << (31 - gg);
     else
-      on = ((gg < 64 ? mlo[j] : mhi[j]) >> (gg & 63)) & 1u;
-    // inactive (t, g) blocks are never read
-    if (BUF) Rg::issue_buf(st, va, on ? aoff[j] : kOffDead, 2u * k0, j);
-    else Rg::issue_ptr(st, on ? abase[j] + k0 : zero, j);
+      dead = (uint32_t)(((gg < 64 ? nlo[j] : nhi[j]) << (63 - (gg & 63))) >> 32);
+    dead &= kOffDead;
+    if (BUF) Rg::issue_buf(st, va, dead | aoff[j], 2u * k0, j);
+    else Rg::issue_ptr(st, dead ? zero : abase[j] + k0, j);
   };
   auto ldb = [&](uint16_t* st, int k0, int j) {
     if (BUF) Rg::issue_buf(st, vb, boff[j], 2u * k0, j);

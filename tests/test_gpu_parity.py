@@ -297,17 +297,20 @@ def test_qkvo_fp32_small(orc):
     check_qkvo(orc, c, kind="f32")
 
 
-def test_o_poisoned_inactive_blocks(orc):
-    """Inactive blocks of the attention output are never read."""
+@pytest.mark.parametrize("n_q,n_kv,hd,G", [(8, 2, 128, 256), (64, 8, 128, 128), (136, 8, 64, 64)])
+def test_o_poisoned_inactive_blocks(orc, n_q, n_kv, hd, G):
+    """Inactive blocks of the attention output are never read: 4, 64 and 136
+    groups cover the dense-masked K axis with its rows' mask words in
+    registers (up to 32 and up to 128 groups) and in LDS (beyond)."""
     for M, kpath in ((300, 1), (300, 2), (20, 0)):
-        say("o poison", M, kpath)
+        say("o poison", n_q, hd, G, M, kpath)
         W.wide_set_option("k_path", kpath)
-        c = synth.attn_case(9, M, 256, 8, 2, 128, 256, mask="bernoulli")
+        c = synth.attn_case(9, M, 256, n_q, n_kv, hd, G, mask="bernoulli")
         d = attn_dev(c)
         a = d["a"].clone()
         inactive = torch.from_numpy(np.repeat(c.mask == 0, c.G, axis=1)).to(dev())
         a[inactive] = float("nan")
-        y = W.wide_qkvo_masked(W.PHASE_O, a, d["mask"], c.G, 8, 2, 128, w_o=d["w_o"])
+        y = W.wide_qkvo_masked(W.PHASE_O, a, d["mask"], c.G, n_q, n_kv, hd, w_o=d["w_o"])
         torch.cuda.synchronize()
         check_kproj(orc, c.a, c.w_o, c.mask, c.G, y, what="o poisoned")
 
