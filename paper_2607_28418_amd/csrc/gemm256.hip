@@ -78,7 +78,7 @@ __host__ __device__ __forceinline__ int mn256_share(int tiles) { return (tiles +
 // The k loop of one tile with the wave's live A fragments and A loads:
 // `act` tile rows are active, always a prefix (rows past the active count, or
 // past M, come last in a tile).
-template <class Rg, class Koff, class LdA, class LdB>
+template <class Rg, int BL, class Koff, class LdA, class LdB>
 __device__ __forceinline__ void run_tile(uint16_t* smem, int nsteps, Koff koff, LdA lda, LdB ldb, const int (&bb)[4],
                                          int64_t act, f32x16 (&acc)[4][4]) {
   const int p = (int)(act < 0 ? 0 : act > BM ? BM : act);
@@ -88,17 +88,17 @@ __device__ __forceinline__ void run_tile(uint16_t* smem, int nsteps, Koff koff, 
   // (nl, aon): (4|3, true) full or nearly; (2|1, true|false); (0, false) -- the
   // waves of the lower half of a tile with at most 128 active rows
   switch (nl) {
-    case 4: mainloop<Rg, 4, true>(smem, nsteps, koff, lda, ldb, bb, acc); break;
-    case 3: mainloop<Rg, 3, true>(smem, nsteps, koff, lda, ldb, bb, acc); break;
+    case 4: mainloop<Rg, 4, true, BL>(smem, nsteps, koff, lda, ldb, bb, acc); break;
+    case 3: mainloop<Rg, 3, true, BL>(smem, nsteps, koff, lda, ldb, bb, acc); break;
     case 2:
-      if (aon) mainloop<Rg, 2, true>(smem, nsteps, koff, lda, ldb, bb, acc);
-      else mainloop<Rg, 2, false>(smem, nsteps, koff, lda, ldb, bb, acc);
+      if (aon) mainloop<Rg, 2, true, BL>(smem, nsteps, koff, lda, ldb, bb, acc);
+      else mainloop<Rg, 2, false, BL>(smem, nsteps, koff, lda, ldb, bb, acc);
       break;
     case 1:
-      if (aon) mainloop<Rg, 1, true>(smem, nsteps, koff, lda, ldb, bb, acc);
-      else mainloop<Rg, 1, false>(smem, nsteps, koff, lda, ldb, bb, acc);
+      if (aon) mainloop<Rg, 1, true, BL>(smem, nsteps, koff, lda, ldb, bb, acc);
+      else mainloop<Rg, 1, false, BL>(smem, nsteps, koff, lda, ldb, bb, acc);
       break;
-    default: mainloop<Rg, 0, false>(smem, nsteps, koff, lda, ldb, bb, acc); break;
+    default: mainloop<Rg, 0, false, BL>(smem, nsteps, koff, lda, ldb, bb, acc); break;
   }
 }
 }  // namespace
@@ -398,10 +398,10 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
   // up column c (B rows 128..255), so a wave takes 64 gate rows (fragments 0
   // and 1) and the same 64 up rows (fragments 2 and 3)
   const int wn = wave_id() & 1;
+  constexpr int BL = SWIGLU ? 1 : 0;
   int bb[4];
 #pragma unroll
-  for (int fn = 0; fn < 4; ++fn)
-    bb[fn] = SWIGLU ? (fn >> 1) * 128 + wn * 64 + (fn & 1) * 32 : wn * 128 + fn * 32;
+  for (int fn = 0; fn < 4; ++fn) bb[fn] = (SWIGLU ? wn * 64 : wn * 128) + bfrag_off<BL>(fn);
 
   f32x16 acc[4][4];
   zero_acc(acc);
@@ -419,7 +419,7 @@ __global__ __launch_bounds__(NT, 1) void wide_mn256(MN256Args a) {
   int my_row = -1;
   if (job < 0 && tid < BM && m0 + tid < M) my_row = rows ? rows[m0 + tid] : (int)(m0 + tid);
   // l = 2: fragments wholly past the active prefix issue no MFMA
-  run_tile<Rg>(smem, ns, koff, lda, ldb, bb, cnt - m0, acc);
+  run_tile<Rg, BL>(smem, ns, koff, lda, ldb, bb, cnt - m0, acc);
   const int col = acc_col();
 
   if (job >= 0) {  // tail chunk: fp32 partial tile [256 rows][256 B-tile rows]
@@ -652,7 +652,7 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
   const int lane = lane_id(), wn = wave_id() & 1;
   int bb[4];
 #pragma unroll
-  for (int fn = 0; fn < 4; ++fn) bb[fn] = wn * 128 + fn * 32;
+  for (int fn = 0; fn < 4; ++fn) bb[fn] = wn * 128 + bfrag_off<0>(fn);
 
   f32x16 acc[4][4];
   zero_acc(acc);
@@ -714,7 +714,7 @@ __global__ __launch_bounds__(NT, 1) void wide_kd256(KArgs a) {
   };
   int my_row = -1;
   if (tid < BM && m0 + tid < a.M) my_row = (int)token(m0 + tid);
-  run_tile<Rg>(smem, nsteps, koff, lda, ldb, bb, a.M - m0, acc);
+  run_tile<Rg, 0>(smem, nsteps, koff, lda, ldb, bb, a.M - m0, acc);
 
   const int* map = stage_row_map(smem, my_row);
   const int col = acc_col();
@@ -767,7 +767,7 @@ __global__ __launch_bounds__(NT, 1) void wide_ks256(KArgs a) {
   const int wn = wave_id() & 1;
   int bb[4];
 #pragma unroll
-  for (int fn = 0; fn < 4; ++fn) bb[fn] = wn * 128 + fn * 32;
+  for (int fn = 0; fn < 4; ++fn) bb[fn] = wn * 128 + bfrag_off<0>(fn);
   const int col = acc_col();
   const int* map = reinterpret_cast<const int*>(smem);
   const uint16_t* wpanel = uniform_ptr(a.w + (int64_t)n0 * a.K);
@@ -809,7 +809,7 @@ __global__ __launch_bounds__(NT, 1) void wide_ks256(KArgs a) {
     int my_row = -1;
     if ((int)threadIdx.x < BM && m0 + (int)threadIdx.x < cnt) my_row = rows[m0 + threadIdx.x];
     __syncthreads();  // the previous group's epilogue is done with the row map in the ring
-    run_tile<Rg>(smem, a.G / BK, koff, lda, ldb, bb, cnt - m0, acc);  // l = 2: dead fragments skipped
+    run_tile<Rg, 0>(smem, a.G / BK, koff, lda, ldb, bb, cnt - m0, acc);  // l = 2: dead fragments skipped
     stage_row_map(smem, my_row);
 #pragma unroll
     for (int fm = 0; fm < 4; ++fm) {

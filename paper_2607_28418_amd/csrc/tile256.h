@@ -145,17 +145,34 @@ struct Frags {
 
 // Fragment read r of a sub-step, in the order the MFMAs first use them:
 // A0, B0, B1, B2, B3, A1, A2, A3.
-template <class Rg>
+// B fragment fn of a wave starts bfrag_off<BL>(fn) tile rows after its
+// first, bb[0] (a multiple of 32): BL 0, four consecutive 32-row fragments;
+// BL 1 (gate/up pairs), two consecutive fragments of gate rows and the same
+// two of up rows, 128 rows on.  Kernels build bb[fn] = bb[0] + bfrag_off.
+template <int BL>
+__host__ __device__ constexpr int bfrag_off(int fn) {
+  return BL == 0 ? fn * 32 : (fn >> 1) * 128 + (fn & 1) * 32;
+}
+
+// Every fragment starts at a tile row that is a multiple of 32, so its
+// swizzle depends on the lane alone: the address is the fragment's row base
+// times BK plus one per-lane offset per sub-step, the same for A and B.  The
+// row bases are a wave-uniform value plus constants, so a sub-step's four A
+// and four B reads share two address registers and differ by immediate
+// offsets (an XOR over the whole row, or a base per fragment, needed one add
+// per read).
+template <class Rg, int BL>
 __device__ __forceinline__ void read_frag(const uint16_t* as, const uint16_t* bs, int kk, const int (&bb)[4],
                                           Frags& f, int r) {
   const int lane = lane_id(), l32 = lane & 31;
   const int ch = kk * 2 + (lane >> 5);
   const int wm = wave_id() >> 1;
+  const int lo = l32 * BK + ((ch ^ Rg::f(l32)) << 3);  // = swz(base + l32, ch) - base * BK
   if (r == 0 || r >= 5) {
     const int fm = r == 0 ? 0 : r - 4;
-    f.a[fm] = *reinterpret_cast<const u32x4*>(&as[Rg::swz(wm * 128 + fm * 32 + l32, ch)]);
+    f.a[fm] = *reinterpret_cast<const u32x4*>(as + wm * 128 * BK + lo + fm * 32 * BK);
   } else {
-    f.b[r - 1] = *reinterpret_cast<const u32x4*>(&bs[Rg::swz(bb[r - 1] + l32, ch)]);
+    f.b[r - 1] = *reinterpret_cast<const u32x4*>(bs + bb[0] * BK + lo + bfrag_off<BL>(r - 1) * BK);
   }
 }
 
@@ -226,7 +243,7 @@ __device__ __forceinline__ void substep(const Frags& f, f32x16 (&acc)[4][4], Rd 
 // NL < 4 (a partial tile) skips the dead A fragments' reads and MFMAs at
 // compile time.  A wave's A load slots cover tile rows [64 w, 64 w + 64);
 // AON = false (all of them past the active rows) skips its A loads.
-template <class Rg, int NL, bool AON, class Koff, class LdA, class LdB>
+template <class Rg, int NL, bool AON, int BL, class Koff, class LdA, class LdB>
 __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Koff koff, LdA lda, LdB ldb, const int (&bb)[4],
                                          f32x16 (&acc)[4][4]) {
   constexpr int S = Rg::SLOTS, LEAD = Rg::LEAD;
@@ -253,7 +270,7 @@ __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Koff koff, 
     Frags f0, f1;
     if (NL > 0) {
 #pragma unroll
-      for (int r = 0; r < RDN; ++r) read_frag<Rg>(Rg::a_stage(smem, 0), Rg::b_stage(smem, 0), 0, bb, f0, r);
+      for (int r = 0; r < RDN; ++r) read_frag<Rg, BL>(Rg::a_stage(smem, 0), Rg::b_stage(smem, 0), 0, bb, f0, r);
     }
     // LS: issue B of kt+1; LA: A of kt+LEAD; NEXT: step kt+1 exists; WN: loads
     // allowed in flight when waiting for step kt+1
@@ -267,7 +284,7 @@ __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Koff koff, 
       uint16_t* la = Rg::a_stage(smem, kt + LEAD);
       const int kb = LS ? koff(kt + 1) : 0;
       const int ka = LA ? koff(kt + LEAD) : 0;
-      auto rd = [&](int kk, Frags& f) { return [&, kk](int r) { read_frag<Rg>(as, bs, kk, bb, f, r); }; };
+      auto rd = [&](int kk, Frags& f) { return [&, kk](int r) { read_frag<Rg, BL>(as, bs, kk, bb, f, r); }; };
       auto none = [](int) {};
       sched_fence();
       substep<NL, 0, 16, RDN, LS ? S : 0>(f0, acc, rd(1, f1), [&](int j) { ldb(lb, kb, j); });
@@ -281,7 +298,7 @@ __device__ __forceinline__ void mainloop(uint16_t* smem, int nsteps, Koff koff, 
       sched_fence();
       const uint16_t* an = Rg::a_stage(smem, kt + 1);
       const uint16_t* bn = Rg::b_stage(smem, kt + 1);
-      substep<NL, PRE, 16, NEXT ? RDN : 0, 0>(f1, acc, [&](int r) { read_frag<Rg>(an, bn, 0, bb, f0, r); }, none);
+      substep<NL, PRE, 16, NEXT ? RDN : 0, 0>(f1, acc, [&](int r) { read_frag<Rg, BL>(an, bn, 0, bb, f0, r); }, none);
     };
     using T = std::true_type;
     using F = std::false_type;
