@@ -18,8 +18,9 @@ bottleneck router (rank 32) over the same tokens.
 value = active FLOPs of the step (FLOPs of the executed groups only, the
 paper's accounting) / step time, in TFLOP/s.  The JSON line also carries the
 prefill and decode figures separately, the speedup over dense bf16 GEMMs
-(hipBLASLt through torch) and over the same kernels with an all-ones mask,
-the roofline of the dominant kernel (HIP-event durations recorded inside the
+(hipBLASLt through torch) and over the same kernels with an all-ones mask
+(the decode references, like the masked decode pass, timed right after a
+prefill pass; back-to-back replays beside them), the roofline of the dominant kernel (HIP-event durations recorded inside the
 timed region) and the fp64 CPU oracle timed on a bounded sample of the same
 workload.
 """
