@@ -49,7 +49,10 @@ def ffn_dev(c):
     (4096, 86, "topk"), (8192, 112, "topk"), (1000, 5, "zeros"), (1000, 5, "ones"),
     # single-kernel path up to 32768 tokens (1024-token chunks, ragged tails), three-kernel beyond
     (1024, 7, "bernoulli"), (1025, 3, "bernoulli"), (32768, 24, "bernoulli"), (32769, 24, "bernoulli"),
-    (65573, 112, "topk")])
+    (65573, 112, "topk"),
+    # single-kernel path at its largest sizes and group counts of 32..128
+    (64, 32, "ones"), (65, 48, "zeros"), (1000, 64, "bernoulli"), (32767, 128, "bernoulli"),
+    (32768, 112, "topk")])
 def test_reorder_bit_exact(orc, M, ng, kind):
     say("reorder", M, ng, kind)
     g = synth.rng(M + ng)
